@@ -1,0 +1,120 @@
+/*
+ * hco.h -- plain, slow, single-threaded CPU oracle for lossless homomorphic
+ * gradient compression (Count Sketch + bitmap index + peeling recovery).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the CPU
+ * baseline leg of the benchmark may load this library.  The GPU library never
+ * links, includes or calls it, and it shares no code with the GPU library.
+ *
+ * What it computes (paper sections cited per function in hco.c):
+ *   Phase I   (Algorithm 1, sections 3.1, 3.2, 3.4): Count Sketch Y and bitmap B
+ *             of one worker's gradient X.
+ *   Aggregate (Algorithm 1, between the phases): Y <- sum of Y_w, B <- OR of B_w.
+ *   Phase II  (Algorithm 1, section 3.2): synchronous peeling rounds, then the
+ *             Count Sketch median estimate for whatever could not be peeled.
+ *
+ * Value types: int32 fixed point (sums wrap modulo 2^32, the way an integer
+ * switch adds) and a floating-point path that the oracle runs in fp64.
+ *
+ * Sketch format (the paper fixes none of these details; the readings are
+ * listed with the design notes of the repository):
+ *   batch b = p / c, column t = p mod c             (section 3.4, c = 1024)
+ *   h_j(b)  = SplitMix64 output number 3*b + j for state `seed`, j = 0, 1, 2
+ *   rows    : r_0 = mulhi32(lo32(h_0), R)
+ *             r_1 = mulhi32(lo32(h_1), R-1), then skip r_0
+ *             r_2 = mulhi32(lo32(h_2), R-2), then skip min(r_0,r_1) and max(r_0,r_1)
+ *             so the three rows of a batch are distinct (the three hash
+ *             indexes of an element are different, section 3.1)
+ *   bias_j  = (h_j >> 32) & (c - 1)                 (random rotation, section 3.4)
+ *   g_j     = +1 if bit 63 of h_j is 0, else -1     (sign hash, section 3.1)
+ *   cell_j(p) = r_j * c + ((t + bias_j) & (c - 1))
+ *   B bit p = bit (p & 31) of 32-bit word p >> 5; bits past n are zero.
+ */
+#ifndef HCO_H
+#define HCO_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct {
+    uint64_t n;     /* gradient length N, 1 .. 2^32-1                         */
+    uint32_t k;     /* number of hashes; the paper uses three, only 3 accepted */
+    uint32_t c;     /* batch width, power of two in [1, 1024]                 */
+    uint64_t rows;  /* sketch rows R >= 3; cells = R * c < 2^32               */
+    uint64_t seed;  /* hash seed shared by all workers                        */
+} hco_geom;
+
+typedef struct {
+    uint64_t n_support;    /* set bits of the aggregated bitmap                 */
+    uint64_t n_recovered;  /* elements recovered by peeling                     */
+    uint64_t rounds;       /* synchronous peeling rounds that peeled >= 1       */
+    uint32_t success;      /* 1 iff every element of the support was peeled     */
+    uint32_t pad;
+} hco_info;
+
+/* 0 on success, -1 on an invalid geometry. */
+int hco_check_geom(const hco_geom *g);
+/* rows = max(3, ceil(ceil(gamma * n_nonzero) / c)) -- sketch size >= gamma*n
+ * (section 3.2, gamma = 1.23). */
+uint64_t hco_rows_for(uint64_t n_nonzero, double gamma, uint32_t c);
+
+/* SplitMix64: `count` consecutive outputs for state `seed`. */
+void hco_splitmix64(uint64_t seed, uint64_t count, uint64_t *out);
+/* rows, biases and signs of batch b. */
+void hco_batch_hash(const hco_geom *g, uint64_t b, uint64_t row[3],
+                    uint32_t bias[3], int32_t sign[3]);
+/* cells[3*i+j], signs[3*i+j] for the parameters idx[0..m). */
+void hco_cells(const hco_geom *g, const uint64_t *idx, uint64_t m,
+               uint64_t *cells, int32_t *signs);
+
+/* Phase I on a dense gradient.  Y[cells], B[ceil(n/32)] are overwritten. */
+int hco_encode_i32(const hco_geom *g, const int32_t *x, int32_t *Y, uint32_t *B);
+int hco_encode_f64(const hco_geom *g, const double *x, double *Y, uint32_t *B);
+/* Phase I on COO input (idx distinct, any order; zero values are skipped). */
+int hco_encode_coo_i32(const hco_geom *g, const uint32_t *idx, const int32_t *val,
+                       uint64_t nnz, int32_t *Y, uint32_t *B);
+int hco_encode_coo_f64(const hco_geom *g, const uint32_t *idx, const double *val,
+                       uint64_t nnz, double *Y, uint32_t *B);
+
+/* Aggregation: Yout = sum over w of Yin[w] (int32 wraps; fp64 adds in worker
+ * order 0..W-1), Bout = OR over w of Bin[w]. */
+void hco_aggregate_i32(uint32_t W, uint64_t cells, uint64_t words,
+                       const int32_t *Yin, const uint32_t *Bin,
+                       int32_t *Yout, uint32_t *Bout);
+void hco_aggregate_f64(uint32_t W, uint64_t cells, uint64_t words,
+                       const double *Yin, const uint32_t *Bin,
+                       double *Yout, uint32_t *Bout);
+
+/* Phase II with synchronous rounds.  Y and B are not modified.
+ * x_out[n]: recovered value, the median estimate for unpeeled members of the
+ *           support, 0 outside the support.
+ * mask[ceil(n/32)] (may be NULL): bit p set iff p was recovered by peeling.
+ * round_of[n] (may be NULL): 1-based round that peeled p, 0 otherwise.
+ * Returns 0, or -1 on an invalid geometry / allocation failure. */
+int hco_decode_i32(const hco_geom *g, const int32_t *Y, const uint32_t *B,
+                   int32_t *x_out, uint32_t *mask, hco_info *info,
+                   uint32_t *round_of);
+int hco_decode_f64(const hco_geom *g, const double *Y, const uint32_t *B,
+                   double *x_out, uint32_t *mask, hco_info *info,
+                   uint32_t *round_of);
+
+/* Independent cross-check: one-at-a-time peeling from a FIFO queue of pure
+ * cells.  Same outputs as hco_decode_i32 except that info->rounds is 0. */
+int hco_decode_queue_i32(const hco_geom *g, const int32_t *Y, const uint32_t *B,
+                         int32_t *x_out, uint32_t *mask, hco_info *info);
+
+/* Count Sketch query of section 3.1 for one parameter p: the median over j of
+ * g_j(p) * Y[h_j(p)], on a sketch as given (no peeling). */
+int32_t hco_query_i32(const hco_geom *g, const int32_t *Y, uint64_t p);
+double  hco_query_f64(const hco_geom *g, const double *Y, uint64_t p);
+
+/* Median of three (exposed for fixture tests of the estimator). */
+int32_t hco_median3_i32(int32_t a, int32_t b, int32_t c);
+double  hco_median3_f64(double a, double b, double c);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

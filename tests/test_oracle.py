@@ -1,0 +1,533 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Every check here is independent of the oracle's own code path: published
+vectors, closed forms, brute force over tiny inputs, algebraic identities
+(homomorphism, linearity), cross-checks between two independently written
+peelers, and the plain definition of the result (the direct sum of the
+workers' gradients).
+"""
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+from scipy.optimize import brentq
+
+import oracle as o
+import workloads as wl
+from conftest import read_golden
+
+U32 = np.uint64(0xFFFFFFFF)
+
+
+def wrap_sum(arrs):
+    """Sum of int32 arrays modulo 2^32, as int32 (the plain definition)."""
+    acc = np.zeros(arrs[0].shape, np.int64)
+    for a in arrs:
+        acc += a.astype(np.int64)
+    return (acc & 0xFFFFFFFF).astype(np.uint32).view(np.int32)
+
+
+def support_bits(B, n):
+    bits = np.unpackbits(B.view(np.uint8), bitorder="little")[:n]
+    return np.nonzero(bits)[0]
+
+
+def mask_set(mask, n):
+    return set(support_bits(mask, n).tolist())
+
+
+# ----------------------------------------------------------------- hashing
+
+def test_splitmix64_published_vector(golden_dir):
+    g = read_golden(os.path.join(golden_dir, "splitmix64_seed1234567.txt"))
+    seed = int(g["seed"][0][0])
+    want = [int(v) for v in g["values"]]
+    got = [int(v) for v in o.splitmix64(seed, len(want))]
+    assert got == want
+
+
+@pytest.mark.parametrize("rows", [3, 4, 7, 1000, 123457])
+def test_batch_rows_distinct_and_in_range(rows):
+    # section 3.1: an element's three hash indexes are different
+    for seed in (1, 2, 99):
+        g = o.Geom(n=2**32 - 1, rows=rows, seed=seed, c=1024)
+        for b in range(0, 4000, 7):
+            r, bias, s = o.batch_hash(g, b)
+            assert len(set(int(v) for v in r)) == 3
+            assert all(0 <= int(v) < rows for v in r)
+            assert all(0 <= int(v) < 1024 for v in bias)
+            assert set(int(v) for v in s) <= {-1, 1}
+
+
+def test_rows_uniform_and_signs_balanced():
+    rows, nb = 16, 6000
+    g = o.Geom(n=2**32 - 1, rows=rows, seed=5, c=64)
+    counts = np.zeros((3, rows))
+    signs = []
+    for b in range(nb):
+        r, bias, s = o.batch_hash(g, b)
+        for j in range(3):
+            counts[j, int(r[j])] += 1
+        signs += [int(v) for v in s]
+    # every row equally likely for every j: chi-square, 15 dof, p ~ 1e-6 cut
+    for j in range(3):
+        exp = nb / rows
+        chi2 = float(((counts[j] - exp) ** 2 / exp).sum())
+        assert chi2 < 50, chi2
+    frac = np.mean(np.array(signs) > 0)
+    assert abs(frac - 0.5) < 0.02
+
+
+@pytest.mark.parametrize("c", [1024, 64, 8])
+def test_batch_maps_to_rotated_row(c):
+    # section 3.4: the c parameters of a batch share one row per hash, in the
+    # original order rotated by a random bias in [0, c)
+    g = o.Geom(n=10 * c, rows=11, seed=3, c=c)
+    for b in (0, 3, 9):
+        idx = np.arange(b * c, (b + 1) * c, dtype=np.uint64)
+        cl, sg = o.cells(g, idx)
+        r, bias, s = o.batch_hash(g, b)
+        for j in range(3):
+            col = cl[:, j] % np.uint64(c)
+            row = cl[:, j] // np.uint64(c)
+            assert np.all(row == r[j])
+            assert np.all((col - np.arange(c, dtype=np.uint64)) % np.uint64(c) == bias[j])
+            assert sorted(col.tolist()) == list(range(c))
+            assert np.all(sg[:, j] == s[j])
+
+
+# --------------------------------------------------------------- geometry
+
+def test_rows_for_gamma():
+    for n in (1, 100, 1636, 10**6, 9_305_915):
+        for c in (1, 64, 1024):
+            rows = o.rows_for(n, 1.23, c)
+            assert rows >= 3
+            assert rows * c >= 1.23 * n
+            if rows > 3:
+                assert (rows - 1) * c < 1.23 * n
+
+
+def test_recovery_threshold_of_section4():
+    # section 4.1: the sketch needed for full recovery is 1.23 * (1 - 0.304) =
+    # 85.6 % of the original size for VGG19 (30.4 % zeros)
+    N = 140_000_000
+    rows = o.rows_for(round(N * (1 - 0.304)), 1.23, 1024)
+    assert abs(rows * 1024 / N - 0.856) < 0.0005
+
+
+def test_invalid_geometry_rejected():
+    assert o.check(o.Geom(n=100, rows=3, seed=1, c=1024))
+    for g in (o.Geom(n=100, rows=2, seed=1), o.Geom(n=100, rows=3, seed=1, c=3),
+              o.Geom(n=100, rows=3, seed=1, c=2048), o.Geom(n=0, rows=3, seed=1),
+              o.Geom(n=100, rows=3, seed=1, k=2), o.Geom(n=100, rows=2**23, seed=1, c=1024)):
+        assert not o.check(g)
+
+
+# ----------------------------------------------------------------- encode
+
+def test_single_nonzero_hits_three_cells():
+    # section 3.1: x_i is added to Y[h_j(i)] with sign g_j(i), j = 1, 2, 3
+    g = o.Geom(n=5000, rows=5, seed=17, c=1024)
+    for p, v in ((0, 7), (4999, -123456), (2047, 2**31 - 1)):
+        x = np.zeros(g.n, np.int32)
+        x[p] = v
+        Y, B = o.encode(g, x)
+        assert support_bits(B, g.n).tolist() == [p]
+        nz = np.nonzero(Y)[0]
+        assert len(nz) == 3
+        assert sorted(np.abs(Y[nz].astype(np.int64)).tolist()) == [abs(v)] * 3
+        assert o.query(g, Y, p) == v  # isolated element: estimate is exact
+
+
+def test_dense_equals_coo():
+    w = wl.make("tiny")
+    g = o.geometry(w.n, w.n_agg, w.hash_seed)
+    for i in range(w.W):
+        Yd, Bd = o.encode(g, w.dense(i))
+        Yc, Bc = o.encode_coo(g, w.idx[i], w.val[i])
+        assert np.array_equal(Yd, Yc) and np.array_equal(Bd, Bc)
+
+
+def test_linearity_int32_with_wraparound():
+    rng = np.random.default_rng(3)
+    g = o.Geom(n=70_001, rows=7, seed=23, c=256)
+    a = np.zeros(g.n, np.int32)
+    b = np.zeros(g.n, np.int32)
+    ia = rng.choice(g.n, 900, replace=False)
+    ib = rng.choice(g.n, 900, replace=False)
+    a[ia] = rng.integers(2**30, 2**31 - 1, ia.size)   # large: sums wrap
+    b[ib] = rng.integers(-2**31 + 1, -2**30, ib.size)
+    s = wrap_sum([a, b])
+    Ya, Ba = o.encode(g, a)
+    Yb, Bb = o.encode(g, b)
+    Ys, Bs = o.encode(g, s)
+    assert np.array_equal(Ys, wrap_sum([Ya, Yb]))
+    cancel = (s == 0) & ((a != 0) | (b != 0))
+    assert not cancel.any()
+    assert np.array_equal(Bs, Ba | Bb)
+
+
+def test_aggregate_is_homomorphic():
+    # Algorithm 1: the aggregation API turns S(X) into S(sum X)
+    w = wl.make("tiny", W=4)
+    g = o.geometry(w.n, w.n_agg, w.hash_seed)
+    enc = [o.encode(g, w.dense(i)) for i in range(w.W)]
+    Yagg, Bagg = o.aggregate(np.stack([e[0] for e in enc]), np.stack([e[1] for e in enc]))
+    xs = wrap_sum([w.dense(i) for i in range(w.W)])
+    Ys, Bs = o.encode(g, xs)
+    assert np.array_equal(Yagg, Ys)
+    # OR of bitmaps covers the support of the sum; equal unless a sum cancels
+    assert np.array_equal(Bs & ~Bagg, np.zeros_like(Bs))
+    if (xs[np.unique(np.concatenate(w.idx))] != 0).all():
+        assert np.array_equal(Bagg, Bs)
+
+
+def test_aggregate_fp64_worker_order():
+    rng = np.random.default_rng(0)
+    Ys = rng.normal(size=(5, 300))
+    Bs = rng.integers(0, 2**32, (5, 10), dtype=np.uint64).astype(np.uint32)
+    Y, B = o.aggregate(Ys, Bs)
+    acc = np.zeros(300)
+    for w in range(5):
+        acc = acc + Ys[w]
+    assert np.array_equal(Y, acc)
+    assert np.array_equal(B, np.bitwise_or.reduce(Bs, axis=0))
+
+
+# ----------------------------------------------------------------- decode
+
+def brute_two_core(cell_sets):
+    """Largest stopping set: a subset T in which every cell touched by T is
+    touched at least twice by T.  The union of all stopping sets, by
+    enumeration of every subset (only for tiny supports)."""
+    m = len(cell_sets)
+    core = set()
+    for mask in range(1, 1 << m):
+        T = [i for i in range(m) if mask >> i & 1]
+        cnt = {}
+        for i in T:
+            for cc in cell_sets[i]:
+                cnt[cc] = cnt.get(cc, 0) + 1
+        if all(v >= 2 for v in cnt.values()):
+            core |= set(T)
+    return core
+
+
+def brute_rounds(cell_sets):
+    """Synchronous peeling round of each element from its recursive definition:
+    r(e) = 1 + min over cells of e of max r(e') over the other elements e' in
+    that cell (0 if none); infinity for elements that are never peeled."""
+    m = len(cell_sets)
+    members = {}
+    for i, cs in enumerate(cell_sets):
+        for cc in cs:
+            members.setdefault(cc, []).append(i)
+    r = [math.inf] * m
+    changed = True
+    while changed:
+        changed = False
+        for e in range(m):
+            best = math.inf
+            for cc in cell_sets[e]:
+                others = [r[x] for x in members[cc] if x != e]
+                best = min(best, max(others) if others else 0)
+            if best + 1 < r[e]:
+                r[e] = best + 1
+                changed = True
+    return r
+
+
+def check_against_brute(g, S, vals):
+    x = np.zeros(g.n, np.int32)
+    x[S] = vals
+    Y, B = o.encode(g, x)
+    out, mask, info, rof = o.decode(g, Y, B, want_rounds=True)
+    cl, _ = o.cells(g, np.array(S, np.uint64))
+    cell_sets = [tuple(int(v) for v in r) for r in cl]
+    core = brute_two_core(cell_sets)
+    peeled = {S[i] for i in range(len(S)) if i not in core}
+    assert mask_set(mask, g.n) == peeled
+    assert info.n_support == len(S)
+    assert info.n_recovered == len(peeled)
+    assert info.success == (len(core) == 0)
+    for p in peeled:
+        assert out[p] == x[p]
+    rr = brute_rounds(cell_sets)
+    for i, p in enumerate(S):
+        assert rof[p] == (0 if rr[i] == math.inf else rr[i])
+    assert info.rounds == max([v for v in rr if v != math.inf], default=0)
+    return info
+
+
+def test_exhaustive_supports_tiny():
+    # every support of a 10-parameter gradient, two small geometries
+    rng = np.random.default_rng(11)
+    fails = 0
+    for (c, rows, seed) in ((1, 5, 3), (2, 4, 8)):
+        g = o.Geom(n=10, rows=rows, seed=seed, c=c)
+        for k in range(1, 1 << g.n):
+            S = [p for p in range(g.n) if k >> p & 1]
+            vals = rng.integers(-1000, 1000, len(S))
+            vals[vals == 0] = 1
+            info = check_against_brute(g, S, vals)
+            fails += not info.success
+    assert fails > 0  # the enumeration does reach decode failures
+
+
+@pytest.mark.parametrize("c,rows", [(1, 9), (2, 6), (4, 3), (8, 3), (8, 6)])
+def test_random_supports_vs_stopping_sets(c, rows):
+    rng = np.random.default_rng(c * 100 + rows)
+    g = o.Geom(n=64, rows=rows, seed=c + rows, c=c)
+    for trial in range(25):
+        m = int(rng.integers(1, 15))
+        S = sorted(rng.choice(64, m, replace=False).tolist())
+        vals = rng.integers(1, 2**20, m) * rng.choice([-1, 1], m)
+        check_against_brute(g, S, vals)
+
+
+def test_figure1_peeling_order(golden_dir):
+    fx = read_golden(os.path.join(golden_dir, "fig1_example.txt"))
+    g = o.Geom(n=int(fx["n"][0][0]), rows=int(fx["rows"][0][0]), seed=int(fx["seed"][0][0]),
+               c=int(fx["c"][0][0]))
+    z = int(fx["z"][0][0])
+    cl, _ = o.cells(g, [0, 1, 2])
+    for i, row in enumerate(fx["cells"]):
+        assert sorted(int(v) for v in cl[int(row[0])]) == [int(v) for v in row[1:]]
+    x = np.array([5, -9, 12], np.int32)
+    Y, B = o.encode(g, x)
+    out, mask, info, rof = o.decode(g, Y, B, want_rounds=True)
+    assert info.success and info.rounds == 2
+    assert rof[z] == 1
+    assert all(rof[i] == 2 for i in range(3) if i != z)
+    assert np.array_equal(out, x)
+
+
+def test_decode_equals_direct_sum_tiny():
+    w = wl.make("tiny")
+    g = o.geometry(w.n, w.n_agg, w.hash_seed)
+    enc = [o.encode(g, w.dense(i)) for i in range(w.W)]
+    Y, B = o.aggregate(np.stack([e[0] for e in enc]), np.stack([e[1] for e in enc]))
+    out, mask, info = o.decode(g, Y, B)
+    assert info.success and info.n_support == w.n_agg == info.n_recovered
+    assert np.array_equal(out, wrap_sum([w.dense(i) for i in range(w.W)]))
+
+
+@pytest.mark.parametrize("c", [1024, 64, 1])
+def test_decode_direct_sum_multi_tile(c):
+    # several rows and batches, a ragged tail (n not a multiple of c or 32)
+    w = wl.make("synthetic", n=300_007, W=4, density=0.01, overlap=0.3)
+    g = o.geometry(w.n, w.n_agg, w.hash_seed, c=c)
+    enc = [o.encode_coo(g, w.idx[i], w.val[i]) for i in range(w.W)]
+    Y, B = o.aggregate(np.stack([e[0] for e in enc]), np.stack([e[1] for e in enc]))
+    out, mask, info = o.decode(g, Y, B)
+    assert info.success, info
+    assert np.array_equal(out, wrap_sum([w.dense(i) for i in range(w.W)]))
+    x2, m2, i2 = o.decode_queue(g, Y, B)
+    assert np.array_equal(out, x2) and np.array_equal(mask, m2)
+
+
+@pytest.mark.parametrize("ratio", [1.05, 1.15, 1.2])
+def test_queue_peeler_agrees_on_failures(ratio):
+    rng = np.random.default_rng(int(ratio * 100))
+    n, N = 20000, 400_000
+    S = np.sort(rng.choice(N, n, replace=False)).astype(np.uint32)
+    v = rng.integers(-2**31 + 1, 2**31 - 1, n).astype(np.int32)
+    v[v == 0] = 1
+    g = o.Geom(n=N, rows=int(math.ceil(ratio * n / 64)), seed=77, c=64)
+    Y, B = o.encode_coo(g, S, v)
+    x1, m1, i1 = o.decode(g, Y, B)
+    x2, m2, i2 = o.decode_queue(g, Y, B)
+    assert not i1.success
+    assert np.array_equal(m1, m2)
+    assert np.array_equal(x1, x2)  # peeled values and leftover estimates
+    assert (i1.n_support, i1.n_recovered) == (i2.n_support, i2.n_recovered)
+
+
+def core_fraction(lam):
+    """Fraction of edges in the 2-core of a random 3-uniform hypergraph with
+    lam edges per vertex: x^3 for the largest root of x = 1 - exp(-3 lam x^2)."""
+    xs = np.linspace(1e-9, 1.0, 200001)
+    f = xs - (1 - np.exp(-3 * lam * xs**2))
+    idx = np.nonzero(np.sign(f[:-1]) != np.sign(f[1:]))[0]
+    if idx.size == 0:
+        return 0.0
+    i = idx[-1]
+    x = brentq(lambda t: t - (1 - np.exp(-3 * lam * t * t)), xs[i], xs[i + 1])
+    return x**3
+
+
+def test_two_core_threshold_closed_form():
+    # peeling threshold 0.81847 edges per cell, i.e. a sketch of 1.2218 n cells;
+    # gamma = 1.23 of section 3.2 sits just above it
+    lam_star = min(-np.log1p(-x) / (3 * x * x) for x in np.linspace(0.01, 0.99, 9801))
+    assert abs(1 / lam_star - 1.2218) < 0.0005
+    rng = np.random.default_rng(2)
+    n, N = 100_000, 2_000_000
+    S = np.sort(rng.choice(N, n, replace=False)).astype(np.uint32)
+    v = rng.integers(1, 1000, n).astype(np.int32)
+    for ratio, c in ((1.10, 1), (1.15, 1), (1.10, 1024), (1.15, 1024)):
+        g = o.Geom(n=N, rows=int(math.ceil(ratio * n / c)), seed=9, c=c)
+        Y, B = o.encode_coo(g, S, v)
+        _, _, info = o.decode(g, Y, B)
+        left = 1 - info.n_recovered / n
+        assert abs(left - core_fraction(n / g.cells)) < 0.03, (ratio, c, left)
+    for c in (1, 1024):
+        g = o.Geom(n=N, rows=int(math.ceil(1.3 * n / c)), seed=9, c=c)
+        Y, B = o.encode_coo(g, S, v)
+        x, _, info = o.decode(g, Y, B)
+        assert info.success
+        assert np.array_equal(x[S], v)
+
+
+def test_rounds_order_of_loglog():
+    # section 3.2: log log n + O(1) rounds well above the threshold (the O(1)
+    # is not given; this checks only the order of magnitude at ratio 2)
+    rng = np.random.default_rng(4)
+    for n in (10_000, 100_000):
+        N = 20 * n
+        S = np.sort(rng.choice(N, n, replace=False)).astype(np.uint32)
+        v = np.ones(n, np.int32)
+        g = o.Geom(n=N, rows=int(math.ceil(2.0 * n / 1024)), seed=1, c=1024)
+        Y, B = o.encode_coo(g, S, v)
+        _, _, info = o.decode(g, Y, B)
+        ll = math.log2(math.log2(n))
+        assert info.success and ll <= info.rounds <= ll + 5
+
+
+# ------------------------------------------------------------- estimator
+
+def test_median_fixture(golden_dir):
+    fx = read_golden(os.path.join(golden_dir, "count_sketch_query.txt"))
+    cnt = [int(v) for v in fx["counters"][0]]
+    sg = [int(v) for v in fx["signs"][0]]
+    want = int(fx["estimate"][0][0])
+    prods = [s * c for s, c in zip(sg, cnt)]
+    assert o.median3(*prods) == want
+    assert o.median3(*[float(v) for v in prods]) == float(want)
+    for perm in itertools.permutations(prods):
+        assert o.median3(*perm) == want
+
+
+def test_forced_failure_single_row_cells():
+    # c = 1 and three rows: every parameter maps to all three cells, so any
+    # support of two or more has no pure cell and nothing can be peeled
+    g = o.Geom(n=40, rows=3, seed=5, c=1)
+    cl, sg = o.cells(g, np.arange(40, dtype=np.uint64))
+    assert all(sorted(int(v) for v in r) == [0, 1, 2] for r in cl)
+    x = np.zeros(40, np.int32)
+    x[7] = 55
+    Y, B = o.encode(g, x)
+    out, mask, info = o.decode(g, Y, B)
+    assert info.success and out[7] == 55
+    x[[3, 7, 30]] = [10, 55, -4]
+    Y, B = o.encode(g, x)
+    out, mask, info = o.decode(g, Y, B)
+    assert (info.success, info.n_recovered, info.rounds, info.n_support) == (0, 0, 0, 3)
+    assert not mask.any()
+    # leftovers are the Count Sketch query on the (unpeeled) sketch
+    for p in (3, 7, 30):
+        cells = [int(v) for v in cl[p]]
+        est = sorted(int(sg[p][j]) * int(Y[cells[j]]) for j in range(3))[1]
+        assert out[p] == est
+    assert np.count_nonzero(out) <= 3
+
+
+def test_leftover_estimate_unbiased():
+    # section 3.1: signs make collisions symmetric, so the estimate of an
+    # unpeeled parameter is centred on its true value
+    rng = np.random.default_rng(8)
+    n, N = 30000, 600_000
+    S = np.sort(rng.choice(N, n, replace=False)).astype(np.uint32)
+    v = rng.integers(-1000, 1000, n).astype(np.int32)
+    v[v == 0] = 1
+    g = o.Geom(n=N, rows=int(math.ceil(1.0 * n / 16)), seed=31, c=16)
+    Y, B = o.encode_coo(g, S, v)
+    x, mask, info = o.decode(g, Y, B)
+    un = np.array(sorted(set(S.tolist()) - mask_set(mask, N)))
+    assert un.size > 1000
+    truth = np.zeros(N, np.int64)
+    truth[S] = v
+    err = x[un].astype(np.int64) - truth[un]
+    assert abs(err.mean()) < 4 * err.std() / math.sqrt(un.size)
+    assert np.corrcoef(x[un], truth[un])[0, 1] > 0.3
+
+
+def test_exact_zero_aggregate_is_recovered_as_zero():
+    # footnote of section 3.2: a sum can be exactly zero while its bit is set
+    g = o.Geom(n=5000, rows=4, seed=2, c=1024)
+    a = np.zeros(g.n, np.int32)
+    b = np.zeros(g.n, np.int32)
+    a[[10, 20, 4000]] = [5, 6, 7]
+    b[[10, 3000]] = [-5, 9]
+    enc = [o.encode(g, a), o.encode(g, b)]
+    Y, B = o.aggregate(np.stack([e[0] for e in enc]), np.stack([e[1] for e in enc]))
+    out, mask, info = o.decode(g, Y, B)
+    assert info.n_support == 4 and info.success
+    assert 10 in mask_set(mask, g.n) and out[10] == 0
+    assert np.array_equal(out, wrap_sum([a, b]))
+
+
+def test_fp64_path_matches_structure_and_values():
+    w = wl.make("synthetic", n=200_003, W=3, density=0.01, overlap=0.4, vtype="f32")
+    g = o.geometry(w.n, w.n_agg, w.hash_seed, c=1024)
+    enc = [o.encode(g, w.dense(i)) for i in range(w.W)]
+    Y, B = o.aggregate(np.stack([e[0] for e in enc]), np.stack([e[1] for e in enc]))
+    out, mask, info = o.decode(g, Y, B)
+    truth = sum(w.dense(i).astype(np.float64) for i in range(w.W))
+    assert info.success
+    assert np.max(np.abs(out - truth)) <= 1e-12 * np.max(np.abs(truth))
+    # same support as an int32 run: identical structure (mask and rounds)
+    ints = [np.where(w.dense(i) != 0, 1, 0).astype(np.int32) for i in range(w.W)]
+    enc_i = [o.encode(g, xi) for xi in ints]
+    Yi, Bi = o.aggregate(np.stack([e[0] for e in enc_i]), np.stack([e[1] for e in enc_i]))
+    _, mask_i, info_i = o.decode(g, Yi, Bi)
+    assert np.array_equal(mask_i, mask) and info_i.rounds == info.rounds
+
+
+def _fixture_sketch(golden_dir, order=(0, 1, 2)):
+    """A c = 1, three-row sketch (every parameter maps to all three cells) with
+    the counters of the section 3.1 query example placed under a parameter
+    whose signs are those of the example, the three (counter, sign) pairs taken
+    in the given order of j."""
+    fx = read_golden(os.path.join(golden_dir, "count_sketch_query.txt"))
+    cnt = [int(fx["counters"][0][i]) for i in order]
+    sg = [int(fx["signs"][0][i]) for i in order]
+    want = int(fx["estimate"][0][0])
+    g = o.Geom(n=64, rows=3, seed=12, c=1)
+    cl, signs = o.cells(g, np.arange(64, dtype=np.uint64))
+    p = next(i for i in range(64) if [int(s) for s in signs[i]] == sg)
+    Y = np.zeros(g.cells, np.int32)
+    for j in range(3):
+        Y[int(cl[p][j])] = cnt[j]
+    return g, p, Y, want
+
+
+ORDERS = list(itertools.permutations(range(3)))
+
+
+@pytest.mark.parametrize("order", ORDERS)
+def test_query_example_through_sketch(golden_dir, order):
+    g, p, Y, want = _fixture_sketch(golden_dir, order)
+    assert o.query(g, Y, p) == want
+    assert o.query(g, Y.astype(np.float64), p) == float(want)
+
+
+@pytest.mark.parametrize("order", ORDERS)
+def test_leftover_estimate_example_through_decode(golden_dir, order):
+    # two parameters sharing all three cells: nothing peels, both get the
+    # Count Sketch estimate of Algorithm 1's last recovery step
+    g, p, Y, want = _fixture_sketch(golden_dir, order)
+    q = (p + 1) % g.n
+    B = np.zeros(g.words, np.uint32)
+    for v in (p, q):
+        B[v >> 5] |= np.uint32(1 << (v & 31))
+    out, mask, info = o.decode(g, Y, B)
+    assert (info.success, info.n_recovered, info.n_support) == (0, 0, 2)
+    assert out[p] == want
+    out_f, _, _ = o.decode(g, Y.astype(np.float64), B)
+    assert out_f[p] == float(want)
+    x2, _, _ = o.decode_queue(g, Y, B)
+    assert x2[p] == want
