@@ -1,0 +1,152 @@
+/*
+ * hc.h -- C ABI of the MI355X (gfx950) library for lossless homomorphic
+ * gradient compression: a Count Sketch plus a bitmap index per worker, summed
+ * and OR-ed across workers, and decoded by parallel peeling.
+ *
+ * Paper: "Accelerating Distributed Deep Learning using Lossless Homomorphic
+ * Compression", arXiv 2402.07529.  Algorithm 1 has two phases around the
+ * aggregation API; this library exposes one call per stage:
+ *
+ *   hc_encode / hc_encode_coo   Algorithm 1, phase I (sections 3.1, 3.2, 3.4)
+ *   hc_aggregate                what the aggregation API does between the
+ *                               phases: Y <- sum Y, B <- OR B (section 3)
+ *   hc_decode                   Algorithm 1, phase II (section 3.2 peeling,
+ *                               section 3.1 median estimate for leftovers)
+ *   hc_geometry / hc_sizes      sketch sizing, |Y| >= gamma * n (section 3.2)
+ *
+ * Conventions for every call:
+ *   - Buffer pointers are DEVICE pointers unless marked "host".  The caller
+ *     owns all memory; the library allocates no device memory in any call.
+ *   - Calls are asynchronous on `stream` (0 = the null stream).  A returned
+ *     HC_OK means the arguments were valid and the kernels were enqueued.
+ *   - Errors are returned as hc_status; nothing is thrown across the ABI.
+ *     hc_last_error() gives a message for the last failing call of the
+ *     calling host thread.  Invalid arguments are detected before anything
+ *     is enqueued.
+ *   - Value, index and bitmap buffers need their natural 4-byte alignment
+ *     (16-byte alignment lets the kernels use vector memory operations);
+ *     the decode workspace must be 256-byte aligned and the decode info
+ *     8-byte aligned.  hipMalloc and PyTorch allocations satisfy all of it.
+ *
+ * Sketch format (identical for every worker; the paper leaves these details
+ * open):
+ *   cells = rows * c.  Parameter p lies in batch b = p / c at column
+ *   t = p mod c.  Three 64-bit hashes h_j = SplitMix64 output number 3b + j for
+ *   state `seed` (j = 0, 1, 2) give three distinct rows r_j (scaled from the
+ *   low 32 bits of h_j, later rows skipping earlier ones), rotations
+ *   bias_j = (h_j >> 32) mod c and signs g_j = -1 if bit 63 of h_j is set,
+ *   else +1.  Cell j of p is r_j * c + ((t + bias_j) mod c).
+ *   Y[cells] holds int32 (wrapping, like a switch's integer adders) or fp32.
+ *   B[ceil(n/32)] is a bitmap, bit p = bit (p mod 32) of word p / 32; bits at
+ *   or past n are zero.
+ */
+#ifndef HC_H
+#define HC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    HC_OK = 0,
+    HC_EINVAL = 1,        /* invalid argument (null pointer, bad geometry, size) */
+    HC_EWORKSPACE = 2,    /* decode workspace smaller than hc_sizes reports       */
+    HC_EHIP = 3,          /* a HIP runtime call failed (launch, device query)     */
+    HC_EUNSUPPORTED = 4   /* valid but not implemented (k != 3)                   */
+} hc_status;
+
+typedef enum { HC_I32 = 0, HC_F32 = 1 } hc_vtype;
+
+/* Sketch geometry, shared by every worker of one aggregation. */
+typedef struct {
+    uint64_t n;        /* gradient length N, 1 .. 2^32 - 1                        */
+    uint32_t k;        /* hashes per parameter; the paper's three (only 3)       */
+    uint32_t c;        /* batch width of section 3.4, power of two in [1, 1024]  */
+    uint64_t rows;     /* sketch rows R >= 3; cells = rows * c must be < 2^32    */
+    uint64_t seed;     /* hash seed                                               */
+    uint32_t vtype;    /* hc_vtype of the gradient and sketch values             */
+    uint32_t reserved; /* must be 0                                               */
+} hc_params;
+
+/* Written by hc_decode into DEVICE memory. */
+typedef struct {
+    uint64_t n_support;   /* set bits of the aggregated bitmap (nonzeros of sum X) */
+    uint64_t n_recovered; /* of those, recovered exactly by peeling                */
+    uint64_t rounds;      /* synchronous peeling rounds that recovered >= 1        */
+    uint32_t success;     /* 1 iff n_recovered == n_support                        */
+    uint32_t status;      /* 0 ok; 1 n_support exceeded max_support (nothing was
+                             peeled, every element got the median estimate);
+                             2 the round loop's barrier gave up waiting (a
+                             device fault; outputs are not valid)               */
+} hc_decode_info;
+
+/* Geometry for a gradient of n parameters whose aggregate has about n_nonzero
+ * nonzeros: rows = max(3, ceil(ceil(gamma * n_nonzero) / c)), so the sketch
+ * has at least gamma * n_nonzero cells (section 3.2 uses gamma = 1.23; section
+ * 3.4 uses c = 1024).  `out` is a HOST pointer.  HC_EINVAL if the result is not
+ * a valid geometry. */
+hc_status hc_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
+                      uint64_t seed, hc_vtype vtype, hc_params *out);
+
+/* Byte sizes (HOST outputs, each may be NULL): one sketch Y, one bitmap B, and
+ * the decode workspace for a support of up to max_support nonzeros
+ * (0 means n, which always suffices). */
+hc_status hc_sizes(const hc_params *p, uint64_t max_support, size_t *y_bytes,
+                   size_t *b_bytes, size_t *ws_bytes);
+
+/* Phase I on a dense gradient x[n] (int32 or fp32 per p->vtype).  Overwrites
+ * y[cells] with the Count Sketch (Y[h_j(p)] += g_j(p) * x_p for every nonzero
+ * x_p, section 3.1 with the batching of 3.4) and b[ceil(n/32)] with the
+ * nonzero bitmap (section 3.2).  No pre-zeroing is needed.  fp32 sums are
+ * accumulated with atomics, so their rounding order is not fixed. */
+hc_status hc_encode(const hc_params *p, const void *x, void *y, uint32_t *b,
+                    hipStream_t stream);
+
+/* Phase I on COO input: idx[nnz] (uint32, each < n, any order) and
+ * val[nnz].  Zero values are skipped; repeated indices are summed.  Same
+ * outputs as hc_encode of the equivalent dense gradient. */
+hc_status hc_encode_coo(const hc_params *p, const uint32_t *idx, const void *val,
+                        uint64_t nnz, void *y, uint32_t *b, hipStream_t stream);
+
+/* The aggregation step: y_out[i] = sum over w < W of y_in[w * cells + i]
+ * (int32 wraps modulo 2^32; fp32 adds in worker order 0..W-1) and
+ * b_out[i] = OR over w of b_in[w * words + i], words = ceil(n/32).  Inputs are
+ * W sketches and W bitmaps stored back to back.  Outputs may not alias
+ * inputs.  W >= 1. */
+hc_status hc_aggregate(const hc_params *p, const void *y_in, const uint32_t *b_in,
+                       uint32_t W, void *y_out, uint32_t *b_out, hipStream_t stream);
+
+/* Phase II on an aggregated sketch.  y_agg and b_agg are not modified.
+ * Outputs (each may be NULL):
+ *   x_out[n]              dense sum X: recovered values, the Count Sketch
+ *                         median estimate for members of the support that
+ *                         could not be peeled, 0 outside the support;
+ *   coo_idx, coo_val      the support in ascending order with its values, at
+ *                         most coo_cap entries (entries past coo_cap are not
+ *                         written; n_support in info tells how many exist);
+ *   mask[ceil(n/32)]      bit p set iff p was recovered by peeling;
+ *   info (one struct)     summary, DEVICE memory.
+ * ws/ws_bytes: device workspace of at least the ws_bytes hc_sizes reports for
+ * the same max_support; contents on entry are ignored.
+ * Peeling runs as synchronous rounds entirely on the device (one cooperative
+ * kernel; no host round trips).  Decode failure is data (info->success), not
+ * an error status. */
+hc_status hc_decode(const hc_params *p, const void *y_agg, const uint32_t *b_agg,
+                    void *x_out, uint32_t *coo_idx, void *coo_val, uint64_t coo_cap,
+                    uint32_t *mask, hc_decode_info *info, uint64_t max_support,
+                    void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Human-readable name of a status, and the message of the calling thread's
+ * last failing call ("" if none). */
+const char *hc_status_string(hc_status s);
+const char *hc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

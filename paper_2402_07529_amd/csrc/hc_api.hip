@@ -1,0 +1,205 @@
+// hc_api.hip -- the C ABI of include/hc.h: argument validation, sketch
+// geometry, workspace sizing and kernel launches.  Host code only.
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+#include <string>
+
+#include "../../include/hc.h"
+#include "hc_internal.h"
+
+namespace hc {
+
+namespace {
+
+thread_local std::string g_last_error;
+
+hc_status fail(hc_status s, const char* msg) {
+    g_last_error = msg;
+    return s;
+}
+
+hc_status fail_hip(hipError_t e, const char* where) {
+    g_last_error = std::string(where) + ": " + hipGetErrorString(e);
+    return HC_EHIP;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+// Validate the public params and convert them to the kernels' form.
+hc_status to_geo(const hc_params* p, Geo* g) {
+    if (p == nullptr) return fail(HC_EINVAL, "params is NULL");
+    if (p->reserved != 0) return fail(HC_EINVAL, "params.reserved must be 0");
+    if (p->k != 3) return fail(HC_EUNSUPPORTED, "only k = 3 hashes are implemented");
+    if (p->vtype != HC_I32 && p->vtype != HC_F32) return fail(HC_EINVAL, "unknown vtype");
+    if (p->n == 0 || p->n > 0xffffffffull) return fail(HC_EINVAL, "n must be in [1, 2^32 - 1]");
+    if (p->c == 0 || p->c > 1024 || (p->c & (p->c - 1)) != 0)
+        return fail(HC_EINVAL, "c must be a power of two in [1, 1024]");
+    if (p->rows < 3) return fail(HC_EINVAL, "rows must be >= 3");
+    if (p->rows > 0xffffffffull / p->c) return fail(HC_EINVAL, "rows * c must be < 2^32");
+    g->n = p->n;
+    g->words = (p->n + 31) / 32;
+    g->rows = (uint32_t)p->rows;
+    g->c = p->c;
+    g->cmask = p->c - 1;
+    g->log2c = 0;
+    while ((1u << g->log2c) < p->c) g->log2c++;
+    g->cells = (uint32_t)(p->rows * p->c);
+    g->seed = p->seed;
+    g->f32 = p->vtype == HC_F32;
+    return HC_OK;
+}
+
+std::mutex g_dev_mu;
+int g_dev_cus[64];
+
+}  // namespace
+
+hipError_t device_info(DeviceInfo* out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lk(g_dev_mu);
+    const int slot = dev & 63;
+    if (g_dev_cus[slot] == 0) {
+        int cus = 0;
+        e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        g_dev_cus[slot] = cus > 0 ? cus : 1;
+    }
+    out->cus = g_dev_cus[slot];
+    return hipSuccess;
+}
+
+}  // namespace hc
+
+using namespace hc;
+
+extern "C" {
+
+const char* hc_status_string(hc_status s) {
+    switch (s) {
+        case HC_OK: return "HC_OK";
+        case HC_EINVAL: return "HC_EINVAL";
+        case HC_EWORKSPACE: return "HC_EWORKSPACE";
+        case HC_EHIP: return "HC_EHIP";
+        case HC_EUNSUPPORTED: return "HC_EUNSUPPORTED";
+    }
+    return "HC_UNKNOWN";
+}
+
+const char* hc_last_error(void) { return g_last_error.c_str(); }
+
+hc_status hc_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c, uint64_t seed,
+                      hc_vtype vtype, hc_params* out) {
+    g_last_error.clear();
+    if (out == nullptr) return fail(HC_EINVAL, "out is NULL");
+    if (!(gamma > 0.0) || !isfinite(gamma)) return fail(HC_EINVAL, "gamma must be > 0");
+    if (c == 0 || c > 1024 || (c & (c - 1)) != 0)
+        return fail(HC_EINVAL, "c must be a power of two in [1, 1024]");
+    const double need = gamma * (double)n_nonzero;
+    if (need > 1.8e19) return fail(HC_EINVAL, "sketch too large");
+    uint64_t cells = (uint64_t)need;
+    if ((double)cells < need) cells++;
+    uint64_t rows = (cells + c - 1) / c;
+    if (rows < 3) rows = 3;
+    hc_params p;
+    memset(&p, 0, sizeof(p));
+    p.n = n;
+    p.k = 3;
+    p.c = c;
+    p.rows = rows;
+    p.seed = seed;
+    p.vtype = (uint32_t)vtype;
+    Geo g;
+    const hc_status s = to_geo(&p, &g);
+    if (s != HC_OK) return s;
+    *out = p;
+    return HC_OK;
+}
+
+hc_status hc_sizes(const hc_params* p, uint64_t max_support, size_t* y_bytes, size_t* b_bytes,
+                   size_t* ws_bytes) {
+    g_last_error.clear();
+    Geo g;
+    const hc_status s = to_geo(p, &g);
+    if (s != HC_OK) return s;
+    if (y_bytes) *y_bytes = (size_t)g.cells * 4;
+    if (b_bytes) *b_bytes = (size_t)g.words * 4;
+    if (ws_bytes) *ws_bytes = decode_layout(g, max_support).total;
+    return HC_OK;
+}
+
+hc_status hc_encode(const hc_params* p, const void* x, void* y, uint32_t* b, hipStream_t stream) {
+    g_last_error.clear();
+    Geo g;
+    const hc_status s = to_geo(p, &g);
+    if (s != HC_OK) return s;
+    if (!x || !y || !b) return fail(HC_EINVAL, "x, y and b must be non-NULL");
+    if (!aligned(x, 4) || !aligned(y, 4) || !aligned(b, 4))
+        return fail(HC_EINVAL, "x, y and b must be 4-byte aligned");
+    const hipError_t e = launch_encode_dense(g, x, y, b, stream);
+    return e == hipSuccess ? HC_OK : fail_hip(e, "hc_encode");
+}
+
+hc_status hc_encode_coo(const hc_params* p, const uint32_t* idx, const void* val, uint64_t nnz,
+                        void* y, uint32_t* b, hipStream_t stream) {
+    g_last_error.clear();
+    Geo g;
+    const hc_status s = to_geo(p, &g);
+    if (s != HC_OK) return s;
+    if (!y || !b) return fail(HC_EINVAL, "y and b must be non-NULL");
+    if (nnz > 0 && (!idx || !val)) return fail(HC_EINVAL, "idx and val must be non-NULL");
+    if (!aligned(y, 4) || !aligned(b, 4) || (nnz > 0 && (!aligned(idx, 4) || !aligned(val, 4))))
+        return fail(HC_EINVAL, "buffers must be 4-byte aligned");
+    const hipError_t e = launch_encode_coo(g, idx, val, nnz, y, b, stream);
+    return e == hipSuccess ? HC_OK : fail_hip(e, "hc_encode_coo");
+}
+
+hc_status hc_aggregate(const hc_params* p, const void* y_in, const uint32_t* b_in, uint32_t W,
+                       void* y_out, uint32_t* b_out, hipStream_t stream) {
+    g_last_error.clear();
+    Geo g;
+    const hc_status s = to_geo(p, &g);
+    if (s != HC_OK) return s;
+    if (W == 0) return fail(HC_EINVAL, "W must be >= 1");
+    if (!y_in || !b_in || !y_out || !b_out) return fail(HC_EINVAL, "buffers must be non-NULL");
+    if (!aligned(y_in, 4) || !aligned(b_in, 4) || !aligned(y_out, 4) || !aligned(b_out, 4))
+        return fail(HC_EINVAL, "buffers must be 4-byte aligned");
+    const hipError_t e = launch_aggregate(g, y_in, b_in, W, y_out, b_out, stream);
+    return e == hipSuccess ? HC_OK : fail_hip(e, "hc_aggregate");
+}
+
+hc_status hc_decode(const hc_params* p, const void* y_agg, const uint32_t* b_agg, void* x_out,
+                    uint32_t* coo_idx, void* coo_val, uint64_t coo_cap, uint32_t* mask,
+                    hc_decode_info* info, uint64_t max_support, void* ws, size_t ws_bytes,
+                    hipStream_t stream) {
+    g_last_error.clear();
+    Geo g;
+    const hc_status s = to_geo(p, &g);
+    if (s != HC_OK) return s;
+    if (!y_agg || !b_agg || !info || !ws) return fail(HC_EINVAL, "y_agg, b_agg, info and ws must be non-NULL");
+    if (!aligned(y_agg, 4) || !aligned(b_agg, 4) || (x_out && !aligned(x_out, 4)) ||
+        (mask && !aligned(mask, 4)) || (coo_idx && !aligned(coo_idx, 4)) ||
+        (coo_val && !aligned(coo_val, 4)))
+        return fail(HC_EINVAL, "buffers must be 4-byte aligned");
+    if (!aligned(ws, 256) || !aligned(info, 8))
+        return fail(HC_EINVAL, "ws must be 256-byte and info 8-byte aligned");
+    if ((coo_idx == nullptr) != (coo_val == nullptr))
+        return fail(HC_EINVAL, "coo_idx and coo_val must both be given or both be NULL");
+    const DecodeLayout L = decode_layout(g, max_support);
+    if (ws_bytes < L.total) return fail(HC_EWORKSPACE, "workspace smaller than hc_sizes reports");
+    DecodeOut out;
+    out.x_out = x_out;
+    out.coo_idx = coo_idx;
+    out.coo_val = coo_val;
+    out.coo_cap = coo_cap;
+    out.mask = mask;
+    out.info = info;
+    const hipError_t e = launch_decode(g, y_agg, b_agg, out, L, ws, stream);
+    return e == hipSuccess ? HC_OK : fail_hip(e, "hc_decode");
+}
+
+}  // extern "C"

@@ -1,0 +1,627 @@
+// hc_decode.hip -- recovery (Algorithm 1, phase II) for gfx950.
+//
+// Stages (one stream, no host round trips):
+//   prep   copy the aggregated sketch into a residual Yw, clear the per-cell
+//          counters and round stamps, clear the control block;
+//   count  popcount of the bitmap per chunk of 1024 words;
+//   scan   exclusive scan of the chunk counts (one workgroup) -> offsets and
+//          the support size |S|;
+//   build  compaction of the set bits into the ascending element list E
+//          ("we know the indexes of all non-zero parameters", section 3.2)
+//          and, per element, one 64-bit atomic add per cell into a packed
+//          counter  cnt = deg * 2^32 + (sum of element positions):  a cell is
+//          pure (one live element) exactly when cnt >> 32 == 1, and then its
+//          low word is that element's position;
+//   peel   one cooperative persistent kernel running synchronous rounds
+//          (section 3.2, parallel peeling).  The frontier of round r is the
+//          list of cells that became pure during round r-1 (all pure cells
+//          for r = 0), kept in one append-only queue.  An element owning
+//          several frontier cells is claimed by the one with the smallest j;
+//          a per-cell stamp (the round in whose frontier the cell sits) tells
+//          which of its cells were pure at the round start without racing
+//          with the round's own updates.  The claimer recovers x = g_j * Y,
+//          and subtracts g * x and the element from its other two cells with
+//          atomics; a cell whose count drops to one joins the next frontier.
+//          One grid barrier per round; rounds end when a frontier is empty.
+//          Elements never peeled get the Count Sketch median estimate from
+//          the residual sketch (Algorithm 1, last recovery step);
+//   emit   dense output, recovered mask and COO from E and the values.
+#include <type_traits>
+
+#include "hc_device.h"
+#include "hc_internal.h"
+
+namespace hc {
+
+namespace {
+
+constexpr int kBlock = 256;
+constexpr uint32_t kNever = 0xffffffffu;
+constexpr unsigned long long kOne = 1ull << 32;  // one incidence in a packed counter
+constexpr uint64_t kChunkBits = (uint64_t)kChunkWords * 32;
+constexpr uint64_t kBarrierTimeoutTicks = 500000000ull;  // 5 s at the 100 MHz real-time clock
+
+struct Ctrl {
+    unsigned long long n_support;
+    unsigned long long recovered;
+    unsigned int tail;      // queue length
+    unsigned int fend;      // end of the current frontier in the queue
+    unsigned int rounds;
+    unsigned int overflow;  // |S| > capacity
+    unsigned int abort;     // barrier timeout
+    unsigned int bar_count;
+    unsigned int bar_gen;
+    unsigned int pad[5];
+};
+static_assert(sizeof(Ctrl) == 64, "control block layout");
+
+// device mirror of hc_decode_info
+struct InfoDev {
+    unsigned long long n_support, n_recovered, rounds;
+    unsigned int success, status;
+};
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
+    for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d);
+    return v;
+}
+
+// Exclusive scan over the 256 lanes of a workgroup; *total gets the sum.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s_tmp,
+                                                         uint32_t* total) {
+    const uint32_t lane = lane_id();
+    const uint32_t wave = threadIdx.x >> 6;
+    const uint32_t nwaves = blockDim.x >> 6;
+    uint32_t x = v;
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t y = __shfl_up(x, d);
+        if (lane >= (uint32_t)d) x += y;
+    }
+    if (lane == 63) s_tmp[wave] = x;
+    __syncthreads();
+    uint32_t off = 0, tot = 0;
+    for (uint32_t w = 0; w < nwaves; w++) {
+        const uint32_t s = s_tmp[w];
+        if (w < wave) off += s;
+        tot += s;
+    }
+    __syncthreads();
+    *total = tot;
+    return off + x - v;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void prep_kernel(const T* __restrict__ y_agg,
+                                                      T* __restrict__ yw,
+                                                      unsigned long long* __restrict__ cnt,
+                                                      uint32_t* __restrict__ stamp,
+                                                      uint32_t cells, Ctrl* __restrict__ ctrl) {
+    if (blockIdx.x == 0 && threadIdx.x < sizeof(Ctrl) / 4)
+        reinterpret_cast<uint32_t*>(ctrl)[threadIdx.x] = 0u;
+    const uint64_t step = (uint64_t)gridDim.x * kBlock;
+    for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < cells; i += step) {
+        yw[i] = y_agg[i];
+        cnt[i] = 0ull;
+        stamp[i] = kNever;
+    }
+}
+
+// Bitmap word k, with bits at or past n cleared in the last word.
+__device__ __forceinline__ uint32_t load_word(const uint32_t* b, uint64_t k, uint64_t words,
+                                              uint32_t last_mask) {
+    if (k >= words) return 0u;
+    const uint32_t w = b[k];
+    return k == words - 1 ? (w & last_mask) : w;
+}
+
+__global__ __launch_bounds__(kBlock) void count_kernel(const uint32_t* __restrict__ b,
+                                                       uint64_t words, uint32_t last_mask,
+                                                       uint32_t* __restrict__ blk) {
+    __shared__ uint32_t s_tmp[kBlock / 64];
+    const uint64_t w0 = (uint64_t)blockIdx.x * kChunkWords + 4ull * threadIdx.x;
+    uint32_t c = 0;
+#pragma unroll
+    for (int k = 0; k < 4; k++) c += __popc(load_word(b, w0 + k, words, last_mask));
+    c = wave_sum(c);
+    if (lane_id() == 0) s_tmp[threadIdx.x >> 6] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t t = 0;
+        for (int w = 0; w < kBlock / 64; w++) t += s_tmp[w];
+        blk[blockIdx.x] = t;
+    }
+}
+
+// One workgroup of 1024 lanes: chunk counts -> exclusive offsets.
+__global__ __launch_bounds__(1024) void scan_kernel(uint32_t* __restrict__ blk, uint64_t nchunks,
+                                                    Ctrl* __restrict__ ctrl, uint64_t cap) {
+    __shared__ uint32_t s_tmp[16];
+    const uint64_t per = (nchunks + 1023) / 1024;
+    const uint64_t lo = (uint64_t)threadIdx.x * per;
+    const uint64_t hi = lo + per < nchunks ? lo + per : nchunks;
+    uint32_t s = 0;
+    for (uint64_t i = lo; i < hi; i++) s += blk[i];
+    uint32_t total;
+    uint32_t off = block_exclusive_scan(s, s_tmp, &total);
+    for (uint64_t i = lo; i < hi; i++) {
+        const uint32_t v = blk[i];
+        blk[i] = off;
+        off += v;
+    }
+    if (threadIdx.x == 0) {
+        ctrl->n_support = total;
+        ctrl->overflow = (uint64_t)total > cap ? 1u : 0u;
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void build_kernel(
+    const uint32_t* __restrict__ b, uint64_t words, uint32_t last_mask,
+    const uint32_t* __restrict__ blk, uint32_t* __restrict__ elem, uint8_t* __restrict__ peeled,
+    unsigned long long* __restrict__ cnt, const Ctrl* __restrict__ ctrl, uint64_t seed,
+    uint32_t rows, uint32_t c, uint32_t cmask, uint32_t log2c) {
+    __shared__ uint32_t s_tmp[kBlock / 64];
+    if (ctrl->overflow) return;
+    const uint64_t w0 = (uint64_t)blockIdx.x * kChunkWords + 4ull * threadIdx.x;
+    uint32_t w4[4];
+    uint32_t mine = 0;
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+        w4[k] = load_word(b, w0 + k, words, last_mask);
+        mine += __popc(w4[k]);
+    }
+    uint32_t total;
+    uint32_t pos = blk[blockIdx.x] + block_exclusive_scan(mine, s_tmp, &total);
+    uint64_t cached_batch = ~0ull;
+    BatchHash h;
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+        uint32_t w = w4[k];
+        while (w) {
+            const uint32_t bit = __builtin_ctz(w);
+            w &= w - 1u;
+            const uint64_t p = (w0 + k) * 32ull + bit;
+            const uint64_t batch = p >> log2c;
+            if (batch != cached_batch) {
+                h = batch_hash(seed, rows, cmask, batch);
+                cached_batch = batch;
+            }
+            elem[pos] = (uint32_t)p;
+            peeled[pos] = 0;
+            const uint32_t t = (uint32_t)p & cmask;
+            const unsigned long long inc = kOne + pos;
+#pragma unroll
+            for (int j = 0; j < 3; j++) atomicAdd(cnt + cell_of(h, j, t, c, cmask), inc);
+            pos++;
+        }
+    }
+}
+
+template <typename T>
+struct PeelArgs {
+    Ctrl* ctrl;
+    const uint32_t* elem;
+    T* vals;
+    uint8_t* peeled;
+    unsigned long long* cnt;
+    T* yw;
+    uint32_t* stamp;
+    uint32_t* queue;
+    InfoDev* info;
+    uint64_t seed;
+    uint32_t rows, c, cmask, log2c, cells;
+};
+
+// Append `cell` to the queue for lanes with pred, one atomic per wave.
+__device__ __forceinline__ void wave_push(bool pred, uint32_t cell, uint32_t round_stamp,
+                                          Ctrl* ctrl, uint32_t* queue, uint32_t* stamp,
+                                          uint32_t cells) {
+    const uint64_t m = __ballot(pred);
+    if (m == 0) return;
+    const uint32_t leader = (uint32_t)__ffsll((unsigned long long)m) - 1u;
+    uint32_t base = 0;
+    if (lane_id() == leader) base = atomicAdd(&ctrl->tail, (unsigned int)__popcll(m));
+    base = __shfl(base, leader);
+    if (pred) {
+        const uint32_t slot = base + lanes_below(m);
+        if (slot < cells) {  // each cell becomes pure at most once, so this always holds
+            queue[slot] = cell;
+            stamp[cell] = round_stamp;
+        }
+    }
+}
+
+// Grid-wide barrier.  The last block to arrive publishes the end of the next
+// frontier.  Returns false if the wait timed out (then ctrl->abort is set).
+__device__ bool grid_barrier(Ctrl* ctrl, uint32_t nblocks) {
+    __shared__ uint32_t s_ok;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t ok = 1;
+        const uint32_t gen =
+            __hip_atomic_load(&ctrl->bar_gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint32_t arrived = __hip_atomic_fetch_add(&ctrl->bar_count, 1u, __ATOMIC_ACQ_REL,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
+        if (arrived == nblocks - 1u) {
+            const uint32_t t =
+                __hip_atomic_load(&ctrl->tail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&ctrl->fend, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&ctrl->bar_count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&ctrl->bar_gen, gen + 1u, __ATOMIC_RELEASE,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+            while (__hip_atomic_load(&ctrl->bar_gen, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) ==
+                   gen) {
+                __builtin_amdgcn_s_sleep(1);
+                if (__builtin_amdgcn_s_memrealtime() - t0 > kBarrierTimeoutTicks) {
+                    __hip_atomic_store(&ctrl->abort, 1u, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                    ok = 0;
+                    break;
+                }
+            }
+        }
+        if (__hip_atomic_load(&ctrl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) ok = 0;
+        s_ok = ok;
+    }
+    __syncthreads();
+    return s_ok != 0;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void peel_kernel(PeelArgs<T> a) {
+    Ctrl* ctrl = a.ctrl;
+    const uint32_t lane = lane_id();
+    const uint32_t waves_per_block = kBlock / 64;
+    const uint32_t gwave = blockIdx.x * waves_per_block + (threadIdx.x >> 6);
+    const uint32_t nwaves = gridDim.x * waves_per_block;
+    const uint32_t nthreads = gridDim.x * kBlock;
+    const uint32_t gtid = blockIdx.x * kBlock + threadIdx.x;
+    const bool overflow = ctrl->overflow != 0;
+    bool ok = true;
+
+    if (!overflow) {
+        // round-0 frontier: every cell with exactly one element
+        for (uint32_t i0 = gwave * 64u; i0 < a.cells; i0 += nwaves * 64u) {
+            const uint32_t cidx = i0 + lane;
+            bool pure = false;
+            if (cidx < a.cells) pure = (a.cnt[cidx] >> 32) == 1ull;
+            wave_push(pure, cidx, 0u, ctrl, a.queue, a.stamp, a.cells);
+        }
+        ok = grid_barrier(ctrl, gridDim.x);
+
+        const uint32_t nsup = (uint32_t)ctrl->n_support;
+        uint32_t qs = 0;
+        for (uint32_t r = 0; ok; r++) {
+            uint32_t qe =
+                __hip_atomic_load(&ctrl->fend, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (qe > a.cells) qe = a.cells;  // the queue holds each cell at most once
+            if (qe <= qs) break;
+            for (uint32_t i0 = qs + gwave * 64u; i0 < qe; i0 += nwaves * 64u) {
+                const uint32_t i = i0 + lane;
+                bool claimed = false, push_a = false, push_b = false;
+                uint32_t cell_a = 0, cell_b = 0;
+                if (i < qe) {
+                    const uint32_t cidx = a.queue[i];
+                    const unsigned long long v = __hip_atomic_load(
+                        a.cnt + cidx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if ((v >> 32) == 1ull && (uint32_t)v < nsup) {
+                        const uint32_t pos = (uint32_t)v;
+                        const uint32_t p = a.elem[pos];
+                        const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p >> a.log2c);
+                        const uint32_t t = p & a.cmask;
+                        uint32_t cl[3];
+#pragma unroll
+                        for (int j = 0; j < 3; j++) cl[j] = cell_of(h, j, t, a.c, a.cmask);
+                        const int j = cl[0] == cidx ? 0 : (cl[1] == cidx ? 1 : 2);
+                        // claimed by the smallest j among its cells pure at the round start
+                        bool mine = true;
+                        if (j >= 1 && a.stamp[cl[0]] == r) mine = false;
+                        if (j == 2 && mine && a.stamp[cl[1]] == r) mine = false;
+                        if (mine) {
+                            const T val = Val<T>::sign(a.yw[cidx], (h.neg >> j) & 1u);
+                            a.vals[pos] = val;
+                            a.peeled[pos] = 1;
+                            claimed = true;
+                            const int ja = j == 0 ? 1 : 0;
+                            const int jb = j == 2 ? 1 : 2;
+                            const unsigned long long dec = 0ull - (kOne + pos);
+                            const unsigned long long old_a = atomicAdd(a.cnt + cl[ja], dec);
+                            const unsigned long long old_b = atomicAdd(a.cnt + cl[jb], dec);
+                            Val<T>::atomic_add(a.yw + cl[ja],
+                                               Val<T>::sign(val, !((h.neg >> ja) & 1u)));
+                            Val<T>::atomic_add(a.yw + cl[jb],
+                                               Val<T>::sign(val, !((h.neg >> jb) & 1u)));
+                            push_a = ((old_a + dec) >> 32) == 1ull;
+                            push_b = ((old_b + dec) >> 32) == 1ull;
+                            cell_a = cl[ja];
+                            cell_b = cl[jb];
+                        }
+                    }
+                }
+                const uint64_t mc = __ballot(claimed);
+                if (mc != 0 && lane == (uint32_t)__ffsll((unsigned long long)mc) - 1u) {
+                    atomicAdd(&ctrl->recovered, (unsigned long long)__popcll(mc));
+                    atomicMax(&ctrl->rounds, r + 1u);
+                }
+                wave_push(push_a, cell_a, r + 1u, ctrl, a.queue, a.stamp, a.cells);
+                wave_push(push_b, cell_b, r + 1u, ctrl, a.queue, a.stamp, a.cells);
+            }
+            qs = qe;
+            ok = grid_barrier(ctrl, gridDim.x);
+        }
+
+        // leftovers: Count Sketch median estimate from the residual sketch
+        if (ok) {
+            for (uint32_t pos = gtid; pos < nsup; pos += nthreads) {
+                if (a.peeled[pos]) continue;
+                const uint32_t p = a.elem[pos];
+                const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p >> a.log2c);
+                const uint32_t t = p & a.cmask;
+                T e3[3];
+#pragma unroll
+                for (int j = 0; j < 3; j++)
+                    e3[j] = Val<T>::sign(a.yw[cell_of(h, j, t, a.c, a.cmask)], (h.neg >> j) & 1u);
+                a.vals[pos] = median3(e3[0], e3[1], e3[2]);
+            }
+        }
+    }
+
+    if (gtid == 0) {
+        const unsigned long long ns = ctrl->n_support;
+        const unsigned long long rec = overflow ? 0ull : ctrl->recovered;
+        a.info->n_support = ns;
+        a.info->n_recovered = rec;
+        a.info->rounds = overflow ? 0ull : ctrl->rounds;
+        a.info->success = (!overflow && ok && rec == ns) ? 1u : 0u;
+        a.info->status = overflow ? 1u : (ok ? 0u : 2u);
+    }
+}
+
+template <typename T>
+struct EmitArgs {
+    const uint32_t* b;
+    const uint32_t* blk;
+    const uint32_t* elem;
+    const T* vals;
+    const uint8_t* peeled;
+    const T* y_agg;
+    const Ctrl* ctrl;
+    T* x_out;
+    uint32_t* coo_idx;
+    T* coo_val;
+    uint64_t coo_cap;
+    uint32_t* mask;
+    uint64_t n, words, seed;
+    uint32_t rows, c, cmask, log2c, last_mask;
+    bool x_vec;  // x_out is 16-byte aligned
+};
+
+template <typename T>
+__device__ __forceinline__ T estimate_raw(const EmitArgs<T>& a, uint32_t p) {
+    const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p >> a.log2c);
+    const uint32_t t = p & a.cmask;
+    T e3[3];
+#pragma unroll
+    for (int j = 0; j < 3; j++)
+        e3[j] = Val<T>::sign(a.y_agg[cell_of(h, j, t, a.c, a.cmask)], (h.neg >> j) & 1u);
+    return median3(e3[0], e3[1], e3[2]);
+}
+
+// One workgroup per chunk of 1024 bitmap words (32768 parameters).
+template <typename T>
+__global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
+    typedef T V4 __attribute__((ext_vector_type(4)));
+    __shared__ uint32_t s_words[kChunkWords];
+    __shared__ uint32_t s_pref[kChunkWords];
+    __shared__ uint32_t s_tmp[kBlock / 64];
+    const uint32_t lane = lane_id();
+    const uint32_t wave = threadIdx.x >> 6;
+    const uint64_t chunk = blockIdx.x;
+    const uint64_t w0 = chunk * kChunkWords + 4ull * threadIdx.x;
+    uint32_t w4[4], mine = 0;
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+        w4[k] = load_word(a.b, w0 + k, a.words, a.last_mask);
+        mine += __popc(w4[k]);
+    }
+    uint32_t total;
+    uint32_t run = block_exclusive_scan(mine, s_tmp, &total);
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+        s_words[4 * threadIdx.x + k] = w4[k];
+        s_pref[4 * threadIdx.x + k] = run;
+        run += __popc(w4[k]);
+    }
+    __syncthreads();
+    const uint64_t off = a.blk[chunk];
+    const bool overflow = a.ctrl->overflow != 0;
+    const uint64_t chunk_p = chunk * kChunkBits;
+
+    for (uint32_t it = 0; it < kChunkBits / (4 * kBlock); it++) {
+        const uint32_t e0 = it * (4 * kBlock) + 4u * threadIdx.x;  // offset in the chunk
+        const uint64_t p0 = chunk_p + e0;
+        const uint32_t wi = e0 >> 5, sh = e0 & 31u;
+        const uint32_t word = s_words[wi];
+        uint64_t rank = off + s_pref[wi] + __popc(word & ((1u << sh) - 1u));
+        T out[4];
+        bool rec[4];
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            out[k] = T(0);
+            rec[k] = false;
+            if ((word >> (sh + k)) & 1u) {
+                const uint32_t p = (uint32_t)(p0 + k);
+                if (!overflow) {
+                    out[k] = a.vals[rank];
+                    rec[k] = a.peeled[rank] != 0;
+                } else {
+                    out[k] = estimate_raw(a, p);
+                }
+                if (a.coo_idx != nullptr && rank < a.coo_cap) {
+                    a.coo_idx[rank] = p;
+                    a.coo_val[rank] = out[k];
+                }
+                rank++;
+            }
+        }
+        if (a.x_out != nullptr && p0 < a.n) {
+            if (a.x_vec && p0 + 4 <= a.n) {
+                V4 v = {out[0], out[1], out[2], out[3]};
+                __builtin_nontemporal_store(v, reinterpret_cast<V4*>(a.x_out + p0));
+            } else {
+                for (int k = 0; k < 4; k++)
+                    if (p0 + k < a.n) a.x_out[p0 + k] = out[k];
+            }
+        }
+        if (a.mask != nullptr) {
+            const uint64_t m0 = __ballot(rec[0]), m1 = __ballot(rec[1]);
+            const uint64_t m2 = __ballot(rec[2]), m3 = __ballot(rec[3]);
+            if (lane < 8) {
+                const uint32_t s8 = 8u * lane;
+                const uint32_t mw = spread4((uint32_t)(m0 >> s8)) |
+                                    (spread4((uint32_t)(m1 >> s8)) << 1) |
+                                    (spread4((uint32_t)(m2 >> s8)) << 2) |
+                                    (spread4((uint32_t)(m3 >> s8)) << 3);
+                const uint64_t widx = ((chunk_p + it * (4 * kBlock) + wave * 256u) >> 5) + lane;
+                if (widx < a.words) a.mask[widx] = mw;
+            }
+        }
+    }
+}
+
+int peel_grid_cache[64];
+
+template <typename T>
+hipError_t launch_decode_t(const Geo& g, const void* y_agg_v, const uint32_t* b,
+                           const DecodeOut& out, const DecodeLayout& L, void* ws,
+                           hipStream_t s) {
+    char* base = static_cast<char*>(ws);
+    Ctrl* ctrl = reinterpret_cast<Ctrl*>(base + L.ctrl);
+    uint32_t* blk = reinterpret_cast<uint32_t*>(base + L.blk);
+    uint32_t* elem = reinterpret_cast<uint32_t*>(base + L.elem);
+    T* vals = reinterpret_cast<T*>(base + L.vals);
+    uint8_t* peeled = reinterpret_cast<uint8_t*>(base + L.peeled);
+    unsigned long long* cnt = reinterpret_cast<unsigned long long*>(base + L.cnt);
+    T* yw = reinterpret_cast<T*>(base + L.yw);
+    uint32_t* stamp = reinterpret_cast<uint32_t*>(base + L.stamp);
+    uint32_t* queue = reinterpret_cast<uint32_t*>(base + L.queue);
+    const T* y_agg = static_cast<const T*>(y_agg_v);
+
+    DeviceInfo di;
+    hipError_t e = device_info(&di);
+    if (e != hipSuccess) return e;
+
+    uint64_t grid = ((uint64_t)g.cells + kBlock - 1) / kBlock;
+    if (grid > (uint64_t)di.cus * 16) grid = (uint64_t)di.cus * 16;
+    hipLaunchKernelGGL(prep_kernel<T>, dim3((uint32_t)grid), dim3(kBlock), 0, s, y_agg, yw, cnt,
+                       stamp, g.cells, ctrl);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const uint32_t last_mask = (g.n & 31u) ? ((1u << (g.n & 31u)) - 1u) : 0xffffffffu;
+    hipLaunchKernelGGL(count_kernel, dim3((uint32_t)L.nchunks), dim3(kBlock), 0, s, b, g.words,
+                       last_mask, blk);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, s, blk, L.nchunks, ctrl, L.cap);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(build_kernel, dim3((uint32_t)L.nchunks), dim3(kBlock), 0, s, b, g.words,
+                       last_mask, blk, elem, peeled, cnt, ctrl, g.seed, g.rows, g.c, g.cmask, g.log2c);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+
+    // persistent peel: every workgroup must be resident (cooperative launch)
+    int dev = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    const int slot = (dev & 31) * 2 + (std::is_same<T, float>::value ? 1 : 0);
+    if (peel_grid_cache[slot] == 0) {
+        int per_cu = 0;
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &per_cu, reinterpret_cast<const void*>(&peel_kernel<T>), kBlock, 0);
+        if (e != hipSuccess) return e;
+        if (per_cu < 1) return hipErrorInvalidConfiguration;
+        if (per_cu > 2) per_cu = 2;
+        peel_grid_cache[slot] = per_cu * di.cus;
+    }
+    PeelArgs<T> pa;
+    pa.ctrl = ctrl;
+    pa.elem = elem;
+    pa.vals = vals;
+    pa.peeled = peeled;
+    pa.cnt = cnt;
+    pa.yw = yw;
+    pa.stamp = stamp;
+    pa.queue = queue;
+    pa.info = static_cast<InfoDev*>(out.info);
+    pa.seed = g.seed;
+    pa.rows = g.rows;
+    pa.c = g.c;
+    pa.cmask = g.cmask;
+    pa.log2c = g.log2c;
+    pa.cells = g.cells;
+    void* args[] = {&pa};
+    e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&peel_kernel<T>),
+                                   dim3((uint32_t)peel_grid_cache[slot]), dim3(kBlock), args, 0,
+                                   s);
+    if (e != hipSuccess) return e;
+
+    if (out.x_out != nullptr || out.mask != nullptr || out.coo_idx != nullptr) {
+        EmitArgs<T> ea;
+        ea.b = b;
+        ea.blk = blk;
+        ea.elem = elem;
+        ea.vals = vals;
+        ea.peeled = peeled;
+        ea.y_agg = y_agg;
+        ea.ctrl = ctrl;
+        ea.x_out = static_cast<T*>(out.x_out);
+        ea.coo_idx = out.coo_idx;
+        ea.coo_val = static_cast<T*>(out.coo_val);
+        ea.coo_cap = out.coo_idx != nullptr && out.coo_val != nullptr ? out.coo_cap : 0;
+        if (ea.coo_cap == 0) ea.coo_idx = nullptr;
+        ea.mask = out.mask;
+        ea.n = g.n;
+        ea.words = g.words;
+        ea.seed = g.seed;
+        ea.rows = g.rows;
+        ea.c = g.c;
+        ea.cmask = g.cmask;
+        ea.log2c = g.log2c;
+        ea.last_mask = last_mask;
+        ea.x_vec = (reinterpret_cast<uintptr_t>(out.x_out) & 15u) == 0;
+        hipLaunchKernelGGL(emit_kernel<T>, dim3((uint32_t)L.nchunks), dim3(kBlock), 0, s, ea);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+}  // namespace
+
+DecodeLayout decode_layout(const Geo& g, uint64_t max_support) {
+    DecodeLayout L;
+    uint64_t cap = max_support == 0 ? g.n : max_support;
+    if (cap > g.n) cap = g.n;
+    if (cap > 0x7fffffffull) cap = 0x7fffffffull;  // packed counters need |S| < 2^31
+    L.cap = cap;
+    L.nchunks = (g.words + kChunkWords - 1) / kChunkWords;
+    const size_t vsz = 4;  // int32 or fp32
+    size_t o = 0;
+    L.ctrl = o;    o = align256(o + sizeof(Ctrl));
+    L.blk = o;     o = align256(o + L.nchunks * 4);
+    L.elem = o;    o = align256(o + cap * 4);
+    L.vals = o;    o = align256(o + cap * vsz);
+    L.peeled = o;  o = align256(o + cap);
+    L.cnt = o;     o = align256(o + (size_t)g.cells * 8);
+    L.yw = o;      o = align256(o + (size_t)g.cells * vsz);
+    L.stamp = o;   o = align256(o + (size_t)g.cells * 4);
+    L.queue = o;   o = align256(o + (size_t)g.cells * 4);
+    L.total = o;
+    return L;
+}
+
+hipError_t launch_decode(const Geo& g, const void* y_agg, const uint32_t* b_agg,
+                         const DecodeOut& out, const DecodeLayout& L, void* ws, hipStream_t s) {
+    if (g.f32) return launch_decode_t<float>(g, y_agg, b_agg, out, L, ws, s);
+    return launch_decode_t<int32_t>(g, y_agg, b_agg, out, L, ws, s);
+}
+
+}  // namespace hc

@@ -1,0 +1,129 @@
+// hc_device.h -- device-side helpers shared by the gfx950 kernels: the sketch
+// hash, cell arithmetic, value types and wave-level utilities.
+//
+// The sketch format is the one documented in include/hc.h: per batch of c
+// parameters (section 3.4) and per hash j < 3 (section 3.1) one 64-bit
+// SplitMix64 output gives a row, a rotation and a sign.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hc {
+
+constexpr uint64_t kGolden = 0x9e3779b97f4a7c15ull;   // SplitMix64 increment
+constexpr uint64_t kMix1 = 0xbf58476d1ce4e5b9ull;     // SplitMix64 finalizer
+constexpr uint64_t kMix2 = 0x94d049bb133111ebull;
+
+// SplitMix64 (Steele, Lea and Flood 2014): output number i of state `seed`.
+__device__ __forceinline__ uint64_t splitmix(uint64_t seed, uint64_t i) {
+    uint64_t z = seed + (i + 1ull) * kGolden;
+    z = (z ^ (z >> 30)) * kMix1;
+    z = (z ^ (z >> 27)) * kMix2;
+    return z ^ (z >> 31);
+}
+
+// Row, rotation and sign of one batch for each of the three hashes.
+struct BatchHash {
+    uint32_t row[3];
+    uint32_t bias[3];
+    uint32_t neg;   // bit j set: g_j = -1
+};
+
+// rows: R >= 3 (< 2^32).  cmask = c - 1.
+__device__ __forceinline__ BatchHash batch_hash(uint64_t seed, uint32_t rows, uint32_t cmask,
+                                                uint64_t b) {
+    const uint64_t h0 = splitmix(seed, 3ull * b + 0ull);
+    const uint64_t h1 = splitmix(seed, 3ull * b + 1ull);
+    const uint64_t h2 = splitmix(seed, 3ull * b + 2ull);
+    BatchHash h;
+    // three distinct rows: scale the low words into [0,R), [0,R-1), [0,R-2)
+    // and step later rows over the earlier ones
+    uint32_t r0 = __umulhi((uint32_t)h0, rows);
+    uint32_t r1 = __umulhi((uint32_t)h1, rows - 1u);
+    r1 += (r1 >= r0);
+    const uint32_t lo = min(r0, r1), hi = max(r0, r1);
+    uint32_t r2 = __umulhi((uint32_t)h2, rows - 2u);
+    r2 += (r2 >= lo);
+    r2 += (r2 >= hi);
+    h.row[0] = r0;
+    h.row[1] = r1;
+    h.row[2] = r2;
+    h.bias[0] = (uint32_t)(h0 >> 32) & cmask;
+    h.bias[1] = (uint32_t)(h1 >> 32) & cmask;
+    h.bias[2] = (uint32_t)(h2 >> 32) & cmask;
+    h.neg = (uint32_t)(h0 >> 63) | ((uint32_t)(h1 >> 63) << 1) | ((uint32_t)(h2 >> 63) << 2);
+    return h;
+}
+
+// Cell of column t under hash j.  c = cmask + 1 is a power of two.
+__device__ __forceinline__ uint32_t cell_of(const BatchHash& h, int j, uint32_t t, uint32_t c,
+                                            uint32_t cmask) {
+    return h.row[j] * c + ((t + h.bias[j]) & cmask);
+}
+
+// ---- value types: int32 sums wrap (computed on uint32), fp32 plain ----------
+
+template <typename T> struct Val;
+
+template <> struct Val<int32_t> {
+    __device__ __forceinline__ static int32_t sign(int32_t v, bool neg) {
+        return neg ? (int32_t)(0u - (uint32_t)v) : v;
+    }
+    __device__ __forceinline__ static void atomic_add(int32_t* a, int32_t v) {
+        atomicAdd(reinterpret_cast<unsigned int*>(a), (unsigned int)v);
+    }
+    __device__ __forceinline__ static int32_t add(int32_t a, int32_t b) {
+        return (int32_t)((uint32_t)a + (uint32_t)b);
+    }
+    __device__ __forceinline__ static bool nonzero(int32_t v) { return v != 0; }
+};
+
+template <> struct Val<float> {
+    __device__ __forceinline__ static float sign(float v, bool neg) { return neg ? -v : v; }
+    __device__ __forceinline__ static void atomic_add(float* a, float v) {
+        unsafeAtomicAdd(a, v);
+    }
+    __device__ __forceinline__ static float add(float a, float b) { return a + b; }
+    __device__ __forceinline__ static bool nonzero(float v) { return v != 0.0f; }
+};
+
+template <typename T>
+__device__ __forceinline__ T median3(T a, T b, T c) {
+    const T lo = a < b ? a : b;
+    const T hi = a < b ? b : a;
+    return c < lo ? lo : (c > hi ? hi : c);
+}
+
+// ---- wave64 utilities --------------------------------------------------------
+
+__device__ __forceinline__ uint32_t lane_id() {
+    return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+
+// Number of set bits of `mask` at lanes below this one.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+__device__ __forceinline__ uint32_t uniform(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+}
+
+__device__ __forceinline__ uint64_t uniform64(uint64_t v) {
+    const uint32_t lo = uniform((uint32_t)v);
+    const uint32_t hi = uniform((uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Bits 0..7 of b moved to bits 0, 4, 8, ..., 28.
+__device__ __forceinline__ uint32_t spread4(uint32_t b) {
+    b &= 0xffu;
+    b = (b | (b << 12)) & 0x000f000fu;
+    b = (b | (b << 6)) & 0x03030303u;
+    b = (b | (b << 3)) & 0x11111111u;
+    return b;
+}
+
+}  // namespace hc

@@ -1,0 +1,61 @@
+// hc_internal.h -- host-side launchers of the gfx950 kernels (internal to
+// libhc; the public surface is include/hc.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace hc {
+
+// Validated geometry in the form the kernels take it.
+struct Geo {
+    uint64_t n;       // gradient length
+    uint64_t words;   // ceil(n / 32)
+    uint32_t rows;    // R
+    uint32_t c;       // batch width (power of two)
+    uint32_t cmask;   // c - 1
+    uint32_t log2c;
+    uint32_t cells;   // rows * c
+    uint64_t seed;
+    bool f32;         // value type: fp32 (else int32)
+};
+
+struct DeviceInfo {
+    int cus;          // compute units
+};
+hipError_t device_info(DeviceInfo* out);
+
+// encode
+hipError_t launch_fill_u32(uint32_t* p, uint64_t count, uint32_t value, hipStream_t s);
+hipError_t launch_encode_dense(const Geo& g, const void* x, void* y, uint32_t* b,
+                               hipStream_t s);
+hipError_t launch_encode_coo(const Geo& g, const uint32_t* idx, const void* val,
+                             uint64_t nnz, void* y, uint32_t* b, hipStream_t s);
+
+// aggregate
+hipError_t launch_aggregate(const Geo& g, const void* y_in, const uint32_t* b_in, uint32_t W,
+                            void* y_out, uint32_t* b_out, hipStream_t s);
+
+// decode workspace layout (byte offsets into the caller's workspace)
+struct DecodeLayout {
+    uint64_t cap;       // max support the workspace holds
+    uint64_t nchunks;   // bitmap chunks of kChunkWords words
+    size_t ctrl, blk, elem, vals, peeled, cnt, yw, stamp, queue, total;
+};
+constexpr uint32_t kChunkWords = 1024;
+DecodeLayout decode_layout(const Geo& g, uint64_t max_support);
+
+struct DecodeOut {
+    void* x_out;
+    uint32_t* coo_idx;
+    void* coo_val;
+    uint64_t coo_cap;
+    uint32_t* mask;
+    void* info;   // hc_decode_info*
+};
+hipError_t launch_decode(const Geo& g, const void* y_agg, const uint32_t* b_agg,
+                         const DecodeOut& out, const DecodeLayout& L, void* ws,
+                         hipStream_t s);
+
+}  // namespace hc

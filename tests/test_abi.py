@@ -1,0 +1,81 @@
+"""The C-ABI library loads on the host and exports every entry point that
+include/hc.h declares; host-side validation (no GPU work) behaves as the
+header documents."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_entry_points():
+    with open(os.path.join(ROOT, "include", "hc.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hc_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2402_07529_amd as hc
+    names = declared_entry_points()
+    assert set(names) == set(hc.EXPORTS)
+    lib = ctypes.CDLL(hc.LIB_PATH)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_geometry_and_sizes_host_only():
+    import oracle
+    import paper_2402_07529_amd as hc
+    for n, nnz, c in ((65536, 1636, 1024), (109_482_240, 9_305_915, 1024), (1000, 10, 1),
+                      (2**32 - 1, 10**6, 64)):
+        p = hc.hc_geometry(n, nnz, 1.23, c, 7, "i32")
+        assert p.rows == oracle.rows_for(nnz, 1.23, c)
+        y, b, ws = hc.hc_sizes(p)
+        assert y == p.rows * c * 4 and b == (n + 31) // 32 * 4
+        assert ws > 8 * p.cells
+        _, _, ws_small = hc.hc_sizes(p, max_support=1000)
+        assert ws_small < ws or n <= 1000
+
+
+@pytest.mark.parametrize("kw", [dict(c=3), dict(c=2048), dict(n=0), dict(n=2**32)])
+def test_geometry_rejects_invalid(kw):
+    import paper_2402_07529_amd as hc
+    args = dict(n=1000, nnz=100, c=1024)
+    args.update(kw)
+    with pytest.raises(hc.HCError) as ei:
+        hc.hc_geometry(args["n"], args["nnz"], 1.23, args["c"], 1)
+    assert ei.value.status == hc.HC_EINVAL
+
+
+def test_sizes_reject_bad_params():
+    import paper_2402_07529_amd as hc
+    for p, st in ((hc.make_params(1000, 2, 1), hc.HC_EINVAL),
+                  (hc.hc_params(1000, 2, 1024, 5, 1, 0, 0), hc.HC_EUNSUPPORTED),
+                  (hc.hc_params(1000, 3, 1024, 5, 1, 7, 0), hc.HC_EINVAL),
+                  (hc.hc_params(1000, 3, 1024, 2**23, 1, 0, 0), hc.HC_EINVAL)):
+        with pytest.raises(hc.HCError) as ei:
+            hc.hc_sizes(p)
+        assert ei.value.status == st
+        assert hc.lib().hc_last_error()
+
+
+def test_null_and_misaligned_pointers_rejected_before_launch():
+    import paper_2402_07529_amd as hc
+    L = hc.lib()
+    p = hc.make_params(1000, 3, 1)
+    assert L.hc_encode(ctypes.byref(p), None, None, None, None) == hc.HC_EINVAL
+    assert L.hc_aggregate(ctypes.byref(p), ctypes.c_void_p(16), ctypes.c_void_p(16), 0,
+                          ctypes.c_void_p(16), ctypes.c_void_p(16), None) == hc.HC_EINVAL
+    assert L.hc_encode(ctypes.byref(p), ctypes.c_void_p(18), ctypes.c_void_p(32),
+                       ctypes.c_void_p(48), None) == hc.HC_EINVAL
+    assert b"aligned" in L.hc_last_error()
+    assert L.hc_decode(ctypes.byref(p), ctypes.c_void_p(16), ctypes.c_void_p(16), None, None,
+                       None, 0, None, ctypes.c_void_p(16), 0, ctypes.c_void_p(64), 10**9,
+                       None) == hc.HC_EINVAL
+    assert b"aligned" in L.hc_last_error()
+    assert L.hc_decode(ctypes.byref(p), ctypes.c_void_p(16), ctypes.c_void_p(16), None, None,
+                       None, 0, None, ctypes.c_void_p(16), 0, ctypes.c_void_p(256), 10,
+                       None) == hc.HC_EWORKSPACE

@@ -1,0 +1,204 @@
+"""GPU (gfx950) parity of encode -> aggregate -> decode against the CPU oracle.
+
+Bar: int32 fixed-point results are bit-exact (sketches, bitmaps, decoded
+gradient, recovered mask, COO, and the support size / recovered count / round
+count / success flag).  fp32: the structural outputs (bitmaps, mask, counts,
+rounds, success) are exact, and values agree with the oracle's fp64 result to
+1e-6 of the gradient's largest magnitude (normwise relative error), the
+tolerance the method's fp32 variant is held to.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from hc_pipeline import gpu_run, oracle_run, wrap_sum
+
+pytestmark = pytest.mark.gpu
+
+FP32_TOL = 1e-6
+
+
+def _hc():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2402_07529_amd as hc
+    return hc
+
+
+def assert_same_info(gi, oi):
+    assert (gi.n_support, gi.n_recovered, gi.rounds, gi.success) == \
+        (oi.n_support, oi.n_recovered, oi.rounds, oi.success), (gi, oi)
+    assert gi.status == 0
+
+
+def check_int(w, rows, c, coo_input=False):
+    g = gpu_run(w, rows, c, coo_input=coo_input)
+    o = oracle_run(w, rows, c)
+    for i in range(w.W):
+        assert np.array_equal(g["Y"][i], o["Y"][i]), f"worker {i} sketch"
+        assert np.array_equal(g["B"][i], o["B"][i]), f"worker {i} bitmap"
+    assert np.array_equal(g["Ya"], o["Ya"])
+    assert np.array_equal(g["Ba"], o["Ba"])
+    assert np.array_equal(g["x"], o["x"])
+    assert np.array_equal(g["mask"], o["mask"])
+    assert_same_info(g["info"], o["info"])
+    sup = np.nonzero(np.unpackbits(o["Ba"].view(np.uint8), bitorder="little")[:w.n])[0]
+    assert np.array_equal(g["coo_idx"], sup.astype(np.uint32))
+    assert np.array_equal(g["coo_val"], o["x"][sup])
+    return g, o
+
+
+def test_tiny_int32_all_stages():
+    _hc()
+    w = wl.make("tiny")
+    rows = oracle.rows_for(w.n_agg)
+    g, o = check_int(w, rows, 1024)
+    assert g["info"].success
+    assert np.array_equal(g["x"], wrap_sum([w.dense(i) for i in range(w.W)]))
+
+
+@pytest.mark.parametrize("c", [1024, 512, 256, 128, 64, 16, 4, 2, 1])
+def test_multi_tile_ragged_int32(c):
+    # several rows and tiles, n not a multiple of the tile, the word or c
+    _hc()
+    w = wl.make("synthetic", n=1_000_003, W=4, density=0.01, overlap=0.4, data_seed=c)
+    rows = oracle.rows_for(w.n_agg, 1.23, c)
+    g, o = check_int(w, rows, c)
+    assert g["info"].success
+    assert np.array_equal(g["x"], wrap_sum([w.dense(i) for i in range(w.W)]))
+
+
+@pytest.mark.parametrize("c", [1024, 64, 1])
+def test_coo_encode_matches_dense(c):
+    _hc()
+    w = wl.make("synthetic", n=777_777, W=3, density=0.02, overlap=0.5, data_seed=40 + c)
+    rows = oracle.rows_for(w.n_agg, 1.23, c)
+    check_int(w, rows, c, coo_input=True)
+
+
+@pytest.mark.parametrize("ratio,c", [(1.10, 1024), (1.15, 64), (1.20, 1), (0.8, 1024)])
+def test_undersized_sketch_failure_parity(ratio, c):
+    # below the peeling threshold: partial recovery, leftover estimates
+    _hc()
+    w = wl.make("synthetic", n=2_000_000, W=4, density=0.01, overlap=0.3, data_seed=int(ratio * 100))
+    rows = max(3, int(math.ceil(ratio * w.n_agg / c)))
+    g, o = check_int(w, rows, c)
+    assert not g["info"].success and g["info"].n_recovered < g["info"].n_support
+
+
+def test_forced_failure_three_cells():
+    _hc()
+    w = wl.make("synthetic", n=5000, W=2, density=0.002, overlap=0.0, data_seed=3)
+    g, o = check_int(w, 3, 1)
+    assert g["info"].n_recovered == 0 and g["info"].rounds == 0
+
+
+def test_fp32_all_stages():
+    _hc()
+    w = wl.make("synthetic", n=1_500_001, W=8, density=0.01, overlap=0.3, vtype="f32",
+                data_seed=77)
+    rows = oracle.rows_for(w.n_agg, 1.23, 1024)
+    g = gpu_run(w, rows, 1024)
+    o = oracle_run(w, rows, 1024)
+    for i in range(w.W):
+        assert np.array_equal(g["B"][i], o["B"][i])
+        scale = np.max(np.abs(o["Y"][i]))
+        assert np.max(np.abs(g["Y"][i] - o["Y"][i])) <= FP32_TOL * scale
+    assert np.array_equal(g["Ba"], o["Ba"])
+    assert np.array_equal(g["mask"], o["mask"])
+    assert_same_info(g["info"], o["info"])
+    scale = np.max(np.abs(o["x"]))
+    err = np.max(np.abs(g["x"].astype(np.float64) - o["x"]))
+    assert err <= FP32_TOL * scale, err / scale
+    truth = sum(w.dense(i).astype(np.float64) for i in range(w.W))
+    assert np.max(np.abs(g["x"] - truth)) <= FP32_TOL * np.max(np.abs(truth))
+
+
+def test_fp32_undersized_structure_exact():
+    _hc()
+    w = wl.make("synthetic", n=600_000, W=4, density=0.01, overlap=0.3, vtype="f32", data_seed=5)
+    rows = int(math.ceil(1.1 * w.n_agg / 1024))
+    g = gpu_run(w, rows, 1024)
+    o = oracle_run(w, rows, 1024)
+    assert np.array_equal(g["mask"], o["mask"])
+    assert_same_info(g["info"], o["info"])
+    rec = np.unpackbits(o["mask"].view(np.uint8), bitorder="little")[:w.n].astype(bool)
+    scale = np.max(np.abs(o["x"]))
+    assert np.max(np.abs(g["x"][rec] - o["x"][rec])) <= FP32_TOL * scale
+
+
+def test_overflow_falls_back_to_estimates():
+    # support larger than the workspace capacity: nothing is peeled and every
+    # member of the support gets the Count Sketch query of the aggregate
+    hc = _hc()
+    w = wl.make("synthetic", n=300_000, W=2, density=0.01, overlap=0.5, data_seed=9)
+    rows = oracle.rows_for(w.n_agg, 1.23, 1024)
+    g = gpu_run(w, rows, 1024, max_support=100)
+    o = oracle_run(w, rows, 1024)
+    inf = g["info"]
+    assert (inf.status, inf.success, inf.n_recovered, inf.rounds) == (1, 0, 0, 0)
+    assert inf.n_support == w.n_agg
+    assert not g["mask"].any()
+    sup = np.nonzero(np.unpackbits(o["Ba"].view(np.uint8), bitorder="little")[:w.n])[0]
+    est = np.array([oracle.query(o["g"], o["Ya"], int(p)) for p in sup], np.int32)
+    assert np.array_equal(g["x"][sup], est)
+    other = np.ones(w.n, bool)
+    other[sup] = False
+    assert not g["x"][other].any()
+
+
+@pytest.mark.parametrize("n", [1, 31, 32, 33, 1023, 1025, 4097])
+def test_tiny_and_ragged_lengths(n):
+    _hc()
+    rng = np.random.default_rng(n)
+    k = max(1, n // 10)
+    idx = np.sort(rng.choice(n, k, replace=False)).astype(np.uint32)
+    vals = rng.integers(1, 1000, k).astype(np.int32)
+    w = wl.Workload("edge", n, 1, "i32", [idx], [vals], 0, 99)
+    for c in (1, 32, 1024):
+        check_int(w, 3 + n // 16, c)
+
+
+def test_empty_support():
+    _hc()
+    w = wl.Workload("empty", 100_000, 2, "i32", [np.zeros(0, np.uint32)] * 2,
+                    [np.zeros(0, np.int32)] * 2, 0, 5)
+    g, o = check_int(w, 5, 1024)
+    assert g["info"].success and g["info"].n_support == 0 and not g["x"].any()
+
+
+def test_int32_wraparound_sums():
+    _hc()
+    n = 200_000
+    rng = np.random.default_rng(1)
+    idx = np.sort(rng.choice(n, 2000, replace=False)).astype(np.uint32)
+    big = [rng.integers(2**30, 2**31 - 1, idx.size).astype(np.int32) for _ in range(3)]
+    w = wl.Workload("wrap", n, 3, "i32", [idx] * 3, big, 0, 17)
+    g, o = check_int(w, oracle.rows_for(idx.size), 1024)
+    assert np.array_equal(g["x"], wrap_sum([w.dense(i) for i in range(3)]))
+
+
+def test_deterministic_int32_repeat():
+    _hc()
+    w = wl.make("synthetic", n=3_000_000, W=4, density=0.01, overlap=0.5, data_seed=123)
+    rows = oracle.rows_for(w.n_agg)
+    a = gpu_run(w, rows, 1024, keep_workers=False)
+    b = gpu_run(w, rows, 1024, keep_workers=False)
+    for k in ("Ya", "Ba", "x", "mask", "coo_idx", "coo_val"):
+        assert np.array_equal(a[k], b[k]), k
+    assert a["info"] == b["info"]
+
+
+def test_coo_capacity_truncates():
+    _hc()
+    w = wl.make("tiny")
+    rows = oracle.rows_for(w.n_agg)
+    g = gpu_run(w, rows, 1024, coo_cap=100)
+    o = oracle_run(w, rows, 1024)
+    sup = np.nonzero(np.unpackbits(o["Ba"].view(np.uint8), bitorder="little")[:w.n])[0]
+    assert np.array_equal(g["coo_idx"], sup[:100].astype(np.uint32))
+    assert np.array_equal(g["coo_val"], o["x"][sup[:100]])
