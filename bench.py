@@ -1,0 +1,214 @@
+"""Throughput of one simulated aggregation iteration on one MI355X.
+
+One step = W worker encodes of dense gradients (hc_encode), the W-way
+aggregation (hc_aggregate) and the peeling decode to a dense gradient
+(hc_decode), all through the C ABI, inputs resident in HBM.  The metric is
+dense-gradient GB/s: the aggregated gradient's 4N bytes counted once per
+iteration (the paper's convention for aggregation throughput, section 4.2),
+divided by the iteration time.
+
+Prints ONE JSON line.  Default workload: the NCF-shaped embedding gradient
+(2^24 rows x 64 dims, 8 workers, 4096 Zipf rows each, int32 fixed point).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "encode+aggregate+decode dense-gradient GB/s at 1 GPU; % HBM peak; decode success"
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="ncf", choices=["tiny", "ncf", "lstm", "vgg19", "bert"])
+    ap.add_argument("--vtype", default="i32", choices=["i32", "f32"])
+    ap.add_argument("--density", type=float, default=None)
+    ap.add_argument("--overlap", type=float, default=None)
+    ap.add_argument("--ratio", type=float, default=None,
+                    help="sketch cells / aggregate nonzeros (default: gamma = 1.23)")
+    ap.add_argument("--c", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def make_workload(a):
+    import workloads as wl
+    kw = {}
+    if a.density is not None:
+        kw["density"] = a.density
+    if a.overlap is not None:
+        kw["overlap"] = a.overlap
+    return wl.make(a.config, vtype=a.vtype, **kw)
+
+
+def algorithmic_bytes(n, W, cells, n_sup):
+    """Bytes the method must move per stage (reads + writes of HBM)."""
+    words_b = (n + 31) // 32 * 4
+    enc = 4 * n + words_b + 4 * cells                     # read x, write B, clear/write Y
+    agg = (W + 1) * (4 * cells + words_b)                  # W sketches+bitmaps in, one out
+    dec = words_b + 4 * cells + 8 * n_sup + 4 * n          # B, Y, element list+values, dense out
+    return enc, agg, dec
+
+
+def cpu_baseline(w, rows, c):
+    """The CPU oracle, as it stands, on a bounded sample of the same workload:
+    one worker's dense encode (timed), the other workers encoded from COO
+    (untimed), the W-way aggregate and the decode (timed).  The iteration
+    time is W x encode + aggregate + decode."""
+    import oracle
+    g = oracle.Geom(n=w.n, rows=rows, seed=w.hash_seed, c=c)
+    dt = np.int32 if w.vtype == "i32" else np.float64
+    x0 = w.dense(0).astype(dt, copy=False)
+    t0 = time.perf_counter()
+    Y0, B0 = oracle.encode(g, x0)
+    t_enc = time.perf_counter() - t0
+    del x0
+    Ys = np.empty((w.W, g.cells), Y0.dtype)
+    Bs = np.empty((w.W, g.words), np.uint32)
+    Ys[0], Bs[0] = Y0, B0
+    for i in range(1, w.W):
+        Ys[i], Bs[i] = oracle.encode_coo(g, w.idx[i], w.val[i].astype(dt))
+    t0 = time.perf_counter()
+    Ya, Ba = oracle.aggregate(Ys, Bs)
+    t_agg = time.perf_counter() - t0
+    del Ys, Bs
+    t0 = time.perf_counter()
+    _, _, info = oracle.decode(g, Ya, Ba)
+    t_dec = time.perf_counter() - t0
+    t_iter = w.W * t_enc + t_agg + t_dec
+    return dict(value=round(4 * w.n / t_iter / 1e9, 4), unit="GB/s", cores=1, kind="oracle",
+                sample=(f"{w.name}: 1 of {w.W} dense encodes timed ({t_enc:.2f} s, scaled x{w.W}), "
+                        f"aggregate {t_agg:.2f} s, decode {t_dec:.2f} s; single-threaded C"),
+                success=int(info.success), rounds=int(info.rounds))
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py measures one GPU only (the W workers are simulated on it); "
+              f"--gpus {a.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2402_07529_amd as hc
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    t0 = time.perf_counter()
+    w = make_workload(a)
+    n_agg = w.n_agg
+    ratio = a.ratio if a.ratio is not None else hc.GAMMA
+    p = hc.hc_geometry(w.n, n_agg, ratio, a.c, w.hash_seed, w.vtype)
+    cells, words, W = p.cells, p.words, w.W
+    log(f"[bench] workload {w.name} n={w.n} W={W} n_agg={n_agg} rows={p.rows} cells={cells} "
+        f"gen {time.perf_counter() - t0:.1f}s")
+
+    vt = torch.int32 if w.vtype == "i32" else torch.float32
+    x = torch.zeros((W, w.n), dtype=vt, device=dev)
+    for i in range(W):
+        x[i][torch.from_numpy(w.idx[i].astype(np.int64)).to(dev)] = torch.from_numpy(w.val[i]).to(dev)
+    Y = torch.empty((W, cells), dtype=vt, device=dev)
+    B = torch.empty((W, words), dtype=torch.int32, device=dev)
+    Ya = torch.empty(cells, dtype=vt, device=dev)
+    Ba = torch.empty(words, dtype=torch.int32, device=dev)
+    out = torch.empty(w.n, dtype=vt, device=dev)
+    mask = torch.empty(words, dtype=torch.int32, device=dev)
+    info = hc.alloc_info(dev)
+    ws = hc.alloc_workspace(p, n_agg, dev)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        for i in range(W):
+            hc.hc_encode(p, x[i], Y[i], B[i], stream)
+        if ev is not None:
+            ev[1].record(stream)
+        hc.hc_aggregate(p, Y, B, W, Ya, Ba, stream)
+        if ev is not None:
+            ev[2].record(stream)
+        hc.hc_decode(p, Ya, Ba, info, ws, x_out=out, mask=mask, max_support=n_agg, stream=stream)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(a.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for k in range(a.steps):
+        step(evs[k])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    ms = total_ms / a.steps
+    enc_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) / W
+    agg_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    dec_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    inf = hc.read_info(info)
+
+    # correctness of the timed result against the direct sum of the inputs
+    direct = x.sum(dim=0, dtype=torch.int64 if vt == torch.int32 else torch.float64)
+    if vt == torch.int32:
+        direct = ((direct + 2**31) % 2**32 - 2**31).to(torch.int32)
+        exact = bool(torch.equal(out, direct)) if inf.success else False
+    else:
+        exact = bool((out.double() - direct).abs().max().item() <=
+                     1e-5 * direct.abs().max().item()) if inf.success else False
+    del direct
+
+    enc_b, agg_b, dec_b = algorithmic_bytes(w.n, W, cells, inf.n_support)
+    iter_b = W * enc_b + agg_b + dec_b
+    value = 4 * w.n / (ms * 1e-3) / 1e9
+    enc_gbs = enc_b / (enc_ms * 1e-3) / 1e9
+    res = {
+        "metric": METRIC, "value": round(value, 3), "unit": "GB/s", "n_gpus": 1,
+        "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int32" if vt == torch.int32 else "fp32", "data": "synthetic",
+        "config": {"workload": w.name, "n": w.n, "workers": W, "n_agg": n_agg,
+                   "rows": int(p.rows), "c": a.c, "cells": cells, "ratio": round(cells / max(n_agg, 1), 4),
+                   **{k: v for k, v in w.params.items() if k in ("density", "overlap", "rows_per_worker")}},
+        "roofline": {"bound": "hbm", "kernel": "hc_encode (Y clear + dense encode)",
+                     "achieved": round(enc_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(enc_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "bytes_per_launch": enc_b, "avg_launch_ms": round(enc_ms, 4)},
+        "hbm_frac_iteration": round(iter_b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "stages_ms": {"encode_per_worker": round(enc_ms, 4), "aggregate": round(agg_ms, 4),
+                      "decode": round(dec_ms, 4)},
+        "stages_gbs_dense": {"encode": round(4 * w.n / (enc_ms * 1e-3) / 1e9, 1),
+                             "aggregate": round(4 * w.n / (agg_ms * 1e-3) / 1e9, 1),
+                             "decode": round(4 * w.n / (dec_ms * 1e-3) / 1e9, 1)},
+        "decode": {"success": inf.success, "n_support": inf.n_support,
+                   "n_recovered": inf.n_recovered, "rounds": inf.rounds, "status": inf.status,
+                   "equals_direct_sum": exact},
+    }
+    del x, Y, B, ws
+    torch.cuda.empty_cache()
+    if not a.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample ...")
+        res["cpu_baseline"] = cpu_baseline(w, int(p.rows), a.c)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -26,6 +26,8 @@
 //          Elements never peeled get the Count Sketch median estimate from
 //          the residual sketch (Algorithm 1, last recovery step);
 //   emit   dense output, recovered mask and COO from E and the values.
+#include <stdlib.h>
+
 #include <type_traits>
 
 #include "hc_device.h"
@@ -36,6 +38,7 @@ namespace hc {
 namespace {
 
 constexpr int kBlock = 256;
+constexpr int kPeelBlock = 1024;  // lanes per workgroup of the persistent peel kernel
 constexpr uint32_t kNever = 0xffffffffu;
 constexpr unsigned long long kOne = 1ull << 32;  // one incidence in a packed counter
 constexpr uint64_t kChunkBits = (uint64_t)kChunkWords * 32;
@@ -51,7 +54,8 @@ struct Ctrl {
     unsigned int abort;     // barrier timeout
     unsigned int bar_count;
     unsigned int bar_gen;
-    unsigned int pad[5];
+    unsigned int done;      // workgroups finished
+    unsigned int pad[4];
 };
 static_assert(sizeof(Ctrl) == 64, "control block layout");
 
@@ -211,27 +215,57 @@ struct PeelArgs {
     uint32_t rows, c, cmask, log2c, cells;
 };
 
-// Append `cell` to the queue for lanes with pred, one atomic per wave.
-__device__ __forceinline__ void wave_push(bool pred, uint32_t cell, uint32_t round_stamp,
-                                          Ctrl* ctrl, uint32_t* queue, uint32_t* stamp,
-                                          uint32_t cells) {
+// Cells that became pure, staged in LDS by one workgroup and appended to the
+// global queue with one atomic per flush (a single global counter bumped by
+// every wave would serialize the whole grid on one cache line).
+constexpr uint32_t kPushCap = 4 * kPeelBlock;
+
+struct PushBuf {
+    uint32_t count;
+    uint32_t base;
+    uint32_t cell[kPushCap];
+};
+
+__device__ __forceinline__ void lds_push(PushBuf& q, bool pred, uint32_t cell,
+                                         uint32_t round_stamp, uint32_t* stamp) {
     const uint64_t m = __ballot(pred);
     if (m == 0) return;
+    const uint32_t lane = lane_id();
     const uint32_t leader = (uint32_t)__ffsll((unsigned long long)m) - 1u;
-    uint32_t base = 0;
-    if (lane_id() == leader) base = atomicAdd(&ctrl->tail, (unsigned int)__popcll(m));
-    base = __shfl(base, leader);
+    uint32_t off = 0;
+    if (lane == leader) off = atomicAdd(&q.count, (unsigned int)__popcll(m));
+    off = __shfl(off, leader);
     if (pred) {
-        const uint32_t slot = base + lanes_below(m);
-        if (slot < cells) {  // each cell becomes pure at most once, so this always holds
-            queue[slot] = cell;
-            stamp[cell] = round_stamp;
-        }
+        q.cell[off + lanes_below(m)] = cell;
+        stamp[cell] = round_stamp;
     }
 }
 
+// Called by every lane of the workgroup with the same arguments.  Appends the
+// staged cells to the global queue if `force` or if the buffer could not take
+// another `room` pushes.
+__device__ void flush_pushes(PushBuf& q, bool force, uint32_t room, Ctrl* ctrl, uint32_t* queue,
+                             uint32_t cells) {
+    __syncthreads();
+    const uint32_t n = q.count;
+    __syncthreads();  // every lane has read n before any lane pushes again
+    if (n == 0 || (!force && n + room <= kPushCap)) return;
+    if (threadIdx.x == 0) q.base = atomicAdd(&ctrl->tail, n);
+    __syncthreads();
+    const uint32_t base = q.base;
+    for (uint32_t k = threadIdx.x; k < n; k += blockDim.x)
+        if (base + k < cells) queue[base + k] = q.cell[k];  // a cell is pushed at most once
+    __syncthreads();
+    if (threadIdx.x == 0) q.count = 0;
+    __syncthreads();
+}
+
 // Grid-wide barrier.  The last block to arrive publishes the end of the next
-// frontier.  Returns false if the wait timed out (then ctrl->abort is set).
+// frontier.  Each block makes its writes visible with one release fence
+// before arriving and picks up everyone else's with one acquire fence after
+// the wait; the wait itself polls with relaxed loads, so spinning blocks do
+// not keep invalidating their caches.  Returns false if the wait timed out
+// (then ctrl->abort is set).
 __device__ bool grid_barrier(Ctrl* ctrl, uint32_t nblocks) {
     __shared__ uint32_t s_ok;
     __syncthreads();
@@ -239,9 +273,11 @@ __device__ bool grid_barrier(Ctrl* ctrl, uint32_t nblocks) {
         uint32_t ok = 1;
         const uint32_t gen =
             __hip_atomic_load(&ctrl->bar_gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const uint32_t arrived = __hip_atomic_fetch_add(&ctrl->bar_count, 1u, __ATOMIC_ACQ_REL,
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        const uint32_t arrived = __hip_atomic_fetch_add(&ctrl->bar_count, 1u, __ATOMIC_RELAXED,
                                                         __HIP_MEMORY_SCOPE_AGENT);
         if (arrived == nblocks - 1u) {
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             const uint32_t t =
                 __hip_atomic_load(&ctrl->tail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_store(&ctrl->fend, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -250,9 +286,9 @@ __device__ bool grid_barrier(Ctrl* ctrl, uint32_t nblocks) {
                                __HIP_MEMORY_SCOPE_AGENT);
         } else {
             const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-            while (__hip_atomic_load(&ctrl->bar_gen, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) ==
+            while (__hip_atomic_load(&ctrl->bar_gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
                    gen) {
-                __builtin_amdgcn_s_sleep(1);
+                __builtin_amdgcn_s_sleep(2);
                 if (__builtin_amdgcn_s_memrealtime() - t0 > kBarrierTimeoutTicks) {
                     __hip_atomic_store(&ctrl->abort, 1u, __ATOMIC_RELAXED,
                                        __HIP_MEMORY_SCOPE_AGENT);
@@ -261,6 +297,7 @@ __device__ bool grid_barrier(Ctrl* ctrl, uint32_t nblocks) {
                 }
             }
         }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         if (__hip_atomic_load(&ctrl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) ok = 0;
         s_ok = ok;
     }
@@ -269,25 +306,38 @@ __device__ bool grid_barrier(Ctrl* ctrl, uint32_t nblocks) {
 }
 
 template <typename T>
-__global__ __launch_bounds__(kBlock) void peel_kernel(PeelArgs<T> a) {
+__global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
+    __shared__ PushBuf q;
+    __shared__ uint32_t s_red[2];
     Ctrl* ctrl = a.ctrl;
     const uint32_t lane = lane_id();
-    const uint32_t waves_per_block = kBlock / 64;
-    const uint32_t gwave = blockIdx.x * waves_per_block + (threadIdx.x >> 6);
+    const uint32_t waves_per_block = kPeelBlock / 64;
+    // wave-sized chunks of work go round-robin over the workgroups, so small
+    // frontiers still spread over every CU
+    const uint32_t gwave = (threadIdx.x >> 6) * gridDim.x + blockIdx.x;
     const uint32_t nwaves = gridDim.x * waves_per_block;
-    const uint32_t nthreads = gridDim.x * kBlock;
-    const uint32_t gtid = blockIdx.x * kBlock + threadIdx.x;
+    const uint32_t nthreads = gridDim.x * kPeelBlock;
+    const uint32_t gtid = gwave * 64u + lane;
     const bool overflow = ctrl->overflow != 0;
     bool ok = true;
+    uint32_t my_recovered = 0, my_last_round = 0;
+    if (threadIdx.x == 0) {
+        q.count = 0;
+        s_red[0] = 0;
+        s_red[1] = 0;
+    }
+    __syncthreads();
 
     if (!overflow) {
         // round-0 frontier: every cell with exactly one element
-        for (uint32_t i0 = gwave * 64u; i0 < a.cells; i0 += nwaves * 64u) {
-            const uint32_t cidx = i0 + lane;
+        for (uint32_t base = 0; base < a.cells; base += nthreads) {
+            const uint32_t cidx = base + gtid;
             bool pure = false;
             if (cidx < a.cells) pure = (a.cnt[cidx] >> 32) == 1ull;
-            wave_push(pure, cidx, 0u, ctrl, a.queue, a.stamp, a.cells);
+            lds_push(q, pure, cidx, 0u, a.stamp);
+            flush_pushes(q, false, kPeelBlock, ctrl, a.queue, a.cells);
         }
+        flush_pushes(q, true, 0, ctrl, a.queue, a.cells);
         ok = grid_barrier(ctrl, gridDim.x);
 
         const uint32_t nsup = (uint32_t)ctrl->n_support;
@@ -297,9 +347,10 @@ __global__ __launch_bounds__(kBlock) void peel_kernel(PeelArgs<T> a) {
                 __hip_atomic_load(&ctrl->fend, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (qe > a.cells) qe = a.cells;  // the queue holds each cell at most once
             if (qe <= qs) break;
-            for (uint32_t i0 = qs + gwave * 64u; i0 < qe; i0 += nwaves * 64u) {
-                const uint32_t i = i0 + lane;
-                bool claimed = false, push_a = false, push_b = false;
+            const uint32_t nsweep = (qe - qs + nwaves * 64u - 1u) / (nwaves * 64u);
+            for (uint32_t sw = 0; sw < nsweep; sw++) {
+                const uint32_t i = qs + (sw * nwaves + gwave) * 64u + lane;
+                bool push_a = false, push_b = false;
                 uint32_t cell_a = 0, cell_b = 0;
                 if (i < qe) {
                     const uint32_t cidx = a.queue[i];
@@ -322,7 +373,8 @@ __global__ __launch_bounds__(kBlock) void peel_kernel(PeelArgs<T> a) {
                             const T val = Val<T>::sign(a.yw[cidx], (h.neg >> j) & 1u);
                             a.vals[pos] = val;
                             a.peeled[pos] = 1;
-                            claimed = true;
+                            my_recovered++;
+                            my_last_round = r + 1u;
                             const int ja = j == 0 ? 1 : 0;
                             const int jb = j == 2 ? 1 : 2;
                             const unsigned long long dec = 0ull - (kOne + pos);
@@ -339,14 +391,11 @@ __global__ __launch_bounds__(kBlock) void peel_kernel(PeelArgs<T> a) {
                         }
                     }
                 }
-                const uint64_t mc = __ballot(claimed);
-                if (mc != 0 && lane == (uint32_t)__ffsll((unsigned long long)mc) - 1u) {
-                    atomicAdd(&ctrl->recovered, (unsigned long long)__popcll(mc));
-                    atomicMax(&ctrl->rounds, r + 1u);
-                }
-                wave_push(push_a, cell_a, r + 1u, ctrl, a.queue, a.stamp, a.cells);
-                wave_push(push_b, cell_b, r + 1u, ctrl, a.queue, a.stamp, a.cells);
+                lds_push(q, push_a, cell_a, r + 1u, a.stamp);
+                lds_push(q, push_b, cell_b, r + 1u, a.stamp);
+                flush_pushes(q, false, 2u * kPeelBlock, ctrl, a.queue, a.cells);
             }
+            flush_pushes(q, true, 0, ctrl, a.queue, a.cells);
             qs = qe;
             ok = grid_barrier(ctrl, gridDim.x);
         }
@@ -367,14 +416,36 @@ __global__ __launch_bounds__(kBlock) void peel_kernel(PeelArgs<T> a) {
         }
     }
 
-    if (gtid == 0) {
-        const unsigned long long ns = ctrl->n_support;
-        const unsigned long long rec = overflow ? 0ull : ctrl->recovered;
-        a.info->n_support = ns;
-        a.info->n_recovered = rec;
-        a.info->rounds = overflow ? 0ull : ctrl->rounds;
-        a.info->success = (!overflow && ok && rec == ns) ? 1u : 0u;
-        a.info->status = overflow ? 1u : (ok ? 0u : 2u);
+    // per-workgroup totals, one atomic each; the last workgroup to finish
+    // writes the summary
+    my_recovered = wave_sum(my_recovered);
+    uint32_t wmax = my_last_round;
+    for (int d = 32; d >= 1; d >>= 1) wmax = max(wmax, (uint32_t)__shfl_xor(wmax, d));
+    if (lane == 0) {
+        atomicAdd(&s_red[0], my_recovered);
+        atomicMax(&s_red[1], wmax);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        if (s_red[0]) atomicAdd(&ctrl->recovered, (unsigned long long)s_red[0]);
+        if (s_red[1]) atomicMax(&ctrl->rounds, s_red[1]);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        const uint32_t done = __hip_atomic_fetch_add(&ctrl->done, 1u, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+        if (done == gridDim.x - 1u) {
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            const bool aborted = __hip_atomic_load(&ctrl->abort, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT) != 0;
+            const unsigned long long ns = ctrl->n_support;
+            const unsigned long long rec = overflow ? 0ull :
+                __hip_atomic_load(&ctrl->recovered, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            a.info->n_support = ns;
+            a.info->n_recovered = rec;
+            a.info->rounds = overflow ? 0ull :
+                __hip_atomic_load(&ctrl->rounds, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            a.info->success = (!overflow && !aborted && rec == ns) ? 1u : 0u;
+            a.info->status = overflow ? 1u : (aborted ? 2u : 0u);
+        }
     }
 }
 
@@ -534,11 +605,16 @@ hipError_t launch_decode_t(const Geo& g, const void* y_agg_v, const uint32_t* b,
     if (peel_grid_cache[slot] == 0) {
         int per_cu = 0;
         e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per_cu, reinterpret_cast<const void*>(&peel_kernel<T>), kBlock, 0);
+            &per_cu, reinterpret_cast<const void*>(&peel_kernel<T>), kPeelBlock, 0);
         if (e != hipSuccess) return e;
         if (per_cu < 1) return hipErrorInvalidConfiguration;
-        if (per_cu > 2) per_cu = 2;
-        peel_grid_cache[slot] = per_cu * di.cus;
+        // one resident workgroup per CU: enough lanes for the largest
+        // frontiers while keeping the barrier's arrival count low
+        int want = 1;
+        if (const char* env = getenv("HC_PEEL_BLOCKS_PER_CU")) want = atoi(env);
+        if (want < 1) want = 1;
+        if (want > per_cu) want = per_cu;
+        peel_grid_cache[slot] = want * di.cus;
     }
     PeelArgs<T> pa;
     pa.ctrl = ctrl;
@@ -558,8 +634,8 @@ hipError_t launch_decode_t(const Geo& g, const void* y_agg_v, const uint32_t* b,
     pa.cells = g.cells;
     void* args[] = {&pa};
     e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&peel_kernel<T>),
-                                   dim3((uint32_t)peel_grid_cache[slot]), dim3(kBlock), args, 0,
-                                   s);
+                                   dim3((uint32_t)peel_grid_cache[slot]), dim3(kPeelBlock), args,
+                                   0, s);
     if (e != hipSuccess) return e;
 
     if (out.x_out != nullptr || out.mask != nullptr || out.coo_idx != nullptr) {

@@ -1,15 +1,14 @@
 // hc_encode.hip -- worker-side compression (Algorithm 1, phase I) for gfx950.
 //
-// Dense path.  A workgroup of 256 lanes takes tiles of 1024 consecutive
-// parameters; each lane loads four with one 16-byte nontemporal load (the
-// gradient is read once, so it should not evict the sketch from L2/MALL).
-// Per wave (256 parameters):
-//   - four ballots of "x != 0" become the eight bitmap words of the wave
-//     (section 3.2), written by lanes 0..7;
+// Dense path.  Each wave takes tiles of 1024 consecutive parameters, read as
+// four coalesced 16-byte nontemporal loads per lane (the gradient is read
+// once, so it should not evict the sketch from L2/MALL).  Per tile:
+//   - sixteen ballots of "x != 0" become the tile's 32 bitmap words (section
+//     3.2), one full 128-byte line written by a single store;
 //   - every nonzero adds g_j * x to its three cells (section 3.1) with
 //     fire-and-forget global atomics.  Within one batch the cells of a hash
 //     are one sketch row rotated by a bias (section 3.4), so the atomics of a
-//     wave land in at most three 4 KiB rows.
+//     load land in at most three 4 KiB rows.
 // The batch hash is wave-uniform when c >= 256 (computed on the scalar unit
 // once per wave and tile), per lane when 4 <= c < 256, per element below.
 #include "hc_device.h"
@@ -20,7 +19,7 @@ namespace hc {
 namespace {
 
 constexpr int kBlock = 256;
-constexpr uint64_t kTile = 1024;  // parameters per workgroup and iteration
+constexpr uint64_t kTile = 1024;  // parameters per wave tile
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
@@ -47,7 +46,101 @@ __global__ __launch_bounds__(kBlock) void fill_u32_kernel(uint32_t* __restrict__
     if (blockIdx.x == 0 && threadIdx.x < count - nvec * 4) p[nvec * 4 + threadIdx.x] = value;
 }
 
-// MODE 0: c >= 256, MODE 1: 4 <= c < 256, MODE 2: c < 4.
+// Sketch updates for the parameters of one load: e[k] is parameter p0 + k of
+// this lane, p0 = lbase + 4 * lane, lbase the load's first parameter.
+template <typename T, int MODE>
+__device__ __forceinline__ void scatter_load(const T (&e)[4], const bool (&nz)[4], uint64_t lbase,
+                                             uint64_t p0, T* __restrict__ y, uint64_t seed,
+                                             uint32_t rows, uint32_t c, uint32_t cmask,
+                                             uint32_t log2c) {
+    if (MODE == 0) {
+        const BatchHash h = batch_hash(seed, rows, cmask, uniform64(lbase >> log2c));
+        if (nz[0] | nz[1] | nz[2] | nz[3]) {
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                if (!nz[k]) continue;
+                const uint32_t t = (uint32_t)(p0 + k) & cmask;
+#pragma unroll
+                for (int j = 0; j < 3; j++)
+                    Val<T>::atomic_add(y + cell_of(h, j, t, c, cmask),
+                                       Val<T>::sign(e[k], (h.neg >> j) & 1u));
+            }
+        }
+    } else if (MODE == 1) {
+        if (nz[0] | nz[1] | nz[2] | nz[3]) {
+            const BatchHash h = batch_hash(seed, rows, cmask, p0 >> log2c);
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                if (!nz[k]) continue;
+                const uint32_t t = (uint32_t)(p0 + k) & cmask;
+#pragma unroll
+                for (int j = 0; j < 3; j++)
+                    Val<T>::atomic_add(y + cell_of(h, j, t, c, cmask),
+                                       Val<T>::sign(e[k], (h.neg >> j) & 1u));
+            }
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            if (!nz[k]) continue;
+            const uint64_t p = p0 + k;
+            const BatchHash h = batch_hash(seed, rows, cmask, p >> log2c);
+            const uint32_t t = (uint32_t)p & cmask;
+#pragma unroll
+            for (int j = 0; j < 3; j++)
+                Val<T>::atomic_add(y + cell_of(h, j, t, c, cmask),
+                                   Val<T>::sign(e[k], (h.neg >> j) & 1u));
+        }
+    }
+}
+
+// One wave tile: 1024 consecutive parameters from `tbase` (a multiple of
+// 1024), four loads of 256 per wave, e[l][k] = parameter tbase + 256 l +
+// 4 lane + k.  Its 32 bitmap words form one 128-byte line, built from the 16
+// ballots and written by lanes 0..31 with a single store.
+template <typename T, int MODE>
+__device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, uint32_t lane,
+                                            T* __restrict__ y, uint32_t* __restrict__ b,
+                                            uint64_t words, uint64_t seed, uint32_t rows,
+                                            uint32_t c, uint32_t cmask, uint32_t log2c) {
+    bool nz[4][4];
+    uint64_t m[4][4];
+#pragma unroll
+    for (int l = 0; l < 4; l++)
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            nz[l][k] = Val<T>::nonzero(e[l][k]);
+            m[l][k] = __ballot(nz[l][k]);
+        }
+    // word w = 8 l + i holds parameters 32 w .. 32 w + 31: lanes 8i..8i+7 of
+    // load l, parameter 4 lane' + k at bit 4 (lane' - 8 i) + k
+    if (lane < 32) {
+        const uint32_t l = lane >> 3, sh = 8u * (lane & 7u);
+        uint32_t word = 0;
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            const uint64_t mk = l == 0 ? m[0][k] : l == 1 ? m[1][k] : l == 2 ? m[2][k] : m[3][k];
+            word |= spread4((uint32_t)(mk >> sh)) << k;
+        }
+        const uint64_t widx = (tbase >> 5) + lane;
+        if (widx < words) b[widx] = word;
+    }
+#pragma unroll
+    for (int l = 0; l < 4; l++) {
+        if ((m[l][0] | m[l][1] | m[l][2] | m[l][3]) == 0) continue;
+        const uint64_t lbase = tbase + 256ull * l;
+        scatter_load<T, MODE>(e[l], nz[l], lbase, lbase + 4ull * lane, y, seed, rows, c, cmask,
+                              log2c);
+    }
+}
+
+// MODE 0: c >= 256 (the batch is uniform over a load: hash on the scalar
+// unit), MODE 1: 4 <= c < 256 (per lane), MODE 2: c < 4 (per parameter).
+// Each wave takes its own tiles; the main loop takes them two at a time when
+// both lie wholly inside the gradient, so every lane keeps eight 16-byte
+// nontemporal loads in flight.  The tail takes single tiles with
+// bounds-checked 4-byte loads (also used throughout when x is not 16-byte
+// aligned).
 template <typename T, int MODE>
 __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
     const T* __restrict__ x, T* __restrict__ y, uint32_t* __restrict__ b, uint64_t n,
@@ -55,77 +148,41 @@ __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
     bool vec) {
     typedef typename Vec4<T>::type V;
     const uint32_t lane = lane_id();
-    const uint32_t wave = uniform(threadIdx.x >> 6);
+    const uint64_t gwave = (uint64_t)blockIdx.x * (kBlock / 64) + uniform(threadIdx.x >> 6);
+    const uint64_t nwaves = (uint64_t)gridDim.x * (kBlock / 64);
     const uint64_t ntiles = (n + kTile - 1) / kTile;
+    const uint64_t npairs = vec ? n / (2 * kTile) : 0;
 
-    for (uint64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-        const uint64_t base = tile * kTile + (uint64_t)wave * 256;  // wave's first parameter
-        const uint64_t p0 = base + 4ull * lane;                      // lane's first parameter
-        T e[4];
-        if (vec && tile * kTile + kTile <= n) {
-            const V v = __builtin_nontemporal_load(reinterpret_cast<const V*>(x + p0));
-            e[0] = v.x; e[1] = v.y; e[2] = v.z; e[3] = v.w;
-        } else {
+    for (uint64_t q = gwave; q < npairs; q += nwaves) {
+        const V* src = reinterpret_cast<const V*>(x + q * (2 * kTile)) + lane;
+        V v[8];
 #pragma unroll
-            for (int k = 0; k < 4; k++) e[k] = (p0 + k < n) ? x[p0 + k] : T(0);
-        }
-        bool nz[4];
+        for (int u = 0; u < 8; u++) v[u] = __builtin_nontemporal_load(src + u * 64);
 #pragma unroll
-        for (int k = 0; k < 4; k++) nz[k] = Val<T>::nonzero(e[k]);
-
-        // bitmap: element 4l+k of the wave is bit l of ballot k
-        const uint64_t m0 = __ballot(nz[0]), m1 = __ballot(nz[1]);
-        const uint64_t m2 = __ballot(nz[2]), m3 = __ballot(nz[3]);
-        if (base < n && lane < 8) {
-            const uint32_t sh = 8u * lane;
-            const uint32_t word = spread4((uint32_t)(m0 >> sh)) |
-                                  (spread4((uint32_t)(m1 >> sh)) << 1) |
-                                  (spread4((uint32_t)(m2 >> sh)) << 2) |
-                                  (spread4((uint32_t)(m3 >> sh)) << 3);
-            const uint64_t widx = (base >> 5) + lane;
-            if (widx < words) b[widx] = word;
-        }
-        if ((m0 | m1 | m2 | m3) == 0) continue;
-
-        if (MODE == 0) {
-            const BatchHash h = batch_hash(seed, rows, cmask, uniform64(base >> log2c));
-            if (nz[0] | nz[1] | nz[2] | nz[3]) {
+        for (int h = 0; h < 2; h++) {
+            T e[4][4];
 #pragma unroll
-                for (int k = 0; k < 4; k++) {
-                    if (!nz[k]) continue;
-                    const uint32_t t = (uint32_t)(p0 + k) & cmask;
-#pragma unroll
-                    for (int j = 0; j < 3; j++)
-                        Val<T>::atomic_add(y + cell_of(h, j, t, c, cmask),
-                                           Val<T>::sign(e[k], (h.neg >> j) & 1u));
-                }
+            for (int l = 0; l < 4; l++) {
+                e[l][0] = v[4 * h + l].x;
+                e[l][1] = v[4 * h + l].y;
+                e[l][2] = v[4 * h + l].z;
+                e[l][3] = v[4 * h + l].w;
             }
-        } else if (MODE == 1) {
-            if (nz[0] | nz[1] | nz[2] | nz[3]) {
-                const BatchHash h = batch_hash(seed, rows, cmask, p0 >> log2c);
+            encode_tile<T, MODE>(e, (2 * q + h) * kTile, lane, y, b, words, seed, rows, c, cmask,
+                                 log2c);
+        }
+    }
+    for (uint64_t tile = 2 * npairs + gwave; tile < ntiles; tile += nwaves) {
+        const uint64_t tbase = tile * kTile;
+        T e[4][4];
 #pragma unroll
-                for (int k = 0; k < 4; k++) {
-                    if (!nz[k]) continue;
-                    const uint32_t t = (uint32_t)(p0 + k) & cmask;
-#pragma unroll
-                    for (int j = 0; j < 3; j++)
-                        Val<T>::atomic_add(y + cell_of(h, j, t, c, cmask),
-                                           Val<T>::sign(e[k], (h.neg >> j) & 1u));
-                }
-            }
-        } else {
+        for (int l = 0; l < 4; l++)
 #pragma unroll
             for (int k = 0; k < 4; k++) {
-                if (!nz[k]) continue;
-                const uint64_t p = p0 + k;
-                const BatchHash h = batch_hash(seed, rows, cmask, p >> log2c);
-                const uint32_t t = (uint32_t)p & cmask;
-#pragma unroll
-                for (int j = 0; j < 3; j++)
-                    Val<T>::atomic_add(y + cell_of(h, j, t, c, cmask),
-                                       Val<T>::sign(e[k], (h.neg >> j) & 1u));
+                const uint64_t p = tbase + 256ull * l + 4ull * lane + k;
+                e[l][k] = p < n ? x[p] : T(0);
             }
-        }
+        encode_tile<T, MODE>(e, tbase, lane, y, b, words, seed, rows, c, cmask, log2c);
     }
 }
 
@@ -185,7 +242,8 @@ hipError_t launch_encode_dense(const Geo& g, const void* x, void* y, uint32_t* b
     if (e != hipSuccess) return e;
     e = launch_fill_u32(static_cast<uint32_t*>(y), g.cells, 0u, s);
     if (e != hipSuccess) return e;
-    const uint32_t grid = grid_for((g.n + kTile - 1) / kTile, 1, (uint32_t)di.cus * 8);
+    const uint64_t ntiles = (g.n + kTile - 1) / kTile;
+    const uint32_t grid = grid_for(ntiles, 2 * (kBlock / 64), (uint32_t)di.cus * 8);
     const int mode = g.c >= 256 ? 0 : (g.c >= 4 ? 1 : 2);
     if (g.f32) {
         if (mode == 0) return launch_dense_t<float, 0>(g, x, y, b, s, grid);
