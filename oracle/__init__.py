@@ -13,6 +13,9 @@ Paper passages each entry point follows:
   decode     Algorithm 1 phase II: synchronous peeling (section 3.2) and the
              Count Sketch median estimate for what cannot be peeled (3.1)
   rows_for   sketch size at least gamma * n with gamma = 1.23 (section 3.2)
+  decode_bound  how far floating-point rounding of the sketch can move each
+             decoded value (the imprecision section 4.1 concedes), carried
+             through the decode's schedule; used to set fp32 tolerances
 """
 from __future__ import annotations
 
@@ -100,6 +103,8 @@ def lib():
         for name in ("hco_decode_i32", "hco_decode_f64"):
             getattr(L, name).argtypes = [G, P, P, P, P, ctypes.POINTER(_Info), P]
             getattr(L, name).restype = ctypes.c_int
+        L.hco_decode_bound_f64.argtypes = [G, P, P, P]
+        L.hco_decode_bound_f64.restype = ctypes.c_int
         L.hco_decode_queue_i32.argtypes = [G, P, P, P, P, ctypes.POINTER(_Info)]
         L.hco_decode_queue_i32.restype = ctypes.c_int
         L.hco_query_i32.argtypes = [G, P, ctypes.c_uint64]
@@ -232,6 +237,17 @@ def decode(g: Geom, Y: np.ndarray, B: np.ndarray, want_rounds: bool = False):
         raise ValueError("oracle decode: invalid geometry or out of memory")
     inf = Info(info.n_support, info.n_recovered, info.rounds, info.success)
     return (x, mask, inf, rof) if want_rounds else (x, mask, inf)
+
+
+def decode_bound(g: Geom, dY: np.ndarray, B: np.ndarray) -> np.ndarray:
+    """Per-parameter bound on the decoded value's error given per-cell bounds
+    dY on the sketch's error, carried through the decode's own schedule."""
+    dY = np.ascontiguousarray(dY, np.float64)
+    B = np.ascontiguousarray(B, np.uint32)
+    out = np.zeros(g.n, np.float64)
+    if lib().hco_decode_bound_f64(ctypes.byref(g._c()), _ptr(dY), _ptr(B), _ptr(out)) != 0:
+        raise ValueError("oracle decode_bound: invalid geometry or out of memory")
+    return out
 
 
 def decode_queue(g: Geom, Y: np.ndarray, B: np.ndarray):

@@ -491,6 +491,72 @@ int hco_decode_f64(const hco_geom *g, const double *Y, const uint32_t *B,
     return 0;
 }
 
+/* Error bound carried through the schedule of hco_decode_f64 (see hco.h).
+ * The schedule (which cells are pure in which round) depends only on B and
+ * the hashes, so this repeats it with absolute-value accumulation in place
+ * of subtraction. */
+int hco_decode_bound_f64(const hco_geom *g, const double *dY, const uint32_t *B,
+                         double *bound)
+{
+    if (hco_check_geom(g)) return -1;
+    const uint64_t C = n_cells(g);
+    uint64_t *ps, *cell;
+    int32_t *sign;
+    const uint64_t m = support_of(g, B, &ps, &cell, &sign);
+    if (m == UINT64_MAX) return -1;
+
+    double *Eb = (double *)malloc(C * sizeof(double));    /* accumulated cell error */
+    uint32_t *bits = (uint32_t *)malloc(n_words(g) * sizeof(uint32_t));
+    uint32_t *deg = (uint32_t *)malloc(C * sizeof(uint32_t));
+    double *eb = (double *)malloc((m ? m : 1) * sizeof(double));
+    int8_t *pick = (int8_t *)malloc(m ? m : 1);
+    if (!Eb || !bits || !deg || !eb || !pick) {
+        free(Eb); free(bits); free(deg); free(eb); free(pick);
+        free(ps); free(cell); free(sign);
+        return -1;
+    }
+    for (uint64_t i = 0; i < C; i++) Eb[i] = dY[i] < 0 ? -dY[i] : dY[i];
+    memcpy(bits, B, n_words(g) * sizeof(uint32_t));
+    for (uint64_t p = 0; p < g->n; p++) bound[p] = 0.0;
+
+    for (;;) {
+        memset(deg, 0, C * sizeof(uint32_t));
+        for (uint64_t i = 0; i < m; i++)
+            if (get_bit(bits, ps[i]))
+                for (int j = 0; j < 3; j++) deg[cell[3 * i + j]]++;
+        uint64_t peeled = 0;
+        for (uint64_t i = 0; i < m; i++) {
+            pick[i] = -1;
+            if (!get_bit(bits, ps[i])) continue;
+            for (int j = 0; j < 3; j++) {
+                if (deg[cell[3 * i + j]] == 1) {
+                    pick[i] = (int8_t)j;
+                    eb[i] = Eb[cell[3 * i + j]];
+                    peeled++;
+                    break;
+                }
+            }
+        }
+        if (peeled == 0) break;
+        for (uint64_t i = 0; i < m; i++) {
+            if (pick[i] < 0) continue;
+            bits[ps[i] >> 5] &= ~(1u << (ps[i] & 31));
+            for (int j = 0; j < 3; j++) Eb[cell[3 * i + j]] += eb[i];
+            bound[ps[i]] = eb[i];
+        }
+    }
+    for (uint64_t i = 0; i < m; i++) {
+        if (!get_bit(bits, ps[i])) continue;
+        double b = 0.0;
+        for (int j = 0; j < 3; j++)
+            if (Eb[cell[3 * i + j]] > b) b = Eb[cell[3 * i + j]];
+        bound[ps[i]] = b;
+    }
+    free(Eb); free(bits); free(deg); free(eb); free(pick);
+    free(ps); free(cell); free(sign);
+    return 0;
+}
+
 /* Sequential peeling, one parameter at a time, driven by a FIFO queue of cells
  * that exactly one live parameter maps to (the classic peeling the parallel
  * version speeds up).  Written independently of hco_decode_i32 so the two can

@@ -100,6 +100,17 @@ int hco_decode_f64(const hco_geom *g, const double *Y, const uint32_t *B,
                    double *x_out, uint32_t *mask, hco_info *info,
                    uint32_t *round_of);
 
+/* Worst-case error propagation through the same synchronous schedule as
+ * hco_decode_f64: given per-cell bounds dY[c] >= |error of Y[c]|, writes
+ * bound[p] >= |error of the decoded x_p| for every p of the support (0 for
+ * p outside it), valid for any rounding that stays within dY.  Peeling is
+ * linear in Y for a fixed schedule: x = g_j * (Y[c] - sum of g' x' over the
+ * earlier-peeled members of c), so |dx| <= dY[c] + sum of |dx'|; a leftover
+ * estimate is a median, which moves by at most the largest of its three
+ * cells' errors.  Returns 0 or -1. */
+int hco_decode_bound_f64(const hco_geom *g, const double *dY, const uint32_t *B,
+                         double *bound);
+
 /* Independent cross-check: one-at-a-time peeling from a FIFO queue of pure
  * cells.  Same outputs as hco_decode_i32 except that info->rounds is 0. */
 int hco_decode_queue_i32(const hco_geom *g, const int32_t *Y, const uint32_t *B,

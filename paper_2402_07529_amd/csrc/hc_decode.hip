@@ -96,7 +96,7 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
 
 template <typename T>
 __global__ __launch_bounds__(kBlock) void prep_kernel(const T* __restrict__ y_agg,
-                                                      T* __restrict__ yw,
+                                                      typename Acc<T>::type* __restrict__ yw,
                                                       unsigned long long* __restrict__ cnt,
                                                       uint32_t* __restrict__ stamp,
                                                       uint32_t cells, Ctrl* __restrict__ ctrl) {
@@ -104,7 +104,7 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(const T* __restrict__ y_ag
         reinterpret_cast<uint32_t*>(ctrl)[threadIdx.x] = 0u;
     const uint64_t step = (uint64_t)gridDim.x * kBlock;
     for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < cells; i += step) {
-        yw[i] = y_agg[i];
+        yw[i] = (typename Acc<T>::type)y_agg[i];
         cnt[i] = 0ull;
         stamp[i] = kNever;
     }
@@ -201,7 +201,7 @@ __global__ __launch_bounds__(kBlock) void build_kernel(
 }
 
 template <typename T>
-struct PeelArgs {
+struct PeelArgs {  // T: the decode-side arithmetic type
     Ctrl* ctrl;
     const uint32_t* elem;
     T* vals;
@@ -450,11 +450,11 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
 }
 
 template <typename T>
-struct EmitArgs {
+struct EmitArgs {  // T: the gradient type; values are kept in Acc<T>
     const uint32_t* b;
     const uint32_t* blk;
     const uint32_t* elem;
-    const T* vals;
+    const typename Acc<T>::type* vals;
     const uint8_t* peeled;
     const T* y_agg;
     const Ctrl* ctrl;
@@ -476,7 +476,7 @@ __device__ __forceinline__ T estimate_raw(const EmitArgs<T>& a, uint32_t p) {
 #pragma unroll
     for (int j = 0; j < 3; j++)
         e3[j] = Val<T>::sign(a.y_agg[cell_of(h, j, t, a.c, a.cmask)], (h.neg >> j) & 1u);
-    return median3(e3[0], e3[1], e3[2]);
+    return median3(e3[0], e3[1], e3[2]);  // exact in T: a median selects, it does not round
 }
 
 // One workgroup per chunk of 1024 bitmap words (32768 parameters).
@@ -524,7 +524,7 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
             if ((word >> (sh + k)) & 1u) {
                 const uint32_t p = (uint32_t)(p0 + k);
                 if (!overflow) {
-                    out[k] = a.vals[rank];
+                    out[k] = (T)a.vals[rank];
                     rec[k] = a.peeled[rank] != 0;
                 } else {
                     out[k] = estimate_raw(a, p);
@@ -571,10 +571,11 @@ hipError_t launch_decode_t(const Geo& g, const void* y_agg_v, const uint32_t* b,
     Ctrl* ctrl = reinterpret_cast<Ctrl*>(base + L.ctrl);
     uint32_t* blk = reinterpret_cast<uint32_t*>(base + L.blk);
     uint32_t* elem = reinterpret_cast<uint32_t*>(base + L.elem);
-    T* vals = reinterpret_cast<T*>(base + L.vals);
+    typedef typename Acc<T>::type A;
+    A* vals = reinterpret_cast<A*>(base + L.vals);
     uint8_t* peeled = reinterpret_cast<uint8_t*>(base + L.peeled);
     unsigned long long* cnt = reinterpret_cast<unsigned long long*>(base + L.cnt);
-    T* yw = reinterpret_cast<T*>(base + L.yw);
+    A* yw = reinterpret_cast<A*>(base + L.yw);
     uint32_t* stamp = reinterpret_cast<uint32_t*>(base + L.stamp);
     uint32_t* queue = reinterpret_cast<uint32_t*>(base + L.queue);
     const T* y_agg = static_cast<const T*>(y_agg_v);
@@ -601,11 +602,11 @@ hipError_t launch_decode_t(const Geo& g, const void* y_agg_v, const uint32_t* b,
     // persistent peel: every workgroup must be resident (cooperative launch)
     int dev = 0;
     if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
-    const int slot = (dev & 31) * 2 + (std::is_same<T, float>::value ? 1 : 0);
+    const int slot = (dev & 31) * 2 + (std::is_same<T, float>::value ? 1 : 0);  // per device and type
     if (peel_grid_cache[slot] == 0) {
         int per_cu = 0;
         e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per_cu, reinterpret_cast<const void*>(&peel_kernel<T>), kPeelBlock, 0);
+            &per_cu, reinterpret_cast<const void*>(&peel_kernel<A>), kPeelBlock, 0);
         if (e != hipSuccess) return e;
         if (per_cu < 1) return hipErrorInvalidConfiguration;
         // one resident workgroup per CU: enough lanes for the largest
@@ -616,7 +617,7 @@ hipError_t launch_decode_t(const Geo& g, const void* y_agg_v, const uint32_t* b,
         if (want > per_cu) want = per_cu;
         peel_grid_cache[slot] = want * di.cus;
     }
-    PeelArgs<T> pa;
+    PeelArgs<A> pa;
     pa.ctrl = ctrl;
     pa.elem = elem;
     pa.vals = vals;
@@ -633,7 +634,7 @@ hipError_t launch_decode_t(const Geo& g, const void* y_agg_v, const uint32_t* b,
     pa.log2c = g.log2c;
     pa.cells = g.cells;
     void* args[] = {&pa};
-    e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&peel_kernel<T>),
+    e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&peel_kernel<A>),
                                    dim3((uint32_t)peel_grid_cache[slot]), dim3(kPeelBlock), args,
                                    0, s);
     if (e != hipSuccess) return e;
@@ -679,7 +680,7 @@ DecodeLayout decode_layout(const Geo& g, uint64_t max_support) {
     if (cap > 0x7fffffffull) cap = 0x7fffffffull;  // packed counters need |S| < 2^31
     L.cap = cap;
     L.nchunks = (g.words + kChunkWords - 1) / kChunkWords;
-    const size_t vsz = 4;  // int32 or fp32
+    const size_t vsz = g.f32 ? 8 : 4;  // decode-side values: int32, or fp64 for fp32
     size_t o = 0;
     L.ctrl = o;    o = align256(o + sizeof(Ctrl));
     L.blk = o;     o = align256(o + L.nchunks * 4);

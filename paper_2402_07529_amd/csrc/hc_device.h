@@ -88,6 +88,18 @@ template <> struct Val<float> {
     __device__ __forceinline__ static bool nonzero(float v) { return v != 0.0f; }
 };
 
+template <> struct Val<double> {
+    __device__ __forceinline__ static double sign(double v, bool neg) { return neg ? -v : v; }
+    __device__ __forceinline__ static void atomic_add(double* a, double v) {
+        unsafeAtomicAdd(a, v);
+    }
+};
+
+// Decode-side arithmetic type: the fp32 variant peels in fp64, so decoding
+// adds no rounding of its own beyond the final conversion of each value.
+template <typename T> struct Acc { typedef T type; };
+template <> struct Acc<float> { typedef double type; };
+
 template <typename T>
 __device__ __forceinline__ T median3(T a, T b, T c) {
     const T lo = a < b ? a : b;

@@ -531,3 +531,42 @@ def test_leftover_estimate_example_through_decode(golden_dir, order):
     assert out_f[p] == float(want)
     x2, _, _ = o.decode_queue(g, Y, B)
     assert x2[p] == want
+
+
+# ------------------------------------------------------------ error bounds
+
+@pytest.mark.parametrize("ratio,c", [(1.3, 1024), (1.25, 64), (1.1, 16)])
+def test_decode_bound_covers_perturbations(ratio, c):
+    # decode is linear in Y for a fixed schedule: any perturbation within the
+    # per-cell bounds moves each decoded value by at most decode_bound
+    rng = np.random.default_rng(int(ratio * 100) + c)
+    n, N = 20000, 300_000
+    S = np.sort(rng.choice(N, n, replace=False)).astype(np.uint32)
+    v = rng.normal(0, 1e-3, n)
+    g = o.Geom(n=N, rows=int(math.ceil(ratio * n / c)), seed=4, c=c)
+    Y, B = o.encode_coo(g, S, v)
+    x0, m0, i0 = o.decode(g, Y, B)
+    dY = rng.uniform(0, 1e-9, g.cells)
+    bnd = o.decode_bound(g, dY, B)
+    assert np.all(bnd >= 0) and not bnd[np.setdiff1d(np.arange(N), S)].any()
+    for trial in range(3):
+        sgn = rng.choice([-1.0, 1.0], g.cells) if trial else np.ones(g.cells)
+        x1, m1, i1 = o.decode(g, Y + sgn * dY, B)
+        assert np.array_equal(m0, m1) and i0 == i1
+        assert np.all(np.abs(x1 - x0) <= bnd * (1 + 1e-9) + 1e-18)
+    # peeled values: the bound is attained when every cell error has the same
+    # sign as the coefficient it enters with; at least it is not loose by
+    # more than the propagation it describes
+    rec = support_bits(m0, N)
+    assert np.all(bnd[rec] >= dY.min())
+
+
+def test_decode_bound_simple_chain():
+    # an isolated element: its bound is its own cell's bound
+    g = o.Geom(n=5000, rows=5, seed=17, c=1024)
+    B = np.zeros(g.words, np.uint32)
+    B[7 >> 5] |= np.uint32(1 << 7)
+    dY = np.arange(g.cells, dtype=np.float64)
+    bnd = o.decode_bound(g, dY, B)
+    cl, _ = o.cells(g, [7])
+    assert bnd[7] == float(cl[0][0])  # all three cells pure: the j = 0 one is used
