@@ -1,0 +1,115 @@
+"""Parity at the full sizes of the named workloads, in the launch
+configuration bench.py times: dense hc_encode per worker, hc_aggregate over
+the W sketches, hc_decode with max_support = the aggregate's nonzeros.
+
+int32: every stage bit-exact against the CPU oracle (per-worker sketches and
+bitmaps, aggregate, decoded gradient, mask, support size, recovered count,
+round count, success), and the decoded gradient equals the direct sum of the
+workers' sparse gradients.  fp32 (VGG19): structure exact, values within the
+per-element bound derived in test_gpu_parity.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from hc_pipeline import gpu_run, oracle_run
+from test_gpu_parity import assert_fp32_values, assert_same_info, fp32_cell_bounds
+
+pytestmark = pytest.mark.gpu
+
+
+def _hc():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def sparse_direct_sum(w):
+    """(indices, int32 wrapped sums) of the workers' COO gradients."""
+    idx = np.concatenate(w.idx).astype(np.int64)
+    val = np.concatenate(w.val).astype(np.int64)
+    order = np.argsort(idx, kind="stable")
+    idx, val = idx[order], val[order]
+    uniq, start = np.unique(idx, return_index=True)
+    sums = np.add.reduceat(val, start)
+    return uniq, ((sums + 2**31) % 2**32 - 2**31).astype(np.int32)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["tiny", "ncf", "lstm", "vgg19", "bert"])
+def test_fullsize_int32(name):
+    _hc()
+    w = wl.make(name)
+    n_agg = w.n_agg
+    rows = oracle.rows_for(n_agg)
+    print(f"[fullsize] {name}: n={w.n} W={w.W} n_agg={n_agg} rows={rows}", flush=True)
+    g = gpu_run(w, rows, 1024, want_coo_out=False, max_support=n_agg)
+    o = oracle_run(w, rows, 1024)
+    for i in range(w.W):
+        assert np.array_equal(g["Y"][i], o["Y"][i]), f"worker {i} sketch"
+        assert np.array_equal(g["B"][i], o["B"][i]), f"worker {i} bitmap"
+    assert np.array_equal(g["Ya"], o["Ya"])
+    assert np.array_equal(g["Ba"], o["Ba"])
+    assert_same_info(g["info"], o["info"])
+    assert np.array_equal(g["mask"], o["mask"])
+    assert np.array_equal(g["x"], o["x"])
+    assert g["info"].success and g["info"].n_support == n_agg
+    uniq, sums = sparse_direct_sum(w)
+    assert np.array_equal(g["x"][uniq], sums)
+    assert np.count_nonzero(g["x"]) == np.count_nonzero(sums)
+
+
+@pytest.mark.timeout(900)
+def test_fullsize_vgg19_fp32():
+    _hc()
+    w = wl.make("vgg19", vtype="f32")
+    rows = oracle.rows_for(w.n_agg)
+    g = gpu_run(w, rows, 1024, want_coo_out=False, max_support=w.n_agg)
+    o = oracle_run(w, rows, 1024)
+    wb, ab = fp32_cell_bounds(w, o["g"])
+    for i in range(w.W):
+        assert np.array_equal(g["B"][i], o["B"][i])
+        assert np.all(np.abs(g["Y"][i].astype(np.float64) - o["Y"][i]) <= wb[i] * (1 + 1e-6))
+    assert np.array_equal(g["Ba"], o["Ba"])
+    assert np.all(np.abs(g["Ya"].astype(np.float64) - o["Ya"]) <= ab * (1 + 1e-6))
+    assert np.array_equal(g["mask"], o["mask"])
+    assert_same_info(g["info"], o["info"])
+    sup = np.nonzero(np.unpackbits(o["Ba"].view(np.uint8), bitorder="little")[:w.n])[0]
+    assert_fp32_values(g["x"], o["x"], oracle.decode_bound(o["g"], ab, o["Ba"]), sup)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("density,overlap", [(0.001, 0.9), (0.05, 0.1)])
+def test_fullsize_bert_sweep_corners(density, overlap):
+    # the smallest and the largest aggregate of the BERT-base density/overlap
+    # sweep.  The large corner (79 M aggregate nonzeros) is checked through
+    # the oracle's encode and aggregate and through properties of the decode
+    # that hold at any size: success, the support, and equality with the
+    # direct sum of the workers' gradients.
+    _hc()
+    w = wl.make("bert", density=density, overlap=overlap)
+    n_agg = w.n_agg
+    rows = oracle.rows_for(n_agg)
+    print(f"[fullsize] bert d={density} o={overlap}: n_agg={n_agg} rows={rows}", flush=True)
+    g = gpu_run(w, rows, 1024, want_coo_out=False, max_support=n_agg)
+    gg = oracle.Geom(n=w.n, rows=rows, seed=w.hash_seed, c=1024)
+    Ys, Bs = [], []
+    for i in range(w.W):
+        Y, B = oracle.encode_coo(gg, w.idx[i], w.val[i])
+        assert np.array_equal(g["Y"][i], Y) and np.array_equal(g["B"][i], B), f"worker {i}"
+        Ys.append(Y)
+        Bs.append(B)
+    Ya, Ba = oracle.aggregate(np.stack(Ys), np.stack(Bs))
+    del Ys, Bs
+    assert np.array_equal(g["Ya"], Ya) and np.array_equal(g["Ba"], Ba)
+    inf = g["info"]
+    assert inf.success and inf.n_support == n_agg == inf.n_recovered and inf.status == 0
+    assert np.array_equal(g["mask"], Ba)
+    uniq, sums = sparse_direct_sum(w)
+    assert np.array_equal(g["x"][uniq], sums)
+    assert np.count_nonzero(g["x"]) == np.count_nonzero(sums)
+    if n_agg < 2_000_000:
+        xo, mo, io = oracle.decode(gg, Ya, Ba)
+        assert_same_info(inf, io)
+        assert np.array_equal(g["x"], xo)
