@@ -44,7 +44,23 @@ def parse():
                     help="sketch cells / aggregate nonzeros (default: gamma = 1.23)")
     ap.add_argument("--c", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy 10 times (the known-size kernel "
+                         "against which the HBM byte counters are scaled)")
     return ap.parse_args()
+
+
+def copy_calibration():
+    """A plain copy of 1 GiB (2^30 bytes read, 2^30 written) ten times."""
+    import torch
+    dev = torch.device("cuda:0")
+    src = torch.ones(2**28, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": 2**30, "copy_calibration_bytes_written": 2**30,
+                      "launches": 10}), flush=True)
 
 
 def make_workload(a):
@@ -64,6 +80,28 @@ def algorithmic_bytes(n, W, cells, n_sup):
     agg = (W + 1) * (4 * cells + words_b)                  # W sketches+bitmaps in, one out
     dec = words_b + 4 * cells + 8 * n_sup + 4 * n          # B, Y, element list+values, dense out
     return enc, agg, dec
+
+
+def measured_traffic(workload, vtype):
+    """HBM bytes per encode launch from the committed rocprofv3 counter summary
+    (FETCH_SIZE and WRITE_SIZE runs scaled by a plain copy of known size),
+    or None if there is none for this workload or the encode kernel's sources
+    changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"encode_{workload}_hbm_counters.md")
+    if vtype != "i32" or not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and line.split(":")[0] in ("traffic_bytes_per_launch", "kernel_source_sha256"):
+            k, v = line.split(":", 1)
+            fields[k] = v.strip()
+    csrc = os.path.join(ROOT, "paper_2402_07529_amd", "csrc")
+    src = open(os.path.join(csrc, "hc_encode.hip"), "rb").read() + \
+        open(os.path.join(csrc, "hc_device.h"), "rb").read()
+    if fields.get("kernel_source_sha256") != hashlib.sha256(src).hexdigest():
+        return None
+    return int(fields["traffic_bytes_per_launch"])
 
 
 def cpu_baseline(w, rows, c):
@@ -100,6 +138,9 @@ def cpu_baseline(w, rows, c):
 
 def main():
     a = parse()
+    if a.copy_calibration:
+        copy_calibration()
+        return
     if a.gpus != 1:
         print(f"bench.py measures one GPU only (the W workers are simulated on it); "
               f"--gpus {a.gpus} is not supported", file=sys.stderr)
@@ -190,7 +231,8 @@ def main():
                    **{k: v for k, v in w.params.items() if k in ("density", "overlap", "rows_per_worker")}},
         "roofline": {"bound": "hbm", "kernel": "hc_encode (Y clear + dense encode)",
                      "achieved": round(enc_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(enc_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(enc_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic(w.name, w.vtype),
                      "bytes_per_launch": enc_b, "avg_launch_ms": round(enc_ms, 4)},
         "hbm_frac_iteration": round(iter_b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "stages_ms": {"encode_per_worker": round(enc_ms, 4), "aggregate": round(agg_ms, 4),
