@@ -13,6 +13,8 @@
  *   hc_decode                   Algorithm 1, phase II (section 3.2 peeling,
  *                               section 3.1 median estimate for leftovers)
  *   hc_geometry / hc_sizes      sketch sizing, |Y| >= gamma * n (section 3.2)
+ *   hc_plan_bytes / _build      the inverse row map of a geometry (section 3.4
+ *                               batching), built once, used by the decode
  *
  * Conventions for every call:
  *   - Buffer pointers are DEVICE pointers unless marked "host".  The caller
@@ -82,7 +84,9 @@ typedef struct {
     uint32_t status;      /* 0 ok; 1 n_support exceeded max_support (nothing was
                              peeled, every element got the median estimate);
                              2 the round loop's barrier gave up waiting (a
-                             device fault; outputs are not valid)               */
+                             device fault; outputs are not valid);
+                             3 the plan was built for another geometry
+                             (nothing was peeled, as for 1)                     */
 } hc_decode_info;
 
 /* Geometry for a gradient of n parameters whose aggregate has about n_nonzero
@@ -98,6 +102,18 @@ hc_status hc_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
  * (0 means n, which always suffices). */
 hc_status hc_sizes(const hc_params *p, uint64_t max_support, size_t *y_bytes,
                    size_t *b_bytes, size_t *ws_bytes);
+
+/* Plan: the inverse row map of a geometry.  Under section 3.4's batching each
+ * batch of c parameters lands, per hash, on one whole sketch row; the plan
+ * lists for every row the (batch, hash) pairs landing on it, so that a row can
+ * be assembled by one workgroup that gathers its contributions instead of
+ * receiving scattered atomics.  It depends only on (n, c, rows, seed): build it
+ * once per geometry and reuse it for every worker and iteration.  Requires
+ * c >= 256 (HC_EUNSUPPORTED otherwise).  hc_plan_bytes writes the size to the
+ * HOST pointer `bytes`; hc_plan_build fills a caller-owned, 256-byte aligned
+ * DEVICE buffer of at least that size, asynchronously on `stream`. */
+hc_status hc_plan_bytes(const hc_params *p, size_t *bytes);
+hc_status hc_plan_build(const hc_params *p, void *plan, size_t plan_bytes, hipStream_t stream);
 
 /* Phase I on a dense gradient x[n] (int32 or fp32 per p->vtype).  Overwrites
  * y[cells] with the Count Sketch (Y[h_j(p)] += g_j(p) * x_p for every nonzero
@@ -122,6 +138,10 @@ hc_status hc_aggregate(const hc_params *p, const void *y_in, const uint32_t *b_i
                        uint32_t W, void *y_out, uint32_t *b_out, hipStream_t stream);
 
 /* Phase II on an aggregated sketch.  y_agg and b_agg are not modified.
+ * plan: a plan built for the same geometry (then the per-cell counters are
+ * gathered row by row, without atomics), or NULL (they are built with
+ * atomics).  Results are identical either way; a plan built for another
+ * geometry is detected on the device and reported as status 3.
  * Outputs (each may be NULL):
  *   x_out[n]              dense sum X: recovered values, the Count Sketch
  *                         median estimate for members of the support that
@@ -136,7 +156,8 @@ hc_status hc_aggregate(const hc_params *p, const void *y_in, const uint32_t *b_i
  * Peeling runs as synchronous rounds entirely on the device (one cooperative
  * kernel; no host round trips).  Decode failure is data (info->success), not
  * an error status. */
-hc_status hc_decode(const hc_params *p, const void *y_agg, const uint32_t *b_agg,
+hc_status hc_decode(const hc_params *p, const void *plan, const void *y_agg,
+                    const uint32_t *b_agg,
                     void *x_out, uint32_t *coo_idx, void *coo_val, uint64_t coo_cap,
                     uint32_t *mask, hc_decode_info *info, uint64_t max_support,
                     void *ws, size_t ws_bytes, hipStream_t stream);

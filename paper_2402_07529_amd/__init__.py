@@ -7,6 +7,7 @@ C ABI:
 
     hc_geometry   sketch sizing, |Y| >= gamma * n (section 3.2, gamma = 1.23)
     hc_sizes      byte sizes of Y, B and the decode workspace
+    hc_plan_bytes, hc_plan_build   inverse row map of a geometry (c >= 256)
     hc_encode     Algorithm 1 phase I on a dense gradient (sections 3.1-3.4)
     hc_encode_coo the same from COO input
     hc_aggregate  sum of sketches and OR of bitmaps over W workers (section 3)
@@ -29,8 +30,8 @@ HC_I32, HC_F32 = 0, 1
 GAMMA = 1.23
 INFO_BYTES = 32
 
-EXPORTS = ("hc_geometry", "hc_sizes", "hc_encode", "hc_encode_coo", "hc_aggregate",
-           "hc_decode", "hc_status_string", "hc_last_error")
+EXPORTS = ("hc_geometry", "hc_sizes", "hc_plan_bytes", "hc_plan_build", "hc_encode",
+           "hc_encode_coo", "hc_aggregate", "hc_decode", "hc_status_string", "hc_last_error")
 
 
 class HCError(RuntimeError):
@@ -70,9 +71,12 @@ _lib.hc_sizes.argtypes = [_PP, ctypes.c_uint64, ctypes.POINTER(ctypes.c_size_t),
 _lib.hc_encode.argtypes = [_PP, _P, _P, _P, _P]
 _lib.hc_encode_coo.argtypes = [_PP, _P, _P, ctypes.c_uint64, _P, _P, _P]
 _lib.hc_aggregate.argtypes = [_PP, _P, _P, ctypes.c_uint32, _P, _P, _P]
-_lib.hc_decode.argtypes = [_PP, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, ctypes.c_uint64,
+_lib.hc_decode.argtypes = [_PP, _P, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, ctypes.c_uint64,
                            _P, ctypes.c_size_t, _P]
-for _f in ("hc_geometry", "hc_sizes", "hc_encode", "hc_encode_coo", "hc_aggregate", "hc_decode"):
+_lib.hc_plan_bytes.argtypes = [_PP, ctypes.POINTER(ctypes.c_size_t)]
+_lib.hc_plan_build.argtypes = [_PP, _P, ctypes.c_size_t, _P]
+for _f in ("hc_geometry", "hc_sizes", "hc_plan_bytes", "hc_plan_build", "hc_encode",
+           "hc_encode_coo", "hc_aggregate", "hc_decode"):
     getattr(_lib, _f).restype = ctypes.c_int
 _lib.hc_status_string.argtypes = [ctypes.c_int]
 _lib.hc_status_string.restype = ctypes.c_char_p
@@ -167,10 +171,31 @@ def hc_aggregate(p: hc_params, y_in, b_in, W: int, y_out, b_out, stream=None):
            "hc_aggregate")
 
 
-def hc_decode(p: hc_params, y_agg, b_agg, info, ws, x_out=None, coo_idx=None, coo_val=None,
-              mask=None, max_support: int = 0, stream=None):
+def hc_plan_bytes(p: hc_params) -> int:
+    b = ctypes.c_size_t()
+    _check(_lib.hc_plan_bytes(ctypes.byref(p), ctypes.byref(b)), "hc_plan_bytes")
+    return b.value
+
+
+def hc_plan_build(p: hc_params, plan, stream=None):
     import torch
-    _check(_lib.hc_decode(ctypes.byref(p), _ptr(y_agg, "y_agg", _vdtypes(p), p.cells),
+    _check(_lib.hc_plan_build(ctypes.byref(p), _ptr(plan, "plan", (torch.uint8,)), plan.numel(),
+                              _stream(stream)), "hc_plan_build")
+
+
+def make_plan(p: hc_params, device="cuda", stream=None):
+    """Allocate and build the inverse row map of a geometry (c >= 256)."""
+    import torch
+    plan = torch.empty(hc_plan_bytes(p), dtype=torch.uint8, device=device)
+    hc_plan_build(p, plan, stream)
+    return plan
+
+
+def hc_decode(p: hc_params, y_agg, b_agg, info, ws, x_out=None, coo_idx=None, coo_val=None,
+              mask=None, max_support: int = 0, stream=None, plan=None):
+    import torch
+    _check(_lib.hc_decode(ctypes.byref(p), _ptr(plan, "plan", (torch.uint8,)),
+                          _ptr(y_agg, "y_agg", _vdtypes(p), p.cells),
                           _ptr(b_agg, "b_agg", _u32(), p.words),
                           _ptr(x_out, "x_out", _vdtypes(p), p.n),
                           _ptr(coo_idx, "coo_idx", _u32()), _ptr(coo_val, "coo_val", _vdtypes(p)),

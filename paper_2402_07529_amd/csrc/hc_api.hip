@@ -172,14 +172,39 @@ hc_status hc_aggregate(const hc_params* p, const void* y_in, const uint32_t* b_i
     return e == hipSuccess ? HC_OK : fail_hip(e, "hc_aggregate");
 }
 
-hc_status hc_decode(const hc_params* p, const void* y_agg, const uint32_t* b_agg, void* x_out,
-                    uint32_t* coo_idx, void* coo_val, uint64_t coo_cap, uint32_t* mask,
-                    hc_decode_info* info, uint64_t max_support, void* ws, size_t ws_bytes,
-                    hipStream_t stream) {
+hc_status hc_plan_bytes(const hc_params* p, size_t* bytes) {
     g_last_error.clear();
     Geo g;
     const hc_status s = to_geo(p, &g);
     if (s != HC_OK) return s;
+    if (!bytes) return fail(HC_EINVAL, "bytes is NULL");
+    if (!plan_supported(g)) return fail(HC_EUNSUPPORTED, "plans need c >= 256");
+    *bytes = plan_layout(g).total;
+    return HC_OK;
+}
+
+hc_status hc_plan_build(const hc_params* p, void* plan, size_t plan_bytes, hipStream_t stream) {
+    g_last_error.clear();
+    Geo g;
+    const hc_status s = to_geo(p, &g);
+    if (s != HC_OK) return s;
+    if (!plan_supported(g)) return fail(HC_EUNSUPPORTED, "plans need c >= 256");
+    if (!plan || !aligned(plan, 256)) return fail(HC_EINVAL, "plan must be non-NULL and 256-byte aligned");
+    if (plan_bytes < plan_layout(g).total) return fail(HC_EWORKSPACE, "plan smaller than hc_plan_bytes reports");
+    const hipError_t e = launch_plan_build(g, plan, stream);
+    return e == hipSuccess ? HC_OK : fail_hip(e, "hc_plan_build");
+}
+
+hc_status hc_decode(const hc_params* p, const void* plan, const void* y_agg,
+                    const uint32_t* b_agg, void* x_out, uint32_t* coo_idx, void* coo_val,
+                    uint64_t coo_cap, uint32_t* mask, hc_decode_info* info, uint64_t max_support,
+                    void* ws, size_t ws_bytes, hipStream_t stream) {
+    g_last_error.clear();
+    Geo g;
+    const hc_status s = to_geo(p, &g);
+    if (s != HC_OK) return s;
+    if (plan && (!plan_supported(g) || !aligned(plan, 256)))
+        return fail(HC_EINVAL, "plan given for a geometry with c < 256, or not 256-byte aligned");
     if (!y_agg || !b_agg || !info || !ws) return fail(HC_EINVAL, "y_agg, b_agg, info and ws must be non-NULL");
     if (!aligned(y_agg, 4) || !aligned(b_agg, 4) || (x_out && !aligned(x_out, 4)) ||
         (mask && !aligned(mask, 4)) || (coo_idx && !aligned(coo_idx, 4)) ||
@@ -198,7 +223,7 @@ hc_status hc_decode(const hc_params* p, const void* y_agg, const uint32_t* b_agg
     out.coo_cap = coo_cap;
     out.mask = mask;
     out.info = info;
-    const hipError_t e = launch_decode(g, y_agg, b_agg, out, L, ws, stream);
+    const hipError_t e = launch_decode(g, plan, y_agg, b_agg, out, L, ws, stream);
     return e == hipSuccess ? HC_OK : fail_hip(e, "hc_decode");
 }
 

@@ -1,31 +1,38 @@
 // hc_decode.hip -- recovery (Algorithm 1, phase II) for gfx950.
 //
 // Stages (one stream, no host round trips):
-//   prep   copy the aggregated sketch into a residual Yw, clear the per-cell
-//          counters and round stamps, clear the control block;
-//   count  popcount of the bitmap per chunk of 1024 words;
-//   scan   exclusive scan of the chunk counts (one workgroup) -> offsets and
-//          the support size |S|;
-//   build  compaction of the set bits into the ascending element list E
-//          ("we know the indexes of all non-zero parameters", section 3.2)
-//          and, per element, one 64-bit atomic add per cell into a packed
-//          counter  cnt = deg * 2^32 + (sum of element positions):  a cell is
-//          pure (one live element) exactly when cnt >> 32 == 1, and then its
-//          low word is that element's position;
-//   peel   one cooperative persistent kernel running synchronous rounds
-//          (section 3.2, parallel peeling).  The frontier of round r is the
-//          list of cells that became pure during round r-1 (all pure cells
-//          for r = 0), kept in one append-only queue.  An element owning
-//          several frontier cells is claimed by the one with the smallest j;
-//          a per-cell stamp (the round in whose frontier the cell sits) tells
-//          which of its cells were pure at the round start without racing
-//          with the round's own updates.  The claimer recovers x = g_j * Y,
-//          and subtracts g * x and the element from its other two cells with
-//          atomics; a cell whose count drops to one joins the next frontier.
-//          One grid barrier per round; rounds end when a frontier is empty.
-//          Elements never peeled get the Count Sketch median estimate from
-//          the residual sketch (Algorithm 1, last recovery step);
-//   emit   dense output, recovered mask and COO from E and the values.
+//   prep     copy the aggregated sketch into a residual Yw (fp64 for fp32
+//            gradients), clear the control block (and, without a plan, the
+//            per-cell counters and round stamps);
+//   count    popcount of the bitmap per chunk of 1024 words;
+//   scan     exclusive scan of the chunk counts (one workgroup) -> offsets and
+//            the support size |S|;
+//   compact  the set bits become the ascending element list E ("we know the
+//            indexes of all non-zero parameters", section 3.2) and, with a
+//            plan, every bitmap word's rank offset;
+//   counters per cell  cnt = deg * 2^32 + (sum of member positions):  a cell
+//            is pure (one live element) exactly when cnt >> 32 == 1, and then
+//            its low word is that element's position.  With a plan (the
+//            inverse row map of hc_plan.hip) one workgroup per sketch row
+//            gathers its counters from the bitmap words of the batches that
+//            land on it -- no atomics -- and seeds the round-0 frontier with the
+//            row's pure cells.  Without a plan every element adds itself to its
+//            three cells with 64-bit atomics and the peel kernel finds the
+//            pure cells by a scan;
+//   peel     one cooperative persistent kernel running synchronous rounds
+//            (section 3.2, parallel peeling).  The frontier of round r is the
+//            list of (cell, element) pairs whose cell became pure during round
+//            r-1, kept in one append-only queue.  An element owning several
+//            frontier cells is claimed through the one with the smallest j; a
+//            per-cell stamp (the round in whose frontier the cell sits) tells
+//            which of its cells were pure at the round start without racing
+//            with the round's own updates.  The claimer recovers x = g_j * Y,
+//            and subtracts g * x and the element from its other two cells with
+//            atomics; a cell whose count drops to one joins the next frontier.
+//            One grid barrier per round; rounds end when a frontier is empty.
+//            Elements never peeled get the Count Sketch median estimate from
+//            the residual sketch (Algorithm 1, last recovery step);
+//   emit     dense output, recovered mask and COO from E and the values.
 #include <stdlib.h>
 
 #include <type_traits>
@@ -55,7 +62,8 @@ struct Ctrl {
     unsigned int bar_count;
     unsigned int bar_gen;
     unsigned int done;      // workgroups finished
-    unsigned int pad[4];
+    unsigned int bad_plan;  // the plan was built for another geometry
+    unsigned int pad[3];
 };
 static_assert(sizeof(Ctrl) == 64, "control block layout");
 
@@ -70,7 +78,7 @@ __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
     return v;
 }
 
-// Exclusive scan over the 256 lanes of a workgroup; *total gets the sum.
+// Exclusive scan over the lanes of a workgroup; *total gets the sum.
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s_tmp,
                                                          uint32_t* total) {
     const uint32_t lane = lane_id();
@@ -99,14 +107,17 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(const T* __restrict__ y_ag
                                                       typename Acc<T>::type* __restrict__ yw,
                                                       unsigned long long* __restrict__ cnt,
                                                       uint32_t* __restrict__ stamp,
-                                                      uint32_t cells, Ctrl* __restrict__ ctrl) {
+                                                      uint32_t cells, bool planned,
+                                                      Ctrl* __restrict__ ctrl) {
     if (blockIdx.x == 0 && threadIdx.x < sizeof(Ctrl) / 4)
         reinterpret_cast<uint32_t*>(ctrl)[threadIdx.x] = 0u;
     const uint64_t step = (uint64_t)gridDim.x * kBlock;
     for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < cells; i += step) {
         yw[i] = (typename Acc<T>::type)y_agg[i];
-        cnt[i] = 0ull;
-        stamp[i] = kNever;
+        if (!planned) {
+            cnt[i] = 0ull;
+            stamp[i] = kNever;
+        }
     }
 }
 
@@ -138,7 +149,8 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const uint32_t* __restric
 
 // One workgroup of 1024 lanes: chunk counts -> exclusive offsets.
 __global__ __launch_bounds__(1024) void scan_kernel(uint32_t* __restrict__ blk, uint64_t nchunks,
-                                                    Ctrl* __restrict__ ctrl, uint64_t cap) {
+                                                    Ctrl* __restrict__ ctrl, uint64_t cap,
+                                                    uint32_t* __restrict__ woff, uint64_t words) {
     __shared__ uint32_t s_tmp[16];
     const uint64_t per = (nchunks + 1023) / 1024;
     const uint64_t lo = (uint64_t)threadIdx.x * per;
@@ -155,14 +167,18 @@ __global__ __launch_bounds__(1024) void scan_kernel(uint32_t* __restrict__ blk, 
     if (threadIdx.x == 0) {
         ctrl->n_support = total;
         ctrl->overflow = (uint64_t)total > cap ? 1u : 0u;
+        if (woff != nullptr) woff[words] = total;
     }
 }
 
-__global__ __launch_bounds__(kBlock) void build_kernel(
+// Element list E (ascending), cleared peeled flags, and either the word rank
+// offsets (planned) or the per-cell counters by atomics (unplanned).
+__global__ __launch_bounds__(kBlock) void compact_kernel(
     const uint32_t* __restrict__ b, uint64_t words, uint32_t last_mask,
     const uint32_t* __restrict__ blk, uint32_t* __restrict__ elem, uint8_t* __restrict__ peeled,
-    unsigned long long* __restrict__ cnt, const Ctrl* __restrict__ ctrl, uint64_t seed,
-    uint32_t rows, uint32_t c, uint32_t cmask, uint32_t log2c) {
+    uint32_t* __restrict__ woff, unsigned long long* __restrict__ cnt,
+    const Ctrl* __restrict__ ctrl, uint64_t seed, uint32_t rows, uint32_t c, uint32_t cmask,
+    uint32_t log2c) {
     __shared__ uint32_t s_tmp[kBlock / 64];
     if (ctrl->overflow) return;
     const uint64_t w0 = (uint64_t)blockIdx.x * kChunkWords + 4ull * threadIdx.x;
@@ -179,26 +195,184 @@ __global__ __launch_bounds__(kBlock) void build_kernel(
     BatchHash h;
 #pragma unroll
     for (int k = 0; k < 4; k++) {
+        if (woff != nullptr && w0 + k < words) woff[w0 + k] = pos;
         uint32_t w = w4[k];
         while (w) {
             const uint32_t bit = __builtin_ctz(w);
             w &= w - 1u;
             const uint64_t p = (w0 + k) * 32ull + bit;
-            const uint64_t batch = p >> log2c;
-            if (batch != cached_batch) {
-                h = batch_hash(seed, rows, cmask, batch);
-                cached_batch = batch;
-            }
             elem[pos] = (uint32_t)p;
             peeled[pos] = 0;
-            const uint32_t t = (uint32_t)p & cmask;
-            const unsigned long long inc = kOne + pos;
+            if (woff == nullptr) {
+                const uint64_t batch = p >> log2c;
+                if (batch != cached_batch) {
+                    h = batch_hash(seed, rows, cmask, batch);
+                    cached_batch = batch;
+                }
+                const uint32_t t = (uint32_t)p & cmask;
+                const unsigned long long inc = kOne + pos;
 #pragma unroll
-            for (int j = 0; j < 3; j++) atomicAdd(cnt + cell_of(h, j, t, c, cmask), inc);
+                for (int j = 0; j < 3; j++) atomicAdd(cnt + cell_of(h, j, t, c, cmask), inc);
+            }
             pos++;
         }
     }
 }
+
+// ---- frontier staging ----------------------------------------------------------
+
+// (cell, element position) pairs whose cell became pure, staged in LDS by one
+// workgroup and appended to the global queue with one atomic per flush (a
+// single global counter bumped by every wave would serialize the whole grid
+// on one cache line).
+constexpr uint32_t kPushCap = 4 * kPeelBlock;
+
+struct PushBuf {
+    uint32_t count;
+    uint32_t base;
+    uint2 item[kPushCap];
+};
+
+__device__ __forceinline__ void lds_push(PushBuf& q, bool pred, uint32_t cell, uint32_t pos,
+                                         uint32_t round_stamp, uint32_t* stamp) {
+    const uint64_t m = __ballot(pred);
+    if (m == 0) return;
+    const uint32_t lane = lane_id();
+    const uint32_t leader = (uint32_t)__ffsll((unsigned long long)m) - 1u;
+    uint32_t off = 0;
+    if (lane == leader) off = atomicAdd(&q.count, (unsigned int)__popcll(m));
+    off = __shfl(off, leader);
+    if (pred) {
+        q.item[off + lanes_below(m)] = make_uint2(cell, pos);
+        if (stamp != nullptr) stamp[cell] = round_stamp;
+    }
+}
+
+// Called by every lane of the workgroup with the same arguments.  Appends the
+// staged pairs to the global queue if `force` or if the buffer could not take
+// another `room` pushes.
+__device__ void flush_pushes(PushBuf& q, bool force, uint32_t room, Ctrl* ctrl, uint2* queue,
+                             uint32_t cells) {
+    __syncthreads();
+    const uint32_t n = q.count;
+    __syncthreads();  // every lane has read n before any lane pushes again
+    if (n == 0 || (!force && n + room <= kPushCap)) return;
+    if (threadIdx.x == 0) q.base = atomicAdd(&ctrl->tail, n);
+    __syncthreads();
+    const uint32_t base = q.base;
+    for (uint32_t k = threadIdx.x; k < n; k += blockDim.x)
+        if (base + k < cells) queue[base + k] = q.item[k];  // a cell is pushed at most once
+    __syncthreads();
+    if (threadIdx.x == 0) q.count = 0;
+    __syncthreads();
+}
+
+// ---- counters by row (planned path) --------------------------------------------
+
+struct CounterArgs {
+    const PlanHeader* hdr;
+    const uint32_t* rowoff;
+    const uint2* entry;
+    const uint32_t* b;
+    const uint32_t* woff;   // words + 1 entries
+    unsigned long long* cnt;
+    uint32_t* stamp;
+    uint2* queue;
+    Ctrl* ctrl;
+    uint64_t n, seed, words, nb;
+    uint32_t rows, c, cmask, cells, last_mask;
+};
+
+// One workgroup per sketch row (grid-stride).  Cell k of row r gathers, from
+// every (batch b, hash j) in the row's plan entry list, the parameter
+// t = (k - bias_j(b)) mod c of batch b: if its bit is set it adds 2^32 + its
+// rank in the support.  Integer sums, so the result equals the atomic build
+// exactly whatever the order.  Each wave screens 64 entries at a time (one
+// lane each: is any member of the support in that batch?) and then visits
+// only the batches that have one: lanes 0..C/32-1 load the batch's bitmap
+// words and rank offsets, every lane takes the (at most two) words covering
+// its C/64 consecutive cells by shuffle, and adds into the row's counters in
+// LDS.  The row is then written once, with its stamps, and its pure cells
+// become the round-0 frontier.
+template <int C>
+__global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
+    constexpr uint32_t WPB = C / 32;  // bitmap words per batch
+    constexpr uint32_t CPL = C / 64;  // cells per lane
+    __shared__ unsigned long long s_acc[C];
+    __shared__ PushBuf q;
+    const PlanHeader* hdr = a.hdr;
+    const bool ok = hdr->magic == kPlanMagic && hdr->n == a.n && hdr->seed == a.seed &&
+                    hdr->c == a.c && hdr->rows == a.rows;
+    if (!ok) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) a.ctrl->bad_plan = 1u;
+        return;
+    }
+    if (a.ctrl->overflow) return;
+    const uint32_t lane = lane_id();
+    const uint32_t wave = threadIdx.x >> 6;
+    constexpr uint32_t kWaves = kBlock / 64;
+    if (threadIdx.x == 0) q.count = 0;
+    for (uint32_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
+        for (uint32_t k = threadIdx.x; k < C; k += kBlock) s_acc[k] = 0ull;
+        __syncthreads();
+        const uint32_t e0 = a.rowoff[row], e1 = a.rowoff[row + 1];
+        for (uint32_t base = e0 + wave * 64u; base < e1; base += kWaves * 64u) {
+            const uint32_t e = base + lane;
+            uint2 ent = make_uint2(0xffffffffu, 0u);
+            bool live = false;
+            if (e < e1) {
+                ent = a.entry[e];
+                if (ent.x < a.nb) {
+                    const uint64_t ws = (uint64_t)ent.x * WPB;
+                    const uint64_t we = ws + WPB < a.words ? ws + WPB : a.words;
+                    live = a.woff[we] != a.woff[ws];
+                }
+            }
+            uint64_t m = __ballot(live);
+            while (m) {
+                const uint32_t src = (uint32_t)__ffsll((unsigned long long)m) - 1u;
+                m &= m - 1ull;
+                const uint32_t bidx = __shfl(ent.x, src);
+                const uint32_t bias = __shfl(ent.y, src) & 0xffffu;
+                const uint64_t ws = (uint64_t)bidx * WPB;
+                uint32_t myword = 0, myoff = 0;
+                if (lane < WPB && ws + lane < a.words) {
+                    myword = load_word(a.b, ws + lane, a.words, a.last_mask);
+                    myoff = a.woff[ws + lane];
+                }
+                const uint32_t t0 = (lane * CPL - bias) & (C - 1u);
+                const uint32_t wa = t0 >> 5, wb = ((t0 + CPL - 1u) & (C - 1u)) >> 5;
+                const uint32_t word_a = __shfl(myword, wa), off_a = __shfl(myoff, wa);
+                const uint32_t word_b = __shfl(myword, wb), off_b = __shfl(myoff, wb);
+#pragma unroll
+                for (uint32_t i = 0; i < CPL; i++) {
+                    const uint32_t t = (t0 + i) & (C - 1u);
+                    const bool first = (t >> 5) == wa;
+                    const uint32_t word = first ? word_a : word_b;
+                    const uint32_t bit = t & 31u;
+                    if ((word >> bit) & 1u) {
+                        const uint32_t rank = (first ? off_a : off_b) +
+                                              __popc(word & ((1u << bit) - 1u));
+                        atomicAdd(&s_acc[lane * CPL + i], kOne + rank);
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        for (uint32_t k = threadIdx.x; k < C; k += kBlock) {
+            const unsigned long long acc = s_acc[k];
+            const uint32_t cell = row * C + k;
+            const bool pure = (acc >> 32) == 1ull;
+            a.cnt[cell] = acc;
+            a.stamp[cell] = pure ? 0u : kNever;
+            lds_push(q, pure, cell, (uint32_t)acc, 0u, nullptr);
+        }
+        flush_pushes(q, false, C, a.ctrl, a.queue, a.cells);
+    }
+    flush_pushes(q, true, 0, a.ctrl, a.queue, a.cells);
+}
+
+// ---- peel ------------------------------------------------------------------------
 
 template <typename T>
 struct PeelArgs {  // T: the decode-side arithmetic type
@@ -209,56 +383,12 @@ struct PeelArgs {  // T: the decode-side arithmetic type
     unsigned long long* cnt;
     T* yw;
     uint32_t* stamp;
-    uint32_t* queue;
+    uint2* queue;
     InfoDev* info;
     uint64_t seed;
     uint32_t rows, c, cmask, log2c, cells;
+    bool planned;   // the round-0 frontier is already queued
 };
-
-// Cells that became pure, staged in LDS by one workgroup and appended to the
-// global queue with one atomic per flush (a single global counter bumped by
-// every wave would serialize the whole grid on one cache line).
-constexpr uint32_t kPushCap = 4 * kPeelBlock;
-
-struct PushBuf {
-    uint32_t count;
-    uint32_t base;
-    uint32_t cell[kPushCap];
-};
-
-__device__ __forceinline__ void lds_push(PushBuf& q, bool pred, uint32_t cell,
-                                         uint32_t round_stamp, uint32_t* stamp) {
-    const uint64_t m = __ballot(pred);
-    if (m == 0) return;
-    const uint32_t lane = lane_id();
-    const uint32_t leader = (uint32_t)__ffsll((unsigned long long)m) - 1u;
-    uint32_t off = 0;
-    if (lane == leader) off = atomicAdd(&q.count, (unsigned int)__popcll(m));
-    off = __shfl(off, leader);
-    if (pred) {
-        q.cell[off + lanes_below(m)] = cell;
-        stamp[cell] = round_stamp;
-    }
-}
-
-// Called by every lane of the workgroup with the same arguments.  Appends the
-// staged cells to the global queue if `force` or if the buffer could not take
-// another `room` pushes.
-__device__ void flush_pushes(PushBuf& q, bool force, uint32_t room, Ctrl* ctrl, uint32_t* queue,
-                             uint32_t cells) {
-    __syncthreads();
-    const uint32_t n = q.count;
-    __syncthreads();  // every lane has read n before any lane pushes again
-    if (n == 0 || (!force && n + room <= kPushCap)) return;
-    if (threadIdx.x == 0) q.base = atomicAdd(&ctrl->tail, n);
-    __syncthreads();
-    const uint32_t base = q.base;
-    for (uint32_t k = threadIdx.x; k < n; k += blockDim.x)
-        if (base + k < cells) queue[base + k] = q.cell[k];  // a cell is pushed at most once
-    __syncthreads();
-    if (threadIdx.x == 0) q.count = 0;
-    __syncthreads();
-}
 
 // Grid-wide barrier.  The last block to arrive publishes the end of the next
 // frontier.  Each block makes its writes visible with one release fence
@@ -318,7 +448,7 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
     const uint32_t nwaves = gridDim.x * waves_per_block;
     const uint32_t nthreads = gridDim.x * kPeelBlock;
     const uint32_t gtid = gwave * 64u + lane;
-    const bool overflow = ctrl->overflow != 0;
+    const bool skip = ctrl->overflow != 0 || ctrl->bad_plan != 0;
     bool ok = true;
     uint32_t my_recovered = 0, my_last_round = 0;
     if (threadIdx.x == 0) {
@@ -328,19 +458,25 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
     }
     __syncthreads();
 
-    if (!overflow) {
-        // round-0 frontier: every cell with exactly one element
-        for (uint32_t base = 0; base < a.cells; base += nthreads) {
-            const uint32_t cidx = base + gtid;
-            bool pure = false;
-            if (cidx < a.cells) pure = (a.cnt[cidx] >> 32) == 1ull;
-            lds_push(q, pure, cidx, 0u, a.stamp);
-            flush_pushes(q, false, kPeelBlock, ctrl, a.queue, a.cells);
+    if (!skip) {
+        const uint32_t nsup = (uint32_t)ctrl->n_support;
+        if (!a.planned) {
+            // round-0 frontier: every cell with exactly one element
+            for (uint32_t base = 0; base < a.cells; base += nthreads) {
+                const uint32_t cidx = base + gtid;
+                bool pure = false;
+                unsigned long long v = 0;
+                if (cidx < a.cells) {
+                    v = a.cnt[cidx];
+                    pure = (v >> 32) == 1ull;
+                }
+                lds_push(q, pure, cidx, (uint32_t)v, 0u, a.stamp);
+                flush_pushes(q, false, kPeelBlock, ctrl, a.queue, a.cells);
+            }
+            flush_pushes(q, true, 0, ctrl, a.queue, a.cells);
         }
-        flush_pushes(q, true, 0, ctrl, a.queue, a.cells);
         ok = grid_barrier(ctrl, gridDim.x);
 
-        const uint32_t nsup = (uint32_t)ctrl->n_support;
         uint32_t qs = 0;
         for (uint32_t r = 0; ok; r++) {
             uint32_t qe =
@@ -351,13 +487,13 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
             for (uint32_t sw = 0; sw < nsweep; sw++) {
                 const uint32_t i = qs + (sw * nwaves + gwave) * 64u + lane;
                 bool push_a = false, push_b = false;
-                uint32_t cell_a = 0, cell_b = 0;
+                uint32_t cell_a = 0, cell_b = 0, pos_a = 0, pos_b = 0;
                 if (i < qe) {
-                    const uint32_t cidx = a.queue[i];
-                    const unsigned long long v = __hip_atomic_load(
-                        a.cnt + cidx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    if ((v >> 32) == 1ull && (uint32_t)v < nsup) {
-                        const uint32_t pos = (uint32_t)v;
+                    // the cell was pure with element pos when queued; pos is dead
+                    // if it was peeled through another cell since
+                    const uint2 it = a.queue[i];
+                    const uint32_t cidx = it.x, pos = it.y;
+                    if (pos < nsup && !a.peeled[pos]) {
                         const uint32_t p = a.elem[pos];
                         const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p >> a.log2c);
                         const uint32_t t = p & a.cmask;
@@ -366,7 +502,7 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                         for (int j = 0; j < 3; j++) cl[j] = cell_of(h, j, t, a.c, a.cmask);
                         const int j = cl[0] == cidx ? 0 : (cl[1] == cidx ? 1 : 2);
                         // claimed by the smallest j among its cells pure at the round start
-                        bool mine = true;
+                        bool mine = cl[j] == cidx;
                         if (j >= 1 && a.stamp[cl[0]] == r) mine = false;
                         if (j == 2 && mine && a.stamp[cl[1]] == r) mine = false;
                         if (mine) {
@@ -384,15 +520,18 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                                                Val<T>::sign(val, !((h.neg >> ja) & 1u)));
                             Val<T>::atomic_add(a.yw + cl[jb],
                                                Val<T>::sign(val, !((h.neg >> jb) & 1u)));
-                            push_a = ((old_a + dec) >> 32) == 1ull;
-                            push_b = ((old_b + dec) >> 32) == 1ull;
+                            const unsigned long long new_a = old_a + dec, new_b = old_b + dec;
+                            push_a = (new_a >> 32) == 1ull;
+                            push_b = (new_b >> 32) == 1ull;
                             cell_a = cl[ja];
                             cell_b = cl[jb];
+                            pos_a = (uint32_t)new_a;
+                            pos_b = (uint32_t)new_b;
                         }
                     }
                 }
-                lds_push(q, push_a, cell_a, r + 1u, a.stamp);
-                lds_push(q, push_b, cell_b, r + 1u, a.stamp);
+                lds_push(q, push_a, cell_a, pos_a, r + 1u, a.stamp);
+                lds_push(q, push_b, cell_b, pos_b, r + 1u, a.stamp);
                 flush_pushes(q, false, 2u * kPeelBlock, ctrl, a.queue, a.cells);
             }
             flush_pushes(q, true, 0, ctrl, a.queue, a.cells);
@@ -436,18 +575,22 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             const bool aborted = __hip_atomic_load(&ctrl->abort, __ATOMIC_RELAXED,
                                                    __HIP_MEMORY_SCOPE_AGENT) != 0;
+            const bool overflow = ctrl->overflow != 0;
+            const bool bad_plan = ctrl->bad_plan != 0;
             const unsigned long long ns = ctrl->n_support;
-            const unsigned long long rec = overflow ? 0ull :
+            const unsigned long long rec = skip ? 0ull :
                 __hip_atomic_load(&ctrl->recovered, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             a.info->n_support = ns;
             a.info->n_recovered = rec;
-            a.info->rounds = overflow ? 0ull :
+            a.info->rounds = skip ? 0ull :
                 __hip_atomic_load(&ctrl->rounds, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            a.info->success = (!overflow && !aborted && rec == ns) ? 1u : 0u;
-            a.info->status = overflow ? 1u : (aborted ? 2u : 0u);
+            a.info->success = (!skip && !aborted && rec == ns) ? 1u : 0u;
+            a.info->status = bad_plan ? 3u : (overflow ? 1u : (aborted ? 2u : 0u));
         }
     }
 }
+
+// ---- emit ------------------------------------------------------------------------
 
 template <typename T>
 struct EmitArgs {  // T: the gradient type; values are kept in Acc<T>
@@ -506,7 +649,9 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
     }
     __syncthreads();
     const uint64_t off = a.blk[chunk];
-    const bool overflow = a.ctrl->overflow != 0;
+    // with no valid element list (support over capacity, or a plan for
+    // another geometry) every member gets the estimate from the aggregate
+    const bool raw = a.ctrl->overflow != 0 || a.ctrl->bad_plan != 0;
     const uint64_t chunk_p = chunk * kChunkBits;
 
     for (uint32_t it = 0; it < kChunkBits / (4 * kBlock); it++) {
@@ -523,7 +668,7 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
             rec[k] = false;
             if ((word >> (sh + k)) & 1u) {
                 const uint32_t p = (uint32_t)(p0 + k);
-                if (!overflow) {
+                if (!raw) {
                     out[k] = (T)a.vals[rank];
                     rec[k] = a.peeled[rank] != 0;
                 } else {
@@ -564,21 +709,23 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
 int peel_grid_cache[64];
 
 template <typename T>
-hipError_t launch_decode_t(const Geo& g, const void* y_agg_v, const uint32_t* b,
-                           const DecodeOut& out, const DecodeLayout& L, void* ws,
-                           hipStream_t s) {
+hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
+                           const uint32_t* b, const DecodeOut& out, const DecodeLayout& L,
+                           void* ws, hipStream_t s) {
     char* base = static_cast<char*>(ws);
+    typedef typename Acc<T>::type A;
     Ctrl* ctrl = reinterpret_cast<Ctrl*>(base + L.ctrl);
     uint32_t* blk = reinterpret_cast<uint32_t*>(base + L.blk);
+    uint32_t* woff = plan ? reinterpret_cast<uint32_t*>(base + L.woff) : nullptr;
     uint32_t* elem = reinterpret_cast<uint32_t*>(base + L.elem);
-    typedef typename Acc<T>::type A;
     A* vals = reinterpret_cast<A*>(base + L.vals);
     uint8_t* peeled = reinterpret_cast<uint8_t*>(base + L.peeled);
     unsigned long long* cnt = reinterpret_cast<unsigned long long*>(base + L.cnt);
     A* yw = reinterpret_cast<A*>(base + L.yw);
     uint32_t* stamp = reinterpret_cast<uint32_t*>(base + L.stamp);
-    uint32_t* queue = reinterpret_cast<uint32_t*>(base + L.queue);
+    uint2* queue = reinterpret_cast<uint2*>(base + L.queue);
     const T* y_agg = static_cast<const T*>(y_agg_v);
+    const bool planned = plan != nullptr;
 
     DeviceInfo di;
     hipError_t e = device_info(&di);
@@ -587,17 +734,51 @@ hipError_t launch_decode_t(const Geo& g, const void* y_agg_v, const uint32_t* b,
     uint64_t grid = ((uint64_t)g.cells + kBlock - 1) / kBlock;
     if (grid > (uint64_t)di.cus * 16) grid = (uint64_t)di.cus * 16;
     hipLaunchKernelGGL(prep_kernel<T>, dim3((uint32_t)grid), dim3(kBlock), 0, s, y_agg, yw, cnt,
-                       stamp, g.cells, ctrl);
+                       stamp, g.cells, planned, ctrl);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const uint32_t last_mask = (g.n & 31u) ? ((1u << (g.n & 31u)) - 1u) : 0xffffffffu;
     hipLaunchKernelGGL(count_kernel, dim3((uint32_t)L.nchunks), dim3(kBlock), 0, s, b, g.words,
                        last_mask, blk);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, s, blk, L.nchunks, ctrl, L.cap);
+    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, s, blk, L.nchunks, ctrl, L.cap, woff,
+                       g.words);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(build_kernel, dim3((uint32_t)L.nchunks), dim3(kBlock), 0, s, b, g.words,
-                       last_mask, blk, elem, peeled, cnt, ctrl, g.seed, g.rows, g.c, g.cmask, g.log2c);
+    hipLaunchKernelGGL(compact_kernel, dim3((uint32_t)L.nchunks), dim3(kBlock), 0, s, b, g.words,
+                       last_mask, blk, elem, peeled, woff, cnt, ctrl, g.seed, g.rows, g.c,
+                       g.cmask, g.log2c);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+
+    if (planned) {
+        const PlanLayout PL = plan_layout(g);
+        const char* pb = static_cast<const char*>(plan);
+        CounterArgs ca;
+        ca.hdr = reinterpret_cast<const PlanHeader*>(pb + PL.header);
+        ca.rowoff = reinterpret_cast<const uint32_t*>(pb + PL.rowoff);
+        ca.entry = reinterpret_cast<const uint2*>(pb + PL.entry);
+        ca.b = b;
+        ca.woff = woff;
+        ca.cnt = cnt;
+        ca.stamp = stamp;
+        ca.queue = queue;
+        ca.ctrl = ctrl;
+        ca.n = g.n;
+        ca.seed = g.seed;
+        ca.words = g.words;
+        ca.nb = PL.nb;
+        ca.rows = g.rows;
+        ca.c = g.c;
+        ca.cmask = g.cmask;
+        ca.cells = g.cells;
+        ca.last_mask = last_mask;
+        uint32_t cgrid = g.rows < (uint32_t)di.cus * 8 ? g.rows : (uint32_t)di.cus * 8;
+        if (g.c == 1024)
+            hipLaunchKernelGGL(counter_kernel<1024>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+        else if (g.c == 512)
+            hipLaunchKernelGGL(counter_kernel<512>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+        else
+            hipLaunchKernelGGL(counter_kernel<256>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
 
     // persistent peel: every workgroup must be resident (cooperative launch)
     int dev = 0;
@@ -633,6 +814,7 @@ hipError_t launch_decode_t(const Geo& g, const void* y_agg_v, const uint32_t* b,
     pa.cmask = g.cmask;
     pa.log2c = g.log2c;
     pa.cells = g.cells;
+    pa.planned = planned;
     void* args[] = {&pa};
     e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&peel_kernel<A>),
                                    dim3((uint32_t)peel_grid_cache[slot]), dim3(kPeelBlock), args,
@@ -684,21 +866,22 @@ DecodeLayout decode_layout(const Geo& g, uint64_t max_support) {
     size_t o = 0;
     L.ctrl = o;    o = align256(o + sizeof(Ctrl));
     L.blk = o;     o = align256(o + L.nchunks * 4);
+    L.woff = o;    o = align256(o + (g.words + 1) * 4);
     L.elem = o;    o = align256(o + cap * 4);
     L.vals = o;    o = align256(o + cap * vsz);
     L.peeled = o;  o = align256(o + cap);
     L.cnt = o;     o = align256(o + (size_t)g.cells * 8);
     L.yw = o;      o = align256(o + (size_t)g.cells * vsz);
     L.stamp = o;   o = align256(o + (size_t)g.cells * 4);
-    L.queue = o;   o = align256(o + (size_t)g.cells * 4);
+    L.queue = o;   o = align256(o + (size_t)g.cells * 8);
     L.total = o;
     return L;
 }
 
-hipError_t launch_decode(const Geo& g, const void* y_agg, const uint32_t* b_agg,
+hipError_t launch_decode(const Geo& g, const void* plan, const void* y_agg, const uint32_t* b_agg,
                          const DecodeOut& out, const DecodeLayout& L, void* ws, hipStream_t s) {
-    if (g.f32) return launch_decode_t<float>(g, y_agg, b_agg, out, L, ws, s);
-    return launch_decode_t<int32_t>(g, y_agg, b_agg, out, L, ws, s);
+    if (g.f32) return launch_decode_t<float>(g, plan, y_agg, b_agg, out, L, ws, s);
+    return launch_decode_t<int32_t>(g, plan, y_agg, b_agg, out, L, ws, s);
 }
 
 }  // namespace hc

@@ -37,11 +37,30 @@ hipError_t launch_encode_coo(const Geo& g, const uint32_t* idx, const void* val,
 hipError_t launch_aggregate(const Geo& g, const void* y_in, const uint32_t* b_in, uint32_t W,
                             void* y_out, uint32_t* b_out, hipStream_t s);
 
+// inverse row map of a geometry ("plan"), built once per geometry
+constexpr uint32_t kPlanMagic = 0x31706368u;  // "hcp1"
+struct PlanHeader {
+    uint64_t n;
+    uint64_t seed;
+    uint32_t c;
+    uint32_t rows;
+    uint32_t magic;
+    uint32_t pad;
+};
+struct PlanLayout {
+    uint64_t nb;       // batches
+    uint64_t ntiles;   // scan tiles over the rows
+    size_t header, rowoff, entry, rowcnt, tiles, total;
+};
+PlanLayout plan_layout(const Geo& g);
+bool plan_supported(const Geo& g);  // c >= 256
+hipError_t launch_plan_build(const Geo& g, void* plan, hipStream_t s);
+
 // decode workspace layout (byte offsets into the caller's workspace)
 struct DecodeLayout {
     uint64_t cap;       // max support the workspace holds
     uint64_t nchunks;   // bitmap chunks of kChunkWords words
-    size_t ctrl, blk, elem, vals, peeled, cnt, yw, stamp, queue, total;
+    size_t ctrl, blk, woff, elem, vals, peeled, cnt, yw, stamp, queue, total;
 };
 constexpr uint32_t kChunkWords = 1024;
 DecodeLayout decode_layout(const Geo& g, uint64_t max_support);
@@ -54,8 +73,10 @@ struct DecodeOut {
     uint32_t* mask;
     void* info;   // hc_decode_info*
 };
-hipError_t launch_decode(const Geo& g, const void* y_agg, const uint32_t* b_agg,
-                         const DecodeOut& out, const DecodeLayout& L, void* ws,
-                         hipStream_t s);
+// plan: an inverse row map built for g, or nullptr (then the per-cell
+// counters are built with atomics)
+hipError_t launch_decode(const Geo& g, const void* plan, const void* y_agg,
+                         const uint32_t* b_agg, const DecodeOut& out, const DecodeLayout& L,
+                         void* ws, hipStream_t s);
 
 }  // namespace hc

@@ -34,8 +34,10 @@ def oracle_run(w, rows: int, c: int, coo: bool = True):
 
 
 def gpu_run(w, rows: int, c: int, coo_input: bool = False, want_coo_out: bool = True,
-            max_support: int = 0, keep_workers: bool = True, coo_cap=None):
-    """The same pipeline through libhc on the current GPU."""
+            max_support: int = 0, keep_workers: bool = True, coo_cap=None, use_plan=False,
+            plan=None):
+    """The same pipeline through libhc on the current GPU.  use_plan builds the
+    geometry's inverse row map and decodes with it; `plan` passes one in."""
     import torch
 
     import paper_2402_07529_amd as hc
@@ -65,8 +67,10 @@ def gpu_run(w, rows: int, c: int, coo_input: bool = False, want_coo_out: bool = 
     cap = w.n if coo_cap is None else coo_cap
     coo_idx = torch.empty(cap, dtype=torch.int32, device=dev) if want_coo_out else None
     coo_val = torch.empty(cap, dtype=vt, device=dev) if want_coo_out else None
+    if use_plan and plan is None:
+        plan = hc.make_plan(p, dev)
     hc.hc_decode(p, Ya, Ba, info, ws, x_out=out, coo_idx=coo_idx, coo_val=coo_val, mask=mask,
-                 max_support=max_support)
+                 max_support=max_support, plan=plan)
     torch.cuda.synchronize()
     inf = hc.read_info(info)
     res = dict(p=p, Ya=Ya.cpu().numpy(), Ba=Ba.cpu().numpy().view(np.uint32),

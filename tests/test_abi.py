@@ -72,10 +72,27 @@ def test_null_and_misaligned_pointers_rejected_before_launch():
     assert L.hc_encode(ctypes.byref(p), ctypes.c_void_p(18), ctypes.c_void_p(32),
                        ctypes.c_void_p(48), None) == hc.HC_EINVAL
     assert b"aligned" in L.hc_last_error()
-    assert L.hc_decode(ctypes.byref(p), ctypes.c_void_p(16), ctypes.c_void_p(16), None, None,
-                       None, 0, None, ctypes.c_void_p(16), 0, ctypes.c_void_p(64), 10**9,
-                       None) == hc.HC_EINVAL
+    V = ctypes.c_void_p
+    assert L.hc_decode(ctypes.byref(p), None, V(16), V(16), None, None, None, 0, None, V(16), 0,
+                       V(64), 10**9, None) == hc.HC_EINVAL
     assert b"aligned" in L.hc_last_error()
-    assert L.hc_decode(ctypes.byref(p), ctypes.c_void_p(16), ctypes.c_void_p(16), None, None,
-                       None, 0, None, ctypes.c_void_p(16), 0, ctypes.c_void_p(256), 10,
-                       None) == hc.HC_EWORKSPACE
+    assert L.hc_decode(ctypes.byref(p), None, V(16), V(16), None, None, None, 0, None, V(16), 0,
+                       V(256), 10, None) == hc.HC_EWORKSPACE
+    # a plan is rejected for c < 256
+    p1 = hc.make_params(1000, 3, 1, c=1)
+    assert L.hc_decode(ctypes.byref(p1), V(256), V(16), V(16), None, None, None, 0, None, V(16), 0,
+                       V(256), 10**9, None) == hc.HC_EINVAL
+
+
+def test_plan_sizes():
+    import paper_2402_07529_amd as hc
+    p = hc.hc_geometry(109_482_240, 9_305_915, 1.23, 1024, 3)
+    nb = (109_482_240 + 1023) // 1024
+    bytes_ = hc.hc_plan_bytes(p)
+    assert bytes_ >= 3 * nb * 8 + (p.rows + 1) * 4
+    with pytest.raises(hc.HCError) as ei:
+        hc.hc_plan_bytes(hc.hc_geometry(100000, 1000, 1.23, 64, 3))
+    assert ei.value.status == hc.HC_EUNSUPPORTED
+    L = hc.lib()
+    assert L.hc_plan_build(ctypes.byref(p), ctypes.c_void_p(256), 10, None) == hc.HC_EWORKSPACE
+    assert L.hc_plan_build(ctypes.byref(p), ctypes.c_void_p(100), 10**9, None) == hc.HC_EINVAL

@@ -1,6 +1,7 @@
 """Parity at the full sizes of the named workloads, in the launch
 configuration bench.py times: dense hc_encode per worker, hc_aggregate over
-the W sketches, hc_decode with max_support = the aggregate's nonzeros.
+the W sketches, hc_decode with the geometry's plan and max_support = the
+aggregate's nonzeros.
 
 int32: every stage bit-exact against the CPU oracle (per-worker sketches and
 bitmaps, aggregate, decoded gradient, mask, support size, recovered count,
@@ -44,7 +45,7 @@ def test_fullsize_int32(name):
     n_agg = w.n_agg
     rows = oracle.rows_for(n_agg)
     print(f"[fullsize] {name}: n={w.n} W={w.W} n_agg={n_agg} rows={rows}", flush=True)
-    g = gpu_run(w, rows, 1024, want_coo_out=False, max_support=n_agg)
+    g = gpu_run(w, rows, 1024, want_coo_out=False, max_support=n_agg, use_plan=True)
     o = oracle_run(w, rows, 1024)
     for i in range(w.W):
         assert np.array_equal(g["Y"][i], o["Y"][i]), f"worker {i} sketch"
@@ -65,7 +66,7 @@ def test_fullsize_vgg19_fp32():
     _hc()
     w = wl.make("vgg19", vtype="f32")
     rows = oracle.rows_for(w.n_agg)
-    g = gpu_run(w, rows, 1024, want_coo_out=False, max_support=w.n_agg)
+    g = gpu_run(w, rows, 1024, want_coo_out=False, max_support=w.n_agg, use_plan=True)
     o = oracle_run(w, rows, 1024)
     wb, ab = fp32_cell_bounds(w, o["g"])
     for i in range(w.W):
@@ -92,7 +93,7 @@ def test_fullsize_bert_sweep_corners(density, overlap):
     n_agg = w.n_agg
     rows = oracle.rows_for(n_agg)
     print(f"[fullsize] bert d={density} o={overlap}: n_agg={n_agg} rows={rows}", flush=True)
-    g = gpu_run(w, rows, 1024, want_coo_out=False, max_support=n_agg)
+    g = gpu_run(w, rows, 1024, want_coo_out=False, max_support=n_agg, use_plan=True)
     gg = oracle.Geom(n=w.n, rows=rows, seed=w.hash_seed, c=1024)
     Ys, Bs = [], []
     for i in range(w.W):

@@ -85,8 +85,8 @@ def assert_same_info(gi, oi):
     assert gi.status == 0
 
 
-def check_int(w, rows, c, coo_input=False):
-    g = gpu_run(w, rows, c, coo_input=coo_input)
+def check_int(w, rows, c, coo_input=False, use_plan=False):
+    g = gpu_run(w, rows, c, coo_input=coo_input, use_plan=use_plan)
     o = oracle_run(w, rows, c)
     for i in range(w.W):
         assert np.array_equal(g["Y"][i], o["Y"][i]), f"worker {i} sketch"
@@ -122,6 +122,44 @@ def test_multi_tile_ragged_int32(c):
     assert np.array_equal(g["x"], wrap_sum([w.dense(i) for i in range(w.W)]))
 
 
+@pytest.mark.parametrize("c", [1024, 512, 256])
+def test_multi_tile_ragged_int32_planned(c):
+    # the decode's per-cell counters gathered row by row through the plan
+    _hc()
+    w = wl.make("synthetic", n=1_000_003, W=4, density=0.01, overlap=0.4, data_seed=c + 7)
+    rows = oracle.rows_for(w.n_agg, 1.23, c)
+    g, o = check_int(w, rows, c, use_plan=True)
+    assert g["info"].success
+
+
+@pytest.mark.parametrize("ratio", [1.10, 0.8])
+def test_undersized_sketch_failure_parity_planned(ratio):
+    _hc()
+    w = wl.make("synthetic", n=2_000_000, W=4, density=0.01, overlap=0.3,
+                data_seed=int(ratio * 100) + 1)
+    rows = max(3, int(math.ceil(ratio * w.n_agg / 1024)))
+    g, o = check_int(w, rows, 1024, use_plan=True)
+    assert not g["info"].success
+
+
+def test_plan_for_other_geometry_is_reported():
+    # a plan built for another seed: detected on the device, nothing peeled,
+    # every member of the support gets the estimate from the aggregate
+    hc = _hc()
+    import torch
+    w = wl.make("synthetic", n=300_000, W=2, density=0.01, overlap=0.5, data_seed=19)
+    rows = oracle.rows_for(w.n_agg, 1.23, 1024)
+    other = hc.make_params(w.n, rows, w.hash_seed + 1, 1024)
+    plan = hc.make_plan(other, torch.device("cuda"))
+    g = gpu_run(w, rows, 1024, plan=plan)
+    o = oracle_run(w, rows, 1024)
+    inf = g["info"]
+    assert (inf.status, inf.success, inf.n_recovered) == (3, 0, 0)
+    sup = np.nonzero(np.unpackbits(o["Ba"].view(np.uint8), bitorder="little")[:w.n])[0]
+    est = np.array([oracle.query(o["g"], o["Ya"], int(p)) for p in sup], np.int32)
+    assert np.array_equal(g["x"][sup], est)
+
+
 @pytest.mark.parametrize("c", [1024, 64, 1])
 def test_coo_encode_matches_dense(c):
     _hc()
@@ -147,8 +185,8 @@ def test_forced_failure_three_cells():
     assert g["info"].n_recovered == 0 and g["info"].rounds == 0
 
 
-def check_fp32(w, rows, c):
-    g = gpu_run(w, rows, c)
+def check_fp32(w, rows, c, use_plan=False):
+    g = gpu_run(w, rows, c, use_plan=use_plan)
     o = oracle_run(w, rows, c)
     wb, ab = fp32_cell_bounds(w, o["g"])
     for i in range(w.W):
@@ -167,12 +205,13 @@ def check_fp32(w, rows, c):
     return g, o, bnd
 
 
-def test_fp32_all_stages():
+@pytest.mark.parametrize("use_plan", [False, True])
+def test_fp32_all_stages(use_plan):
     _hc()
     w = wl.make("synthetic", n=1_500_001, W=8, density=0.01, overlap=0.3, vtype="f32",
                 data_seed=77)
     rows = oracle.rows_for(w.n_agg, 1.23, 1024)
-    g, o, bnd = check_fp32(w, rows, 1024)
+    g, o, bnd = check_fp32(w, rows, 1024, use_plan=use_plan)
     assert g["info"].success
     truth = sum(w.dense(i).astype(np.float64) for i in range(w.W))
     sup = np.nonzero(truth)[0]
@@ -251,12 +290,13 @@ def test_int32_wraparound_sums():
     assert np.array_equal(g["x"], wrap_sum([w.dense(i) for i in range(3)]))
 
 
-def test_deterministic_int32_repeat():
+@pytest.mark.parametrize("use_plan", [False, True])
+def test_deterministic_int32_repeat(use_plan):
     _hc()
     w = wl.make("synthetic", n=3_000_000, W=4, density=0.01, overlap=0.5, data_seed=123)
     rows = oracle.rows_for(w.n_agg)
-    a = gpu_run(w, rows, 1024, keep_workers=False)
-    b = gpu_run(w, rows, 1024, keep_workers=False)
+    a = gpu_run(w, rows, 1024, keep_workers=False, use_plan=use_plan)
+    b = gpu_run(w, rows, 1024, keep_workers=False, use_plan=use_plan)
     for k in ("Ya", "Ba", "x", "mask", "coo_idx", "coo_val"):
         assert np.array_equal(a[k], b[k]), k
     assert a["info"] == b["info"]
