@@ -44,6 +44,8 @@ def parse():
                     help="sketch cells / aggregate nonzeros (default: gamma = 1.23)")
     ap.add_argument("--c", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="BERT-base density/overlap grid and sketch-width sweep (one JSON object)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 10 times (the known-size kernel "
                          "against which the HBM byte counters are scaled)")
@@ -136,6 +138,147 @@ def cpu_baseline(w, rows, c):
                 success=int(info.success), rounds=int(info.rounds))
 
 
+def core_fraction(lam):
+    """Edges left in the 2-core of a random 3-uniform hypergraph with lam edges
+    per vertex (x^3 for the largest root of x = 1 - exp(-3 lam x^2)); the
+    textbook prediction of the unpeeled fraction."""
+    xs = np.linspace(1e-9, 1.0, 200001)
+    f = xs - (1 - np.exp(-3 * lam * xs**2))
+    idx = np.nonzero(np.sign(f[:-1]) != np.sign(f[1:]))[0]
+    if idx.size == 0:
+        return 0.0
+    lo, hi = xs[idx[-1]], xs[idx[-1] + 1]
+    for _ in range(60):
+        mid = 0.5 * (lo + hi)
+        if (mid - (1 - np.exp(-3 * lam * mid * mid))) * (lo - (1 - np.exp(-3 * lam * lo * lo))) > 0:
+            lo = mid
+        else:
+            hi = mid
+    return float(lo) ** 3
+
+
+class Runner:
+    """Device buffers of one workload and the timed W-encode + aggregate +
+    decode iteration through the C ABI."""
+
+    def __init__(self, w, c, dev):
+        import torch
+        self.torch = torch
+        self.w, self.c, self.dev = w, c, dev
+        self.vt = torch.int32 if w.vtype == "i32" else torch.float32
+        self.x = torch.zeros((w.W, w.n), dtype=self.vt, device=dev)
+        for i in range(w.W):
+            self.x[i][torch.from_numpy(w.idx[i].astype(np.int64)).to(dev)] = \
+                torch.from_numpy(w.val[i]).to(dev)
+        self.n_agg = w.n_agg
+        self.out = torch.empty(w.n, dtype=self.vt, device=dev)
+        self.mask = torch.empty((w.n + 31) // 32, dtype=torch.int32, device=dev)
+
+    def run(self, ratio, steps, warmup, check=True):
+        import paper_2402_07529_amd as hc
+        torch, w, dev, W = self.torch, self.w, self.dev, self.w.W
+        p = hc.hc_geometry(w.n, self.n_agg, ratio, self.c, w.hash_seed, w.vtype)
+        cells, words = p.cells, p.words
+        Y = torch.empty((W, cells), dtype=self.vt, device=dev)
+        B = torch.empty((W, words), dtype=torch.int32, device=dev)
+        Ya = torch.empty(cells, dtype=self.vt, device=dev)
+        Ba = torch.empty(words, dtype=torch.int32, device=dev)
+        info = hc.alloc_info(dev)
+        ws = hc.alloc_workspace(p, self.n_agg, dev)
+        stream = torch.cuda.current_stream()
+        # the inverse row map depends only on the geometry: built once, like
+        # the sketch geometry itself, before any iteration
+        torch.cuda.synchronize()
+        t_plan = time.perf_counter()
+        plan = hc.make_plan(p, dev) if self.c >= 256 else None
+        torch.cuda.synchronize()
+        plan_ms = (time.perf_counter() - t_plan) * 1e3
+        x, out, mask = self.x, self.out, self.mask
+
+        def step(ev=None):
+            if ev is not None:
+                ev[0].record(stream)
+            for i in range(W):
+                hc.hc_encode(p, x[i], Y[i], B[i], stream)
+            if ev is not None:
+                ev[1].record(stream)
+            hc.hc_aggregate(p, Y, B, W, Ya, Ba, stream)
+            if ev is not None:
+                ev[2].record(stream)
+            hc.hc_decode(p, Ya, Ba, info, ws, x_out=out, mask=mask, max_support=self.n_agg,
+                         stream=stream, plan=plan)
+            if ev is not None:
+                ev[3].record(stream)
+
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(stream)
+        for k in range(steps):
+            step(evs[k])
+        stop.record(stream)
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(stop) / steps
+        enc_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) / W
+        agg_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+        dec_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+        inf = hc.read_info(info)
+        exact = None
+        if check:
+            # correctness of the timed result against the direct sum of the inputs
+            direct = x.sum(dim=0, dtype=torch.int64 if self.vt == torch.int32 else torch.float64)
+            if self.vt == torch.int32:
+                direct = ((direct + 2**31) % 2**32 - 2**31).to(torch.int32)
+                exact = bool(torch.equal(out, direct)) if inf.success else False
+            else:
+                exact = bool((out.double() - direct).abs().max().item() <=
+                             1e-5 * direct.abs().max().item()) if inf.success else False
+            del direct
+        return dict(p=p, ms=ms, enc_ms=enc_ms, agg_ms=agg_ms, dec_ms=dec_ms, info=inf,
+                    exact=exact, plan_ms=plan_ms)
+
+
+def sweep(a, dev):
+    """BERT-base: density x overlap grid at gamma = 1.23, then sketch widths
+    around gamma at 1 % / 50 % overlap, to chart the decode-failure boundary
+    against the 2-core closed form."""
+    import workloads as wl
+    points = []
+    for density in (0.001, 0.01, 0.05):
+        for overlap in (0.1, 0.5, 0.9):
+            w = wl.make("bert", density=density, overlap=overlap)
+            r = Runner(w, 1024, dev)
+            m = r.run(1.23, 3, 1)
+            inf = m["info"]
+            pt = dict(kind="density_overlap", density=density, overlap=overlap, n_agg=r.n_agg,
+                      ratio=round(m["p"].cells / r.n_agg, 4), value=round(4 * w.n / m["ms"] / 1e6, 2),
+                      ms_per_step=round(m["ms"], 4), encode_ms=round(m["enc_ms"], 4),
+                      aggregate_ms=round(m["agg_ms"], 4), decode_ms=round(m["dec_ms"], 4),
+                      success=inf.success, rounds=inf.rounds,
+                      recovered_frac=round(inf.n_recovered / max(inf.n_support, 1), 6),
+                      equals_direct_sum=m["exact"])
+            log(f"[sweep] {pt}")
+            points.append(pt)
+            del r
+    w = wl.make("bert", density=0.01, overlap=0.5)
+    r = Runner(w, 1024, dev)
+    for ratio in (1.10, 1.15, 1.20, 1.22, 1.23, 1.25, 1.30, 1.50, 2.00):
+        m = r.run(ratio, 2, 1, check=False)
+        inf = m["info"]
+        lam = r.n_agg / m["p"].cells
+        pt = dict(kind="width", density=0.01, overlap=0.5, ratio=round(m["p"].cells / r.n_agg, 4),
+                  success=inf.success, rounds=inf.rounds,
+                  unpeeled_frac=round(1 - inf.n_recovered / max(inf.n_support, 1), 6),
+                  predicted_unpeeled=round(core_fraction(lam), 6),
+                  decode_ms=round(m["dec_ms"], 4), ms_per_step=round(m["ms"], 4))
+        log(f"[sweep] {pt}")
+        points.append(pt)
+    print(json.dumps({"sweep": "bert-base", "points": points}), flush=True)
+
+
 def main():
     a = parse()
     if a.copy_calibration:
@@ -146,83 +289,23 @@ def main():
               f"--gpus {a.gpus} is not supported", file=sys.stderr)
         sys.exit(2)
     import torch
-    import paper_2402_07529_amd as hc
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if a.sweep:
+        sweep(a, dev)
+        return
 
+    import paper_2402_07529_amd as hc
     t0 = time.perf_counter()
     w = make_workload(a)
-    n_agg = w.n_agg
     ratio = a.ratio if a.ratio is not None else hc.GAMMA
-    p = hc.hc_geometry(w.n, n_agg, ratio, a.c, w.hash_seed, w.vtype)
-    cells, words, W = p.cells, p.words, w.W
-    log(f"[bench] workload {w.name} n={w.n} W={W} n_agg={n_agg} rows={p.rows} cells={cells} "
-        f"gen {time.perf_counter() - t0:.1f}s")
-
-    vt = torch.int32 if w.vtype == "i32" else torch.float32
-    x = torch.zeros((W, w.n), dtype=vt, device=dev)
-    for i in range(W):
-        x[i][torch.from_numpy(w.idx[i].astype(np.int64)).to(dev)] = torch.from_numpy(w.val[i]).to(dev)
-    Y = torch.empty((W, cells), dtype=vt, device=dev)
-    B = torch.empty((W, words), dtype=torch.int32, device=dev)
-    Ya = torch.empty(cells, dtype=vt, device=dev)
-    Ba = torch.empty(words, dtype=torch.int32, device=dev)
-    out = torch.empty(w.n, dtype=vt, device=dev)
-    mask = torch.empty(words, dtype=torch.int32, device=dev)
-    info = hc.alloc_info(dev)
-    ws = hc.alloc_workspace(p, n_agg, dev)
-    stream = torch.cuda.current_stream()
-    # the inverse row map depends only on the geometry: built once, like the
-    # sketch geometry itself, before any iteration
-    torch.cuda.synchronize()
-    t_plan = time.perf_counter()
-    plan = hc.make_plan(p, dev) if a.c >= 256 else None
-    torch.cuda.synchronize()
-    plan_ms = (time.perf_counter() - t_plan) * 1e3
-
-    def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
-        for i in range(W):
-            hc.hc_encode(p, x[i], Y[i], B[i], stream)
-        if ev is not None:
-            ev[1].record(stream)
-        hc.hc_aggregate(p, Y, B, W, Ya, Ba, stream)
-        if ev is not None:
-            ev[2].record(stream)
-        hc.hc_decode(p, Ya, Ba, info, ws, x_out=out, mask=mask, max_support=n_agg, stream=stream,
-                     plan=plan)
-        if ev is not None:
-            ev[3].record(stream)
-
-    for _ in range(a.warmup):
-        step()
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(a.steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for k in range(a.steps):
-        step(evs[k])
-    stop.record(stream)
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(stop)
-    ms = total_ms / a.steps
-    enc_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) / W
-    agg_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    dec_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-    inf = hc.read_info(info)
-
-    # correctness of the timed result against the direct sum of the inputs
-    direct = x.sum(dim=0, dtype=torch.int64 if vt == torch.int32 else torch.float64)
-    if vt == torch.int32:
-        direct = ((direct + 2**31) % 2**32 - 2**31).to(torch.int32)
-        exact = bool(torch.equal(out, direct)) if inf.success else False
-    else:
-        exact = bool((out.double() - direct).abs().max().item() <=
-                     1e-5 * direct.abs().max().item()) if inf.success else False
-    del direct
+    log(f"[bench] workload {w.name} n={w.n} W={w.W} gen {time.perf_counter() - t0:.1f}s")
+    r = Runner(w, a.c, dev)
+    m = r.run(ratio, a.steps, a.warmup)
+    p, inf, W, n_agg = m["p"], m["info"], w.W, r.n_agg
+    ms, enc_ms, agg_ms, dec_ms = m["ms"], m["enc_ms"], m["agg_ms"], m["dec_ms"]
+    cells = p.cells
 
     enc_b, agg_b, dec_b = algorithmic_bytes(w.n, W, cells, inf.n_support)
     iter_b = W * enc_b + agg_b + dec_b
@@ -232,7 +315,7 @@ def main():
         "metric": METRIC, "value": round(value, 3), "unit": "GB/s", "n_gpus": 1,
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "int32" if vt == torch.int32 else "fp32", "data": "synthetic",
+        "dtype": "int32" if w.vtype == "i32" else "fp32", "data": "synthetic",
         "config": {"workload": w.name, "n": w.n, "workers": W, "n_agg": n_agg,
                    "rows": int(p.rows), "c": a.c, "cells": cells, "ratio": round(cells / max(n_agg, 1), 4),
                    **{k: v for k, v in w.params.items() if k in ("density", "overlap", "rows_per_worker")}},
@@ -247,12 +330,12 @@ def main():
         "stages_gbs_dense": {"encode": round(4 * w.n / (enc_ms * 1e-3) / 1e9, 1),
                              "aggregate": round(4 * w.n / (agg_ms * 1e-3) / 1e9, 1),
                              "decode": round(4 * w.n / (dec_ms * 1e-3) / 1e9, 1)},
-        "plan_build_ms_once": round(plan_ms, 3),
+        "plan_build_ms_once": round(m["plan_ms"], 3),
         "decode": {"success": inf.success, "n_support": inf.n_support,
                    "n_recovered": inf.n_recovered, "rounds": inf.rounds, "status": inf.status,
-                   "equals_direct_sum": exact},
+                   "equals_direct_sum": m["exact"]},
     }
-    del x, Y, B, ws
+    del r
     torch.cuda.empty_cache()
     if not a.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
