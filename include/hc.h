@@ -41,6 +41,19 @@
  *   Y[cells] holds int32 (wrapping, like a switch's integer adders) or fp32.
  *   B[ceil(n/32)] is a bitmap, bit p = bit (p mod 32) of word p / 32; bits at
  *   or past n are zero.
+ *
+ * Blocked sketch (section 3.2: the sketch split into blocks of a fixed size so
+ * that peeling takes O(1) rounds), selected by hc_params.block = K > 0: batch b
+ * belongs to parameter block q = b / K (the last block may be shorter), the
+ * sketch has nblocks = ceil(ceil(n/c) / K) blocks of R_b = rows / nblocks rows
+ * each, and block q owns rows [q * R_b, (q+1) * R_b): the three rows of batch b
+ * are drawn as above from R_b instead of rows and offset by q * R_b.  Every
+ * block then peels on its own.  K * c must be a multiple of 32 and rows a
+ * multiple of nblocks with R_b >= 3.  The library's encode and decode of a
+ * blocked sketch hold one block per workgroup in LDS, which needs K <= 1024
+ * and, per block, R_b * c * (8 for int32, 12 for fp32) + 12 * K + 256 bytes
+ * <= 160 KiB (HC_EUNSUPPORTED otherwise; hc_encode_coo and hc_aggregate
+ * accept any blocked geometry).
  */
 #ifndef HC_H
 #define HC_H
@@ -59,7 +72,8 @@ typedef enum {
     HC_EINVAL = 1,        /* invalid argument (null pointer, bad geometry, size) */
     HC_EWORKSPACE = 2,    /* decode workspace smaller than hc_sizes reports       */
     HC_EHIP = 3,          /* a HIP runtime call failed (launch, device query)     */
-    HC_EUNSUPPORTED = 4   /* valid but not implemented (k != 3)                   */
+    HC_EUNSUPPORTED = 4   /* valid but not implemented (k != 3, blocked sketches
+                             beyond the LDS kernels' limits)                      */
 } hc_status;
 
 typedef enum { HC_I32 = 0, HC_F32 = 1 } hc_vtype;
@@ -72,7 +86,8 @@ typedef struct {
     uint64_t rows;     /* sketch rows R >= 3; cells = rows * c must be < 2^32    */
     uint64_t seed;     /* hash seed                                               */
     uint32_t vtype;    /* hc_vtype of the gradient and sketch values             */
-    uint32_t reserved; /* must be 0                                               */
+    uint32_t block;    /* batches per parameter block of a blocked sketch
+                          (section 3.2); 0 = one global sketch                   */
 } hc_params;
 
 /* Written by hc_decode into DEVICE memory. */
@@ -97,9 +112,25 @@ typedef struct {
 hc_status hc_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
                       uint64_t seed, hc_vtype vtype, hc_params *out);
 
+/* Geometry of a blocked sketch (section 3.2 blocking) whose blocks have at most
+ * block_rows rows: K = floor(block_rows * n / (gamma * n_nonzero)) batches per
+ * block, so that a block's expected share of the aggregate's n_nonzero
+ * nonzeros times gamma fills its rows, clamped to [1, min(1024, batches)] and
+ * rounded down to a multiple of max(1, 32 / c); each block then gets
+ * R_b = min(block_rows, max(3, ceil(ceil(gamma * s) / c))) rows, s = the
+ * expected share of a block of K batches rounded up, and rows = nblocks * R_b.
+ * Per-block supports scatter around the expected share, so gamma must leave
+ * room for the fullest block (about 1.3 at 14 thousand nonzeros per block where
+ * the global sketch needs 1.23).  `out` is a HOST pointer.  HC_EINVAL on invalid
+ * arguments, HC_EUNSUPPORTED if a block would not fit the LDS kernels. */
+hc_status hc_geometry_blocked(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
+                              uint32_t block_rows, uint64_t seed, hc_vtype vtype,
+                              hc_params *out);
+
 /* Byte sizes (HOST outputs, each may be NULL): one sketch Y, one bitmap B, and
  * the decode workspace for a support of up to max_support nonzeros
- * (0 means n, which always suffices). */
+ * (0 means n, which always suffices; a blocked sketch's workspace does not
+ * depend on it). */
 hc_status hc_sizes(const hc_params *p, uint64_t max_support, size_t *y_bytes,
                    size_t *b_bytes, size_t *ws_bytes);
 
@@ -109,7 +140,7 @@ hc_status hc_sizes(const hc_params *p, uint64_t max_support, size_t *y_bytes,
  * be assembled by one workgroup that gathers its contributions instead of
  * receiving scattered atomics.  It depends only on (n, c, rows, seed): build it
  * once per geometry and reuse it for every worker and iteration.  Requires
- * c >= 256 (HC_EUNSUPPORTED otherwise).  hc_plan_bytes writes the size to the
+ * c >= 256 and an unblocked sketch (HC_EUNSUPPORTED otherwise).  hc_plan_bytes writes the size to the
  * HOST pointer `bytes`; hc_plan_build fills a caller-owned, 256-byte aligned
  * DEVICE buffer of at least that size, asynchronously on `stream`. */
 hc_status hc_plan_bytes(const hc_params *p, size_t *bytes);
@@ -119,7 +150,8 @@ hc_status hc_plan_build(const hc_params *p, void *plan, size_t plan_bytes, hipSt
  * y[cells] with the Count Sketch (Y[h_j(p)] += g_j(p) * x_p for every nonzero
  * x_p, section 3.1 with the batching of 3.4) and b[ceil(n/32)] with the
  * nonzero bitmap (section 3.2).  No pre-zeroing is needed.  fp32 sums are
- * accumulated with atomics, so their rounding order is not fixed. */
+ * accumulated with atomics (global, or in LDS for a blocked sketch), so their
+ * rounding order is not fixed. */
 hc_status hc_encode(const hc_params *p, const void *x, void *y, uint32_t *b,
                     hipStream_t stream);
 
@@ -141,7 +173,10 @@ hc_status hc_aggregate(const hc_params *p, const void *y_in, const uint32_t *b_i
  * plan: a plan built for the same geometry (then the per-cell counters are
  * gathered row by row, without atomics), or NULL (they are built with
  * atomics).  Results are identical either way; a plan built for another
- * geometry is detected on the device and reported as status 3.
+ * geometry is detected on the device and reported as status 3.  A blocked
+ * sketch takes no plan (HC_EINVAL if one is given): each block is peeled by one
+ * workgroup in LDS, in the same synchronous rounds; info->rounds is then the
+ * largest round count of any block, and max_support is not used.
  * Outputs (each may be NULL):
  *   x_out[n]              dense sum X: recovered values, the Count Sketch
  *                         median estimate for members of the support that

@@ -34,7 +34,8 @@ GAMMA = 1.23  # section 3.2
 
 class _Geom(ctypes.Structure):
     _fields_ = [("n", ctypes.c_uint64), ("k", ctypes.c_uint32), ("c", ctypes.c_uint32),
-                ("rows", ctypes.c_uint64), ("seed", ctypes.c_uint64)]
+                ("rows", ctypes.c_uint64), ("seed", ctypes.c_uint64),
+                ("block", ctypes.c_uint32), ("pad", ctypes.c_uint32)]
 
 
 class _Info(ctypes.Structure):
@@ -50,17 +51,28 @@ class Geom:
     seed: int
     c: int = 1024
     k: int = 3
+    block: int = 0  # batches per parameter block of a blocked sketch; 0 = one sketch
 
     @property
     def cells(self) -> int:
         return self.rows * self.c
 
     @property
+    def nblocks(self) -> int:
+        if self.block == 0:
+            return 1
+        return ((self.n + self.c - 1) // self.c + self.block - 1) // self.block
+
+    @property
+    def block_rows(self) -> int:
+        return self.rows // self.nblocks
+
+    @property
     def words(self) -> int:
         return (self.n + 31) // 32
 
     def _c(self) -> _Geom:
-        return _Geom(self.n, self.k, self.c, self.rows, self.seed & (2**64 - 1))
+        return _Geom(self.n, self.k, self.c, self.rows, self.seed & (2**64 - 1), self.block, 0)
 
 
 @dataclass(frozen=True)
@@ -84,6 +96,11 @@ def lib():
         L.hco_check_geom.restype = ctypes.c_int
         L.hco_rows_for.argtypes = [ctypes.c_uint64, ctypes.c_double, ctypes.c_uint32]
         L.hco_rows_for.restype = ctypes.c_uint64
+        L.hco_blocked_geometry.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double,
+                                           ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
+                                           ctypes.POINTER(ctypes.c_uint32),
+                                           ctypes.POINTER(ctypes.c_uint64)]
+        L.hco_blocked_geometry.restype = ctypes.c_int
         L.hco_splitmix64.argtypes = [ctypes.c_uint64, ctypes.c_uint64, P]
         L.hco_splitmix64.restype = None
         L.hco_batch_hash.argtypes = [G, ctypes.c_uint64, P, P, P]
@@ -134,6 +151,17 @@ def rows_for(n_nonzero: int, gamma: float = GAMMA, c: int = 1024) -> int:
 
 def geometry(n: int, n_nonzero: int, seed: int, c: int = 1024, gamma: float = GAMMA) -> Geom:
     return Geom(n=n, rows=rows_for(n_nonzero, gamma, c), seed=seed, c=c)
+
+
+def blocked_geometry(n: int, n_nonzero: int, seed: int, c: int = 1024, gamma: float = GAMMA,
+                     block_rows: int = 16, max_block: int = 1024) -> Geom:
+    """Blocked sketch sized for an expected n_nonzero (hco_blocked_geometry)."""
+    blk = ctypes.c_uint32()
+    rows = ctypes.c_uint64()
+    if lib().hco_blocked_geometry(n, n_nonzero, gamma, c, block_rows, max_block,
+                                  ctypes.byref(blk), ctypes.byref(rows)):
+        raise ValueError("invalid blocked geometry arguments")
+    return Geom(n=n, rows=int(rows.value), seed=seed, c=c, block=int(blk.value))
 
 
 def check(g: Geom) -> bool:

@@ -9,7 +9,7 @@ def build(verbose: bool = False) -> str:
     src = os.path.join(HERE, "hco.c")
     out = os.path.join(HERE, "libhco.so")
     tmp = out + ".tmp"
-    cmd = ["gcc", "-std=c99", "-O2", "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, src]
+    cmd = ["gcc", "-std=c99", "-O2", "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, src, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)

@@ -10,6 +10,7 @@
  */
 #include "hco.h"
 
+#include <math.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -45,6 +46,15 @@ static uint64_t scale32(uint64_t h, uint64_t range)
     return ((h & 0xffffffffULL) * range) >> 32;
 }
 
+uint64_t hco_nblocks(const hco_geom *g)
+{
+    if (g->block == 0) return 1;
+    uint64_t batches = (g->n + g->c - 1) / g->c;
+    return (batches + g->block - 1) / g->block;
+}
+
+uint64_t hco_block_rows(const hco_geom *g) { return g->rows / hco_nblocks(g); }
+
 int hco_check_geom(const hco_geom *g)
 {
     if (!g) return -1;
@@ -53,6 +63,12 @@ int hco_check_geom(const hco_geom *g)
     if (g->n == 0 || g->n > 0xffffffffULL) return -1;
     if (g->rows < 3) return -1;
     if (g->rows > 0xffffffffULL / g->c) return -1; /* cells < 2^32 */
+    if (g->block != 0) {
+        /* every block owns the same whole number of rows, at least three */
+        uint64_t nb = hco_nblocks(g);
+        if (((uint64_t)g->block * g->c) % 32 != 0) return -1;
+        if (g->rows % nb != 0 || g->rows / nb < 3) return -1;
+    }
     return 0;
 }
 
@@ -67,15 +83,42 @@ uint64_t hco_rows_for(uint64_t n_nonzero, double gamma, uint32_t c)
     return rows < 3 ? 3 : rows;
 }
 
+int hco_blocked_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
+                         uint32_t block_rows, uint32_t max_block, uint32_t *block,
+                         uint64_t *rows)
+{
+    if (n == 0 || n_nonzero == 0 || n_nonzero > n || !(gamma > 0.0)) return -1;
+    if (c == 0 || c > 1024 || (c & (c - 1)) != 0 || block_rows < 3 || max_block == 0) return -1;
+    uint64_t batches = (n + c - 1) / c;
+    /* batches whose expected support times gamma fills block_rows rows */
+    double k = floor((double)block_rows * (double)n / (gamma * (double)n_nonzero));
+    uint64_t K = k < 1.0 ? 1 : (uint64_t)k;
+    if (K > max_block) K = max_block;
+    if (K > batches) K = batches;
+    uint64_t unit = c >= 32 ? 1 : 32 / c; /* whole bitmap words per block */
+    K -= K % unit;
+    if (K == 0) K = unit;
+    /* the expected support of a block of K batches, and the rows it needs */
+    double share = (double)n_nonzero * (double)(K * c) / (double)n;
+    uint64_t rb = hco_rows_for((uint64_t)ceil(share), gamma, c);
+    if (rb > block_rows) rb = block_rows;
+    uint64_t nblocks = (batches + K - 1) / K;
+    *block = (uint32_t)K;
+    *rows = nblocks * rb;
+    return 0;
+}
+
 /* Section 3.1: three hash indexes and three signs per index; section 3.4: one
- * row index and one random rotation per batch of c parameters and per hash. */
+ * row index and one random rotation per batch of c parameters and per hash;
+ * section 3.2: with a blocked sketch the rows come from the batch's block. */
 void hco_batch_hash(const hco_geom *g, uint64_t b, uint64_t row[3],
                     uint32_t bias[3], int32_t sign[3])
 {
     uint64_t h[3];
     for (int j = 0; j < 3; j++) h[j] = sm64_output(g->seed, 3u * b + (uint64_t)j);
 
-    uint64_t R = g->rows;
+    uint64_t R = g->block ? hco_block_rows(g) : g->rows;
+    uint64_t base = g->block ? (b / g->block) * R : 0;
     uint64_t r0 = scale32(h[0], R);
     uint64_t r1 = scale32(h[1], R - 1);
     if (r1 >= r0) r1++;
@@ -84,9 +127,9 @@ void hco_batch_hash(const hco_geom *g, uint64_t b, uint64_t row[3],
     uint64_t r2 = scale32(h[2], R - 2);
     if (r2 >= lo) r2++;
     if (r2 >= hi) r2++;
-    row[0] = r0;
-    row[1] = r1;
-    row[2] = r2;
+    row[0] = base + r0;
+    row[1] = base + r1;
+    row[2] = base + r2;
 
     for (int j = 0; j < 3; j++) {
         bias[j] = (uint32_t)((h[j] >> 32) & (uint64_t)(g->c - 1));

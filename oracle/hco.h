@@ -29,6 +29,15 @@
  *   g_j     = +1 if bit 63 of h_j is 0, else -1     (sign hash, section 3.1)
  *   cell_j(p) = r_j * c + ((t + bias_j) & (c - 1))
  *   B bit p = bit (p & 31) of 32-bit word p >> 5; bits past n are zero.
+ *
+ * Blocked sketch (section 3.2: the sketch split into blocks of a fixed size
+ * so that peeling ends in O(1) rounds).  With block = K > 0 the batches are
+ * grouped K at a time into parameter blocks q = b / K (the last one may be
+ * shorter), and block q owns its own R_b = rows / nblocks consecutive rows:
+ * the three rows above are drawn from R_b instead of R and offset by q * R_b.
+ * An element's cells then all lie in its block's rows, so the blocks peel
+ * independently.  K * c must be a multiple of 32 (whole bitmap words per
+ * block).  block = 0 is the single global sketch (one block).
  */
 #ifndef HCO_H
 #define HCO_H
@@ -44,6 +53,8 @@ typedef struct {
     uint32_t c;     /* batch width, power of two in [1, 1024]                 */
     uint64_t rows;  /* sketch rows R >= 3; cells = R * c < 2^32               */
     uint64_t seed;  /* hash seed shared by all workers                        */
+    uint32_t block; /* batches per parameter block; 0 = one global sketch     */
+    uint32_t pad;
 } hco_geom;
 
 typedef struct {
@@ -59,6 +70,22 @@ int hco_check_geom(const hco_geom *g);
 /* rows = max(3, ceil(ceil(gamma * n_nonzero) / c)) -- sketch size >= gamma*n
  * (section 3.2, gamma = 1.23). */
 uint64_t hco_rows_for(uint64_t n_nonzero, double gamma, uint32_t c);
+
+/* Blocked sizing (a reading; the paper fixes only that blocks have a fixed
+ * size): every block has block_rows rows; a block holds
+ * K = floor(block_rows * n / (gamma * n_nonzero)) batches, clamped to
+ * [1, min(max_block, batches)], so that its expected share of the support
+ * times gamma fills its rows, then rounded down to a multiple of
+ * max(1, 32 / c) so that a block holds whole bitmap words; R_b is
+ * rows_for(the expected share of a block of K batches), at most block_rows.
+ * Writes *block = K and *rows = nblocks * R_b.  Returns 0, or -1 on invalid
+ * arguments. */
+int hco_blocked_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
+                         uint32_t block_rows, uint32_t max_block, uint32_t *block,
+                         uint64_t *rows);
+/* Number of parameter blocks and rows per block of a geometry. */
+uint64_t hco_nblocks(const hco_geom *g);
+uint64_t hco_block_rows(const hco_geom *g);
 
 /* SplitMix64: `count` consecutive outputs for state `seed`. */
 void hco_splitmix64(uint64_t seed, uint64_t count, uint64_t *out);

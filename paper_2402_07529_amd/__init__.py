@@ -6,6 +6,7 @@ PyTorch supplies device memory and the current stream.  The names mirror the
 C ABI:
 
     hc_geometry   sketch sizing, |Y| >= gamma * n (section 3.2, gamma = 1.23)
+    hc_geometry_blocked  the same for a blocked sketch (section 3.2 blocking)
     hc_sizes      byte sizes of Y, B and the decode workspace
     hc_plan_bytes, hc_plan_build   inverse row map of a geometry (c >= 256)
     hc_encode     Algorithm 1 phase I on a dense gradient (sections 3.1-3.4)
@@ -30,7 +31,7 @@ HC_I32, HC_F32 = 0, 1
 GAMMA = 1.23
 INFO_BYTES = 32
 
-EXPORTS = ("hc_geometry", "hc_sizes", "hc_plan_bytes", "hc_plan_build", "hc_encode",
+EXPORTS = ("hc_geometry", "hc_geometry_blocked", "hc_sizes", "hc_plan_bytes", "hc_plan_build", "hc_encode",
            "hc_encode_coo", "hc_aggregate", "hc_decode", "hc_status_string", "hc_last_error")
 
 
@@ -43,7 +44,7 @@ class HCError(RuntimeError):
 class hc_params(ctypes.Structure):
     _fields_ = [("n", ctypes.c_uint64), ("k", ctypes.c_uint32), ("c", ctypes.c_uint32),
                 ("rows", ctypes.c_uint64), ("seed", ctypes.c_uint64),
-                ("vtype", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
+                ("vtype", ctypes.c_uint32), ("block", ctypes.c_uint32)]
 
     @property
     def cells(self) -> int:
@@ -57,6 +58,16 @@ class hc_params(ctypes.Structure):
     def is_f32(self) -> bool:
         return int(self.vtype) == HC_F32
 
+    @property
+    def nblocks(self) -> int:
+        if int(self.block) == 0:
+            return 1
+        return ((int(self.n) + int(self.c) - 1) // int(self.c) + int(self.block) - 1) // int(self.block)
+
+    @property
+    def block_rows(self) -> int:
+        return int(self.rows) // self.nblocks
+
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"libhc.so not built at {LIB_PATH}; run python -m paper_2402_07529_amd.build")
@@ -66,6 +77,9 @@ _P = ctypes.c_void_p
 _PP = ctypes.POINTER(hc_params)
 _lib.hc_geometry.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double, ctypes.c_uint32,
                              ctypes.c_uint64, ctypes.c_int, _PP]
+_lib.hc_geometry_blocked.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double,
+                                     ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64,
+                                     ctypes.c_int, _PP]
 _lib.hc_sizes.argtypes = [_PP, ctypes.c_uint64, ctypes.POINTER(ctypes.c_size_t),
                           ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)]
 _lib.hc_encode.argtypes = [_PP, _P, _P, _P, _P]
@@ -75,7 +89,7 @@ _lib.hc_decode.argtypes = [_PP, _P, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P,
                            _P, ctypes.c_size_t, _P]
 _lib.hc_plan_bytes.argtypes = [_PP, ctypes.POINTER(ctypes.c_size_t)]
 _lib.hc_plan_build.argtypes = [_PP, _P, ctypes.c_size_t, _P]
-for _f in ("hc_geometry", "hc_sizes", "hc_plan_bytes", "hc_plan_build", "hc_encode",
+for _f in ("hc_geometry", "hc_geometry_blocked", "hc_sizes", "hc_plan_bytes", "hc_plan_build", "hc_encode",
            "hc_encode_coo", "hc_aggregate", "hc_decode"):
     getattr(_lib, _f).restype = ctypes.c_int
 _lib.hc_status_string.argtypes = [ctypes.c_int]
@@ -134,8 +148,19 @@ def hc_geometry(n: int, n_nonzero: int, gamma: float = GAMMA, c: int = 1024, see
     return p
 
 
-def make_params(n: int, rows: int, seed: int, c: int = 1024, vtype: str = "i32") -> hc_params:
-    return hc_params(n, 3, c, rows, seed & (2**64 - 1), HC_F32 if vtype == "f32" else HC_I32, 0)
+def hc_geometry_blocked(n: int, n_nonzero: int, gamma: float = 1.3, c: int = 1024,
+                        block_rows: int = 18, seed: int = 0, vtype: str = "i32") -> hc_params:
+    p = hc_params()
+    vt = HC_F32 if vtype in ("f32", HC_F32) else HC_I32
+    _check(_lib.hc_geometry_blocked(n, n_nonzero, gamma, c, block_rows, seed & (2**64 - 1), vt,
+                                    ctypes.byref(p)), "hc_geometry_blocked")
+    return p
+
+
+def make_params(n: int, rows: int, seed: int, c: int = 1024, vtype: str = "i32",
+                block: int = 0) -> hc_params:
+    return hc_params(n, 3, c, rows, seed & (2**64 - 1), HC_F32 if vtype == "f32" else HC_I32,
+                     block)
 
 
 def hc_sizes(p: hc_params, max_support: int = 0):

@@ -5,7 +5,8 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = ["hc_api.hip", "hc_encode.hip", "hc_aggregate.hip", "hc_decode.hip", "hc_plan.hip"]
+SOURCES = ["hc_api.hip", "hc_encode.hip", "hc_aggregate.hip", "hc_decode.hip", "hc_plan.hip",
+           "hc_blocked.hip"]
 LIB = os.path.join(HERE, "libhc.so")
 ARCH = os.environ.get("HC_OFFLOAD_ARCH", "gfx950")
 

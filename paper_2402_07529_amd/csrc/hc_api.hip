@@ -31,7 +31,6 @@ bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 // Validate the public params and convert them to the kernels' form.
 hc_status to_geo(const hc_params* p, Geo* g) {
     if (p == nullptr) return fail(HC_EINVAL, "params is NULL");
-    if (p->reserved != 0) return fail(HC_EINVAL, "params.reserved must be 0");
     if (p->k != 3) return fail(HC_EUNSUPPORTED, "only k = 3 hashes are implemented");
     if (p->vtype != HC_I32 && p->vtype != HC_F32) return fail(HC_EINVAL, "unknown vtype");
     if (p->n == 0 || p->n > 0xffffffffull) return fail(HC_EINVAL, "n must be in [1, 2^32 - 1]");
@@ -49,6 +48,33 @@ hc_status to_geo(const hc_params* p, Geo* g) {
     g->cells = (uint32_t)(p->rows * p->c);
     g->seed = p->seed;
     g->f32 = p->vtype == HC_F32;
+    g->block = p->block;
+    g->brows = g->rows;
+    g->nblocks = 1;
+    if (p->block != 0) {
+        // section 3.2 blocking: whole bitmap words per block, and every block
+        // owning the same whole number (>= 3) of rows
+        if (((uint64_t)p->block * p->c) % 32 != 0)
+            return fail(HC_EINVAL, "block * c must be a multiple of 32");
+        const uint64_t batches = (p->n + p->c - 1) / p->c;
+        const uint64_t nblocks = (batches + p->block - 1) / p->block;
+        if (p->rows % nblocks != 0)
+            return fail(HC_EINVAL, "rows must be a multiple of the number of blocks");
+        if (p->rows / nblocks < 3) return fail(HC_EINVAL, "every block needs >= 3 rows");
+        g->brows = (uint32_t)(p->rows / nblocks);
+        g->nblocks = (uint32_t)nblocks;
+    }
+    return HC_OK;
+}
+
+// The LDS kernels of a blocked sketch hold one block per workgroup.
+hc_status blocked_supported(const Geo& g) {
+    if (g.block > kBlockedMaxBatches) return fail(HC_EUNSUPPORTED, "block must be <= 1024 batches");
+    if ((uint64_t)g.brows * g.c > 65536) return fail(HC_EUNSUPPORTED, "a block's sketch must have <= 65536 cells");
+    // the kernels' own static LDS (barrier reductions) comes on top
+    if (blocked_encode_lds(g) + kLdsReserve > kLdsBytes ||
+        blocked_decode_lds(g) + kLdsReserve > kLdsBytes)
+        return fail(HC_EUNSUPPORTED, "a block's sketch does not fit in one workgroup's LDS");
     return HC_OK;
 }
 
@@ -120,6 +146,52 @@ hc_status hc_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c, 
     return HC_OK;
 }
 
+hc_status hc_geometry_blocked(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
+                              uint32_t block_rows, uint64_t seed, hc_vtype vtype, hc_params* out) {
+    g_last_error.clear();
+    if (out == nullptr) return fail(HC_EINVAL, "out is NULL");
+    if (!(gamma > 0.0) || !isfinite(gamma)) return fail(HC_EINVAL, "gamma must be > 0");
+    if (c == 0 || c > 1024 || (c & (c - 1)) != 0)
+        return fail(HC_EINVAL, "c must be a power of two in [1, 1024]");
+    if (n == 0 || n > 0xffffffffull) return fail(HC_EINVAL, "n must be in [1, 2^32 - 1]");
+    if (n_nonzero == 0 || n_nonzero > n) return fail(HC_EINVAL, "n_nonzero must be in [1, n]");
+    if (block_rows < 3) return fail(HC_EINVAL, "block_rows must be >= 3");
+    const uint64_t batches = (n + c - 1) / c;
+    // batches per block whose expected share of the support, times gamma,
+    // fills block_rows rows; whole bitmap words per block
+    const double kk = floor((double)block_rows * (double)n / (gamma * (double)n_nonzero));
+    uint64_t K = kk < 1.0 ? 1 : (kk > 1e18 ? (uint64_t)1e18 : (uint64_t)kk);
+    if (K > kBlockedMaxBatches) K = kBlockedMaxBatches;
+    if (K > batches) K = batches;
+    const uint64_t unit = c >= 32 ? 1 : 32 / c;
+    K -= K % unit;
+    if (K == 0) K = unit;
+    // rows of one block: sized for the expected share, at most block_rows
+    const double share = ceil((double)n_nonzero * (double)(K * c) / (double)n);
+    const double need = gamma * share;
+    uint64_t cells = (uint64_t)need;
+    if ((double)cells < need) cells++;
+    uint64_t rb = (cells + c - 1) / c;
+    if (rb < 3) rb = 3;
+    if (rb > block_rows) rb = block_rows;
+    const uint64_t nblocks = (batches + K - 1) / K;
+    hc_params p;
+    memset(&p, 0, sizeof(p));
+    p.n = n;
+    p.k = 3;
+    p.c = c;
+    p.rows = nblocks * rb;
+    p.seed = seed;
+    p.vtype = (uint32_t)vtype;
+    p.block = (uint32_t)K;
+    Geo g;
+    hc_status s = to_geo(&p, &g);
+    if (s != HC_OK) return s;
+    if ((s = blocked_supported(g)) != HC_OK) return s;
+    *out = p;
+    return HC_OK;
+}
+
 hc_status hc_sizes(const hc_params* p, uint64_t max_support, size_t* y_bytes, size_t* b_bytes,
                    size_t* ws_bytes) {
     g_last_error.clear();
@@ -128,7 +200,8 @@ hc_status hc_sizes(const hc_params* p, uint64_t max_support, size_t* y_bytes, si
     if (s != HC_OK) return s;
     if (y_bytes) *y_bytes = (size_t)g.cells * 4;
     if (b_bytes) *b_bytes = (size_t)g.words * 4;
-    if (ws_bytes) *ws_bytes = decode_layout(g, max_support).total;
+    if (ws_bytes)
+        *ws_bytes = g.block ? blocked_layout(g).total : decode_layout(g, max_support).total;
     return HC_OK;
 }
 
@@ -140,6 +213,12 @@ hc_status hc_encode(const hc_params* p, const void* x, void* y, uint32_t* b, hip
     if (!x || !y || !b) return fail(HC_EINVAL, "x, y and b must be non-NULL");
     if (!aligned(x, 4) || !aligned(y, 4) || !aligned(b, 4))
         return fail(HC_EINVAL, "x, y and b must be 4-byte aligned");
+    if (g.block) {
+        const hc_status bs = blocked_supported(g);
+        if (bs != HC_OK) return bs;
+        const hipError_t e = launch_encode_blocked(g, x, y, b, stream);
+        return e == hipSuccess ? HC_OK : fail_hip(e, "hc_encode");
+    }
     const hipError_t e = launch_encode_dense(g, x, y, b, stream);
     return e == hipSuccess ? HC_OK : fail_hip(e, "hc_encode");
 }
@@ -178,6 +257,7 @@ hc_status hc_plan_bytes(const hc_params* p, size_t* bytes) {
     const hc_status s = to_geo(p, &g);
     if (s != HC_OK) return s;
     if (!bytes) return fail(HC_EINVAL, "bytes is NULL");
+    if (g.block) return fail(HC_EUNSUPPORTED, "a blocked sketch is decoded without a plan");
     if (!plan_supported(g)) return fail(HC_EUNSUPPORTED, "plans need c >= 256");
     *bytes = plan_layout(g).total;
     return HC_OK;
@@ -188,6 +268,7 @@ hc_status hc_plan_build(const hc_params* p, void* plan, size_t plan_bytes, hipSt
     Geo g;
     const hc_status s = to_geo(p, &g);
     if (s != HC_OK) return s;
+    if (g.block) return fail(HC_EUNSUPPORTED, "a blocked sketch is decoded without a plan");
     if (!plan_supported(g)) return fail(HC_EUNSUPPORTED, "plans need c >= 256");
     if (!plan || !aligned(plan, 256)) return fail(HC_EINVAL, "plan must be non-NULL and 256-byte aligned");
     if (plan_bytes < plan_layout(g).total) return fail(HC_EWORKSPACE, "plan smaller than hc_plan_bytes reports");
@@ -203,6 +284,7 @@ hc_status hc_decode(const hc_params* p, const void* plan, const void* y_agg,
     Geo g;
     const hc_status s = to_geo(p, &g);
     if (s != HC_OK) return s;
+    if (plan && g.block) return fail(HC_EINVAL, "a blocked sketch is decoded without a plan");
     if (plan && (!plan_supported(g) || !aligned(plan, 256)))
         return fail(HC_EINVAL, "plan given for a geometry with c < 256, or not 256-byte aligned");
     if (!y_agg || !b_agg || !info || !ws) return fail(HC_EINVAL, "y_agg, b_agg, info and ws must be non-NULL");
@@ -214,8 +296,6 @@ hc_status hc_decode(const hc_params* p, const void* plan, const void* y_agg,
         return fail(HC_EINVAL, "ws must be 256-byte and info 8-byte aligned");
     if ((coo_idx == nullptr) != (coo_val == nullptr))
         return fail(HC_EINVAL, "coo_idx and coo_val must both be given or both be NULL");
-    const DecodeLayout L = decode_layout(g, max_support);
-    if (ws_bytes < L.total) return fail(HC_EWORKSPACE, "workspace smaller than hc_sizes reports");
     DecodeOut out;
     out.x_out = x_out;
     out.coo_idx = coo_idx;
@@ -223,6 +303,16 @@ hc_status hc_decode(const hc_params* p, const void* plan, const void* y_agg,
     out.coo_cap = coo_cap;
     out.mask = mask;
     out.info = info;
+    if (g.block) {
+        const hc_status bs = blocked_supported(g);
+        if (bs != HC_OK) return bs;
+        const BlockedLayout BL = blocked_layout(g);
+        if (ws_bytes < BL.total) return fail(HC_EWORKSPACE, "workspace smaller than hc_sizes reports");
+        const hipError_t e = launch_decode_blocked(g, y_agg, b_agg, out, BL, ws, stream);
+        return e == hipSuccess ? HC_OK : fail_hip(e, "hc_decode");
+    }
+    const DecodeLayout L = decode_layout(g, max_support);
+    if (ws_bytes < L.total) return fail(HC_EWORKSPACE, "workspace smaller than hc_sizes reports");
     const hipError_t e = launch_decode(g, plan, y_agg, b_agg, out, L, ws, stream);
     return e == hipSuccess ? HC_OK : fail_hip(e, "hc_decode");
 }

@@ -1,0 +1,617 @@
+// hc_blocked.hip -- the blocked sketch of section 3.2 (the Count Sketch split
+// into blocks of a fixed size, so that peeling ends in O(1) rounds), encoded
+// and decoded with one workgroup per block and the block's sketch in LDS.
+//
+// Layout: parameter block q holds batches [q*K, (q+1)*K) (K = block, the last
+// block may be shorter) and owns sketch rows [q*R_b, (q+1)*R_b).  Every cell an
+// element of block q hashes to lies in those rows, so one workgroup builds and
+// peels a block's R_b * c cells without touching any other block.
+//
+// encode  the workgroup zeroes the block's sketch in LDS, streams the block's
+//         gradient once (wave tiles of 1024 parameters, 16 coalesced dword
+//         loads per lane), writes each tile's 32 bitmap words with one 128-byte
+//         store, adds every nonzero to its three cells with LDS atomics, and
+//         stores the finished block sketch with plain coalesced stores: no
+//         global atomics and no pre-zeroing of Y.
+// decode  the workgroup loads the block's aggregated sketch into LDS as the
+//         residual and builds per-cell counters deg * 2^20 + (sum of the
+//         members' batch numbers within the block) from the bitmap.  A cell of
+//         degree one therefore names its member: the batch, whose hash table
+//         entry for the cell's row gives j and the column.  Synchronous peeling
+//         rounds (section 3.2) follow, separated by workgroup barriers: in the
+//         first half of a round every pure cell checks whether a pure cell of
+//         its member with a smaller j exists (the smallest-j rule of the global
+//         decode); in the second half the claiming cells recover x = g_j * Y,
+//         subtract g * x and the member from its other two cells, and keep
+//         their own value, marked as claimed.  The block's dense output,
+//         recovered mask and COO entries are then written by the same
+//         workgroup: a recovered element finds its value in its claimed cell,
+//         an unrecovered one gets the median estimate from the residual.
+#include <mutex>
+
+#include "../../include/hc.h"
+#include "hc_device.h"
+#include "hc_internal.h"
+
+namespace hc {
+
+namespace {
+
+constexpr int kEncThreads = 1024;
+constexpr int kDecThreads = 1024;
+constexpr uint32_t kWaveTile = 1024;          // parameters per wave tile (16 per lane)
+constexpr uint32_t kOutStep = 4 * kDecThreads;  // parameters per output iteration
+constexpr uint32_t kDegShift = 20;
+constexpr uint32_t kDegOne = 1u << kDegShift;
+constexpr uint32_t kSumMask = kDegOne - 1u;
+constexpr uint32_t kClaimed = 0x80000000u;
+constexpr uint32_t kScratchWords = 64;
+
+// Control block of the blocked decode (zeroed before the decode kernel).
+struct BCtrl {
+    unsigned long long support;
+    unsigned long long recovered;
+    unsigned int rounds;
+    unsigned int done;   // workgroups finished
+    unsigned int pad[10];
+};
+static_assert(sizeof(BCtrl) == 64, "blocked control block layout");
+
+// Hash table entry of (batch, j) within a block: local row * c in bits 0..15,
+// rotation in bits 16..25, sign in bit 31.
+__device__ __forceinline__ uint32_t tab_pack(const BatchHash& h, int j, uint32_t c) {
+    return h.row[j] * c | (h.bias[j] << 16) | (((h.neg >> j) & 1u) << 31);
+}
+__device__ __forceinline__ uint32_t tab_cell(uint32_t e, uint32_t t, uint32_t cmask) {
+    return (e & 0xffffu) + ((t + ((e >> 16) & 0x3ffu)) & cmask);
+}
+__device__ __forceinline__ bool tab_neg(uint32_t e) { return (e >> 31) != 0u; }
+
+struct BlockRange {
+    uint64_t b0;   // first batch
+    uint64_t p0;   // first parameter
+    uint64_t p1;   // one past the last parameter (<= n)
+    uint32_t nb;   // batches in the block
+};
+
+__device__ __forceinline__ BlockRange block_range(uint32_t q, uint32_t block, uint32_t log2c,
+                                                  uint32_t cmask, uint64_t n) {
+    BlockRange r;
+    r.b0 = (uint64_t)q * block;
+    r.p0 = r.b0 << log2c;
+    const uint64_t pend = r.p0 + ((uint64_t)block << log2c);
+    r.p1 = pend < n ? pend : n;
+    r.nb = (uint32_t)((r.p1 - r.p0 + cmask) >> log2c);
+    return r;
+}
+
+// Local rows, rotations and signs of the block's batches (rows drawn from the
+// block's brows rows, section 3.2 blocking of the section 3.1/3.4 hash).
+__device__ __forceinline__ void fill_table(uint32_t* s_tab, const BlockRange& r, uint64_t seed,
+                                           uint32_t brows, uint32_t c, uint32_t cmask) {
+    for (uint32_t i = threadIdx.x; i < r.nb; i += blockDim.x) {
+        const BatchHash h = batch_hash(seed, brows, cmask, r.b0 + i);
+#pragma unroll
+        for (int j = 0; j < 3; j++) s_tab[3 * i + j] = tab_pack(h, j, c);
+    }
+}
+
+template <typename T> struct LdsAdd;
+template <> struct LdsAdd<int32_t> {
+    __device__ __forceinline__ static void add(int32_t* a, int32_t v) {
+        atomicAdd(reinterpret_cast<unsigned int*>(a), (unsigned int)v);
+    }
+};
+template <> struct LdsAdd<float> {
+    __device__ __forceinline__ static void add(float* a, float v) { atomicAdd(a, v); }
+};
+template <> struct LdsAdd<double> {
+    __device__ __forceinline__ static void add(double* a, double v) { atomicAdd(a, v); }
+};
+
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+    for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d);
+    return v;
+}
+
+// Sum over the workgroup (every lane gets it).
+__device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* s_tmp) {
+    const uint32_t lane = lane_id(), wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+    v = wave_sum_u32(v);
+    if (lane == 0) s_tmp[wave] = v;
+    __syncthreads();
+    uint32_t t = 0;
+    for (uint32_t w = 0; w < nwaves; w++) t += s_tmp[w];
+    __syncthreads();
+    return t;
+}
+
+// Exclusive scan over the workgroup; *total gets the sum.
+__device__ __forceinline__ uint32_t block_scan(uint32_t v, uint32_t* s_tmp, uint32_t* total) {
+    const uint32_t lane = lane_id(), wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+    uint32_t x = v;
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t y = __shfl_up(x, d);
+        if (lane >= (uint32_t)d) x += y;
+    }
+    if (lane == 63) s_tmp[wave] = x;
+    __syncthreads();
+    uint32_t off = 0, tot = 0;
+    for (uint32_t w = 0; w < nwaves; w++) {
+        const uint32_t s = s_tmp[w];
+        if (w < wave) off += s;
+        tot += s;
+    }
+    __syncthreads();
+    *total = tot;
+    return off + x - v;
+}
+
+// Position of the r-th (0-based) set bit of w; r < popcount(w).
+__device__ __forceinline__ uint32_t select_bit(uint32_t w, uint32_t r) {
+    uint32_t pos = 0;
+#pragma unroll
+    for (uint32_t width = 16; width >= 1; width >>= 1) {
+        const uint32_t c = __popc(w & ((1u << width) - 1u));
+        if (r >= c) {
+            r -= c;
+            w >>= width;
+            pos += width;
+        }
+    }
+    return pos;
+}
+
+__device__ __forceinline__ uint32_t load_bword(const uint32_t* b, uint64_t k, uint64_t words,
+                                               uint32_t last_mask) {
+    if (k >= words) return 0u;
+    const uint32_t w = b[k];
+    return k == words - 1 ? (w & last_mask) : w;
+}
+
+// ---- encode ------------------------------------------------------------------
+
+template <typename T>
+struct EncArgs {
+    const T* x;
+    T* y;
+    uint32_t* b;
+    uint64_t n, seed;
+    uint32_t block, brows, bcells, c, cmask, log2c, y_vec;
+};
+
+template <typename T>
+__global__ __launch_bounds__(kEncThreads) void encode_blocked_kernel(EncArgs<T> a) {
+    extern __shared__ __align__(16) unsigned char lds_raw[];
+    T* s_y = reinterpret_cast<T*>(lds_raw);
+    uint32_t* s_tab = reinterpret_cast<uint32_t*>(lds_raw + (size_t)a.bcells * sizeof(T));
+    const uint32_t q = blockIdx.x;
+    const BlockRange r = block_range(q, a.block, a.log2c, a.cmask, a.n);
+    for (uint32_t i = threadIdx.x; i < a.bcells; i += kEncThreads) s_y[i] = T(0);
+    fill_table(s_tab, r, a.seed, a.brows, a.c, a.cmask);
+    __syncthreads();
+
+    const uint32_t lane = lane_id();
+    const uint32_t wave = threadIdx.x >> 6;
+    const uint32_t ntiles = (uint32_t)((r.p1 - r.p0 + kWaveTile - 1) / kWaveTile);
+    for (uint32_t tile = wave; tile < ntiles; tile += kEncThreads / 64) {
+        const uint64_t tp = r.p0 + (uint64_t)tile * kWaveTile;
+        T v[16];
+        if (tp + kWaveTile <= r.p1) {
+#pragma unroll
+            for (int m = 0; m < 16; m++) v[m] = __builtin_nontemporal_load(a.x + tp + 64u * m + lane);
+        } else {
+#pragma unroll
+            for (int m = 0; m < 16; m++) {
+                const uint64_t p = tp + 64u * m + lane;
+                v[m] = p < r.p1 ? a.x[p] : T(0);
+            }
+        }
+        // bitmap: ballot m covers parameters 64m .. 64m+63 = words 2m, 2m+1
+        uint32_t myword = 0;
+#pragma unroll
+        for (int m = 0; m < 16; m++) {
+            const uint64_t bal = __ballot(Val<T>::nonzero(v[m]));
+            if ((lane >> 1) == (uint32_t)m) myword = (lane & 1u) ? (uint32_t)(bal >> 32) : (uint32_t)bal;
+        }
+        if (lane < 32 && tp + 32ull * lane < r.p1) a.b[(tp >> 5) + lane] = myword;
+        // sketch: three LDS atomics per nonzero; the lanes of one m hold
+        // consecutive columns of one batch, i.e. consecutive cells of a row
+#pragma unroll
+        for (int m = 0; m < 16; m++) {
+            if (Val<T>::nonzero(v[m])) {
+                const uint64_t p = tp + 64u * m + lane;
+                const uint32_t bl = (uint32_t)((p >> a.log2c) - r.b0);
+                const uint32_t t = (uint32_t)p & a.cmask;
+#pragma unroll
+                for (int j = 0; j < 3; j++) {
+                    const uint32_t e = s_tab[3 * bl + j];
+                    LdsAdd<T>::add(s_y + tab_cell(e, t, a.cmask), Val<T>::sign(v[m], tab_neg(e)));
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    T* yb = a.y + (uint64_t)q * a.bcells;
+    if (a.y_vec) {
+        typedef T V4 __attribute__((ext_vector_type(4)));
+        for (uint32_t i = 4u * threadIdx.x; i < a.bcells; i += 4u * kEncThreads) {
+            const V4 v = {s_y[i], s_y[i + 1], s_y[i + 2], s_y[i + 3]};
+            __builtin_nontemporal_store(v, reinterpret_cast<V4*>(yb + i));
+        }
+    } else {
+        for (uint32_t i = threadIdx.x; i < a.bcells; i += kEncThreads) yb[i] = s_y[i];
+    }
+}
+
+// ---- decode ------------------------------------------------------------------
+
+template <typename T>
+struct DecArgs {
+    const T* y_agg;
+    const uint32_t* b;
+    const uint32_t* blk;   // support offsets of bitmap chunks (COO output only)
+    T* x_out;
+    uint32_t* mask;
+    uint32_t* coo_idx;
+    T* coo_val;
+    uint64_t coo_cap;
+    BCtrl* bctrl;
+    hc_decode_info* info;
+    uint64_t n, words, seed;
+    uint32_t block, brows, bcells, c, cmask, log2c, last_mask, x_vec;
+};
+
+__global__ void zero_bctrl_kernel(BCtrl* c) {
+    if (threadIdx.x < sizeof(BCtrl) / 4) reinterpret_cast<uint32_t*>(c)[threadIdx.x] = 0u;
+}
+
+// Which hash j of batch bl lands on the row of cell i, its table entry, and
+// the column of the member in that batch.
+__device__ __forceinline__ uint32_t member_of(const uint32_t* s_tab, uint32_t bl, uint32_t i,
+                                              uint32_t cmask, uint32_t* t_out) {
+    const uint32_t rowbase = i & ~cmask;
+    uint32_t j = 0;
+    uint32_t e = s_tab[3 * bl];
+    if ((e & 0xffffu) != rowbase) {
+        j = 1;
+        e = s_tab[3 * bl + 1];
+        if ((e & 0xffffu) != rowbase) {
+            j = 2;
+            e = s_tab[3 * bl + 2];
+        }
+    }
+    *t_out = ((i & cmask) - ((e >> 16) & 0x3ffu)) & cmask;
+    return j;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> a) {
+    typedef typename Acc<T>::type A;
+    extern __shared__ __align__(16) unsigned char lds_raw[];
+    A* s_val = reinterpret_cast<A*>(lds_raw);
+    uint32_t* s_cnt = reinterpret_cast<uint32_t*>(lds_raw + (size_t)a.bcells * sizeof(A));
+    uint32_t* s_tab = s_cnt + a.bcells;
+    uint32_t* s_tmp = s_tab + 3 * a.block;
+
+    const uint32_t q = blockIdx.x;
+    const uint32_t tid = threadIdx.x;
+    const uint32_t lane = lane_id();
+    const uint32_t wave = threadIdx.x >> 6;
+    const uint32_t cmask = a.cmask;
+    const BlockRange r = block_range(q, a.block, a.log2c, cmask, a.n);
+
+    // residual sketch and counters
+    const T* yb = a.y_agg + (uint64_t)q * a.bcells;
+    for (uint32_t i = tid; i < a.bcells; i += kDecThreads) {
+        s_val[i] = (A)yb[i];
+        s_cnt[i] = 0u;
+    }
+    fill_table(s_tab, r, a.seed, a.brows, a.c, cmask);
+    __syncthreads();
+
+    // counters from the bitmap: every wave takes 64 words at a time and hands
+    // their set bits out to its lanes in order (prefix sums of popcounts and a
+    // binary search over them), so the LDS atomics of one pass hit nearby
+    // columns of few batches
+    const uint64_t w0 = r.p0 >> 5;
+    const uint64_t w1 = (r.p1 + 31) >> 5;
+    uint32_t support = 0;
+    for (uint64_t base = w0 + 64ull * wave; base < w1; base += 64ull * (kDecThreads / 64)) {
+        const uint64_t wi = base + lane;
+        const uint32_t word = wi < w1 ? load_bword(a.b, wi, a.words, a.last_mask) : 0u;
+        const uint32_t cw = __popc(word);
+        support += cw;
+        uint32_t incl = cw;
+        for (int d = 1; d < 64; d <<= 1) {
+            const uint32_t y = __shfl_up(incl, d);
+            if (lane >= (uint32_t)d) incl += y;
+        }
+        const uint32_t total = (uint32_t)__shfl(incl, 63);
+        const uint32_t excl = incl - cw;
+        for (uint32_t s0 = 0; s0 < total; s0 += 64) {
+            const uint32_t s = s0 + lane;
+            uint32_t lo = 0;
+#pragma unroll
+            for (uint32_t step = 32; step >= 1; step >>= 1) {
+                const uint32_t cand = lo + step;
+                if ((uint32_t)__shfl(excl, (int)cand) <= s) lo = cand;
+            }
+            const uint32_t wrd = (uint32_t)__shfl(word, (int)lo);
+            const uint32_t rank = s - (uint32_t)__shfl(excl, (int)lo);
+            if (s < total) {
+                const uint64_t p = (base + lo) * 32ull + select_bit(wrd, rank);
+                const uint32_t bl = (uint32_t)((p >> a.log2c) - r.b0);
+                const uint32_t t = (uint32_t)p & cmask;
+#pragma unroll
+                for (int j = 0; j < 3; j++)
+                    atomicAdd(s_cnt + tab_cell(s_tab[3 * bl + j], t, cmask), kDegOne + bl);
+            }
+        }
+    }
+    __syncthreads();
+
+    // synchronous peeling rounds
+    const uint32_t per = (a.bcells + kDecThreads - 1) / kDecThreads;  // <= 32
+    uint32_t rounds = 0, recovered = 0;
+    for (;;) {
+        uint32_t claims = 0;
+        for (uint32_t k = 0; k < per; k++) {
+            const uint32_t i = tid + kDecThreads * k;
+            if (i >= a.bcells) break;
+            const uint32_t cc = s_cnt[i];
+            if ((cc >> kDegShift) != 1u) continue;
+            const uint32_t bl = cc & kSumMask;
+            uint32_t t;
+            const uint32_t j = member_of(s_tab, bl, i, cmask, &t);
+            bool first = true;
+            for (uint32_t jj = 0; jj < j; jj++)
+                if ((s_cnt[tab_cell(s_tab[3 * bl + jj], t, cmask)] >> kDegShift) == 1u) first = false;
+            if (first) claims |= 1u << k;
+        }
+        if (!__syncthreads_or(claims != 0u)) break;
+        rounds++;
+        while (claims) {
+            const uint32_t k = __builtin_ctz(claims);
+            claims &= claims - 1u;
+            const uint32_t i = tid + kDecThreads * k;
+            const uint32_t bl = s_cnt[i] & kSumMask;
+            uint32_t t;
+            const uint32_t j = member_of(s_tab, bl, i, cmask, &t);
+            const A xv = Val<A>::sign(s_val[i], tab_neg(s_tab[3 * bl + j]));  // x = g_j * Y
+#pragma unroll
+            for (uint32_t jj = 0; jj < 3; jj++) {
+                if (jj == j) continue;
+                const uint32_t e = s_tab[3 * bl + jj];
+                const uint32_t cell = tab_cell(e, t, cmask);
+                atomicSub(s_cnt + cell, kDegOne + bl);
+                LdsAdd<A>::add(s_val + cell, Val<A>::sign(xv, !tab_neg(e)));  // -= g * x
+            }
+            s_cnt[i] = kClaimed | bl;  // keeps g_j * x in s_val[i]
+            recovered++;
+        }
+        __syncthreads();
+    }
+
+    const uint32_t sup_total = block_sum(support, s_tmp);
+    const uint32_t rec_total = block_sum(recovered, s_tmp);
+
+    // outputs: 4 consecutive parameters per lane
+    const bool want_coo = a.coo_idx != nullptr;
+    uint64_t rank_base = 0;
+    if (want_coo) {
+        const uint64_t chunk = w0 / kChunkWords;
+        uint32_t part = 0;
+        for (uint64_t w = chunk * kChunkWords + tid; w < w0; w += kDecThreads)
+            part += __popc(load_bword(a.b, w, a.words, a.last_mask));
+        rank_base = (uint64_t)a.blk[chunk] + block_sum(part, s_tmp);
+    }
+    typedef T V4 __attribute__((ext_vector_type(4)));
+    for (uint64_t it0 = r.p0; it0 < r.p1; it0 += kOutStep) {
+        const uint64_t pp = it0 + 4u * tid;
+        uint32_t bits = 0;
+        if (pp < r.p1) bits = (load_bword(a.b, pp >> 5, a.words, a.last_mask) >> (pp & 31u)) & 0xfu;
+        uint32_t rank = 0, it_total = 0;
+        if (want_coo) rank = block_scan((uint32_t)__popc(bits), s_tmp, &it_total);
+        T out[4];
+        bool rec[4];
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            out[k] = T(0);
+            rec[k] = false;
+            if ((bits >> k) & 1u) {
+                const uint64_t p = pp + k;
+                const uint32_t bl = (uint32_t)((p >> a.log2c) - r.b0);
+                const uint32_t t = (uint32_t)p & cmask;
+                A est[3];
+                A val = A(0);
+                bool found = false;
+#pragma unroll
+                for (int j = 0; j < 3; j++) {
+                    const uint32_t e = s_tab[3 * bl + j];
+                    const uint32_t cell = tab_cell(e, t, cmask);
+                    est[j] = Val<A>::sign(s_val[cell], tab_neg(e));
+                    if (s_cnt[cell] == (kClaimed | bl)) {
+                        val = est[j];
+                        found = true;
+                    }
+                }
+                if (!found) val = median3(est[0], est[1], est[2]);
+                out[k] = (T)val;
+                rec[k] = found;
+                if (want_coo) {
+                    const uint64_t rr = rank_base + rank;
+                    if (rr < a.coo_cap) {
+                        a.coo_idx[rr] = (uint32_t)p;
+                        a.coo_val[rr] = out[k];
+                    }
+                    rank++;
+                }
+            }
+        }
+        if (a.x_out != nullptr && pp < r.p1) {
+            if (a.x_vec && pp + 4 <= a.n) {
+                const V4 v = {out[0], out[1], out[2], out[3]};
+                __builtin_nontemporal_store(v, reinterpret_cast<V4*>(a.x_out + pp));
+            } else {
+                for (int k = 0; k < 4; k++)
+                    if (pp + k < a.n) a.x_out[pp + k] = out[k];
+            }
+        }
+        if (a.mask != nullptr) {
+            const uint64_t m0 = __ballot(rec[0]), m1 = __ballot(rec[1]);
+            const uint64_t m2 = __ballot(rec[2]), m3 = __ballot(rec[3]);
+            if (lane < 8) {
+                const uint32_t s8 = 8u * lane;
+                const uint32_t mw = spread4((uint32_t)(m0 >> s8)) |
+                                    (spread4((uint32_t)(m1 >> s8)) << 1) |
+                                    (spread4((uint32_t)(m2 >> s8)) << 2) |
+                                    (spread4((uint32_t)(m3 >> s8)) << 3);
+                const uint64_t widx = ((it0 + 256u * wave) >> 5) + lane;
+                if (widx < w1) a.mask[widx] = mw;
+            }
+        }
+        rank_base += it_total;
+    }
+
+    // block totals; the last workgroup to finish writes the summary
+    if (tid == 0) {
+        atomicAdd(&a.bctrl->support, (unsigned long long)sup_total);
+        atomicAdd(&a.bctrl->recovered, (unsigned long long)rec_total);
+        atomicMax(&a.bctrl->rounds, rounds);
+        __threadfence();
+        const uint32_t ticket = atomicAdd(&a.bctrl->done, 1u);
+        if (ticket == gridDim.x - 1) {
+            __threadfence();
+            const unsigned long long sup =
+                __hip_atomic_load(&a.bctrl->support, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const unsigned long long rec =
+                __hip_atomic_load(&a.bctrl->recovered, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const unsigned int rnd =
+                __hip_atomic_load(&a.bctrl->rounds, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            a.info->n_support = sup;
+            a.info->n_recovered = rec;
+            a.info->rounds = rnd;
+            a.info->success = rec == sup ? 1u : 0u;
+            a.info->status = 0u;
+        }
+    }
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+template <typename K>
+hipError_t allow_lds(K kernel, std::once_flag& flag) {
+    hipError_t e = hipSuccess;
+    std::call_once(flag, [&] {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)(kLdsBytes - kLdsReserve));
+    });
+    return e;
+}
+
+std::once_flag g_enc_i32, g_enc_f32, g_dec_i32, g_dec_f32;
+
+template <typename T>
+hipError_t launch_encode_blocked_t(const Geo& g, const void* x, void* y, uint32_t* b,
+                                   hipStream_t s, std::once_flag& flag) {
+    hipError_t e = allow_lds(&encode_blocked_kernel<T>, flag);
+    if (e != hipSuccess) return e;
+    EncArgs<T> a;
+    a.x = static_cast<const T*>(x);
+    a.y = static_cast<T*>(y);
+    a.b = b;
+    a.n = g.n;
+    a.seed = g.seed;
+    a.block = g.block;
+    a.brows = g.brows;
+    a.bcells = g.brows * g.c;
+    a.c = g.c;
+    a.cmask = g.cmask;
+    a.log2c = g.log2c;
+    a.y_vec = (reinterpret_cast<uintptr_t>(y) & 15u) == 0 && (a.bcells & 3u) == 0;
+    hipLaunchKernelGGL(encode_blocked_kernel<T>, dim3(g.nblocks), dim3(kEncThreads),
+                       blocked_encode_lds(g), s, a);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_decode_blocked_t(const Geo& g, const void* y_agg, const uint32_t* b,
+                                   const DecodeOut& out, const BlockedLayout& L, void* ws,
+                                   hipStream_t s, std::once_flag& flag) {
+    hipError_t e = allow_lds(&decode_blocked_kernel<T>, flag);
+    if (e != hipSuccess) return e;
+    char* base = static_cast<char*>(ws);
+    BCtrl* bctrl = reinterpret_cast<BCtrl*>(base + L.bctrl);
+    uint32_t* blk = reinterpret_cast<uint32_t*>(base + L.blk);
+    hipLaunchKernelGGL(zero_bctrl_kernel, dim3(1), dim3(64), 0, s, bctrl);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    DecArgs<T> a;
+    a.coo_cap = out.coo_idx != nullptr && out.coo_val != nullptr ? out.coo_cap : 0;
+    a.coo_idx = a.coo_cap ? out.coo_idx : nullptr;
+    a.coo_val = a.coo_cap ? static_cast<T*>(out.coo_val) : nullptr;
+    if (a.coo_idx != nullptr) {
+        e = launch_support_offsets(g, b, blk, base + L.ctrl, s);
+        if (e != hipSuccess) return e;
+    }
+    a.y_agg = static_cast<const T*>(y_agg);
+    a.b = b;
+    a.blk = blk;
+    a.x_out = static_cast<T*>(out.x_out);
+    a.mask = out.mask;
+    a.bctrl = bctrl;
+    a.info = static_cast<hc_decode_info*>(out.info);
+    a.n = g.n;
+    a.words = g.words;
+    a.seed = g.seed;
+    a.block = g.block;
+    a.brows = g.brows;
+    a.bcells = g.brows * g.c;
+    a.c = g.c;
+    a.cmask = g.cmask;
+    a.log2c = g.log2c;
+    a.last_mask = (g.n & 31u) ? ((1u << (g.n & 31u)) - 1u) : 0xffffffffu;
+    a.x_vec = (reinterpret_cast<uintptr_t>(out.x_out) & 15u) == 0;
+    hipLaunchKernelGGL(decode_blocked_kernel<T>, dim3(g.nblocks), dim3(kDecThreads),
+                       blocked_decode_lds(g), s, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t blocked_encode_lds(const Geo& g) {
+    return (size_t)g.brows * g.c * 4 + (size_t)g.block * 12;
+}
+
+size_t blocked_decode_lds(const Geo& g) {
+    const size_t vsz = g.f32 ? 8 : 4;  // residual: int32, or fp64 for fp32 gradients
+    return (size_t)g.brows * g.c * (vsz + 4) + (size_t)g.block * 12 + kScratchWords * 4;
+}
+
+BlockedLayout blocked_layout(const Geo& g) {
+    BlockedLayout L;
+    L.nchunks = (g.words + kChunkWords - 1) / kChunkWords;
+    size_t o = 0;
+    L.ctrl = o;   o = align256(o + 64);
+    L.bctrl = o;  o = align256(o + sizeof(BCtrl));
+    L.blk = o;    o = align256(o + L.nchunks * 4);
+    L.total = o;
+    return L;
+}
+
+hipError_t launch_encode_blocked(const Geo& g, const void* x, void* y, uint32_t* b,
+                                 hipStream_t s) {
+    if (g.f32) return launch_encode_blocked_t<float>(g, x, y, b, s, g_enc_f32);
+    return launch_encode_blocked_t<int32_t>(g, x, y, b, s, g_enc_i32);
+}
+
+hipError_t launch_decode_blocked(const Geo& g, const void* y_agg, const uint32_t* b_agg,
+                                 const DecodeOut& out, const BlockedLayout& L, void* ws,
+                                 hipStream_t s) {
+    if (g.f32) return launch_decode_blocked_t<float>(g, y_agg, b_agg, out, L, ws, s, g_dec_f32);
+    return launch_decode_blocked_t<int32_t>(g, y_agg, b_agg, out, L, ws, s, g_dec_i32);
+}
+
+}  // namespace hc

@@ -878,6 +878,20 @@ DecodeLayout decode_layout(const Geo& g, uint64_t max_support) {
     return L;
 }
 
+hipError_t launch_support_offsets(const Geo& g, const uint32_t* b, uint32_t* blk, void* ctrl,
+                                  hipStream_t s) {
+    const uint64_t nchunks = (g.words + kChunkWords - 1) / kChunkWords;
+    const uint32_t last_mask = (g.n & 31u) ? ((1u << (g.n & 31u)) - 1u) : 0xffffffffu;
+    Ctrl* c = static_cast<Ctrl*>(ctrl);
+    hipLaunchKernelGGL(count_kernel, dim3((uint32_t)nchunks), dim3(kBlock), 0, s, b, g.words,
+                       last_mask, blk);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, s, blk, nchunks, c, g.n,
+                       static_cast<uint32_t*>(nullptr), g.words);
+    return hipGetLastError();
+}
+
 hipError_t launch_decode(const Geo& g, const void* plan, const void* y_agg, const uint32_t* b_agg,
                          const DecodeOut& out, const DecodeLayout& L, void* ws, hipStream_t s) {
     if (g.f32) return launch_decode_t<float>(g, plan, y_agg, b_agg, out, L, ws, s);

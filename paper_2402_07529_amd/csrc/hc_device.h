@@ -56,6 +56,22 @@ __device__ __forceinline__ BatchHash batch_hash(uint64_t seed, uint32_t rows, ui
     return h;
 }
 
+// The same hash for a blocked sketch: batch b belongs to parameter block
+// b / block, whose brows rows start at row (b / block) * brows; the three rows
+// are drawn from those brows.  block == 0: one global sketch of brows rows.
+__device__ __forceinline__ BatchHash batch_hash_blocked(uint64_t seed, uint32_t brows,
+                                                        uint32_t cmask, uint64_t b,
+                                                        uint32_t block) {
+    BatchHash h = batch_hash(seed, brows, cmask, b);
+    if (block != 0) {
+        const uint32_t base = (uint32_t)(b / block) * brows;
+        h.row[0] += base;
+        h.row[1] += base;
+        h.row[2] += base;
+    }
+    return h;
+}
+
 // Cell of column t under hash j.  c = cmask + 1 is a power of two.
 __device__ __forceinline__ uint32_t cell_of(const BatchHash& h, int j, uint32_t t, uint32_t c,
                                             uint32_t cmask) {

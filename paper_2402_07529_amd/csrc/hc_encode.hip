@@ -189,15 +189,15 @@ __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
 template <typename T>
 __global__ __launch_bounds__(kBlock) void encode_coo_kernel(
     const uint32_t* __restrict__ idx, const T* __restrict__ val, uint64_t nnz,
-    T* __restrict__ y, uint32_t* __restrict__ b, uint64_t n, uint64_t seed, uint32_t rows,
-    uint32_t c, uint32_t cmask, uint32_t log2c) {
+    T* __restrict__ y, uint32_t* __restrict__ b, uint64_t n, uint64_t seed, uint32_t brows,
+    uint32_t block, uint32_t c, uint32_t cmask, uint32_t log2c) {
     const uint64_t stride = (uint64_t)gridDim.x * kBlock;
     for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < nnz; i += stride) {
         const uint32_t p = idx[i];
         const T v = val[i];
         if (p >= n || !Val<T>::nonzero(v)) continue;
         atomicOr(b + (p >> 5), 1u << (p & 31u));
-        const BatchHash h = batch_hash(seed, rows, cmask, (uint64_t)(p >> log2c));
+        const BatchHash h = batch_hash_blocked(seed, brows, cmask, (uint64_t)(p >> log2c), block);
         const uint32_t t = p & cmask;
 #pragma unroll
         for (int j = 0; j < 3; j++)
@@ -269,11 +269,11 @@ hipError_t launch_encode_coo(const Geo& g, const uint32_t* idx, const void* val,
     if (g.f32)
         hipLaunchKernelGGL(encode_coo_kernel<float>, dim3(grid), dim3(kBlock), 0, s, idx,
                            static_cast<const float*>(val), nnz, static_cast<float*>(y), b, g.n,
-                           g.seed, g.rows, g.c, g.cmask, g.log2c);
+                           g.seed, g.brows, g.block, g.c, g.cmask, g.log2c);
     else
         hipLaunchKernelGGL(encode_coo_kernel<int32_t>, dim3(grid), dim3(kBlock), 0, s, idx,
                            static_cast<const int32_t*>(val), nnz, static_cast<int32_t*>(y), b,
-                           g.n, g.seed, g.rows, g.c, g.cmask, g.log2c);
+                           g.n, g.seed, g.brows, g.block, g.c, g.cmask, g.log2c);
     return hipGetLastError();
 }
 

@@ -19,6 +19,12 @@ struct Geo {
     uint32_t cells;   // rows * c
     uint64_t seed;
     bool f32;         // value type: fp32 (else int32)
+    // blocked sketch (section 3.2): block batches per parameter block, each
+    // block owning brows consecutive rows; block == 0 is one global sketch
+    // (then brows == rows and nblocks == 1)
+    uint32_t block;
+    uint32_t brows;
+    uint32_t nblocks;
 };
 
 struct DeviceInfo {
@@ -56,6 +62,20 @@ PlanLayout plan_layout(const Geo& g);
 bool plan_supported(const Geo& g);  // c >= 256
 hipError_t launch_plan_build(const Geo& g, void* plan, hipStream_t s);
 
+// blocked sketch, one workgroup per block with the block's sketch in LDS
+constexpr uint32_t kBlockedMaxBatches = 1024;  // packed LDS counters: deg * 2^20 + sum of batches
+constexpr size_t kLdsBytes = 163840;           // LDS per workgroup on gfx950
+constexpr size_t kLdsReserve = 1024;           // for the kernels' own static LDS
+size_t blocked_encode_lds(const Geo& g);
+size_t blocked_decode_lds(const Geo& g);
+struct BlockedLayout {
+    uint64_t nchunks;
+    size_t ctrl, bctrl, blk, total;
+};
+BlockedLayout blocked_layout(const Geo& g);
+hipError_t launch_encode_blocked(const Geo& g, const void* x, void* y, uint32_t* b,
+                                 hipStream_t s);
+
 // decode workspace layout (byte offsets into the caller's workspace)
 struct DecodeLayout {
     uint64_t cap;       // max support the workspace holds
@@ -78,5 +98,12 @@ struct DecodeOut {
 hipError_t launch_decode(const Geo& g, const void* plan, const void* y_agg,
                          const uint32_t* b_agg, const DecodeOut& out, const DecodeLayout& L,
                          void* ws, hipStream_t s);
+hipError_t launch_decode_blocked(const Geo& g, const void* y_agg, const uint32_t* b_agg,
+                                 const DecodeOut& out, const BlockedLayout& L, void* ws,
+                                 hipStream_t s);
+// support offsets of the bitmap chunks: blk[i] = set bits before chunk i of
+// kChunkWords words; ctrl is a 64-byte control block that the scan also uses
+hipError_t launch_support_offsets(const Geo& g, const uint32_t* b, uint32_t* blk, void* ctrl,
+                                  hipStream_t s);
 
 }  // namespace hc

@@ -96,3 +96,52 @@ def test_plan_sizes():
     L = hc.lib()
     assert L.hc_plan_build(ctypes.byref(p), ctypes.c_void_p(256), 10, None) == hc.HC_EWORKSPACE
     assert L.hc_plan_build(ctypes.byref(p), ctypes.c_void_p(100), 10**9, None) == hc.HC_EINVAL
+
+
+def test_blocked_geometry_matches_oracle():
+    import oracle
+    import paper_2402_07529_amd as hc
+    for n, nnz, gamma, c, br in ((109_482_240, 9_305_915, 1.3, 1024, 18),
+                                 (109_482_240, 273_579, 1.3, 1024, 18),
+                                 (143_667_240, 8_476_348, 1.3, 1024, 16),
+                                 (10_000, 500, 1.3, 8, 4), (65_536, 1636, 1.6, 64, 16),
+                                 (1_000_000, 999_999, 1.25, 256, 12)):
+        p = hc.hc_geometry_blocked(n, nnz, gamma, c, br, 5, "i32")
+        g = oracle.blocked_geometry(n, nnz, 5, c, gamma, br)
+        assert (int(p.block), int(p.rows)) == (g.block, g.rows)
+        assert p.nblocks == g.nblocks and p.block_rows == g.block_rows
+        _, _, ws = hc.hc_sizes(p)
+        assert ws < 4096 + (n // 32 // 1024 + 1) * 4 + 512  # control blocks and chunk offsets only
+
+
+def test_blocked_params_rejected():
+    import paper_2402_07529_amd as hc
+    L = hc.lib()
+    V = ctypes.c_void_p
+    bad = ((hc.make_params(10_000, 84, 1, c=8, block=61), hc.HC_EINVAL),    # 61 * 8 % 32
+           (hc.make_params(10_000, 85, 1, c=8, block=60), hc.HC_EINVAL),    # 85 % 21 blocks
+           (hc.make_params(10_000, 42, 1, c=8, block=60), hc.HC_EINVAL))    # 2 rows per block
+    for p, st in bad:
+        with pytest.raises(hc.HCError) as ei:
+            hc.hc_sizes(p)
+        assert ei.value.status == st
+    # valid format, beyond the LDS kernels: 30 rows of 1024 cells per block
+    p = hc.make_params(2_000_000, 30 * 62, 1, c=1024, block=32)
+    hc.hc_sizes(p)
+    assert L.hc_encode(ctypes.byref(p), V(256), V(256), V(256), None) == hc.HC_EUNSUPPORTED
+    assert L.hc_decode(ctypes.byref(p), None, V(256), V(256), None, None, None, 0, None, V(256), 0,
+                       V(256), 10**9, None) == hc.HC_EUNSUPPORTED
+    assert b"LDS" in L.hc_last_error()
+    # more than 1024 batches per block
+    p = hc.make_params(2 * 1050 * 1024, 3 * 2, 1, c=1024, block=1050)
+    assert L.hc_encode(ctypes.byref(p), V(256), V(256), V(256), None) == hc.HC_EUNSUPPORTED
+    # a blocked sketch takes no plan
+    p = hc.hc_geometry_blocked(109_482_240, 9_305_915, 1.3, 1024, 18, 3)
+    with pytest.raises(hc.HCError) as ei:
+        hc.hc_plan_bytes(p)
+    assert ei.value.status == hc.HC_EUNSUPPORTED
+    assert L.hc_decode(ctypes.byref(p), V(256), V(256), V(256), None, None, None, 0, None, V(256), 0,
+                       V(256), 10**9, None) == hc.HC_EINVAL
+    # workspace too small
+    assert L.hc_decode(ctypes.byref(p), None, V(256), V(256), None, None, None, 0, None, V(256), 0,
+                       V(256), 64, None) == hc.HC_EWORKSPACE

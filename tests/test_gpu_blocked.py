@@ -1,0 +1,211 @@
+"""GPU parity of the blocked sketch (section 3.2 blocking; one workgroup per
+block with the block's sketch in LDS) against the CPU oracle.
+
+Same bar as the global sketch: int32 sketches, bitmaps, decoded gradient,
+recovered mask, COO output and the support size / recovered count / round
+count / success flag are bit-exact, on successes and on failures; fp32 values
+stay within the per-element bounds derived in test_gpu_parity.  The round
+count of a blocked decode is the largest round count of any block, which the
+oracle's synchronous rounds over the whole sketch give by construction.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from hc_pipeline import gpu_run, oracle_run, wrap_sum
+from test_gpu_parity import assert_fp32_values, assert_same_info, fp32_cell_bounds
+
+pytestmark = pytest.mark.gpu
+
+
+def _hc():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2402_07529_amd as hc
+    return hc
+
+
+def check_blocked_int(w, g, coo_input=False):
+    print(f"[blocked] {w.name} n={w.n} c={g.c} block={g.block} rows={g.rows} "
+          f"nblocks={g.nblocks} coo_input={coo_input}", flush=True)
+    r = gpu_run(w, g.rows, g.c, coo_input=coo_input, block=g.block)
+    o = oracle_run(w, g.rows, g.c, block=g.block)
+    for i in range(w.W):
+        assert np.array_equal(r["Y"][i], o["Y"][i]), f"worker {i} sketch"
+        assert np.array_equal(r["B"][i], o["B"][i]), f"worker {i} bitmap"
+    assert np.array_equal(r["Ya"], o["Ya"])
+    assert np.array_equal(r["Ba"], o["Ba"])
+    assert np.array_equal(r["x"], o["x"])
+    assert np.array_equal(r["mask"], o["mask"])
+    assert_same_info(r["info"], o["info"])
+    sup = np.nonzero(np.unpackbits(o["Ba"].view(np.uint8), bitorder="little")[:w.n])[0]
+    assert np.array_equal(r["coo_idx"], sup.astype(np.uint32))
+    assert np.array_equal(r["coo_val"], o["x"][sup])
+    return r, o
+
+
+@pytest.mark.parametrize("c,block_rows,gamma", [(1024, 3, 1.3), (256, 4, 1.5), (64, 16, 1.6)])
+def test_blocked_tiny_int32(c, block_rows, gamma):
+    _hc()
+    w = wl.make("tiny")
+    g = oracle.blocked_geometry(w.n, w.n_agg, w.hash_seed, c, gamma, block_rows)
+    r, _ = check_blocked_int(w, g)
+    assert r["info"].success
+    assert np.array_equal(r["x"], wrap_sum([w.dense(i) for i in range(w.W)]))
+
+
+@pytest.mark.parametrize("c", [1024, 512, 256, 64, 32, 8, 1])
+def test_blocked_multi_block_ragged_int32(c):
+    # n is not a multiple of c, of 32 or of a block; the last block is short
+    _hc()
+    w = wl.make("synthetic", n=1_000_003, W=4, density=0.01, overlap=0.4, data_seed=300 + c)
+    g = oracle.blocked_geometry(w.n, w.n_agg, w.hash_seed, c, 1.3, max(3, 6144 // c))
+    assert g.nblocks > 1
+    r, _ = check_blocked_int(w, g)
+    if c >= 64:
+        assert r["info"].success
+        assert np.array_equal(r["x"], wrap_sum([w.dense(i) for i in range(w.W)]))
+
+
+@pytest.mark.parametrize("c", [1024, 64])
+def test_blocked_coo_encode(c):
+    _hc()
+    w = wl.make("synthetic", n=700_001, W=3, density=0.02, overlap=0.2, data_seed=400 + c)
+    g = oracle.blocked_geometry(w.n, w.n_agg, w.hash_seed, c, 1.3, max(3, 8192 // c))
+    check_blocked_int(w, g, coo_input=True)
+
+
+@pytest.mark.parametrize("gamma", [1.0, 1.12, 1.2])
+def test_blocked_failure_parity(gamma):
+    # undersized blocks: many fail; leftovers, masks and counts stay exact
+    _hc()
+    w = wl.make("synthetic", n=2_000_000, W=4, density=0.01, overlap=0.3,
+                data_seed=int(gamma * 100))
+    g = oracle.blocked_geometry(w.n, w.n_agg, w.hash_seed, 1024, gamma, 8)
+    r, o = check_blocked_int(w, g)
+    assert not o["info"].success
+
+
+def test_blocked_one_block_overloaded():
+    # one overloaded block fails alone; every other block is exact
+    _hc()
+    c, block, brows, nbk = 1024, 4, 3, 8   # 4096 parameters and 3072 cells per block
+    n = nbk * block * c
+    rng = np.random.default_rng(12)
+    idx, val = [], []
+    for wk in range(2):
+        parts = []
+        for q in range(nbk):
+            m = 3000 if q == 5 else 800
+            parts.append(rng.choice(block * c, m, replace=False) + q * block * c)
+        ii = np.unique(np.concatenate(parts)).astype(np.uint32)
+        idx.append(ii)
+        val.append((rng.integers(1, 2**20, ii.size) * rng.choice([-1, 1], ii.size)).astype(np.int32))
+    w = wl.Workload("overloaded", n, 2, "i32", idx, val, 1, 91)
+    g = oracle.Geom(n=n, rows=nbk * brows, seed=91, c=c, block=block)
+    r, o = check_blocked_int(w, g)
+    assert not r["info"].success
+    direct = wrap_sum([w.dense(i) for i in range(w.W)])
+    outside = np.ones(n, bool)
+    outside[5 * block * c:6 * block * c] = False
+    assert np.array_equal(r["x"][outside], direct[outside])
+
+
+@pytest.mark.parametrize("n", [1, 31, 32, 33, 1000, 4097])
+def test_blocked_tiny_lengths(n):
+    _hc()
+    W = 2
+    rng = np.random.default_rng(n)
+    idx, val = [], []
+    for wk in range(W):
+        m = max(1, n // 10)
+        ii = np.sort(rng.choice(n, m, replace=False)).astype(np.uint32)
+        idx.append(ii)
+        val.append(rng.integers(1, 1000, m).astype(np.int32))
+    w = wl.Workload("short", n, W, "i32", idx, val, 1, 5 + n)
+    for c, block, brows in ((32, 1, 3), (1024, 1, 3), (8, 4, 5)):
+        nb = ((n + c - 1) // c + block - 1) // block
+        g = oracle.Geom(n=n, rows=nb * brows, seed=5 + n, c=c, block=block)
+        check_blocked_int(w, g)
+
+
+def test_blocked_empty_support():
+    hc = _hc()
+    import torch
+    n, c = 100_000, 1024
+    p = hc.make_params(n, 3 * 4, 3, c, "i32", block=26)
+    assert p.nblocks == 4
+    dev = torch.device("cuda")
+    x = torch.zeros(n, dtype=torch.int32, device=dev)
+    Y = torch.full((p.cells,), 7, dtype=torch.int32, device=dev)
+    B = torch.full((p.words,), -1, dtype=torch.int32, device=dev)
+    hc.hc_encode(p, x, Y, B)
+    assert not Y.any() and not B.any()
+    out = torch.full((n,), 5, dtype=torch.int32, device=dev)
+    mask = torch.full((p.words,), -1, dtype=torch.int32, device=dev)
+    info = hc.alloc_info(dev)
+    hc.hc_decode(p, Y, B, info, hc.alloc_workspace(p, 0, dev), x_out=out, mask=mask)
+    inf = hc.read_info(info)
+    assert (inf.n_support, inf.n_recovered, inf.rounds, inf.success, inf.status) == (0, 0, 0, 1, 0)
+    assert not out.any() and not mask.any()
+
+
+def test_blocked_deterministic_repeat():
+    _hc()
+    w = wl.make("synthetic", n=1_500_000, W=4, density=0.02, overlap=0.3, data_seed=77)
+    g = oracle.blocked_geometry(w.n, w.n_agg, w.hash_seed, 1024, 1.3, 12)
+    a = gpu_run(w, g.rows, 1024, block=g.block)
+    b = gpu_run(w, g.rows, 1024, block=g.block)
+    for k in ("Ya", "Ba", "x", "mask", "coo_idx", "coo_val"):
+        assert np.array_equal(a[k], b[k]), k
+    assert a["info"] == b["info"]
+
+
+def test_blocked_coo_capacity_truncates():
+    _hc()
+    w = wl.make("synthetic", n=300_000, W=2, density=0.02, overlap=0.5, data_seed=5)
+    g = oracle.blocked_geometry(w.n, w.n_agg, w.hash_seed, 1024, 1.3, 6)
+    cap = w.n_agg // 3
+    r = gpu_run(w, g.rows, 1024, coo_cap=cap, block=g.block)
+    o = oracle_run(w, g.rows, 1024, block=g.block)
+    sup = np.nonzero(np.unpackbits(o["Ba"].view(np.uint8), bitorder="little")[:w.n])[0]
+    assert r["info"].n_support == sup.size
+    assert np.array_equal(r["coo_idx"], sup[:cap].astype(np.uint32))
+    assert np.array_equal(r["coo_val"], o["x"][sup[:cap]])
+
+
+@pytest.mark.parametrize("c,block_rows,gamma", [(1024, 6, 1.3), (64, 96, 1.3)])
+def test_blocked_fp32(c, block_rows, gamma):
+    _hc()
+    w = wl.make("synthetic", n=1_000_003, W=4, density=0.01, overlap=0.4, data_seed=500 + c,
+                vtype="f32")
+    g = oracle.blocked_geometry(w.n, w.n_agg, w.hash_seed, c, gamma, block_rows)
+    print(f"[blocked fp32] c={c} block={g.block} rows={g.rows} nblocks={g.nblocks}", flush=True)
+    r = gpu_run(w, g.rows, c, block=g.block)
+    o = oracle_run(w, g.rows, c, block=g.block)
+    wb, ab = fp32_cell_bounds(w, o["g"])
+    for i in range(w.W):
+        assert np.array_equal(r["B"][i], o["B"][i])
+        assert np.all(np.abs(r["Y"][i].astype(np.float64) - o["Y"][i]) <= wb[i] * (1 + 1e-6))
+    assert np.array_equal(r["Ba"], o["Ba"])
+    assert np.all(np.abs(r["Ya"].astype(np.float64) - o["Ya"]) <= ab * (1 + 1e-6))
+    assert np.array_equal(r["mask"], o["mask"])
+    assert_same_info(r["info"], o["info"])
+    sup = np.nonzero(np.unpackbits(o["Ba"].view(np.uint8), bitorder="little")[:w.n])[0]
+    assert_fp32_values(r["x"], o["x"], oracle.decode_bound(o["g"], ab, o["Ba"]), sup)
+    assert np.array_equal(r["coo_idx"], sup.astype(np.uint32))
+    assert np.array_equal(r["coo_val"], r["x"][sup])
+
+
+def test_blocked_fp32_failures_structure_exact():
+    _hc()
+    w = wl.make("synthetic", n=1_000_000, W=3, density=0.01, overlap=0.3, data_seed=9,
+                vtype="f32")
+    g = oracle.blocked_geometry(w.n, w.n_agg, w.hash_seed, 1024, 1.05, 6)
+    r = gpu_run(w, g.rows, 1024, block=g.block)
+    o = oracle_run(w, g.rows, 1024, block=g.block)
+    assert not o["info"].success
+    assert np.array_equal(r["mask"], o["mask"])
+    assert_same_info(r["info"], o["info"])
