@@ -43,6 +43,11 @@ def parse():
     ap.add_argument("--ratio", type=float, default=None,
                     help="sketch cells / aggregate nonzeros (default: gamma = 1.23)")
     ap.add_argument("--c", type=int, default=1024)
+    ap.add_argument("--blocked", action="store_true",
+                    help="blocked sketch (section 3.2 blocking), one block per workgroup in LDS; "
+                         "default ratio 1.3")
+    ap.add_argument("--block-rows", type=int, default=None,
+                    help="rows per block of the blocked sketch (default 18 for int32, 12 for fp32)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", action="store_true",
                     help="BERT-base density/overlap grid and sketch-width sweep (one JSON object)")
@@ -75,12 +80,15 @@ def make_workload(a):
     return wl.make(a.config, vtype=a.vtype, **kw)
 
 
-def algorithmic_bytes(n, W, cells, n_sup):
+def algorithmic_bytes(n, W, cells, n_sup, blocked=False):
     """Bytes the method must move per stage (reads + writes of HBM)."""
     words_b = (n + 31) // 32 * 4
     enc = 4 * n + words_b + 4 * cells                     # read x, write B, clear/write Y
     agg = (W + 1) * (4 * cells + words_b)                  # W sketches+bitmaps in, one out
-    dec = words_b + 4 * cells + 8 * n_sup + 4 * n          # B, Y, element list+values, dense out
+    if blocked:
+        dec = words_b + 4 * cells + 4 * n                  # B, Y, dense out (blocks peel in LDS)
+    else:
+        dec = words_b + 4 * cells + 8 * n_sup + 4 * n      # B, Y, element list+values, dense out
     return enc, agg, dec
 
 
@@ -106,13 +114,13 @@ def measured_traffic(workload, vtype):
     return int(fields["traffic_bytes_per_launch"])
 
 
-def cpu_baseline(w, rows, c):
+def cpu_baseline(w, rows, c, block=0):
     """The CPU oracle, as it stands, on a bounded sample of the same workload:
     one worker's dense encode (timed), the other workers encoded from COO
     (untimed), the W-way aggregate and the decode (timed).  The iteration
     time is W x encode + aggregate + decode."""
     import oracle
-    g = oracle.Geom(n=w.n, rows=rows, seed=w.hash_seed, c=c)
+    g = oracle.Geom(n=w.n, rows=rows, seed=w.hash_seed, c=c, block=block)
     dt = np.int32 if w.vtype == "i32" else np.float64
     x0 = w.dense(0).astype(dt, copy=False)
     t0 = time.perf_counter()
@@ -174,10 +182,16 @@ class Runner:
         self.out = torch.empty(w.n, dtype=self.vt, device=dev)
         self.mask = torch.empty((w.n + 31) // 32, dtype=torch.int32, device=dev)
 
-    def run(self, ratio, steps, warmup, check=True):
+    def run(self, ratio, steps, warmup, check=True, block_rows=None):
+        """block_rows: None for the global sketch, else the rows per block of
+        a blocked sketch."""
         import paper_2402_07529_amd as hc
         torch, w, dev, W = self.torch, self.w, self.dev, self.w.W
-        p = hc.hc_geometry(w.n, self.n_agg, ratio, self.c, w.hash_seed, w.vtype)
+        if block_rows is None:
+            p = hc.hc_geometry(w.n, self.n_agg, ratio, self.c, w.hash_seed, w.vtype)
+        else:
+            p = hc.hc_geometry_blocked(w.n, self.n_agg, ratio, self.c, block_rows, w.hash_seed,
+                                       w.vtype)
         cells, words = p.cells, p.words
         Y = torch.empty((W, cells), dtype=self.vt, device=dev)
         B = torch.empty((W, words), dtype=torch.int32, device=dev)
@@ -190,7 +204,7 @@ class Runner:
         # the sketch geometry itself, before any iteration
         torch.cuda.synchronize()
         t_plan = time.perf_counter()
-        plan = hc.make_plan(p, dev) if self.c >= 256 else None
+        plan = hc.make_plan(p, dev) if self.c >= 256 and block_rows is None else None
         torch.cuda.synchronize()
         plan_ms = (time.perf_counter() - t_plan) * 1e3
         x, out, mask = self.x, self.out, self.mask
@@ -299,15 +313,18 @@ def main():
     import paper_2402_07529_amd as hc
     t0 = time.perf_counter()
     w = make_workload(a)
-    ratio = a.ratio if a.ratio is not None else hc.GAMMA
+    block_rows = None
+    if a.blocked:
+        block_rows = a.block_rows or (18 if w.vtype == "i32" else 12)
+    ratio = a.ratio if a.ratio is not None else (1.3 if a.blocked else hc.GAMMA)
     log(f"[bench] workload {w.name} n={w.n} W={w.W} gen {time.perf_counter() - t0:.1f}s")
     r = Runner(w, a.c, dev)
-    m = r.run(ratio, a.steps, a.warmup)
+    m = r.run(ratio, a.steps, a.warmup, block_rows=block_rows)
     p, inf, W, n_agg = m["p"], m["info"], w.W, r.n_agg
     ms, enc_ms, agg_ms, dec_ms = m["ms"], m["enc_ms"], m["agg_ms"], m["dec_ms"]
     cells = p.cells
 
-    enc_b, agg_b, dec_b = algorithmic_bytes(w.n, W, cells, inf.n_support)
+    enc_b, agg_b, dec_b = algorithmic_bytes(w.n, W, cells, inf.n_support, a.blocked)
     iter_b = W * enc_b + agg_b + dec_b
     value = 4 * w.n / (ms * 1e-3) / 1e9
     enc_gbs = enc_b / (enc_ms * 1e-3) / 1e9
@@ -318,11 +335,15 @@ def main():
         "dtype": "int32" if w.vtype == "i32" else "fp32", "data": "synthetic",
         "config": {"workload": w.name, "n": w.n, "workers": W, "n_agg": n_agg,
                    "rows": int(p.rows), "c": a.c, "cells": cells, "ratio": round(cells / max(n_agg, 1), 4),
+                   "sketch": (f"blocked: {int(p.block)} batches and {p.block_rows} rows per block, "
+                              f"{p.nblocks} blocks") if a.blocked else "global",
                    **{k: v for k, v in w.params.items() if k in ("density", "overlap", "rows_per_worker")}},
-        "roofline": {"bound": "hbm", "kernel": "hc_encode (Y clear + dense encode)",
+        "roofline": {"bound": "hbm",
+                     "kernel": ("hc_encode (blocked LDS encode)" if a.blocked
+                                else "hc_encode (Y clear + dense encode)"),
                      "achieved": round(enc_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(enc_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(w.name, w.vtype),
+                     "traffic": None if a.blocked else measured_traffic(w.name, w.vtype),
                      "bytes_per_launch": enc_b, "avg_launch_ms": round(enc_ms, 4)},
         "hbm_frac_iteration": round(iter_b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "stages_ms": {"encode_per_worker": round(enc_ms, 4), "aggregate": round(agg_ms, 4),
@@ -339,7 +360,7 @@ def main():
     torch.cuda.empty_cache()
     if not a.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
-        res["cpu_baseline"] = cpu_baseline(w, int(p.rows), a.c)
+        res["cpu_baseline"] = cpu_baseline(w, int(p.rows), a.c, int(p.block))
     print(json.dumps(res), flush=True)
 
 

@@ -46,6 +46,7 @@ constexpr uint32_t kDegOne = 1u << kDegShift;
 constexpr uint32_t kSumMask = kDegOne - 1u;
 constexpr uint32_t kClaimed = 0x80000000u;
 constexpr uint32_t kScratchWords = 64;
+constexpr int kAhead = 8;  // global loads a lane keeps in flight in the decode's streaming loops
 
 // Control block of the blocked decode (zeroed before the decode kernel).
 struct BCtrl {
@@ -267,33 +268,74 @@ __global__ void zero_bctrl_kernel(BCtrl* c) {
     if (threadIdx.x < sizeof(BCtrl) / 4) reinterpret_cast<uint32_t*>(c)[threadIdx.x] = 0u;
 }
 
-// Which hash j of batch bl lands on the row of cell i, its table entry, and
-// the column of the member in that batch.
-__device__ __forceinline__ uint32_t member_of(const uint32_t* s_tab, uint32_t bl, uint32_t i,
-                                              uint32_t cmask, uint32_t* t_out) {
+// The member of a degree-one cell i, whose counter names its batch bl: the
+// three table entries are loaded together; j is the hash whose row is the
+// cell's row, t the member's column.
+struct Member {
+    uint32_t e[3];
+    uint32_t j, t;
+};
+
+__device__ __forceinline__ Member member_of(const uint32_t* s_tab, uint32_t bl, uint32_t i,
+                                            uint32_t cmask) {
+    Member m;
+    m.e[0] = s_tab[3 * bl];
+    m.e[1] = s_tab[3 * bl + 1];
+    m.e[2] = s_tab[3 * bl + 2];
     const uint32_t rowbase = i & ~cmask;
-    uint32_t j = 0;
-    uint32_t e = s_tab[3 * bl];
-    if ((e & 0xffffu) != rowbase) {
-        j = 1;
-        e = s_tab[3 * bl + 1];
-        if ((e & 0xffffu) != rowbase) {
-            j = 2;
-            e = s_tab[3 * bl + 2];
-        }
+    m.j = (m.e[0] & 0xffffu) == rowbase ? 0u : ((m.e[1] & 0xffffu) == rowbase ? 1u : 2u);
+    const uint32_t ej = m.j == 0 ? m.e[0] : (m.j == 1 ? m.e[1] : m.e[2]);
+    m.t = ((i & cmask) - ((ej >> 16) & 0x3ffu)) & cmask;
+    return m;
+}
+
+// Hands the set bits of the lanes' words (one word per lane) out to the
+// lanes in order, 64 at a time: f(s, valid, owner, bit) is called by every
+// lane of the wave with s = the rank of its bit among all set bits, owner =
+// the lane holding it and bit its position (valid = s < total).  Returns the
+// number of set bits.  Consecutive lanes get consecutive bits, so the LDS
+// accesses of one call hit nearby columns.
+template <typename F>
+__device__ __forceinline__ uint32_t for_each_set_bit(uint32_t word, F&& f) {
+    // exclusive prefix of the lanes' popcounts (0..32, six bits) from one
+    // ballot per bit: no cross-lane data movement through LDS
+    const uint32_t lane = lane_id();
+    const uint32_t cw = __popc(word);
+    uint32_t excl = 0, total = 0;
+#pragma unroll
+    for (int b = 0; b < 6; b++) {
+        const uint64_t m = __ballot((cw >> b) & 1u);
+        excl += lanes_below(m) << b;
+        total += (uint32_t)__popcll(m) << b;
     }
-    *t_out = ((i & cmask) - ((e >> 16) & 0x3ffu)) & cmask;
-    return j;
+    for (uint32_t s0 = 0; s0 < total; s0 += 64) {
+        const uint32_t s = s0 + lane;
+        uint32_t lo = 0;
+#pragma unroll
+        for (uint32_t step = 32; step >= 1; step >>= 1) {
+            const uint32_t cand = lo + step;
+            if ((uint32_t)__shfl(excl, (int)cand) <= s) lo = cand;
+        }
+        const uint32_t wrd = (uint32_t)__shfl(word, (int)lo);
+        const uint32_t r = s - (uint32_t)__shfl(excl, (int)lo);
+        f(s, s < total, lo, select_bit(wrd, r));
+    }
+    return total;
 }
 
 template <typename T>
 __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> a) {
     typedef typename Acc<T>::type A;
+    constexpr uint32_t kWaves = kDecThreads / 64;
     extern __shared__ __align__(16) unsigned char lds_raw[];
+    const uint32_t bcells = a.bcells;
     A* s_val = reinterpret_cast<A*>(lds_raw);
-    uint32_t* s_cnt = reinterpret_cast<uint32_t*>(lds_raw + (size_t)a.bcells * sizeof(A));
-    uint32_t* s_tab = s_cnt + a.bcells;
-    uint32_t* s_tmp = s_tab + 3 * a.block;
+    uint32_t* s_cnt = reinterpret_cast<uint32_t*>(lds_raw + (size_t)bcells * sizeof(A));
+    uint16_t* s_q = reinterpret_cast<uint16_t*>(s_cnt + bcells);  // frontier queue of cells
+    uint32_t* s_tab = reinterpret_cast<uint32_t*>(s_q + ((bcells + 1) & ~1u));
+    uint32_t* s_tmp = s_tab + 3 * a.block;  // kScratchWords: reductions, wave totals, flags
+    uint32_t* s_any = s_tmp + 48;           // a claim was made, by round parity
+    uint32_t* s_tail = s_tmp + 50;          // queue length
 
     const uint32_t q = blockIdx.x;
     const uint32_t tid = threadIdx.x;
@@ -302,46 +344,57 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
     const uint32_t cmask = a.cmask;
     const BlockRange r = block_range(q, a.block, a.log2c, cmask, a.n);
 
-    // residual sketch and counters
-    const T* yb = a.y_agg + (uint64_t)q * a.bcells;
-    for (uint32_t i = tid; i < a.bcells; i += kDecThreads) {
-        s_val[i] = (A)yb[i];
-        s_cnt[i] = 0u;
+    // residual sketch and counters; kAhead loads in flight per lane (one
+    // workgroup per CU leaves no other wave to hide the latency)
+    const T* yb = a.y_agg + (uint64_t)q * bcells;
+    for (uint32_t k0 = 0; k0 < bcells; k0 += kAhead * kDecThreads) {
+        T v[kAhead];
+#pragma unroll
+        for (int u = 0; u < kAhead; u++) {
+            const uint32_t i = k0 + u * kDecThreads + tid;
+            v[u] = i < bcells ? yb[i] : T(0);
+        }
+#pragma unroll
+        for (int u = 0; u < kAhead; u++) {
+            const uint32_t i = k0 + u * kDecThreads + tid;
+            if (i < bcells) {
+                s_val[i] = (A)v[u];
+                s_cnt[i] = 0u;
+            }
+        }
     }
     fill_table(s_tab, r, a.seed, a.brows, a.c, cmask);
+    if (tid < 4) s_tmp[48 + tid] = 0u;
     __syncthreads();
 
-    // counters from the bitmap: every wave takes 64 words at a time and hands
-    // their set bits out to its lanes in order (prefix sums of popcounts and a
-    // binary search over them), so the LDS atomics of one pass hit nearby
-    // columns of few batches
+    // counters from the bitmap.  Wave w takes a contiguous range of groups of
+    // 64 words (the output pass below takes the same range, so the support
+    // ranks of its COO entries follow from the waves' totals); each lane adds
+    // the members of its own word: lanes hold columns 32 apart, which fall on
+    // different LDS banks once rotated.
     const uint64_t w0 = r.p0 >> 5;
     const uint64_t w1 = (r.p1 + 31) >> 5;
-    uint32_t support = 0;
-    for (uint64_t base = w0 + 64ull * wave; base < w1; base += 64ull * (kDecThreads / 64)) {
-        const uint64_t wi = base + lane;
-        const uint32_t word = wi < w1 ? load_bword(a.b, wi, a.words, a.last_mask) : 0u;
-        const uint32_t cw = __popc(word);
-        support += cw;
-        uint32_t incl = cw;
-        for (int d = 1; d < 64; d <<= 1) {
-            const uint32_t y = __shfl_up(incl, d);
-            if (lane >= (uint32_t)d) incl += y;
-        }
-        const uint32_t total = (uint32_t)__shfl(incl, 63);
-        const uint32_t excl = incl - cw;
-        for (uint32_t s0 = 0; s0 < total; s0 += 64) {
-            const uint32_t s = s0 + lane;
-            uint32_t lo = 0;
+    const uint32_t ngroups = (uint32_t)((w1 - w0 + 63) >> 6);
+    const uint32_t gpw = (ngroups + kWaves - 1) / kWaves;
+    const uint32_t g_lo = wave * gpw < ngroups ? wave * gpw : ngroups;
+    const uint32_t g_hi = g_lo + gpw < ngroups ? g_lo + gpw : ngroups;
+    uint32_t lane_support = 0;
+    for (uint32_t ga = g_lo; ga < g_hi; ga += kAhead) {
+        uint32_t wv[kAhead];
 #pragma unroll
-            for (uint32_t step = 32; step >= 1; step >>= 1) {
-                const uint32_t cand = lo + step;
-                if ((uint32_t)__shfl(excl, (int)cand) <= s) lo = cand;
-            }
-            const uint32_t wrd = (uint32_t)__shfl(word, (int)lo);
-            const uint32_t rank = s - (uint32_t)__shfl(excl, (int)lo);
-            if (s < total) {
-                const uint64_t p = (base + lo) * 32ull + select_bit(wrd, rank);
+        for (int u = 0; u < kAhead; u++) {
+            const uint64_t wi = w0 + 64ull * (ga + u) + lane;
+            wv[u] = (ga + u < g_hi && wi < w1) ? load_bword(a.b, wi, a.words, a.last_mask) : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kAhead; u++) {
+            const uint64_t pw = (w0 + 64ull * (ga + u) + lane) * 32ull;
+            uint32_t word = wv[u];
+            lane_support += __popc(word);
+            while (word) {
+                const uint32_t bit = __builtin_ctz(word);
+                word &= word - 1u;
+                const uint64_t p = pw + bit;
                 const uint32_t bl = (uint32_t)((p >> a.log2c) - r.b0);
                 const uint32_t t = (uint32_t)p & cmask;
 #pragma unroll
@@ -350,135 +403,204 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
             }
         }
     }
+    const uint32_t wave_support = wave_sum_u32(lane_support);
+    if (lane == 0) s_tmp[32 + wave] = wave_support;
     __syncthreads();
 
-    // synchronous peeling rounds
-    const uint32_t per = (a.bcells + kDecThreads - 1) / kDecThreads;  // <= 32
+    // round-0 frontier: every cell of degree one, appended to the queue (one
+    // LDS atomic per wave and step)
+    for (uint32_t i0 = wave * 64u; i0 < bcells; i0 += kDecThreads) {
+        const uint32_t i = i0 + lane;
+        const bool pure = i < bcells && (s_cnt[i] >> kDegShift) == 1u;
+        const uint64_t m = __ballot(pure);
+        if (m == 0ull) continue;
+        const uint32_t leader = (uint32_t)__ffsll((unsigned long long)m) - 1u;
+        uint32_t base = 0;
+        if (lane == leader) base = atomicAdd(s_tail, (uint32_t)__popcll(m));
+        base = (uint32_t)__builtin_amdgcn_readlane((int)base, (int)leader);
+        if (pure) s_q[base + lanes_below(m)] = (uint16_t)i;
+    }
+    __syncthreads();
+
+    // synchronous peeling rounds (section 3.2).  The frontier of a round is
+    // the queue segment [qs, qe): the cells that became pure in the previous
+    // round (every cell enters the queue at most once, when its degree reaches
+    // one).  Thread t examines entries qs + t, qs + t + 1024, ...; the first
+    // half decides, from a state nobody writes, which pure cells recover their
+    // member (the smallest j among the member's pure cells); the second half
+    // applies them and appends the cells that became pure.
+    uint32_t qs = 0, qe = *s_tail;
     uint32_t rounds = 0, recovered = 0;
-    for (;;) {
-        uint32_t claims = 0;
-        for (uint32_t k = 0; k < per; k++) {
-            const uint32_t i = tid + kDecThreads * k;
-            if (i >= a.bcells) break;
-            const uint32_t cc = s_cnt[i];
+    while (qs < qe) {
+        uint32_t claims = 0;  // bit k: entry qs + tid + 1024 k recovers its member
+        for (uint32_t k = 0, idx = qs + tid; idx < qe; k++, idx += kDecThreads) {
+            const uint32_t cell = s_q[idx];
+            const uint32_t cc = s_cnt[cell];
             if ((cc >> kDegShift) != 1u) continue;
-            const uint32_t bl = cc & kSumMask;
-            uint32_t t;
-            const uint32_t j = member_of(s_tab, bl, i, cmask, &t);
+            const Member m = member_of(s_tab, cc & kSumMask, cell, cmask);
             bool first = true;
-            for (uint32_t jj = 0; jj < j; jj++)
-                if ((s_cnt[tab_cell(s_tab[3 * bl + jj], t, cmask)] >> kDegShift) == 1u) first = false;
+            if (m.j >= 1) first = (s_cnt[tab_cell(m.e[0], m.t, cmask)] >> kDegShift) != 1u;
+            if (m.j == 2 && first) first = (s_cnt[tab_cell(m.e[1], m.t, cmask)] >> kDegShift) != 1u;
             if (first) claims |= 1u << k;
         }
-        if (!__syncthreads_or(claims != 0u)) break;
+        const bool wave_claims = __ballot(claims != 0u) != 0ull;  // every lane takes part
+        if (lane == 0 && wave_claims) s_any[rounds & 1u] = 1u;
+        __syncthreads();
+        if (s_any[rounds & 1u] == 0u) break;
+        if (tid == 0) s_any[(rounds + 1u) & 1u] = 0u;
         rounds++;
         while (claims) {
             const uint32_t k = __builtin_ctz(claims);
             claims &= claims - 1u;
-            const uint32_t i = tid + kDecThreads * k;
-            const uint32_t bl = s_cnt[i] & kSumMask;
-            uint32_t t;
-            const uint32_t j = member_of(s_tab, bl, i, cmask, &t);
-            const A xv = Val<A>::sign(s_val[i], tab_neg(s_tab[3 * bl + j]));  // x = g_j * Y
+            const uint32_t cell = s_q[qs + tid + kDecThreads * k];
+            recovered++;
+            const uint32_t bl = s_cnt[cell] & kSumMask;
+            const Member m = member_of(s_tab, bl, cell, cmask);
+            const uint32_t ej = m.j == 0 ? m.e[0] : (m.j == 1 ? m.e[1] : m.e[2]);
+            const A xv = Val<A>::sign(s_val[cell], tab_neg(ej));  // x = g_j * Y
 #pragma unroll
             for (uint32_t jj = 0; jj < 3; jj++) {
-                if (jj == j) continue;
-                const uint32_t e = s_tab[3 * bl + jj];
-                const uint32_t cell = tab_cell(e, t, cmask);
-                atomicSub(s_cnt + cell, kDegOne + bl);
-                LdsAdd<A>::add(s_val + cell, Val<A>::sign(xv, !tab_neg(e)));  // -= g * x
+                if (jj == m.j) continue;
+                const uint32_t c2 = tab_cell(m.e[jj], m.t, cmask);
+                const uint32_t old = atomicSub(s_cnt + c2, kDegOne + bl);
+                if ((old >> kDegShift) == 2u) s_q[atomicAdd(s_tail, 1u)] = (uint16_t)c2;
+                LdsAdd<A>::add(s_val + c2, Val<A>::sign(xv, !tab_neg(m.e[jj])));  // -= g * x
             }
-            s_cnt[i] = kClaimed | bl;  // keeps g_j * x in s_val[i]
-            recovered++;
+            s_cnt[cell] = kClaimed | bl;  // keeps g_j * x in s_val[cell]
         }
         __syncthreads();
+        qs = qe;
+        qe = *s_tail;
+    }
+    recovered = block_sum(recovered, s_tmp);
+
+    uint32_t sup_total = 0, wave_rank = 0;
+    for (uint32_t w = 0; w < kWaves; w++) {
+        const uint32_t s = s_tmp[32 + w];
+        if (w < wave) wave_rank += s;
+        sup_total += s;
     }
 
-    const uint32_t sup_total = block_sum(support, s_tmp);
-    const uint32_t rec_total = block_sum(recovered, s_tmp);
-
-    // outputs: 4 consecutive parameters per lane
+    // outputs, wave w over its range of word groups again (64 words, 2048
+    // parameters).  The members of a group are handed out to the lanes in
+    // order; each finds its value -- in its claimed cell, or the median
+    // estimate from the residual if it was not recovered -- and leaves it in
+    // the wave's staging slots (the queue's LDS, free now) at its rank in the
+    // group, with its COO entry at its support rank.  The group's dense output
+    // is then written as 16-byte vectors, each lane taking 4 parameters and
+    // their values from the staging slots by rank.  A group with more members
+    // than a wave's slots stores its values directly.
     const bool want_coo = a.coo_idx != nullptr;
-    uint64_t rank_base = 0;
+    uint64_t rank = 0;
     if (want_coo) {
         const uint64_t chunk = w0 / kChunkWords;
         uint32_t part = 0;
         for (uint64_t w = chunk * kChunkWords + tid; w < w0; w += kDecThreads)
             part += __popc(load_bword(a.b, w, a.words, a.last_mask));
-        rank_base = (uint64_t)a.blk[chunk] + block_sum(part, s_tmp);
+        rank = (uint64_t)a.blk[chunk] + block_sum(part, s_tmp) + wave_rank;
     }
+    const uint32_t slots = (((bcells + 1) & ~1u) / 2) / kWaves;  // u32 slots per wave
+    T* s_stage = reinterpret_cast<T*>(s_q) + wave * slots;
     typedef T V4 __attribute__((ext_vector_type(4)));
-    for (uint64_t it0 = r.p0; it0 < r.p1; it0 += kOutStep) {
-        const uint64_t pp = it0 + 4u * tid;
-        uint32_t bits = 0;
-        if (pp < r.p1) bits = (load_bword(a.b, pp >> 5, a.words, a.last_mask) >> (pp & 31u)) & 0xfu;
-        uint32_t rank = 0, it_total = 0;
-        if (want_coo) rank = block_scan((uint32_t)__popc(bits), s_tmp, &it_total);
-        T out[4];
-        bool rec[4];
+    for (uint32_t ga = g_lo; ga < g_hi; ga += kAhead) {
+        uint32_t wv[kAhead];
 #pragma unroll
-        for (int k = 0; k < 4; k++) {
-            out[k] = T(0);
-            rec[k] = false;
-            if ((bits >> k) & 1u) {
-                const uint64_t p = pp + k;
-                const uint32_t bl = (uint32_t)((p >> a.log2c) - r.b0);
-                const uint32_t t = (uint32_t)p & cmask;
-                A est[3];
+        for (int u = 0; u < kAhead; u++) {
+            const uint64_t wi2 = w0 + 64ull * (ga + u) + lane;
+            wv[u] = (ga + u < g_hi && wi2 < w1) ? load_bword(a.b, wi2, a.words, a.last_mask) : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kAhead; u++) {
+            if (ga + u >= g_hi) break;  // uniform over the wave
+            const uint64_t base = w0 + 64ull * (ga + u);
+            const uint32_t word = wv[u];
+            if (a.mask != nullptr && base + lane < w1) a.mask[base + lane] = word;
+            // rank of the first member of each word within the group
+            const uint32_t cw = __popc(word);
+            uint32_t excl = 0;
+#pragma unroll
+            for (int b = 0; b < 6; b++) excl += lanes_below(__ballot((cw >> b) & 1u)) << b;
+            const uint32_t total = for_each_set_bit(word, [&](uint32_t s, bool valid,
+                                                              uint32_t owner, uint32_t bit) {
+                const uint64_t p = (base + owner) * 32ull + bit;
                 A val = A(0);
-                bool found = false;
+                bool found = true;
+                if (valid) {
+                    const uint32_t bl = (uint32_t)((p >> a.log2c) - r.b0);
+                    const uint32_t t = (uint32_t)p & cmask;
+                    A est[3];
+                    found = false;
 #pragma unroll
-                for (int j = 0; j < 3; j++) {
-                    const uint32_t e = s_tab[3 * bl + j];
-                    const uint32_t cell = tab_cell(e, t, cmask);
-                    est[j] = Val<A>::sign(s_val[cell], tab_neg(e));
-                    if (s_cnt[cell] == (kClaimed | bl)) {
-                        val = est[j];
-                        found = true;
+                    for (int j = 0; j < 3; j++) {
+                        const uint32_t e = s_tab[3 * bl + j];
+                        const uint32_t cell = tab_cell(e, t, cmask);
+                        est[j] = Val<A>::sign(s_val[cell], tab_neg(e));
+                        if (s_cnt[cell] == (kClaimed | bl)) {
+                            val = est[j];
+                            found = true;
+                        }
+                    }
+                    if (!found) val = median3(est[0], est[1], est[2]);
+                    const T out = (T)val;
+                    if (s < slots) s_stage[s] = out;
+                    else if (a.x_out != nullptr) a.x_out[p] = out;
+                    if (want_coo) {
+                        const uint64_t rr = rank + s;
+                        if (rr < a.coo_cap) {
+                            a.coo_idx[rr] = (uint32_t)p;
+                            a.coo_val[rr] = out;
+                        }
                     }
                 }
-                if (!found) val = median3(est[0], est[1], est[2]);
-                out[k] = (T)val;
-                rec[k] = found;
-                if (want_coo) {
-                    const uint64_t rr = rank_base + rank;
-                    if (rr < a.coo_cap) {
-                        a.coo_idx[rr] = (uint32_t)p;
-                        a.coo_val[rr] = out[k];
+                // members left unrecovered (failed blocks only) leave the mask
+                if (a.mask != nullptr && __ballot(!found) != 0ull) {
+                    __threadfence_block();  // the plain mask stores above land first
+                    if (!found) atomicAnd(a.mask + (p >> 5), ~(1u << (p & 31u)));
+                }
+            });
+            rank += total;
+            if (a.x_out != nullptr) {
+#pragma unroll
+                for (int k = 0; k < 8; k++) {
+                    const uint32_t off = 256u * k + 4u * lane;  // parameter offset in the group
+                    const uint32_t gw = (uint32_t)__shfl(word, (int)(off >> 5));
+                    const uint32_t ge = (uint32_t)__shfl(excl, (int)(off >> 5));
+                    const uint64_t pp = base * 32ull + off;
+                    if (pp >= r.p1) continue;
+                    const uint32_t sh = off & 31u;
+                    const uint32_t bits = (gw >> sh) & 0xfu;
+                    uint32_t rk = ge + __popc(gw & ((1u << sh) - 1u));  // rank of the first member
+                    T v[4];
+                    bool stored[4];  // value already stored directly (past the slots)
+                    bool any_stored = false;
+#pragma unroll
+                    for (int kk = 0; kk < 4; kk++) {
+                        v[kk] = T(0);
+                        stored[kk] = false;
+                        if ((bits >> kk) & 1u) {
+                            if (rk < slots) v[kk] = s_stage[rk];
+                            else stored[kk] = true;
+                            rk++;
+                        }
+                        any_stored |= stored[kk];
                     }
-                    rank++;
+                    if (!any_stored && a.x_vec && pp + 4 <= a.n) {
+                        const V4 z = {v[0], v[1], v[2], v[3]};
+                        __builtin_nontemporal_store(z, reinterpret_cast<V4*>(a.x_out + pp));
+                    } else {
+#pragma unroll
+                        for (int kk = 0; kk < 4; kk++)
+                            if (!stored[kk] && pp + kk < a.n) a.x_out[pp + kk] = v[kk];
+                    }
                 }
             }
         }
-        if (a.x_out != nullptr && pp < r.p1) {
-            if (a.x_vec && pp + 4 <= a.n) {
-                const V4 v = {out[0], out[1], out[2], out[3]};
-                __builtin_nontemporal_store(v, reinterpret_cast<V4*>(a.x_out + pp));
-            } else {
-                for (int k = 0; k < 4; k++)
-                    if (pp + k < a.n) a.x_out[pp + k] = out[k];
-            }
-        }
-        if (a.mask != nullptr) {
-            const uint64_t m0 = __ballot(rec[0]), m1 = __ballot(rec[1]);
-            const uint64_t m2 = __ballot(rec[2]), m3 = __ballot(rec[3]);
-            if (lane < 8) {
-                const uint32_t s8 = 8u * lane;
-                const uint32_t mw = spread4((uint32_t)(m0 >> s8)) |
-                                    (spread4((uint32_t)(m1 >> s8)) << 1) |
-                                    (spread4((uint32_t)(m2 >> s8)) << 2) |
-                                    (spread4((uint32_t)(m3 >> s8)) << 3);
-                const uint64_t widx = ((it0 + 256u * wave) >> 5) + lane;
-                if (widx < w1) a.mask[widx] = mw;
-            }
-        }
-        rank_base += it_total;
     }
 
     // block totals; the last workgroup to finish writes the summary
     if (tid == 0) {
         atomicAdd(&a.bctrl->support, (unsigned long long)sup_total);
-        atomicAdd(&a.bctrl->recovered, (unsigned long long)rec_total);
+        atomicAdd(&a.bctrl->recovered, (unsigned long long)recovered);
         atomicMax(&a.bctrl->rounds, rounds);
         __threadfence();
         const uint32_t ticket = atomicAdd(&a.bctrl->done, 1u);
@@ -587,7 +709,10 @@ size_t blocked_encode_lds(const Geo& g) {
 
 size_t blocked_decode_lds(const Geo& g) {
     const size_t vsz = g.f32 ? 8 : 4;  // residual: int32, or fp64 for fp32 gradients
-    return (size_t)g.brows * g.c * (vsz + 4) + (size_t)g.block * 12 + kScratchWords * 4;
+    const size_t cells = (size_t)g.brows * g.c;
+    // residual + counters + frontier queue (u16), hash table, scratch
+    return cells * (vsz + 4) + ((cells + 1) & ~(size_t)1) * 2 + (size_t)g.block * 12 +
+           kScratchWords * 4;
 }
 
 BlockedLayout blocked_layout(const Geo& g) {

@@ -209,3 +209,19 @@ def test_blocked_fp32_failures_structure_exact():
     assert not o["info"].success
     assert np.array_equal(r["mask"], o["mask"])
     assert_same_info(r["info"], o["info"])
+
+
+@pytest.mark.parametrize("block_rows,ok", [(192, False), (384, True)])
+def test_blocked_dense_aggregate_c32(block_rows, ok):
+    # about 74 % of the parameters nonzero in the aggregate: many groups of 64
+    # bitmap words hold more members than a wave's staging slots, so the
+    # decode's direct value stores are exercised at scale.  With c = 32,
+    # blocks of 384 rows (about 9,400 members) peel at this density and blocks
+    # of 192 rows do not (the oracle agrees on both)
+    _hc()
+    w = wl.make("synthetic", n=2_000_003, W=4, density=0.2, overlap=0.1, data_seed=606)
+    g = oracle.blocked_geometry(w.n, w.n_agg, w.hash_seed, 32, 1.3, block_rows)
+    r, _ = check_blocked_int(w, g)
+    assert bool(r["info"].success) == ok
+    if ok:
+        assert np.array_equal(r["x"], wrap_sum([w.dense(i) for i in range(w.W)]))
