@@ -47,7 +47,7 @@ def parse():
                     help="blocked sketch (section 3.2 blocking), one block per workgroup in LDS; "
                          "default ratio 1.3")
     ap.add_argument("--block-rows", type=int, default=None,
-                    help="rows per block of the blocked sketch (default 18 for int32, 12 for fp32)")
+                    help="rows per block of the blocked sketch (default 14 for int32, 10 for fp32)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", action="store_true",
                     help="BERT-base density/overlap grid and sketch-width sweep (one JSON object)")
@@ -315,7 +315,7 @@ def main():
     w = make_workload(a)
     block_rows = None
     if a.blocked:
-        block_rows = a.block_rows or (18 if w.vtype == "i32" else 12)
+        block_rows = a.block_rows or (14 if w.vtype == "i32" else 10)
     ratio = a.ratio if a.ratio is not None else (1.3 if a.blocked else hc.GAMMA)
     log(f"[bench] workload {w.name} n={w.n} W={w.W} gen {time.perf_counter() - t0:.1f}s")
     r = Runner(w, a.c, dev)

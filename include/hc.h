@@ -51,9 +51,10 @@
  * block then peels on its own.  K * c must be a multiple of 32 and rows a
  * multiple of nblocks with R_b >= 3.  The library's encode and decode of a
  * blocked sketch hold one block per workgroup in LDS, which needs K <= 1024
- * and, per block, R_b * c * (8 for int32, 12 for fp32) + 12 * K + 256 bytes
- * <= 160 KiB (HC_EUNSUPPORTED otherwise; hc_encode_coo and hc_aggregate
- * accept any blocked geometry).
+ * and, per block, R_b * c * (10 for int32, 14 for fp32) + 12 * K + 256 bytes
+ * <= 159 KiB (at c = 1024: up to 14 rows for int32, 10 for fp32;
+ * HC_EUNSUPPORTED otherwise; hc_encode_coo and hc_aggregate accept any
+ * blocked geometry).
  */
 #ifndef HC_H
 #define HC_H

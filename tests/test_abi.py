@@ -101,9 +101,9 @@ def test_plan_sizes():
 def test_blocked_geometry_matches_oracle():
     import oracle
     import paper_2402_07529_amd as hc
-    for n, nnz, gamma, c, br in ((109_482_240, 9_305_915, 1.3, 1024, 18),
-                                 (109_482_240, 273_579, 1.3, 1024, 18),
-                                 (143_667_240, 8_476_348, 1.3, 1024, 16),
+    for n, nnz, gamma, c, br in ((109_482_240, 9_305_915, 1.3, 1024, 14),
+                                 (109_482_240, 273_579, 1.3, 1024, 14),
+                                 (143_667_240, 8_476_348, 1.3, 1024, 12),
                                  (10_000, 500, 1.3, 8, 4), (65_536, 1636, 1.6, 64, 16),
                                  (1_000_000, 999_999, 1.25, 256, 12)):
         p = hc.hc_geometry_blocked(n, nnz, gamma, c, br, 5, "i32")
@@ -126,6 +126,9 @@ def test_blocked_params_rejected():
             hc.hc_sizes(p)
         assert ei.value.status == st
     # valid format, beyond the LDS kernels: 30 rows of 1024 cells per block
+    with pytest.raises(hc.HCError) as ei:
+        hc.hc_geometry_blocked(109_482_240, 9_305_915, 1.3, 1024, 18, 3)
+    assert ei.value.status == hc.HC_EUNSUPPORTED
     p = hc.make_params(2_000_000, 30 * 62, 1, c=1024, block=32)
     hc.hc_sizes(p)
     assert L.hc_encode(ctypes.byref(p), V(256), V(256), V(256), None) == hc.HC_EUNSUPPORTED
@@ -136,7 +139,7 @@ def test_blocked_params_rejected():
     p = hc.make_params(2 * 1050 * 1024, 3 * 2, 1, c=1024, block=1050)
     assert L.hc_encode(ctypes.byref(p), V(256), V(256), V(256), None) == hc.HC_EUNSUPPORTED
     # a blocked sketch takes no plan
-    p = hc.hc_geometry_blocked(109_482_240, 9_305_915, 1.3, 1024, 18, 3)
+    p = hc.hc_geometry_blocked(109_482_240, 9_305_915, 1.3, 1024, 14, 3)
     with pytest.raises(hc.HCError) as ei:
         hc.hc_plan_bytes(p)
     assert ei.value.status == hc.HC_EUNSUPPORTED
