@@ -8,9 +8,11 @@
 // peels a block's R_b * c cells without touching any other block.
 //
 // encode  the workgroup zeroes the block's sketch in LDS, streams the block's
-//         gradient once (wave tiles of 1024 parameters, 16 coalesced dword
-//         loads per lane), writes each tile's 32 bitmap words with one 128-byte
-//         store, adds every nonzero to its three cells with LDS atomics, and
+//         gradient once (wave tiles of 1024 parameters, four coalesced 16-byte
+//         loads per lane, the next tile in flight while one is encoded), writes
+//         each tile's 32 bitmap
+//         words with one 128-byte store, adds every nonzero to its three cells
+//         with LDS atomics, and
 //         stores the finished block sketch with plain coalesced stores: no
 //         global atomics and no pre-zeroing of Y.
 // decode  the workgroup loads the block's aggregated sketch into LDS as the
@@ -178,7 +180,7 @@ struct EncArgs {
     T* y;
     uint32_t* b;
     uint64_t n, seed;
-    uint32_t block, brows, bcells, c, cmask, log2c, y_vec;
+    uint32_t block, brows, bcells, c, cmask, log2c, y_vec, x_vec;
 };
 
 template <typename T>
@@ -195,42 +197,117 @@ __global__ __launch_bounds__(kEncThreads) void encode_blocked_kernel(EncArgs<T> 
     const uint32_t lane = lane_id();
     const uint32_t wave = threadIdx.x >> 6;
     const uint32_t ntiles = (uint32_t)((r.p1 - r.p0 + kWaveTile - 1) / kWaveTile);
-    for (uint32_t tile = wave; tile < ntiles; tile += kEncThreads / 64) {
+    constexpr uint32_t kWaves = kEncThreads / 64;
+    typedef T V4 __attribute__((ext_vector_type(4)));
+    // A tile is read as four 16-byte loads per lane: e[l][k] = parameter
+    // tp + 256 l + 4 lane + k.  Tiles wholly inside the block (and a 16-byte
+    // aligned gradient) take the vector loads with no branch, so the waits of
+    // the pipelined loop below count exactly the loads they need; the block's
+    // last, partial tile reads element by element, zero past the block's end.
+    auto load_full = [&](uint32_t tile, T (&e)[4][4]) {
+        const V4* src = reinterpret_cast<const V4*>(a.x + r.p0 + (uint64_t)tile * kWaveTile) + lane;
+#pragma unroll
+        for (int l = 0; l < 4; l++) {
+            const V4 v = __builtin_nontemporal_load(src + 64 * l);
+            e[l][0] = v.x;
+            e[l][1] = v.y;
+            e[l][2] = v.z;
+            e[l][3] = v.w;
+        }
+    };
+    auto load_part = [&](uint32_t tile, T (&e)[4][4]) {
         const uint64_t tp = r.p0 + (uint64_t)tile * kWaveTile;
-        T v[16];
-        if (tp + kWaveTile <= r.p1) {
 #pragma unroll
-            for (int m = 0; m < 16; m++) v[m] = __builtin_nontemporal_load(a.x + tp + 64u * m + lane);
-        } else {
+        for (int l = 0; l < 4; l++)
 #pragma unroll
-            for (int m = 0; m < 16; m++) {
-                const uint64_t p = tp + 64u * m + lane;
-                v[m] = p < r.p1 ? a.x[p] : T(0);
+            for (int k = 0; k < 4; k++) {
+                const uint64_t p = tp + 256u * l + 4u * lane + k;
+                e[l][k] = p < r.p1 ? a.x[p] : T(0);
             }
+    };
+    auto encode_tile = [&](uint32_t tile, const T (&e)[4][4]) {
+        const uint64_t tp = r.p0 + (uint64_t)tile * kWaveTile;
+        uint64_t m[4][4];
+#pragma unroll
+        for (int l = 0; l < 4; l++)
+#pragma unroll
+            for (int k = 0; k < 4; k++) m[l][k] = __ballot(Val<T>::nonzero(e[l][k]));
+        // bitmap word w = 8 l + i holds parameters 32 w .. 32 w + 31: lanes
+        // 8i .. 8i+7 of load l, parameter 4 lane' + k at bit 4 (lane' - 8 i) + k
+        if (lane < 32 && tp + 32ull * lane < r.p1) {
+            const uint32_t l = lane >> 3, sh = 8u * (lane & 7u);
+            uint32_t word = 0;
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                const uint64_t mk = l == 0 ? m[0][k] : l == 1 ? m[1][k] : l == 2 ? m[2][k] : m[3][k];
+                word |= spread4((uint32_t)(mk >> sh)) << k;
+            }
+            a.b[(tp >> 5) + lane] = word;
         }
-        // bitmap: ballot m covers parameters 64m .. 64m+63 = words 2m, 2m+1
-        uint32_t myword = 0;
+        // sketch: three LDS atomics per nonzero
 #pragma unroll
-        for (int m = 0; m < 16; m++) {
-            const uint64_t bal = __ballot(Val<T>::nonzero(v[m]));
-            if ((lane >> 1) == (uint32_t)m) myword = (lane & 1u) ? (uint32_t)(bal >> 32) : (uint32_t)bal;
-        }
-        if (lane < 32 && tp + 32ull * lane < r.p1) a.b[(tp >> 5) + lane] = myword;
-        // sketch: three LDS atomics per nonzero; the lanes of one m hold
-        // consecutive columns of one batch, i.e. consecutive cells of a row
+        for (int l = 0; l < 4; l++) {
+            if ((m[l][0] | m[l][1] | m[l][2] | m[l][3]) == 0ull) continue;
+            const uint64_t lbase = tp + 256u * l;
+            if (a.c >= 256) {
+                // a load lies in one batch: its table entries are uniform
+                const uint32_t bl = uniform((uint32_t)((lbase >> a.log2c) - r.b0));
+                const uint32_t e0 = uniform(s_tab[3 * bl]);
+                const uint32_t e1 = uniform(s_tab[3 * bl + 1]);
+                const uint32_t e2 = uniform(s_tab[3 * bl + 2]);
 #pragma unroll
-        for (int m = 0; m < 16; m++) {
-            if (Val<T>::nonzero(v[m])) {
-                const uint64_t p = tp + 64u * m + lane;
-                const uint32_t bl = (uint32_t)((p >> a.log2c) - r.b0);
-                const uint32_t t = (uint32_t)p & a.cmask;
+                for (int k = 0; k < 4; k++) {
+                    if (!Val<T>::nonzero(e[l][k])) continue;
+                    const uint32_t t = ((uint32_t)lbase + 4u * lane + k) & a.cmask;
+                    LdsAdd<T>::add(s_y + tab_cell(e0, t, a.cmask), Val<T>::sign(e[l][k], tab_neg(e0)));
+                    LdsAdd<T>::add(s_y + tab_cell(e1, t, a.cmask), Val<T>::sign(e[l][k], tab_neg(e1)));
+                    LdsAdd<T>::add(s_y + tab_cell(e2, t, a.cmask), Val<T>::sign(e[l][k], tab_neg(e2)));
+                }
+            } else {
 #pragma unroll
-                for (int j = 0; j < 3; j++) {
-                    const uint32_t e = s_tab[3 * bl + j];
-                    LdsAdd<T>::add(s_y + tab_cell(e, t, a.cmask), Val<T>::sign(v[m], tab_neg(e)));
+                for (int k = 0; k < 4; k++) {
+                    if (!Val<T>::nonzero(e[l][k])) continue;
+                    const uint64_t p = lbase + 4u * lane + k;
+                    const uint32_t bl = (uint32_t)((p >> a.log2c) - r.b0);
+                    const uint32_t t = (uint32_t)p & a.cmask;
+#pragma unroll
+                    for (int j = 0; j < 3; j++) {
+                        const uint32_t ee = s_tab[3 * bl + j];
+                        LdsAdd<T>::add(s_y + tab_cell(ee, t, a.cmask), Val<T>::sign(e[l][k], tab_neg(ee)));
+                    }
                 }
             }
         }
+    };
+    // rolling pipeline over the full tiles: the next tile's loads are issued
+    // before the current tile is encoded, so a wave keeps memory in flight
+    // while it works.  The prefetch is never conditional on its own, so every
+    // wait has one known count of younger loads to leave in flight.
+    const uint32_t nfull = a.x_vec ? (uint32_t)((r.p1 - r.p0) / kWaveTile) : 0u;
+    T ea[4][4], eb[4][4];
+    uint32_t tile = wave;
+    if (tile < nfull) {
+        load_full(tile, ea);
+        for (;;) {
+            if (tile + kWaves >= nfull) {
+                encode_tile(tile, ea);
+                break;
+            }
+            load_full(tile + kWaves, eb);
+            encode_tile(tile, ea);
+            tile += kWaves;
+            if (tile + kWaves >= nfull) {
+                encode_tile(tile, eb);
+                break;
+            }
+            load_full(tile + kWaves, ea);
+            encode_tile(tile, eb);
+            tile += kWaves;
+        }
+    }
+    for (tile = nfull + wave; tile < ntiles; tile += kWaves) {
+        load_part(tile, ea);
+        encode_tile(tile, ea);
     }
     __syncthreads();
 
@@ -654,6 +731,7 @@ hipError_t launch_encode_blocked_t(const Geo& g, const void* x, void* y, uint32_
     a.cmask = g.cmask;
     a.log2c = g.log2c;
     a.y_vec = (reinterpret_cast<uintptr_t>(y) & 15u) == 0 && (a.bcells & 3u) == 0;
+    a.x_vec = (reinterpret_cast<uintptr_t>(x) & 15u) == 0;
     hipLaunchKernelGGL(encode_blocked_kernel<T>, dim3(g.nblocks), dim3(kEncThreads),
                        blocked_encode_lds(g), s, a);
     return hipGetLastError();
