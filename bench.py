@@ -47,7 +47,8 @@ def parse():
                     help="blocked sketch (section 3.2 blocking), one block per workgroup in LDS; "
                          "default ratio 1.3")
     ap.add_argument("--block-rows", type=int, default=None,
-                    help="rows per block of the blocked sketch (default 14 for int32, 10 for fp32)")
+                    help="rows per block of the blocked sketch (default: the count, among those "
+                         "whose blocks fit in LDS, that minimises encode waves x block size)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", action="store_true",
                     help="BERT-base density/overlap grid and sketch-width sweep (one JSON object)")
@@ -78,6 +79,27 @@ def make_workload(a):
     if a.overlap is not None:
         kw["overlap"] = a.overlap
     return wl.make(a.config, vtype=a.vtype, **kw)
+
+
+def pick_block_rows(w, n_agg, gamma, c, cus):
+    """Rows per block for the blocked sketch on this GPU.  Each block is one
+    workgroup of the encode and the decode, whose time grows with the block's
+    batches, and the blocks run ceil(nblocks / CUs) workgroups deep per CU: the
+    row count minimising that product (ties to more rows, i.e. fewer and
+    larger blocks, which peel more reliably).  Blocks keep at least 10,240
+    cells: below about ten thousand members a block needs more room than
+    gamma = 1.3 to peel reliably."""
+    import paper_2402_07529_amd as hc
+    best = None
+    for br in range(-(-10240 // c), -(-20480 // c) + 1):
+        try:
+            p = hc.hc_geometry_blocked(w.n, n_agg, gamma, c, br, w.hash_seed, w.vtype)
+        except hc.HCError:
+            continue  # does not fit in LDS
+        cost = -(-p.nblocks // cus) * int(p.block)
+        if best is None or cost <= best[0]:
+            best = (cost, br)
+    return best[1]
 
 
 def algorithmic_bytes(n, W, cells, n_sup, blocked=False):
@@ -314,9 +336,10 @@ def main():
     t0 = time.perf_counter()
     w = make_workload(a)
     block_rows = None
-    if a.blocked:
-        block_rows = a.block_rows or (14 if w.vtype == "i32" else 10)
     ratio = a.ratio if a.ratio is not None else (1.3 if a.blocked else hc.GAMMA)
+    if a.blocked:
+        cus = torch.cuda.get_device_properties(dev).multi_processor_count
+        block_rows = a.block_rows or pick_block_rows(w, w.n_agg, ratio, a.c, cus)
     log(f"[bench] workload {w.name} n={w.n} W={w.W} gen {time.perf_counter() - t0:.1f}s")
     r = Runner(w, a.c, dev)
     m = r.run(ratio, a.steps, a.warmup, block_rows=block_rows)

@@ -137,8 +137,8 @@ __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, 
 // MODE 0: c >= 256 (the batch is uniform over a load: hash on the scalar
 // unit), MODE 1: 4 <= c < 256 (per lane), MODE 2: c < 4 (per parameter).
 // Each wave takes its own tiles; the main loop takes them two at a time when
-// both lie wholly inside the gradient, so every lane keeps eight 16-byte
-// nontemporal loads in flight.  The tail takes single tiles with
+// both lie wholly inside the gradient and issues the next pair's eight 16-byte
+// nontemporal loads per lane before encoding the current pair.  The tail takes single tiles with
 // bounds-checked 4-byte loads (also used throughout when x is not 16-byte
 // aligned).
 template <typename T, int MODE>
@@ -153,11 +153,12 @@ __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
     const uint64_t ntiles = (n + kTile - 1) / kTile;
     const uint64_t npairs = vec ? n / (2 * kTile) : 0;
 
-    for (uint64_t q = gwave; q < npairs; q += nwaves) {
+    auto load_pair = [&](uint64_t q, V (&v)[8]) {
         const V* src = reinterpret_cast<const V*>(x + q * (2 * kTile)) + lane;
-        V v[8];
 #pragma unroll
         for (int u = 0; u < 8; u++) v[u] = __builtin_nontemporal_load(src + u * 64);
+    };
+    auto encode_pair = [&](uint64_t q, const V (&v)[8]) {
 #pragma unroll
         for (int h = 0; h < 2; h++) {
             T e[4][4];
@@ -170,6 +171,30 @@ __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
             }
             encode_tile<T, MODE>(e, (2 * q + h) * kTile, lane, y, b, words, seed, rows, c, cmask,
                                  log2c);
+        }
+    };
+    // rolling pipeline: the next pair's loads are issued before the current
+    // pair is encoded (never conditionally on their own, so the compiler's
+    // load waits leave exactly them in flight)
+    uint64_t q = gwave;
+    if (q < npairs) {
+        V va[8], vb[8];
+        load_pair(q, va);
+        for (;;) {
+            if (q + nwaves >= npairs) {
+                encode_pair(q, va);
+                break;
+            }
+            load_pair(q + nwaves, vb);
+            encode_pair(q, va);
+            q += nwaves;
+            if (q + nwaves >= npairs) {
+                encode_pair(q, vb);
+                break;
+            }
+            load_pair(q + nwaves, va);
+            encode_pair(q, vb);
+            q += nwaves;
         }
     }
     for (uint64_t tile = 2 * npairs + gwave; tile < ntiles; tile += nwaves) {
@@ -214,7 +239,17 @@ uint32_t grid_for(uint64_t work_items, uint64_t per_block, uint32_t cap) {
 
 template <typename T, int MODE>
 hipError_t launch_dense_t(const Geo& g, const void* x, void* y, uint32_t* b, hipStream_t s,
-                          uint32_t grid) {
+                          uint64_t ntiles, int cus) {
+    // one resident wave of workgroups: the kernel strides over the tiles
+    static int per_cu = 0;  // resident workgroups per CU (same on every device here)
+    if (per_cu == 0) {
+        int v = 0;
+        const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &v, reinterpret_cast<const void*>(&encode_dense_kernel<T, MODE>), kBlock, 0);
+        if (e != hipSuccess) return e;
+        per_cu = v > 0 ? v : 1;
+    }
+    const uint32_t grid = grid_for(ntiles, 2 * (kBlock / 64), (uint32_t)(cus * per_cu));
     hipLaunchKernelGGL((encode_dense_kernel<T, MODE>), dim3(grid), dim3(kBlock), 0, s,
                        static_cast<const T*>(x), static_cast<T*>(y), b, g.n, g.words, g.seed,
                        g.rows, g.c, g.cmask, g.log2c,
@@ -243,16 +278,15 @@ hipError_t launch_encode_dense(const Geo& g, const void* x, void* y, uint32_t* b
     e = launch_fill_u32(static_cast<uint32_t*>(y), g.cells, 0u, s);
     if (e != hipSuccess) return e;
     const uint64_t ntiles = (g.n + kTile - 1) / kTile;
-    const uint32_t grid = grid_for(ntiles, 2 * (kBlock / 64), (uint32_t)di.cus * 8);
     const int mode = g.c >= 256 ? 0 : (g.c >= 4 ? 1 : 2);
     if (g.f32) {
-        if (mode == 0) return launch_dense_t<float, 0>(g, x, y, b, s, grid);
-        if (mode == 1) return launch_dense_t<float, 1>(g, x, y, b, s, grid);
-        return launch_dense_t<float, 2>(g, x, y, b, s, grid);
+        if (mode == 0) return launch_dense_t<float, 0>(g, x, y, b, s, ntiles, di.cus);
+        if (mode == 1) return launch_dense_t<float, 1>(g, x, y, b, s, ntiles, di.cus);
+        return launch_dense_t<float, 2>(g, x, y, b, s, ntiles, di.cus);
     }
-    if (mode == 0) return launch_dense_t<int32_t, 0>(g, x, y, b, s, grid);
-    if (mode == 1) return launch_dense_t<int32_t, 1>(g, x, y, b, s, grid);
-    return launch_dense_t<int32_t, 2>(g, x, y, b, s, grid);
+    if (mode == 0) return launch_dense_t<int32_t, 0>(g, x, y, b, s, ntiles, di.cus);
+    if (mode == 1) return launch_dense_t<int32_t, 1>(g, x, y, b, s, ntiles, di.cus);
+    return launch_dense_t<int32_t, 2>(g, x, y, b, s, ntiles, di.cus);
 }
 
 hipError_t launch_encode_coo(const Geo& g, const uint32_t* idx, const void* val, uint64_t nnz,
