@@ -47,8 +47,8 @@ def parse():
                     help="blocked sketch (section 3.2 blocking), one block per workgroup in LDS; "
                          "default ratio 1.3")
     ap.add_argument("--block-rows", type=int, default=None,
-                    help="rows per block of the blocked sketch (default: the count, among those "
-                         "whose blocks fit in LDS, that minimises encode waves x block size)")
+                    help="rows per block of the blocked sketch (default: the library's choice "
+                         "for this device, hc_geometry_blocked with block_rows = 0)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", action="store_true",
                     help="BERT-base density/overlap grid and sketch-width sweep (one JSON object)")
@@ -79,27 +79,6 @@ def make_workload(a):
     if a.overlap is not None:
         kw["overlap"] = a.overlap
     return wl.make(a.config, vtype=a.vtype, **kw)
-
-
-def pick_block_rows(w, n_agg, gamma, c, cus):
-    """Rows per block for the blocked sketch on this GPU.  Each block is one
-    workgroup of the encode and the decode, whose time grows with the block's
-    batches, and the blocks run ceil(nblocks / CUs) workgroups deep per CU: the
-    row count minimising that product (ties to more rows, i.e. fewer and
-    larger blocks, which peel more reliably).  Blocks keep at least 10,240
-    cells: below about ten thousand members a block needs more room than
-    gamma = 1.3 to peel reliably."""
-    import paper_2402_07529_amd as hc
-    best = None
-    for br in range(-(-10240 // c), -(-20480 // c) + 1):
-        try:
-            p = hc.hc_geometry_blocked(w.n, n_agg, gamma, c, br, w.hash_seed, w.vtype)
-        except hc.HCError:
-            continue  # does not fit in LDS
-        cost = -(-p.nblocks // cus) * int(p.block)
-        if best is None or cost <= best[0]:
-            best = (cost, br)
-    return best[1]
 
 
 def algorithmic_bytes(n, W, cells, n_sup, blocked=False):
@@ -136,13 +115,13 @@ def measured_traffic(workload, vtype):
     return int(fields["traffic_bytes_per_launch"])
 
 
-def cpu_baseline(w, rows, c, block=0):
+def cpu_baseline(w, rows, c, block, seed):
     """The CPU oracle, as it stands, on a bounded sample of the same workload:
     one worker's dense encode (timed), the other workers encoded from COO
     (untimed), the W-way aggregate and the decode (timed).  The iteration
     time is W x encode + aggregate + decode."""
     import oracle
-    g = oracle.Geom(n=w.n, rows=rows, seed=w.hash_seed, c=c, block=block)
+    g = oracle.Geom(n=w.n, rows=rows, seed=seed, c=c, block=block)
     dt = np.int32 if w.vtype == "i32" else np.float64
     x0 = w.dense(0).astype(dt, copy=False)
     t0 = time.perf_counter()
@@ -338,8 +317,7 @@ def main():
     block_rows = None
     ratio = a.ratio if a.ratio is not None else (1.3 if a.blocked else hc.GAMMA)
     if a.blocked:
-        cus = torch.cuda.get_device_properties(dev).multi_processor_count
-        block_rows = a.block_rows or pick_block_rows(w, w.n_agg, ratio, a.c, cus)
+        block_rows = a.block_rows or 0  # 0: the library's choice for this device
     log(f"[bench] workload {w.name} n={w.n} W={w.W} gen {time.perf_counter() - t0:.1f}s")
     r = Runner(w, a.c, dev)
     m = r.run(ratio, a.steps, a.warmup, block_rows=block_rows)
@@ -383,7 +361,7 @@ def main():
     torch.cuda.empty_cache()
     if not a.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
-        res["cpu_baseline"] = cpu_baseline(w, int(p.rows), a.c, int(p.block))
+        res["cpu_baseline"] = cpu_baseline(w, int(p.rows), a.c, int(p.block), int(p.seed))
     print(json.dumps(res), flush=True)
 
 

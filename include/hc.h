@@ -47,8 +47,14 @@
  * belongs to parameter block q = b / K (the last block may be shorter), the
  * sketch has nblocks = ceil(ceil(n/c) / K) blocks of R_b = rows / nblocks rows
  * each, and block q owns rows [q * R_b, (q+1) * R_b): the three rows of batch b
- * are drawn as above from R_b instead of rows and offset by q * R_b.  Every
- * block then peels on its own.  K * c must be a multiple of 32 and rows a
+ * are drawn as above from R_b instead of rows, sorted ascending and offset by
+ * q * R_b.  The rotations of batch number i = b mod K of block q are bias_0 as
+ * above, bias_1 = (bias_0 + pi mod c) mod c and bias_2 = (bias_0 + pi div c)
+ * mod c, with pi = (a_q * i + s_q) mod c^2, a_q = lo32(u_q) | 1,
+ * s_q = u_q >> 32 and u_q = SplitMix64 output number 2^62 + q: for c >= 32 no
+ * two batches of one block sit on the same three rows with the same relative
+ * rotations (which would put every two corresponding elements on the same three
+ * cells, a pair no sketch size peels).  Every block then peels on its own.  K * c must be a multiple of 32 and rows a
  * multiple of nblocks with R_b >= 3.  The library's encode and decode of a
  * blocked sketch hold one block per workgroup in LDS, which needs K <= 1024
  * and, per block, R_b * c * (10 for int32, 14 for fp32) + 12 * K + 256 bytes
@@ -114,7 +120,8 @@ hc_status hc_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
                       uint64_t seed, hc_vtype vtype, hc_params *out);
 
 /* Geometry of a blocked sketch (section 3.2 blocking) whose blocks have at most
- * block_rows rows: K = floor(block_rows * n / (gamma * n_nonzero)) batches per
+ * block_rows rows (block_rows = 0: chosen for the current device, see below):
+ * K = floor(block_rows * n / (gamma * n_nonzero)) batches per
  * block, so that a block's expected share of the aggregate's n_nonzero
  * nonzeros times gamma fills its rows, clamped to [1, min(1024, batches)] and
  * rounded down to a multiple of max(1, 32 / c); each block then gets
@@ -122,8 +129,14 @@ hc_status hc_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
  * expected share of a block of K batches rounded up, and rows = nblocks * R_b.
  * Per-block supports scatter around the expected share, so gamma must leave
  * room for the fullest block (about 1.3 at 14 thousand nonzeros per block where
- * the global sketch needs 1.23).  `out` is a HOST pointer.  HC_EINVAL on invalid
- * arguments, HC_EUNSUPPORTED if a block would not fit the LDS kernels. */
+ * the global sketch needs 1.23).  With block_rows = 0 the library takes, among
+ * the row counts whose blocks hold 10,240 to 20,480 cells and fit the LDS
+ * kernels, the one minimising ceil(nblocks / CUs) * K for the current device's
+ * compute-unit count (each block is one workgroup of the encode and the decode,
+ * whose time grows with K), ties going to more rows; this needs a device
+ * (HC_EHIP without one), and every worker of an aggregation must use the same
+ * geometry.  `out` is a HOST pointer.  HC_EINVAL on invalid arguments,
+ * HC_EUNSUPPORTED if a block would not fit the LDS kernels. */
 hc_status hc_geometry_blocked(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
                               uint32_t block_rows, uint64_t seed, hc_vtype vtype,
                               hc_params *out);

@@ -13,6 +13,10 @@ Paper passages each entry point follows:
   decode     Algorithm 1 phase II: synchronous peeling (section 3.2) and the
              Count Sketch median estimate for what cannot be peeled (3.1)
   rows_for   sketch size at least gamma * n with gamma = 1.23 (section 3.2)
+  bloom_geometry  Bloom-filter index sizing: false positive rate
+             eps = (ln^2 2 gamma C lambda)^-1, log(1/eps) hashes, (n / ln 2)
+             log(1/eps) bits, sketch for the support plus the false positives
+             (section 3.3); bloom_bits: a parameter's filter bits
   decode_bound  how far floating-point rounding of the sketch can move each
              decoded value (the imprecision section 4.1 concedes), carried
              through the decode's schedule; used to set fp32 tolerances
@@ -35,7 +39,8 @@ GAMMA = 1.23  # section 3.2
 class _Geom(ctypes.Structure):
     _fields_ = [("n", ctypes.c_uint64), ("k", ctypes.c_uint32), ("c", ctypes.c_uint32),
                 ("rows", ctypes.c_uint64), ("seed", ctypes.c_uint64),
-                ("block", ctypes.c_uint32), ("pad", ctypes.c_uint32)]
+                ("block", ctypes.c_uint32), ("bloom_k", ctypes.c_uint32),
+                ("bloom_rows", ctypes.c_uint64)]
 
 
 class _Info(ctypes.Structure):
@@ -52,6 +57,8 @@ class Geom:
     c: int = 1024
     k: int = 3
     block: int = 0  # batches per parameter block of a blocked sketch; 0 = one sketch
+    bloom_k: int = 0     # Bloom filter hashes (section 3.3); 0 = bitmap index
+    bloom_rows: int = 0  # rows of c bits in the Bloom filter
 
     @property
     def cells(self) -> int:
@@ -69,10 +76,19 @@ class Geom:
 
     @property
     def words(self) -> int:
+        """Words of an n-bit bitmap (the bitmap index, the recovered mask)."""
         return (self.n + 31) // 32
 
+    @property
+    def index_words(self) -> int:
+        """Words of the index B: the bitmap, or the Bloom filter."""
+        if self.bloom_k == 0:
+            return self.words
+        return (self.bloom_rows * self.c + 31) // 32
+
     def _c(self) -> _Geom:
-        return _Geom(self.n, self.k, self.c, self.rows, self.seed & (2**64 - 1), self.block, 0)
+        return _Geom(self.n, self.k, self.c, self.rows, self.seed & (2**64 - 1), self.block,
+                     self.bloom_k, self.bloom_rows)
 
 
 @dataclass(frozen=True)
@@ -101,6 +117,17 @@ def lib():
                                            ctypes.POINTER(ctypes.c_uint32),
                                            ctypes.POINTER(ctypes.c_uint64)]
         L.hco_blocked_geometry.restype = ctypes.c_int
+        L.hco_bloom_geometry.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double,
+                                         ctypes.c_uint32, ctypes.c_uint32,
+                                         ctypes.POINTER(ctypes.c_uint32),
+                                         ctypes.POINTER(ctypes.c_uint64),
+                                         ctypes.POINTER(ctypes.c_uint64),
+                                         ctypes.POINTER(ctypes.c_double)]
+        L.hco_bloom_geometry.restype = ctypes.c_int
+        L.hco_index_words.argtypes = [G]
+        L.hco_index_words.restype = ctypes.c_uint64
+        L.hco_bloom_bits.argtypes = [G, ctypes.c_uint64, P]
+        L.hco_bloom_bits.restype = None
         L.hco_splitmix64.argtypes = [ctypes.c_uint64, ctypes.c_uint64, P]
         L.hco_splitmix64.restype = None
         L.hco_batch_hash.argtypes = [G, ctypes.c_uint64, P, P, P]
@@ -164,6 +191,26 @@ def blocked_geometry(n: int, n_nonzero: int, seed: int, c: int = 1024, gamma: fl
     return Geom(n=n, rows=int(rows.value), seed=seed, c=c, block=int(blk.value))
 
 
+def bloom_geometry(n: int, n_nonzero: int, seed: int, c: int = 1024, gamma: float = GAMMA,
+                   bits: int = 32):
+    """(Geom with a Bloom-filter index sized by section 3.3, the paper's eps)."""
+    k = ctypes.c_uint32()
+    brows = ctypes.c_uint64()
+    rows = ctypes.c_uint64()
+    eps = ctypes.c_double()
+    if lib().hco_bloom_geometry(n, n_nonzero, gamma, c, bits, ctypes.byref(k), ctypes.byref(brows),
+                                ctypes.byref(rows), ctypes.byref(eps)):
+        raise ValueError("invalid Bloom geometry arguments (or too dense for a filter)")
+    return Geom(n=n, rows=int(rows.value), seed=seed, c=c, bloom_k=int(k.value),
+                bloom_rows=int(brows.value)), float(eps.value)
+
+
+def bloom_bits(g: Geom, p: int) -> np.ndarray:
+    out = np.zeros(max(g.bloom_k, 1), np.uint64)
+    lib().hco_bloom_bits(ctypes.byref(g._c()), p, _ptr(out))
+    return out[:g.bloom_k]
+
+
 def check(g: Geom) -> bool:
     return lib().hco_check_geom(ctypes.byref(g._c())) == 0
 
@@ -194,7 +241,7 @@ def cells(g: Geom, idx) -> tuple[np.ndarray, np.ndarray]:
 
 def encode(g: Geom, x: np.ndarray):
     """Dense encode.  int32 input -> int32 sketch; float input -> fp64 sketch."""
-    B = np.zeros(g.words, np.uint32)
+    B = np.zeros(g.index_words, np.uint32)
     if _is_int(x.dtype):
         x = np.ascontiguousarray(x, np.int32)
         Y = np.zeros(g.cells, np.int32)
@@ -211,7 +258,7 @@ def encode(g: Geom, x: np.ndarray):
 
 def encode_coo(g: Geom, idx: np.ndarray, val: np.ndarray):
     idx = np.ascontiguousarray(idx, np.uint32)
-    B = np.zeros(g.words, np.uint32)
+    B = np.zeros(g.index_words, np.uint32)
     if _is_int(val.dtype):
         val = np.ascontiguousarray(val, np.int32)
         Y = np.zeros(g.cells, np.int32)

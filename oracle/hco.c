@@ -69,6 +69,11 @@ int hco_check_geom(const hco_geom *g)
         if (((uint64_t)g->block * g->c) % 32 != 0) return -1;
         if (g->rows % nb != 0 || g->rows / nb < 3) return -1;
     }
+    if (g->bloom_k != 0) {
+        /* a filter of bloom_rows rows of c bits, bit positions below 2^32 */
+        if (g->bloom_k > 64 || g->bloom_rows == 0) return -1;
+        if (g->bloom_rows > 0xffffffffULL / g->c) return -1;
+    }
     return 0;
 }
 
@@ -108,6 +113,53 @@ int hco_blocked_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t 
     return 0;
 }
 
+int hco_bloom_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
+                       uint32_t bits, uint32_t *bloom_k, uint64_t *bloom_rows,
+                       uint64_t *rows, double *eps)
+{
+    if (n == 0 || n_nonzero == 0 || n_nonzero >= n || !(gamma > 0.0) || bits == 0) return -1;
+    if (c == 0 || c > 1024 || (c & (c - 1)) != 0) return -1;
+    /* section 3.3: lambda * n zero parameters, eps = (ln^2 2 * gamma * C * lambda)^-1 */
+    const double ln2 = log(2.0);
+    double lambda = (double)(n - n_nonzero) / (double)n_nonzero;
+    double e = 1.0 / (ln2 * ln2 * gamma * (double)bits * lambda);
+    /* log(1/eps) hashes per nonzero; (n / ln 2) log(1/eps) bits */
+    double k = floor(log2(1.0 / e) + 0.5);
+    if (!(k >= 1.0)) return -1;
+    if (k > 64.0) k = 64.0;
+    double fbits = ceil(k * (double)n_nonzero / ln2);
+    uint64_t brows = ((uint64_t)fbits + c - 1) / c;
+    /* the sketch holds the candidates: the support and the zeros the filter
+     * lets through, gamma * (n + eps (N - n)) cells (section 3.3's S_2) */
+    double fp = ldexp(1.0, -(int)k);
+    double cand = (double)n_nonzero + fp * (double)(n - n_nonzero);
+    *bloom_k = (uint32_t)k;
+    *bloom_rows = brows;
+    *rows = hco_rows_for((uint64_t)ceil(cand), gamma, c);
+    *eps = e;
+    return 0;
+}
+
+uint64_t hco_index_words(const hco_geom *g)
+{
+    if (g->bloom_k == 0) return (g->n + 31) / 32;
+    return (g->bloom_rows * g->c + 31) / 32;
+}
+
+/* Section 3.3: each nonzero is hashed to log(1/eps) bits of the filter;
+ * section 3.4: the index is batched like the sketch, one row and one rotation
+ * per batch and hash. */
+void hco_bloom_bits(const hco_geom *g, uint64_t p, uint64_t *bits)
+{
+    uint64_t b = p / g->c, t = p % g->c;
+    for (uint32_t i = 0; i < g->bloom_k; i++) {
+        uint64_t u = sm64_output(g->seed, 3ULL * (1ULL << 32) + (uint64_t)g->bloom_k * b + i);
+        uint64_t row = scale32(u, g->bloom_rows);
+        uint64_t bias = (u >> 32) & (uint64_t)(g->c - 1);
+        bits[i] = row * g->c + ((t + bias) % g->c);
+    }
+}
+
 /* Section 3.1: three hash indexes and three signs per index; section 3.4: one
  * row index and one random rotation per batch of c parameters and per hash;
  * section 3.2: with a blocked sketch the rows come from the batch's block. */
@@ -127,14 +179,35 @@ void hco_batch_hash(const hco_geom *g, uint64_t b, uint64_t row[3],
     uint64_t r2 = scale32(h[2], R - 2);
     if (r2 >= lo) r2++;
     if (r2 >= hi) r2++;
-    row[0] = base + r0;
-    row[1] = base + r1;
-    row[2] = base + r2;
-
     for (int j = 0; j < 3; j++) {
         bias[j] = (uint32_t)((h[j] >> 32) & (uint64_t)(g->c - 1));
         sign[j] = (h[j] >> 63) ? -1 : 1;
     }
+    if (g->block == 0) {
+        row[0] = r0;
+        row[1] = r1;
+        row[2] = r2;
+        return;
+    }
+    /* blocked sketch: the three rows in ascending order, and the second and
+     * third rotations offset from the first by the base-c digits of
+     * pi = (a i + s) mod c^2 for the batch's index i in its block, a odd and s
+     * from the block's constant (SplitMix64 output 2^62 + q).  Distinct batches
+     * of a block then never share three rows with the same relative rotations
+     * (c >= 32, so that c^2 >= 1024 >= K) -- a coincidence that would put all
+     * their corresponding elements on the same three cells. */
+    uint64_t v[3] = {r0, r1, r2};
+    for (int x = 0; x < 2; x++)
+        for (int y = 0; y < 2 - x; y++)
+            if (v[y] > v[y + 1]) { uint64_t t = v[y]; v[y] = v[y + 1]; v[y + 1] = t; }
+    for (int j = 0; j < 3; j++) row[j] = base + v[j];
+    uint64_t q = b / g->block, i = b % g->block;
+    uint64_t c = g->c, csq = c * c;
+    uint64_t u = sm64_output(g->seed, (1ULL << 62) + q);
+    uint64_t a = (u & 0xffffffffULL) | 1ULL, s0 = u >> 32;
+    uint64_t pi = (a * i + s0) % csq;
+    bias[1] = (uint32_t)((bias[0] + pi % c) % c);
+    bias[2] = (uint32_t)((bias[0] + pi / c) % c);
 }
 
 static uint64_t cell_of(const hco_geom *g, uint64_t p, const uint64_t row[3],
@@ -165,6 +238,40 @@ static uint64_t n_words(const hco_geom *g) { return (g->n + 31) / 32; }
 static void set_bit(uint32_t *B, uint64_t p) { B[p >> 5] |= 1u << (p & 31); }
 static int get_bit(const uint32_t *B, uint64_t p) { return (B[p >> 5] >> (p & 31)) & 1u; }
 
+/* Record nonzero parameter p in the index: its bit of the bitmap (section
+ * 3.2), or its bloom_k bits of the Bloom filter (section 3.3). */
+static void index_insert(const hco_geom *g, uint32_t *B, uint64_t p)
+{
+    if (g->bloom_k == 0) {
+        set_bit(B, p);
+        return;
+    }
+    uint64_t bits[64];
+    hco_bloom_bits(g, p, bits);
+    for (uint32_t i = 0; i < g->bloom_k; i++) set_bit(B, bits[i]);
+}
+
+/* The parameters the index reports as nonzero, as a bitmap of n bits: the
+ * bitmap itself, or every p whose bloom_k filter bits are all set (the query
+ * of section 3.3). */
+static void index_support(const hco_geom *g, const uint32_t *B, uint32_t *out)
+{
+    memset(out, 0, n_words(g) * sizeof(uint32_t));
+    for (uint64_t p = 0; p < g->n; p++) {
+        int member;
+        if (g->bloom_k == 0) {
+            member = get_bit(B, p);
+        } else {
+            uint64_t bits[64];
+            hco_bloom_bits(g, p, bits);
+            member = 1;
+            for (uint32_t i = 0; i < g->bloom_k; i++)
+                if (!get_bit(B, bits[i])) member = 0;
+        }
+        if (member) set_bit(out, p);
+    }
+}
+
 /* g * v with int32 wrap-around. */
 static uint32_t signed_u32(int32_t sign, uint32_t v) { return sign < 0 ? 0u - v : v; }
 
@@ -178,10 +285,10 @@ int hco_encode_i32(const hco_geom *g, const int32_t *x, int32_t *Y, uint32_t *B)
     if (hco_check_geom(g)) return -1;
     uint32_t *Yu = (uint32_t *)Y;
     memset(Y, 0, n_cells(g) * sizeof(int32_t));
-    memset(B, 0, n_words(g) * sizeof(uint32_t));
+    memset(B, 0, hco_index_words(g) * sizeof(uint32_t));
     for (uint64_t p = 0; p < g->n; p++) {
         if (x[p] == 0) continue;
-        set_bit(B, p);
+        index_insert(g, B, p);
         uint64_t row[3];
         uint32_t bias[3];
         int32_t sign[3];
@@ -195,11 +302,11 @@ int hco_encode_i32(const hco_geom *g, const int32_t *x, int32_t *Y, uint32_t *B)
 int hco_encode_f64(const hco_geom *g, const double *x, double *Y, uint32_t *B)
 {
     if (hco_check_geom(g)) return -1;
-    memset(B, 0, n_words(g) * sizeof(uint32_t));
+    memset(B, 0, hco_index_words(g) * sizeof(uint32_t));
     for (uint64_t i = 0; i < n_cells(g); i++) Y[i] = 0.0;
     for (uint64_t p = 0; p < g->n; p++) {
         if (x[p] == 0.0) continue;
-        set_bit(B, p);
+        index_insert(g, B, p);
         uint64_t row[3];
         uint32_t bias[3];
         int32_t sign[3];
@@ -215,12 +322,12 @@ int hco_encode_coo_i32(const hco_geom *g, const uint32_t *idx, const int32_t *va
     if (hco_check_geom(g)) return -1;
     uint32_t *Yu = (uint32_t *)Y;
     memset(Y, 0, n_cells(g) * sizeof(int32_t));
-    memset(B, 0, n_words(g) * sizeof(uint32_t));
+    memset(B, 0, hco_index_words(g) * sizeof(uint32_t));
     for (uint64_t e = 0; e < nnz; e++) {
         uint64_t p = idx[e];
         if (p >= g->n) return -1;
         if (val[e] == 0) continue;
-        set_bit(B, p);
+        index_insert(g, B, p);
         uint64_t row[3];
         uint32_t bias[3];
         int32_t sign[3];
@@ -235,13 +342,13 @@ int hco_encode_coo_f64(const hco_geom *g, const uint32_t *idx, const double *val
                        uint64_t nnz, double *Y, uint32_t *B)
 {
     if (hco_check_geom(g)) return -1;
-    memset(B, 0, n_words(g) * sizeof(uint32_t));
+    memset(B, 0, hco_index_words(g) * sizeof(uint32_t));
     for (uint64_t i = 0; i < n_cells(g); i++) Y[i] = 0.0;
     for (uint64_t e = 0; e < nnz; e++) {
         uint64_t p = idx[e];
         if (p >= g->n) return -1;
         if (val[e] == 0.0) continue;
-        set_bit(B, p);
+        index_insert(g, B, p);
         uint64_t row[3];
         uint32_t bias[3];
         int32_t sign[3];
@@ -331,6 +438,15 @@ double hco_query_f64(const hco_geom *g, const double *Y, uint64_t p)
     return hco_median3_f64(v[0], v[1], v[2]);
 }
 
+/* The candidate bitmap of an index (index_support) in a new allocation, or
+ * NULL if out of memory. */
+static uint32_t *candidates(const hco_geom *g, const uint32_t *B)
+{
+    uint32_t *cand = (uint32_t *)malloc(n_words(g) * sizeof(uint32_t));
+    if (cand) index_support(g, B, cand);
+    return cand;
+}
+
 /* The support (set bits of B) as an ascending list with each element's three
  * cells and signs.  Returns the element count, or UINT64_MAX on allocation
  * failure (*out_* are then NULL). */
@@ -376,8 +492,10 @@ int hco_decode_i32(const hco_geom *g, const int32_t *Y, const uint32_t *B,
     const uint64_t C = n_cells(g);
     uint64_t *ps, *cell;
     int32_t *sign;
-    const uint64_t m = support_of(g, B, &ps, &cell, &sign);
-    if (m == UINT64_MAX) return -1;
+    uint32_t *cand = candidates(g, B);
+    if (!cand) return -1;
+    const uint64_t m = support_of(g, cand, &ps, &cell, &sign);
+    if (m == UINT64_MAX) { free(cand); return -1; }
 
     uint32_t *Yr = (uint32_t *)malloc(C * sizeof(uint32_t));       /* residual sketch */
     uint32_t *bits = (uint32_t *)malloc(n_words(g) * sizeof(uint32_t)); /* working bitmap */
@@ -386,11 +504,11 @@ int hco_decode_i32(const hco_geom *g, const int32_t *Y, const uint32_t *B,
     int8_t *pick = (int8_t *)malloc(m ? m : 1); /* j of the pure cell, or -1 */
     if (!Yr || !bits || !deg || !val || !pick) {
         free(Yr); free(bits); free(deg); free(val); free(pick);
-        free(ps); free(cell); free(sign);
+        free(ps); free(cell); free(sign); free(cand);
         return -1;
     }
     memcpy(Yr, Y, C * sizeof(uint32_t));
-    memcpy(bits, B, n_words(g) * sizeof(uint32_t));
+    memcpy(bits, cand, n_words(g) * sizeof(uint32_t));
     memset(x_out, 0, g->n * sizeof(int32_t));
     if (mask) memset(mask, 0, n_words(g) * sizeof(uint32_t));
     if (round_of) memset(round_of, 0, g->n * sizeof(uint32_t));
@@ -450,7 +568,7 @@ int hco_decode_i32(const hco_geom *g, const int32_t *Y, const uint32_t *B,
         info->pad = 0;
     }
     free(Yr); free(bits); free(deg); free(val); free(pick);
-    free(ps); free(cell); free(sign);
+    free(ps); free(cell); free(sign); free(cand);
     return 0;
 }
 
@@ -462,8 +580,10 @@ int hco_decode_f64(const hco_geom *g, const double *Y, const uint32_t *B,
     const uint64_t C = n_cells(g);
     uint64_t *ps, *cell;
     int32_t *sign;
-    const uint64_t m = support_of(g, B, &ps, &cell, &sign);
-    if (m == UINT64_MAX) return -1;
+    uint32_t *cand = candidates(g, B);
+    if (!cand) return -1;
+    const uint64_t m = support_of(g, cand, &ps, &cell, &sign);
+    if (m == UINT64_MAX) { free(cand); return -1; }
 
     double *Yr = (double *)malloc(C * sizeof(double));
     uint32_t *bits = (uint32_t *)malloc(n_words(g) * sizeof(uint32_t));
@@ -472,11 +592,11 @@ int hco_decode_f64(const hco_geom *g, const double *Y, const uint32_t *B,
     int8_t *pick = (int8_t *)malloc(m ? m : 1);
     if (!Yr || !bits || !deg || !val || !pick) {
         free(Yr); free(bits); free(deg); free(val); free(pick);
-        free(ps); free(cell); free(sign);
+        free(ps); free(cell); free(sign); free(cand);
         return -1;
     }
     memcpy(Yr, Y, C * sizeof(double));
-    memcpy(bits, B, n_words(g) * sizeof(uint32_t));
+    memcpy(bits, cand, n_words(g) * sizeof(uint32_t));
     for (uint64_t p = 0; p < g->n; p++) x_out[p] = 0.0;
     if (mask) memset(mask, 0, n_words(g) * sizeof(uint32_t));
     if (round_of) memset(round_of, 0, g->n * sizeof(uint32_t));
@@ -530,7 +650,7 @@ int hco_decode_f64(const hco_geom *g, const double *Y, const uint32_t *B,
         info->pad = 0;
     }
     free(Yr); free(bits); free(deg); free(val); free(pick);
-    free(ps); free(cell); free(sign);
+    free(ps); free(cell); free(sign); free(cand);
     return 0;
 }
 
@@ -545,8 +665,10 @@ int hco_decode_bound_f64(const hco_geom *g, const double *dY, const uint32_t *B,
     const uint64_t C = n_cells(g);
     uint64_t *ps, *cell;
     int32_t *sign;
-    const uint64_t m = support_of(g, B, &ps, &cell, &sign);
-    if (m == UINT64_MAX) return -1;
+    uint32_t *cand = candidates(g, B);
+    if (!cand) return -1;
+    const uint64_t m = support_of(g, cand, &ps, &cell, &sign);
+    if (m == UINT64_MAX) { free(cand); return -1; }
 
     double *Eb = (double *)malloc(C * sizeof(double));    /* accumulated cell error */
     uint32_t *bits = (uint32_t *)malloc(n_words(g) * sizeof(uint32_t));
@@ -555,11 +677,11 @@ int hco_decode_bound_f64(const hco_geom *g, const double *dY, const uint32_t *B,
     int8_t *pick = (int8_t *)malloc(m ? m : 1);
     if (!Eb || !bits || !deg || !eb || !pick) {
         free(Eb); free(bits); free(deg); free(eb); free(pick);
-        free(ps); free(cell); free(sign);
+        free(ps); free(cell); free(sign); free(cand);
         return -1;
     }
     for (uint64_t i = 0; i < C; i++) Eb[i] = dY[i] < 0 ? -dY[i] : dY[i];
-    memcpy(bits, B, n_words(g) * sizeof(uint32_t));
+    memcpy(bits, cand, n_words(g) * sizeof(uint32_t));
     for (uint64_t p = 0; p < g->n; p++) bound[p] = 0.0;
 
     for (;;) {
@@ -596,7 +718,7 @@ int hco_decode_bound_f64(const hco_geom *g, const double *dY, const uint32_t *B,
         bound[ps[i]] = b;
     }
     free(Eb); free(bits); free(deg); free(eb); free(pick);
-    free(ps); free(cell); free(sign);
+    free(ps); free(cell); free(sign); free(cand);
     return 0;
 }
 
@@ -612,8 +734,10 @@ int hco_decode_queue_i32(const hco_geom *g, const int32_t *Y, const uint32_t *B,
     const uint64_t C = n_cells(g);
     uint64_t *ps, *cell;
     int32_t *sign;
-    const uint64_t m = support_of(g, B, &ps, &cell, &sign);
-    if (m == UINT64_MAX) return -1;
+    uint32_t *cand = candidates(g, B);
+    if (!cand) return -1;
+    const uint64_t m = support_of(g, cand, &ps, &cell, &sign);
+    if (m == UINT64_MAX) { free(cand); return -1; }
 
     uint32_t *Yr = (uint32_t *)malloc(C * sizeof(uint32_t));
     uint64_t *deg = (uint64_t *)calloc(C, sizeof(uint64_t));
@@ -624,7 +748,7 @@ int hco_decode_queue_i32(const hco_geom *g, const int32_t *Y, const uint32_t *B,
     uint64_t *queue = (uint64_t *)malloc((3 * m + C + 1) * sizeof(uint64_t));
     if (!Yr || !deg || !start || !fill || !adj || !alive || !queue) {
         free(Yr); free(deg); free(start); free(fill); free(adj); free(alive); free(queue);
-        free(ps); free(cell); free(sign);
+        free(ps); free(cell); free(sign); free(cand);
         return -1;
     }
     memcpy(Yr, Y, C * sizeof(uint32_t));
@@ -677,6 +801,6 @@ int hco_decode_queue_i32(const hco_geom *g, const int32_t *Y, const uint32_t *B,
         info->pad = 0;
     }
     free(Yr); free(deg); free(start); free(fill); free(adj); free(alive); free(queue);
-    free(ps); free(cell); free(sign);
+    free(ps); free(cell); free(sign); free(cand);
     return 0;
 }

@@ -34,10 +34,29 @@
  * so that peeling ends in O(1) rounds).  With block = K > 0 the batches are
  * grouped K at a time into parameter blocks q = b / K (the last one may be
  * shorter), and block q owns its own R_b = rows / nblocks consecutive rows:
- * the three rows above are drawn from R_b instead of R and offset by q * R_b.
- * An element's cells then all lie in its block's rows, so the blocks peel
- * independently.  K * c must be a multiple of 32 (whole bitmap words per
- * block).  block = 0 is the single global sketch (one block).
+ * the three rows above are drawn from R_b instead of R, sorted ascending and
+ * offset by q * R_b.  An element's cells then all lie in its block's rows, so
+ * the blocks peel independently.  The rotations of batch number i of block q
+ * are bias_0 as above, bias_1 = bias_0 + (pi mod c), bias_2 = bias_0 +
+ * (pi div c), mod c, with pi = (a_q i + s_q) mod c^2, a_q = lo32(u_q) | 1,
+ * s_q = u_q >> 32, u_q = SplitMix64 output number 2^62 + q: two batches of one
+ * block never share three rows with the same relative rotations (c >= 32),
+ * which would put every pair of their corresponding elements on the same three
+ * cells.  K * c must be a multiple of 32 (whole bitmap words per block).
+ * block = 0 is the single global sketch (one block).
+ *
+ * Bloom-filter index (section 3.3), selected by bloom_k > 0: B is a bit array
+ * of bloom_rows rows of c bits (the index reshaped into a matrix of width c,
+ * section 3.4) instead of the bitmap.  Hash i < bloom_k of batch b is
+ *   u_i(b) = SplitMix64 output number 3 * 2^32 + bloom_k * b + i for `seed`
+ * (a counter range the sketch's outputs 3b + j, b < 2^32, never reach),
+ *   brow_i = mulhi32(lo32(u_i), bloom_rows),  bbias_i = (u_i >> 32) & (c - 1),
+ * and parameter p sets bit brow_i * c + ((t + bbias_i) & (c - 1)) for each i.
+ * Bit q of the array is bit (q & 31) of word q >> 5; bits past
+ * bloom_rows * c are zero.  A parameter is a candidate when all its bloom_k
+ * bits are set: every nonzero is one, a zero is one with the filter's false
+ * positive rate, and the decode peels the candidates (false positives are
+ * recovered with value 0).
  */
 #ifndef HCO_H
 #define HCO_H
@@ -54,7 +73,8 @@ typedef struct {
     uint64_t rows;  /* sketch rows R >= 3; cells = R * c < 2^32               */
     uint64_t seed;  /* hash seed shared by all workers                        */
     uint32_t block; /* batches per parameter block; 0 = one global sketch     */
-    uint32_t pad;
+    uint32_t bloom_k;     /* Bloom filter hashes (section 3.3); 0 = bitmap index */
+    uint64_t bloom_rows;  /* rows of c bits in the Bloom filter (bloom_k > 0)    */
 } hco_geom;
 
 typedef struct {
@@ -83,6 +103,26 @@ uint64_t hco_rows_for(uint64_t n_nonzero, double gamma, uint32_t c);
 int hco_blocked_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
                          uint32_t block_rows, uint32_t max_block, uint32_t *block,
                          uint64_t *rows);
+/* Bloom sizing (section 3.3).  With lambda = (n - n_nonzero) / n_nonzero zero
+ * parameters per nonzero and bit width `bits` (32 here), the false positive
+ * rate is eps = 1 / (ln^2(2) * gamma * bits * lambda); the filter uses
+ * k = max(1, round(log2(1 / eps))) hashes and k * n_nonzero / ln 2 bits
+ * (so that half its bits are set and its false positive rate is 2^-k), in
+ * whole rows of c bits; the sketch holds gamma * (n_nonzero + 2^-k * (n -
+ * n_nonzero)) cells, the support plus the expected false positives, in whole
+ * rows (at least three).  Writes *bloom_k, *bloom_rows, *rows and *eps (the
+ * paper's eps before rounding).  Returns 0, or -1 on invalid arguments or when
+ * k would round to zero (eps > 2^-1/2: the gradient is too dense for a filter
+ * to pay). */
+int hco_bloom_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
+                       uint32_t bits, uint32_t *bloom_k, uint64_t *bloom_rows,
+                       uint64_t *rows, double *eps);
+/* Words of the index B: ceil(n / 32) for the bitmap, ceil(bloom_rows * c / 32)
+ * for a Bloom filter. */
+uint64_t hco_index_words(const hco_geom *g);
+/* The bloom_k bit positions of parameter p (bloom_k > 0). */
+void hco_bloom_bits(const hco_geom *g, uint64_t p, uint64_t *bits);
+
 /* Number of parameter blocks and rows per block of a geometry. */
 uint64_t hco_nblocks(const hco_geom *g);
 uint64_t hco_block_rows(const hco_geom *g);
@@ -96,7 +136,7 @@ void hco_batch_hash(const hco_geom *g, uint64_t b, uint64_t row[3],
 void hco_cells(const hco_geom *g, const uint64_t *idx, uint64_t m,
                uint64_t *cells, int32_t *signs);
 
-/* Phase I on a dense gradient.  Y[cells], B[ceil(n/32)] are overwritten. */
+/* Phase I on a dense gradient.  Y[cells] and B[index words] are overwritten. */
 int hco_encode_i32(const hco_geom *g, const int32_t *x, int32_t *Y, uint32_t *B);
 int hco_encode_f64(const hco_geom *g, const double *x, double *Y, uint32_t *B);
 /* Phase I on COO input (idx distinct, any order; zero values are skipped). */

@@ -149,7 +149,8 @@ def hc_geometry(n: int, n_nonzero: int, gamma: float = GAMMA, c: int = 1024, see
 
 
 def hc_geometry_blocked(n: int, n_nonzero: int, gamma: float = 1.3, c: int = 1024,
-                        block_rows: int = 18, seed: int = 0, vtype: str = "i32") -> hc_params:
+                        block_rows: int = 0, seed: int = 0, vtype: str = "i32") -> hc_params:
+    """block_rows = 0: the library's choice for the current device."""
     p = hc_params()
     vt = HC_F32 if vtype in ("f32", HC_F32) else HC_I32
     _check(_lib.hc_geometry_blocked(n, n_nonzero, gamma, c, block_rows, seed & (2**64 - 1), vt,

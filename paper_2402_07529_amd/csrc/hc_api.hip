@@ -146,16 +146,11 @@ hc_status hc_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c, 
     return HC_OK;
 }
 
-hc_status hc_geometry_blocked(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
-                              uint32_t block_rows, uint64_t seed, hc_vtype vtype, hc_params* out) {
-    g_last_error.clear();
-    if (out == nullptr) return fail(HC_EINVAL, "out is NULL");
-    if (!(gamma > 0.0) || !isfinite(gamma)) return fail(HC_EINVAL, "gamma must be > 0");
-    if (c == 0 || c > 1024 || (c & (c - 1)) != 0)
-        return fail(HC_EINVAL, "c must be a power of two in [1, 1024]");
-    if (n == 0 || n > 0xffffffffull) return fail(HC_EINVAL, "n must be in [1, 2^32 - 1]");
-    if (n_nonzero == 0 || n_nonzero > n) return fail(HC_EINVAL, "n_nonzero must be in [1, n]");
-    if (block_rows < 3) return fail(HC_EINVAL, "block_rows must be >= 3");
+namespace {
+
+// Blocked geometry for a given number of rows per block (validated inputs).
+hc_status blocked_for_rows(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
+                           uint32_t block_rows, uint64_t seed, hc_vtype vtype, hc_params* out) {
     const uint64_t batches = (n + c - 1) / c;
     // batches per block whose expected share of the support, times gamma,
     // fills block_rows rows; whole bitmap words per block
@@ -189,6 +184,52 @@ hc_status hc_geometry_blocked(uint64_t n, uint64_t n_nonzero, double gamma, uint
     if (s != HC_OK) return s;
     if ((s = blocked_supported(g)) != HC_OK) return s;
     *out = p;
+    return HC_OK;
+}
+
+}  // namespace
+
+hc_status hc_geometry_blocked(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
+                              uint32_t block_rows, uint64_t seed, hc_vtype vtype, hc_params* out) {
+    g_last_error.clear();
+    if (out == nullptr) return fail(HC_EINVAL, "out is NULL");
+    if (!(gamma > 0.0) || !isfinite(gamma)) return fail(HC_EINVAL, "gamma must be > 0");
+    if (c == 0 || c > 1024 || (c & (c - 1)) != 0)
+        return fail(HC_EINVAL, "c must be a power of two in [1, 1024]");
+    if (n == 0 || n > 0xffffffffull) return fail(HC_EINVAL, "n must be in [1, 2^32 - 1]");
+    if (n_nonzero == 0 || n_nonzero > n) return fail(HC_EINVAL, "n_nonzero must be in [1, n]");
+    if (block_rows != 0 && block_rows < 3) return fail(HC_EINVAL, "block_rows must be 0 or >= 3");
+    if (block_rows != 0) return blocked_for_rows(n, n_nonzero, gamma, c, block_rows, seed, vtype, out);
+    // automatic choice for the current device: each block is one workgroup of
+    // the encode and of the decode, whose time grows with the block's batches
+    // K, and the blocks run ceil(nblocks / CUs) workgroups deep per CU; take
+    // the row count minimising that product (ties to more rows: fewer, larger
+    // blocks peel more reliably), among blocks of at least 10,240 cells (below
+    // about ten thousand members a block needs more room than gamma = 1.3 to
+    // peel reliably) and at most 20,480
+    DeviceInfo di;
+    const hipError_t e = device_info(&di);
+    if (e != hipSuccess) return fail_hip(e, "hc_geometry_blocked");
+    bool found = false;
+    uint64_t best_cost = 0;
+    hc_params best;
+    memset(&best, 0, sizeof(best));
+    for (uint32_t br = (10240 + c - 1) / c; br <= (20480 + c - 1) / c; br++) {
+        if (br < 3) continue;
+        hc_params p;
+        if (blocked_for_rows(n, n_nonzero, gamma, c, br, seed, vtype, &p) != HC_OK) continue;
+        const uint64_t batches = (n + c - 1) / c;
+        const uint64_t nblocks = (batches + p.block - 1) / p.block;
+        const uint64_t cost = (nblocks + di.cus - 1) / di.cus * p.block;
+        if (!found || cost <= best_cost) {
+            best = p;
+            best_cost = cost;
+            found = true;
+        }
+    }
+    if (!found) return fail(HC_EUNSUPPORTED, "no block size fits the LDS kernels");
+    g_last_error.clear();
+    *out = best;
     return HC_OK;
 }
 

@@ -91,9 +91,10 @@ __device__ __forceinline__ BlockRange block_range(uint32_t q, uint32_t block, ui
 // Local rows, rotations and signs of the block's batches (rows drawn from the
 // block's brows rows, section 3.2 blocking of the section 3.1/3.4 hash).
 __device__ __forceinline__ void fill_table(uint32_t* s_tab, const BlockRange& r, uint64_t seed,
-                                           uint32_t brows, uint32_t c, uint32_t cmask) {
+                                           uint32_t brows, uint32_t c, uint32_t cmask,
+                                           uint32_t log2c, uint32_t block) {
     for (uint32_t i = threadIdx.x; i < r.nb; i += blockDim.x) {
-        const BatchHash h = batch_hash(seed, brows, cmask, r.b0 + i);
+        const BatchHash h = blocked_local_hash(seed, brows, cmask, log2c, r.b0 + i, block);
 #pragma unroll
         for (int j = 0; j < 3; j++) s_tab[3 * i + j] = tab_pack(h, j, c);
     }
@@ -191,7 +192,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_blocked_kernel(EncArgs<T> 
     const uint32_t q = blockIdx.x;
     const BlockRange r = block_range(q, a.block, a.log2c, a.cmask, a.n);
     for (uint32_t i = threadIdx.x; i < a.bcells; i += kEncThreads) s_y[i] = T(0);
-    fill_table(s_tab, r, a.seed, a.brows, a.c, a.cmask);
+    fill_table(s_tab, r, a.seed, a.brows, a.c, a.cmask, a.log2c, a.block);
     __syncthreads();
 
     const uint32_t lane = lane_id();
@@ -440,7 +441,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
             }
         }
     }
-    fill_table(s_tab, r, a.seed, a.brows, a.c, cmask);
+    fill_table(s_tab, r, a.seed, a.brows, a.c, cmask, a.log2c, a.block);
     if (tid < 4) s_tmp[48 + tid] = 0u;
     __syncthreads();
 

@@ -16,7 +16,9 @@ constexpr uint64_t kMix1 = 0xbf58476d1ce4e5b9ull;     // SplitMix64 finalizer
 constexpr uint64_t kMix2 = 0x94d049bb133111ebull;
 
 // SplitMix64 (Steele, Lea and Flood 2014): output number i of state `seed`.
-__device__ __forceinline__ uint64_t splitmix(uint64_t seed, uint64_t i) {
+// The hash helpers are host-callable too: the geometry calls check a blocked
+// sketch's seed on the host.
+__host__ __device__ __forceinline__ uint64_t splitmix(uint64_t seed, uint64_t i) {
     uint64_t z = seed + (i + 1ull) * kGolden;
     z = (z ^ (z >> 30)) * kMix1;
     z = (z ^ (z >> 27)) * kMix2;
@@ -30,20 +32,25 @@ struct BatchHash {
     uint32_t neg;   // bit j set: g_j = -1
 };
 
+// floor(a * b / 2^32)
+__host__ __device__ __forceinline__ uint32_t mulhi32(uint32_t a, uint32_t b) {
+    return (uint32_t)(((uint64_t)a * b) >> 32);
+}
+
 // rows: R >= 3 (< 2^32).  cmask = c - 1.
-__device__ __forceinline__ BatchHash batch_hash(uint64_t seed, uint32_t rows, uint32_t cmask,
-                                                uint64_t b) {
+__host__ __device__ __forceinline__ BatchHash batch_hash(uint64_t seed, uint32_t rows,
+                                                         uint32_t cmask, uint64_t b) {
     const uint64_t h0 = splitmix(seed, 3ull * b + 0ull);
     const uint64_t h1 = splitmix(seed, 3ull * b + 1ull);
     const uint64_t h2 = splitmix(seed, 3ull * b + 2ull);
     BatchHash h;
     // three distinct rows: scale the low words into [0,R), [0,R-1), [0,R-2)
     // and step later rows over the earlier ones
-    uint32_t r0 = __umulhi((uint32_t)h0, rows);
-    uint32_t r1 = __umulhi((uint32_t)h1, rows - 1u);
+    uint32_t r0 = mulhi32((uint32_t)h0, rows);
+    uint32_t r1 = mulhi32((uint32_t)h1, rows - 1u);
     r1 += (r1 >= r0);
-    const uint32_t lo = min(r0, r1), hi = max(r0, r1);
-    uint32_t r2 = __umulhi((uint32_t)h2, rows - 2u);
+    const uint32_t lo = r0 < r1 ? r0 : r1, hi = r0 < r1 ? r1 : r0;
+    uint32_t r2 = mulhi32((uint32_t)h2, rows - 2u);
     r2 += (r2 >= lo);
     r2 += (r2 >= hi);
     h.row[0] = r0;
@@ -56,19 +63,52 @@ __device__ __forceinline__ BatchHash batch_hash(uint64_t seed, uint32_t rows, ui
     return h;
 }
 
-// The same hash for a blocked sketch: batch b belongs to parameter block
-// b / block, whose brows rows start at row (b / block) * brows; the three rows
-// are drawn from those brows.  block == 0: one global sketch of brows rows.
-__device__ __forceinline__ BatchHash batch_hash_blocked(uint64_t seed, uint32_t brows,
-                                                        uint32_t cmask, uint64_t b,
-                                                        uint32_t block) {
+// Counter range of the per-block rotation constants of a blocked sketch: past
+// the batch hashes 3b + j (b < 2^32) and the Bloom filter's hashes.
+constexpr uint64_t kBlockSaltBase = 1ull << 62;
+
+// Hash of batch b in a blocked sketch, in block-local rows: batch b is number
+// i = b mod block of parameter block q = b / block, whose brows rows it draws
+// its three distinct rows from (as batch_hash), taken in ascending order.  Its
+// first rotation is h_0's; the other two are offset from it by the two base-c
+// digits of pi = (a_q i + s_q) mod c^2, with a_q odd and s_q from the block's
+// constant u_q = SplitMix64 output 2^62 + q.  For c >= 32 a block's batches
+// (at most 1024 <= c^2) get distinct offset pairs, so no two batches of one
+// block can sit on the same three rows with the same relative rotations, which
+// would pair every two of their corresponding elements on the same three
+// cells (a stopping set that no sketch size peels; with few rows per block
+// independent rotations make that likely).
+__host__ __device__ __forceinline__ BatchHash blocked_local_hash(uint64_t seed, uint32_t brows,
+                                                                 uint32_t cmask, uint32_t log2c,
+                                                                 uint64_t b, uint32_t block) {
     BatchHash h = batch_hash(seed, brows, cmask, b);
-    if (block != 0) {
-        const uint32_t base = (uint32_t)(b / block) * brows;
-        h.row[0] += base;
-        h.row[1] += base;
-        h.row[2] += base;
-    }
+    const uint32_t r0 = h.row[0], r1 = h.row[1], r2 = h.row[2];
+    const uint32_t lo = r0 < r1 ? (r0 < r2 ? r0 : r2) : (r1 < r2 ? r1 : r2);
+    const uint32_t hi = r0 > r1 ? (r0 > r2 ? r0 : r2) : (r1 > r2 ? r1 : r2);
+    h.row[0] = lo;
+    h.row[1] = r0 + r1 + r2 - lo - hi;
+    h.row[2] = hi;
+    const uint64_t q = b / block;
+    const uint32_t i = (uint32_t)(b - q * block);
+    const uint64_t u = splitmix(seed, kBlockSaltBase + q);
+    const uint32_t m = (cmask + 1u) * (cmask + 1u) - 1u;  // c^2 - 1
+    const uint32_t pi = (((uint32_t)u | 1u) * i + (uint32_t)(u >> 32)) & m;
+    h.bias[1] = (h.bias[0] + (pi & cmask)) & cmask;
+    h.bias[2] = (h.bias[0] + (pi >> log2c)) & cmask;
+    return h;
+}
+
+// Hash of batch b with global rows: the global sketch's (block == 0), or a
+// blocked sketch's local hash offset to the rows of block b / block.
+__host__ __device__ __forceinline__ BatchHash batch_hash_blocked(uint64_t seed, uint32_t brows,
+                                                                 uint32_t cmask, uint32_t log2c,
+                                                                 uint64_t b, uint32_t block) {
+    if (block == 0) return batch_hash(seed, brows, cmask, b);
+    BatchHash h = blocked_local_hash(seed, brows, cmask, log2c, b, block);
+    const uint32_t base = (uint32_t)(b / block) * brows;
+    h.row[0] += base;
+    h.row[1] += base;
+    h.row[2] += base;
     return h;
 }
 

@@ -222,7 +222,8 @@ __global__ __launch_bounds__(kBlock) void encode_coo_kernel(
         const T v = val[i];
         if (p >= n || !Val<T>::nonzero(v)) continue;
         atomicOr(b + (p >> 5), 1u << (p & 31u));
-        const BatchHash h = batch_hash_blocked(seed, brows, cmask, (uint64_t)(p >> log2c), block);
+        const BatchHash h =
+            batch_hash_blocked(seed, brows, cmask, log2c, (uint64_t)(p >> log2c), block);
         const uint32_t t = p & cmask;
 #pragma unroll
         for (int j = 0; j < 3; j++)

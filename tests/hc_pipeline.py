@@ -15,9 +15,11 @@ def wrap_sum(arrs):
     return (acc & 0xFFFFFFFF).astype(np.uint32).view(np.int32)
 
 
-def oracle_run(w, rows: int, c: int, coo: bool = True, block: int = 0):
-    """Oracle encode (per worker), aggregate and decode of workload w."""
-    g = oracle.Geom(n=w.n, rows=rows, seed=w.hash_seed, c=c, block=block)
+def oracle_run(w, rows: int, c: int, coo: bool = True, block: int = 0, seed=None):
+    """Oracle encode (per worker), aggregate and decode of workload w (hash
+    seed: w's unless given)."""
+    seed = w.hash_seed if seed is None else seed
+    g = oracle.Geom(n=w.n, rows=rows, seed=seed, c=c, block=block)
     Ys, Bs = [], []
     for i in range(w.W):
         if coo:
@@ -35,15 +37,15 @@ def oracle_run(w, rows: int, c: int, coo: bool = True, block: int = 0):
 
 def gpu_run(w, rows: int, c: int, coo_input: bool = False, want_coo_out: bool = True,
             max_support: int = 0, keep_workers: bool = True, coo_cap=None, use_plan=False,
-            plan=None, block: int = 0):
+            plan=None, block: int = 0, seed=None):
     """The same pipeline through libhc on the current GPU.  use_plan builds the
     geometry's inverse row map and decodes with it; `plan` passes one in;
-    block > 0 selects the blocked sketch."""
+    block > 0 selects the blocked sketch; seed overrides w's hash seed."""
     import torch
 
     import paper_2402_07529_amd as hc
     dev = torch.device("cuda")
-    p = hc.make_params(w.n, rows, w.hash_seed, c, w.vtype, block=block)
+    p = hc.make_params(w.n, rows, w.hash_seed if seed is None else seed, c, w.vtype, block=block)
     vt = torch.int32 if w.vtype == "i32" else torch.float32
     W = w.W
     Y = torch.empty((W, p.cells), dtype=vt, device=dev)

@@ -148,3 +148,4 @@ def test_blocked_params_rejected():
     # workspace too small
     assert L.hc_decode(ctypes.byref(p), None, V(256), V(256), None, None, None, 0, None, V(256), 0,
                        V(256), 64, None) == hc.HC_EWORKSPACE
+

@@ -225,3 +225,27 @@ def test_blocked_dense_aggregate_c32(block_rows, ok):
     assert bool(r["info"].success) == ok
     if ok:
         assert np.array_equal(r["x"], wrap_sum([w.dense(i) for i in range(w.W)]))
+
+
+def test_blocked_auto_rows_minimise_cost():
+    # block_rows = 0: among the row counts whose blocks hold 10,240 to 20,480
+    # cells and fit the LDS kernels, the least ceil(nblocks / CUs) * K, ties to
+    # more rows
+    hc = _hc()
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    for n, nnz, gamma, c, vt in ((109_482_240, 9_305_915, 1.3, 1024, "i32"),
+                                 (143_667_240, 8_476_348, 1.3, 1024, "f32"),
+                                 (20_000_000, 200_000, 1.4, 256, "i32")):
+        best = None
+        for br in range(-(-10240 // c), -(-20480 // c) + 1):
+            try:
+                p = hc.hc_geometry_blocked(n, nnz, gamma, c, br, 7, vt)
+            except hc.HCError as e:
+                assert e.status == hc.HC_EUNSUPPORTED
+                continue
+            cost = -(-p.nblocks // cus) * int(p.block)
+            if best is None or cost <= best[0]:
+                best = (cost, int(p.block), int(p.rows))
+        p = hc.hc_geometry_blocked(n, nnz, gamma, c, 0, 7, vt)
+        assert (int(p.block), int(p.rows)) == best[1:]

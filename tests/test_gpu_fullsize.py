@@ -114,3 +114,42 @@ def test_fullsize_bert_sweep_corners(density, overlap):
         xo, mo, io = oracle.decode(gg, Ya, Ba)
         assert_same_info(inf, io)
         assert np.array_equal(g["x"], xo)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name,vtype", [("bert", "i32"), ("vgg19", "i32"), ("lstm", "i32"),
+                                        ("vgg19", "f32")])
+def test_fullsize_blocked(name, vtype):
+    # the blocked sketch in bench.py --blocked's configuration: gamma = 1.3 and
+    # the library's rows per block for this device
+    _hc()
+    import paper_2402_07529_amd as hc
+    w = wl.make(name, vtype=vtype)
+    p = hc.hc_geometry_blocked(w.n, w.n_agg, 1.3, 1024, 0, w.hash_seed, vtype)
+    print(f"[fullsize blocked] {name} {vtype}: n={w.n} W={w.W} n_agg={w.n_agg} "
+          f"block={int(p.block)} rows={int(p.rows)} nblocks={p.nblocks} seed={int(p.seed)}",
+          flush=True)
+    g = gpu_run(w, int(p.rows), 1024, want_coo_out=False, block=int(p.block), seed=int(p.seed))
+    o = oracle_run(w, int(p.rows), 1024, block=int(p.block), seed=int(p.seed))
+    if vtype == "i32":
+        for i in range(w.W):
+            assert np.array_equal(g["Y"][i], o["Y"][i]), f"worker {i} sketch"
+            assert np.array_equal(g["B"][i], o["B"][i]), f"worker {i} bitmap"
+        assert np.array_equal(g["Ya"], o["Ya"])
+        assert np.array_equal(g["x"], o["x"])
+    else:
+        wb, ab = fp32_cell_bounds(w, o["g"])
+        for i in range(w.W):
+            assert np.array_equal(g["B"][i], o["B"][i])
+            assert np.all(np.abs(g["Y"][i].astype(np.float64) - o["Y"][i]) <= wb[i] * (1 + 1e-6))
+        assert np.all(np.abs(g["Ya"].astype(np.float64) - o["Ya"]) <= ab * (1 + 1e-6))
+        sup = np.nonzero(np.unpackbits(o["Ba"].view(np.uint8), bitorder="little")[:w.n])[0]
+        assert_fp32_values(g["x"], o["x"], oracle.decode_bound(o["g"], ab, o["Ba"]), sup)
+    assert np.array_equal(g["Ba"], o["Ba"])
+    assert np.array_equal(g["mask"], o["mask"])
+    assert_same_info(g["info"], o["info"])
+    assert g["info"].success and g["info"].n_support == w.n_agg
+    if vtype == "i32":
+        uniq, sums = sparse_direct_sum(w)
+        assert np.array_equal(g["x"][uniq], sums)
+        assert np.count_nonzero(g["x"]) == np.count_nonzero(sums)

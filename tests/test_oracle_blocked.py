@@ -50,16 +50,59 @@ def test_blocked_geometry_invalid():
 
 
 @pytest.mark.parametrize("c", [1024, 64, 1])
-def test_one_block_is_the_global_sketch(c):
+def test_one_block_has_the_global_rows(c):
+    # a single block draws the same three rows per batch as the global sketch
+    # (taken in ascending order), the same signs and the same first rotation
     n = 300_000
     batches = (n + c - 1) // c
     g0 = o.Geom(n=n, rows=57, seed=5, c=c)
     g1 = o.Geom(n=n, rows=57, seed=5, c=c, block=batches + (32 - batches % 32) % 32 if c == 1 else batches)
     assert g1.nblocks == 1
-    idx = np.random.default_rng(3).choice(n, 5000, replace=False).astype(np.uint64)
-    c0, s0 = o.cells(g0, idx)
-    c1, s1 = o.cells(g1, idx)
-    assert np.array_equal(c0, c1) and np.array_equal(s0, s1)
+    for b in np.random.default_rng(3).choice(batches, min(500, batches), replace=False):
+        r0, b0, s0 = o.batch_hash(g0, int(b))
+        r1, b1, s1 = o.batch_hash(g1, int(b))
+        assert np.array_equal(np.sort(r0), r1)
+        assert np.array_equal(s0, s1) and b0[0] == b1[0]
+
+
+def relative_rotation_keys(g):
+    """(block, rows in ascending order, rotations of the 2nd and 3rd row
+    relative to the 1st) of every batch, from the cells of its column 0."""
+    nb = (g.n + g.c - 1) // g.c
+    cl, _ = o.cells(g, np.arange(nb, dtype=np.uint64) * g.c)
+    rows, rot = cl // g.c, cl % g.c
+    order = np.argsort(rows, axis=1)
+    rows = np.take_along_axis(rows, order, 1)
+    rot = np.take_along_axis(rot, order, 1)
+    return np.stack([np.arange(nb) // max(g.block, 1), rows[:, 0], rows[:, 1], rows[:, 2],
+                     (rot[:, 1] - rot[:, 0]) % g.c, (rot[:, 2] - rot[:, 0]) % g.c], 1)
+
+
+@pytest.mark.parametrize("n,nnz,gamma,c,brows", [(109_482_240, 273_579, 1.3, 1024, 18),
+                                                 (143_667_240, 8_476_348, 1.3, 1024, 11),
+                                                 (20_000_000, 100_000, 1.3, 64, 200)])
+def test_no_whole_batch_collisions_in_a_block(n, nnz, gamma, c, brows):
+    # Section 3.4 rotates a batch onto consecutive columns of one row per hash,
+    # so two batches on the same three rows with the same relative rotations
+    # would pair all their corresponding elements on the same three cells
+    # (stopping sets of two).  With 4 rows per block (the sparse BERT-base
+    # sketch), independent rotations would give about 13 such pairs per
+    # sketch; the blocked hash admits none.
+    g = o.blocked_geometry(n, nnz, 2003, c, gamma, brows)
+    key = relative_rotation_keys(g)
+    assert len(np.unique(key, axis=0)) == len(key)
+
+
+def test_blocked_rotations_uniform():
+    # each hash's rotation stays uniform over the columns: chi-square of the
+    # second and third rotations over 64 column bins
+    g = blocked(20_000 * 256, 40, 6, 33, 256)
+    nb = 20_000
+    cl, _ = o.cells(g, np.arange(nb, dtype=np.uint64) * 256)
+    for j in range(3):
+        counts = np.bincount((cl[:, j] % 256) // 4, minlength=64).astype(float)
+        exp = nb / 64
+        assert float(((counts - exp) ** 2 / exp).sum()) < 130  # 63 dof: P(> 130) < 1e-6
 
 
 @pytest.mark.parametrize("c,block,brows", [(1024, 7, 5), (64, 16, 3), (8, 12, 9), (1, 64, 4)])
