@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--ratio", type=float, default=None,
                     help="sketch cells / aggregate nonzeros (default: gamma = 1.23)")
     ap.add_argument("--c", type=int, default=1024)
+    ap.add_argument("--index", default="bitmap", choices=["bitmap", "bloom"],
+                    help="index of the nonzeros: the bitmap (section 3.2) or a Bloom filter sized "
+                         "by section 3.3 (global sketch only)")
     ap.add_argument("--blocked", action="store_true",
                     help="blocked sketch (section 3.2 blocking), one block per workgroup in LDS; "
                          "default ratio 1.3")
@@ -81,15 +84,18 @@ def make_workload(a):
     return wl.make(a.config, vtype=a.vtype, **kw)
 
 
-def algorithmic_bytes(n, W, cells, n_sup, blocked=False):
-    """Bytes the method must move per stage (reads + writes of HBM)."""
+def algorithmic_bytes(n, W, cells, n_sup, index_bytes, blocked=False):
+    """Bytes the method must move per stage (reads + writes of HBM).
+    index_bytes: the index B (the n-bit bitmap, or a Bloom filter, which the
+    decode first probes into an n-bit candidate bitmap)."""
     words_b = (n + 31) // 32 * 4
-    enc = 4 * n + words_b + 4 * cells                     # read x, write B, clear/write Y
-    agg = (W + 1) * (4 * cells + words_b)                  # W sketches+bitmaps in, one out
+    enc = 4 * n + index_bytes + 4 * cells                  # read x, write B, clear/write Y
+    agg = (W + 1) * (4 * cells + index_bytes)              # W sketches+indexes in, one out
+    probe = 0 if index_bytes == words_b else index_bytes + words_b
     if blocked:
         dec = words_b + 4 * cells + 4 * n                  # B, Y, dense out (blocks peel in LDS)
     else:
-        dec = words_b + 4 * cells + 8 * n_sup + 4 * n      # B, Y, element list+values, dense out
+        dec = probe + words_b + 4 * cells + 8 * n_sup + 4 * n  # B, Y, element list+values, out
     return enc, agg, dec
 
 
@@ -183,23 +189,28 @@ class Runner:
         self.out = torch.empty(w.n, dtype=self.vt, device=dev)
         self.mask = torch.empty((w.n + 31) // 32, dtype=torch.int32, device=dev)
 
-    def run(self, ratio, steps, warmup, check=True, block_rows=None):
+    def run(self, ratio, steps, warmup, check=True, block_rows=None, bloom=False):
         """block_rows: None for the global sketch, else the rows per block of
-        a blocked sketch."""
+        a blocked sketch; bloom: a Bloom-filter index instead of the bitmap."""
         import paper_2402_07529_amd as hc
         torch, w, dev, W = self.torch, self.w, self.dev, self.w.W
-        if block_rows is None:
+        max_support = self.n_agg
+        if bloom:
+            p, _ = hc.hc_geometry_bloom(w.n, self.n_agg, ratio, self.c, w.hash_seed, w.vtype)
+            # room for four times the filter's expected false positives
+            max_support = int(self.n_agg + 4 * 2.0**-int(p.bloom_k) * (w.n - self.n_agg)) + 1024
+        elif block_rows is None:
             p = hc.hc_geometry(w.n, self.n_agg, ratio, self.c, w.hash_seed, w.vtype)
         else:
             p = hc.hc_geometry_blocked(w.n, self.n_agg, ratio, self.c, block_rows, w.hash_seed,
                                        w.vtype)
-        cells, words = p.cells, p.words
+        cells, words = p.cells, p.index_words
         Y = torch.empty((W, cells), dtype=self.vt, device=dev)
         B = torch.empty((W, words), dtype=torch.int32, device=dev)
         Ya = torch.empty(cells, dtype=self.vt, device=dev)
         Ba = torch.empty(words, dtype=torch.int32, device=dev)
         info = hc.alloc_info(dev)
-        ws = hc.alloc_workspace(p, self.n_agg, dev)
+        ws = hc.alloc_workspace(p, max_support, dev)
         stream = torch.cuda.current_stream()
         # the inverse row map depends only on the geometry: built once, like
         # the sketch geometry itself, before any iteration
@@ -220,7 +231,7 @@ class Runner:
             hc.hc_aggregate(p, Y, B, W, Ya, Ba, stream)
             if ev is not None:
                 ev[2].record(stream)
-            hc.hc_decode(p, Ya, Ba, info, ws, x_out=out, mask=mask, max_support=self.n_agg,
+            hc.hc_decode(p, Ya, Ba, info, ws, x_out=out, mask=mask, max_support=max_support,
                          stream=stream, plan=plan)
             if ev is not None:
                 ev[3].record(stream)
@@ -320,12 +331,16 @@ def main():
         block_rows = a.block_rows or 0  # 0: the library's choice for this device
     log(f"[bench] workload {w.name} n={w.n} W={w.W} gen {time.perf_counter() - t0:.1f}s")
     r = Runner(w, a.c, dev)
-    m = r.run(ratio, a.steps, a.warmup, block_rows=block_rows)
+    if a.index == "bloom" and a.blocked:
+        print("bench.py: the Bloom-filter index needs the global sketch", file=sys.stderr)
+        sys.exit(2)
+    m = r.run(ratio, a.steps, a.warmup, block_rows=block_rows, bloom=a.index == "bloom")
     p, inf, W, n_agg = m["p"], m["info"], w.W, r.n_agg
     ms, enc_ms, agg_ms, dec_ms = m["ms"], m["enc_ms"], m["agg_ms"], m["dec_ms"]
     cells = p.cells
 
-    enc_b, agg_b, dec_b = algorithmic_bytes(w.n, W, cells, inf.n_support, a.blocked)
+    enc_b, agg_b, dec_b = algorithmic_bytes(w.n, W, cells, inf.n_support, 4 * p.index_words,
+                                            a.blocked)
     iter_b = W * enc_b + agg_b + dec_b
     value = 4 * w.n / (ms * 1e-3) / 1e9
     enc_gbs = enc_b / (enc_ms * 1e-3) / 1e9
@@ -335,16 +350,19 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int32" if w.vtype == "i32" else "fp32", "data": "synthetic",
         "config": {"workload": w.name, "n": w.n, "workers": W, "n_agg": n_agg,
-                   "rows": int(p.rows), "c": a.c, "cells": cells, "ratio": round(cells / max(n_agg, 1), 4),
+                   "rows": int(p.rows), "c": int(p.c), "cells": cells, "ratio": round(cells / max(n_agg, 1), 4),
                    "sketch": (f"blocked: {int(p.block)} batches and {p.block_rows} rows per block, "
                               f"{p.nblocks} blocks") if a.blocked else "global",
+                   "index": (f"bloom: {int(p.bloom_k)} hashes, {4 * p.index_words} bytes"
+                             if a.index == "bloom" else "bitmap"),
                    **{k: v for k, v in w.params.items() if k in ("density", "overlap", "rows_per_worker")}},
         "roofline": {"bound": "hbm",
                      "kernel": ("hc_encode (blocked LDS encode)" if a.blocked
                                 else "hc_encode (Y clear + dense encode)"),
                      "achieved": round(enc_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(enc_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": None if a.blocked else measured_traffic(w.name, w.vtype),
+                     "traffic": (None if a.blocked or a.index == "bloom"
+                                 else measured_traffic(w.name, w.vtype)),
                      "bytes_per_launch": enc_b, "avg_launch_ms": round(enc_ms, 4)},
         "hbm_frac_iteration": round(iter_b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "stages_ms": {"encode_per_worker": round(enc_ms, 4), "aggregate": round(agg_ms, 4),
@@ -359,9 +377,13 @@ def main():
     }
     del r
     torch.cuda.empty_cache()
-    if not a.no_cpu_baseline:
+    if not a.no_cpu_baseline and a.index == "bloom":
+        # the oracle's filter query visits every parameter with every hash: far
+        # beyond the bounded sample the baseline is meant to take
+        log("[bench] no CPU baseline for the Bloom-filter index")
+    elif not a.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample ...")
-        res["cpu_baseline"] = cpu_baseline(w, int(p.rows), a.c, int(p.block), int(p.seed))
+        res["cpu_baseline"] = cpu_baseline(w, int(p.rows), int(p.c), int(p.block), int(p.seed))
     print(json.dumps(res), flush=True)
 
 

@@ -13,6 +13,7 @@
  *   hc_decode                   Algorithm 1, phase II (section 3.2 peeling,
  *                               section 3.1 median estimate for leftovers)
  *   hc_geometry / hc_sizes      sketch sizing, |Y| >= gamma * n (section 3.2)
+ *   hc_geometry_bloom           the same with a Bloom-filter index (section 3.3)
  *   hc_plan_bytes / _build      the inverse row map of a geometry (section 3.4
  *                               batching), built once, used by the decode
  *
@@ -42,6 +43,19 @@
  *   B[ceil(n/32)] is a bitmap, bit p = bit (p mod 32) of word p / 32; bits at
  *   or past n are zero.
  *
+ * Bloom-filter index (section 3.3), selected by hc_params.bloom_k = k > 0: B is
+ * a bit array of bloom_rows rows of c bits (the index reshaped into a matrix of
+ * width c as in section 3.4) instead of the bitmap, ceil(bloom_rows * c / 32)
+ * words, bit q = bit (q mod 32) of word q / 32, bits past bloom_rows * c zero.
+ * Hash i < k of batch b is u = SplitMix64 output number 3 * 2^32 + k * b + i
+ * for `seed`, giving row mulhi32(lo32(u), bloom_rows) and rotation
+ * (u >> 32) mod c; a nonzero parameter at column t sets bit
+ * row * c + ((t + rotation) mod c) for each i.  The decode treats as the support
+ * every parameter whose k bits are all set: the nonzeros (a Bloom filter has no
+ * false negatives) and the zeros the filter lets through, which peel to 0.
+ * The filter merges under OR exactly like the bitmap.  Supported with the
+ * global sketch only (HC_EUNSUPPORTED with block > 0).
+ *
  * Blocked sketch (section 3.2: the sketch split into blocks of a fixed size so
  * that peeling takes O(1) rounds), selected by hc_params.block = K > 0: batch b
  * belongs to parameter block q = b / K (the last block may be shorter), the
@@ -50,11 +64,15 @@
  * are drawn as above from R_b instead of rows, sorted ascending and offset by
  * q * R_b.  The rotations of batch number i = b mod K of block q are bias_0 as
  * above, bias_1 = (bias_0 + pi mod c) mod c and bias_2 = (bias_0 + pi div c)
- * mod c, with pi = (a_q * i + s_q) mod c^2, a_q = lo32(u_q) | 1,
- * s_q = u_q >> 32 and u_q = SplitMix64 output number 2^62 + q: for c >= 32 no
- * two batches of one block sit on the same three rows with the same relative
- * rotations (which would put every two corresponding elements on the same three
- * cells, a pair no sketch size peels).  Every block then peels on its own.  K * c must be a multiple of 32 and rows a
+ * mod c, with pi = P(i) for the bijection P of [0, M = c^2) keyed by
+ * u_q = SplitMix64 output number 2^62 + q: with a1, a2 and s the low, middle
+ * and high 20-bit fields of u_q (a1, a2 made odd) and h = ceil(log2(M) / 2),
+ * x = (i + s) mod M, x = x * a1 mod M, x ^= x >> h, x = x * a2 mod M,
+ * x ^= x >> h.  For c >= 32 no two batches of one block then sit on the same
+ * three rows with the same relative rotations (which would put every two
+ * corresponding elements on the same three cells, a pair no sketch size
+ * peels), and the offsets carry no arithmetic structure.  Every block then
+ * peels on its own.  K * c must be a multiple of 32 and rows a
  * multiple of nblocks with R_b >= 3.  The library's encode and decode of a
  * blocked sketch hold one block per workgroup in LDS, which needs K <= 1024
  * and, per block, R_b * c * (10 for int32, 14 for fp32) + 12 * K + 256 bytes
@@ -95,11 +113,18 @@ typedef struct {
     uint32_t vtype;    /* hc_vtype of the gradient and sketch values             */
     uint32_t block;    /* batches per parameter block of a blocked sketch
                           (section 3.2); 0 = one global sketch                   */
+    uint32_t bloom_k;  /* Bloom filter hashes per nonzero (section 3.3), 1..64;
+                          0 = the bitmap index of section 3.2                    */
+    uint32_t reserved; /* must be 0                                              */
+    uint64_t bloom_rows; /* rows of c bits in the Bloom filter (bloom_k > 0);
+                          bloom_rows * c must be < 2^32                          */
 } hc_params;
 
 /* Written by hc_decode into DEVICE memory. */
 typedef struct {
-    uint64_t n_support;   /* set bits of the aggregated bitmap (nonzeros of sum X) */
+    uint64_t n_support;   /* set bits of the aggregated bitmap (nonzeros of sum X);
+                             with a Bloom filter, the parameters it reports as
+                             nonzero (the support plus its false positives)     */
     uint64_t n_recovered; /* of those, recovered exactly by peeling                */
     uint64_t rounds;      /* synchronous peeling rounds that recovered >= 1        */
     uint32_t success;     /* 1 iff n_recovered == n_support                        */
@@ -133,15 +158,34 @@ hc_status hc_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
  * the row counts whose blocks hold 10,240 to 20,480 cells and fit the LDS
  * kernels, the one minimising ceil(nblocks / CUs) * K for the current device's
  * compute-unit count (each block is one workgroup of the encode and the decode,
- * whose time grows with K), ties going to more rows; this needs a device
- * (HC_EHIP without one), and every worker of an aggregation must use the same
- * geometry.  `out` is a HOST pointer.  HC_EINVAL on invalid arguments,
+ * whose time grows with K), ties going to more rows; and if that leaves fewer
+ * than K = 600 * n_nonzero / n batches per block it halves c (down to 32) until
+ * it does not: blocks of few, dense batches have a small batch-to-row graph
+ * whose short cycles line columns of elements up into stopping sets (measured:
+ * such blocks failed for aggregate densities of 40 % and more, larger ones did
+ * not).  out->c then holds the c used.  This needs a device (HC_EHIP without
+ * one), and every worker of an aggregation must use the same geometry.  `out` is a HOST pointer.  HC_EINVAL on invalid arguments,
  * HC_EUNSUPPORTED if a block would not fit the LDS kernels. */
 hc_status hc_geometry_blocked(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
                               uint32_t block_rows, uint64_t seed, hc_vtype vtype,
                               hc_params *out);
 
-/* Byte sizes (HOST outputs, each may be NULL): one sketch Y, one bitmap B, and
+/* Geometry with a Bloom-filter index (section 3.3).  With lambda = (n -
+ * n_nonzero) / n_nonzero zero parameters per nonzero and C = 32-bit values, the
+ * paper's false positive rate is eps = 1 / (ln^2(2) * gamma * C * lambda); the
+ * filter takes k = round(log2(1 / eps)) hashes (at most 64) and
+ * ceil(k * n_nonzero / ln 2) bits, rounded up to whole rows of c bits (half its
+ * bits end up set, so a zero passes with probability about 2^-k), and the
+ * sketch holds gamma times the expected candidates, n_nonzero + 2^-k * (n -
+ * n_nonzero), in whole rows of c cells (at least three).  *eps (HOST, may be
+ * NULL) receives the paper's eps.  HC_EINVAL if n_nonzero is 0 or >= n, or if k
+ * would round to 0 (eps > 2^-1/2: too dense for a filter to pay); `out` is a
+ * HOST pointer. */
+hc_status hc_geometry_bloom(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
+                            uint64_t seed, hc_vtype vtype, hc_params *out, double *eps);
+
+/* Byte sizes (HOST outputs, each may be NULL): one sketch Y, one index B (the
+ * bitmap, or the Bloom filter), and
  * the decode workspace for a support of up to max_support nonzeros
  * (0 means n, which always suffices; a blocked sketch's workspace does not
  * depend on it). */
@@ -162,8 +206,10 @@ hc_status hc_plan_build(const hc_params *p, void *plan, size_t plan_bytes, hipSt
 
 /* Phase I on a dense gradient x[n] (int32 or fp32 per p->vtype).  Overwrites
  * y[cells] with the Count Sketch (Y[h_j(p)] += g_j(p) * x_p for every nonzero
- * x_p, section 3.1 with the batching of 3.4) and b[ceil(n/32)] with the
- * nonzero bitmap (section 3.2).  No pre-zeroing is needed.  fp32 sums are
+ * x_p, section 3.1 with the batching of 3.4) and b with the index: the
+ * nonzero bitmap b[ceil(n/32)] (section 3.2), or the Bloom filter of every
+ * nonzero (section 3.3; b[ceil(bloom_rows * c / 32)]).  No pre-zeroing is
+ * needed.  fp32 sums are
  * accumulated with atomics (global, or in LDS for a blocked sketch), so their
  * rounding order is not fixed. */
 hc_status hc_encode(const hc_params *p, const void *x, void *y, uint32_t *b,
@@ -177,9 +223,10 @@ hc_status hc_encode_coo(const hc_params *p, const uint32_t *idx, const void *val
 
 /* The aggregation step: y_out[i] = sum over w < W of y_in[w * cells + i]
  * (int32 wraps modulo 2^32; fp32 adds in worker order 0..W-1) and
- * b_out[i] = OR over w of b_in[w * words + i], words = ceil(n/32).  Inputs are
- * W sketches and W bitmaps stored back to back.  Outputs may not alias
- * inputs.  W >= 1. */
+ * b_out[i] = OR over w of b_in[w * words + i], words = the index's words
+ * (ceil(n/32) for the bitmap, ceil(bloom_rows * c / 32) for a Bloom filter).
+ * Inputs are W sketches and W indexes stored back to back.  Outputs may not
+ * alias inputs.  W >= 1. */
 hc_status hc_aggregate(const hc_params *p, const void *y_in, const uint32_t *b_in,
                        uint32_t W, void *y_out, uint32_t *b_out, hipStream_t stream);
 
@@ -190,7 +237,10 @@ hc_status hc_aggregate(const hc_params *p, const void *y_in, const uint32_t *b_i
  * geometry is detected on the device and reported as status 3.  A blocked
  * sketch takes no plan (HC_EINVAL if one is given): each block is peeled by one
  * workgroup in LDS, in the same synchronous rounds; info->rounds is then the
- * largest round count of any block, and max_support is not used.
+ * largest round count of any block, and max_support is not used.  With a
+ * Bloom-filter index the support is every parameter whose filter bits are all
+ * set (probed into a bitmap in the workspace first); max_support must then
+ * cover those candidates, false positives included.
  * Outputs (each may be NULL):
  *   x_out[n]              dense sum X: recovered values, the Count Sketch
  *                         median estimate for members of the support that

@@ -128,6 +128,8 @@ def lib():
         L.hco_index_words.restype = ctypes.c_uint64
         L.hco_bloom_bits.argtypes = [G, ctypes.c_uint64, P]
         L.hco_bloom_bits.restype = None
+        L.hco_bloom_query.argtypes = [G, P, P, ctypes.c_uint64, P]
+        L.hco_bloom_query.restype = None
         L.hco_splitmix64.argtypes = [ctypes.c_uint64, ctypes.c_uint64, P]
         L.hco_splitmix64.restype = None
         L.hco_batch_hash.argtypes = [G, ctypes.c_uint64, P, P, P]
@@ -209,6 +211,15 @@ def bloom_bits(g: Geom, p: int) -> np.ndarray:
     out = np.zeros(max(g.bloom_k, 1), np.uint64)
     lib().hco_bloom_bits(ctypes.byref(g._c()), p, _ptr(out))
     return out[:g.bloom_k]
+
+
+def bloom_query(g: Geom, B: np.ndarray, idx) -> np.ndarray:
+    """Section 3.3 query: True where all of a parameter's filter bits are set."""
+    idx = np.ascontiguousarray(idx, np.uint64)
+    B = np.ascontiguousarray(B, np.uint32)
+    out = np.zeros(idx.size, np.uint8)
+    lib().hco_bloom_query(ctypes.byref(g._c()), _ptr(B), _ptr(idx), idx.size, _ptr(out))
+    return out.astype(bool)
 
 
 def check(g: Geom) -> bool:

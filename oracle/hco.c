@@ -160,6 +160,19 @@ void hco_bloom_bits(const hco_geom *g, uint64_t p, uint64_t *bits)
     }
 }
 
+void hco_bloom_query(const hco_geom *g, const uint32_t *B, const uint64_t *idx, uint64_t m,
+                     uint8_t *out)
+{
+    uint64_t bits[64];
+    for (uint64_t e = 0; e < m; e++) {
+        hco_bloom_bits(g, idx[e], bits);
+        uint8_t all = 1;
+        for (uint32_t i = 0; i < g->bloom_k; i++)
+            if (!((B[bits[i] >> 5] >> (bits[i] & 31)) & 1u)) all = 0;
+        out[e] = all;
+    }
+}
+
 /* Section 3.1: three hash indexes and three signs per index; section 3.4: one
  * row index and one random rotation per batch of c parameters and per hash;
  * section 3.2: with a blocked sketch the rows come from the batch's block. */
@@ -191,23 +204,35 @@ void hco_batch_hash(const hco_geom *g, uint64_t b, uint64_t row[3],
     }
     /* blocked sketch: the three rows in ascending order, and the second and
      * third rotations offset from the first by the base-c digits of
-     * pi = (a i + s) mod c^2 for the batch's index i in its block, a odd and s
-     * from the block's constant (SplitMix64 output 2^62 + q).  Distinct batches
-     * of a block then never share three rows with the same relative rotations
-     * (c >= 32, so that c^2 >= 1024 >= K) -- a coincidence that would put all
-     * their corresponding elements on the same three cells. */
+     * pi = P(i), a bijection of [0, c^2) applied to the batch's index i in its
+     * block and keyed by the block's constant u (SplitMix64 output 2^62 + q).
+     * Distinct batches of a block then never share three rows with the same
+     * relative rotations (c >= 32, so that c^2 >= 1024 >= K) -- a coincidence
+     * that would put all their corresponding elements on the same three cells.
+     * P: with M = c^2, a1, a2 and s the low, middle and high 20-bit fields of
+     * u (a1, a2 made odd) and h = half the bits of M rounded up:
+     * x = (i + s) mod M; x = x a1 mod M; x ^= x >> h; x = x a2 mod M; x ^= x >> h. */
     uint64_t v[3] = {r0, r1, r2};
     for (int x = 0; x < 2; x++)
         for (int y = 0; y < 2 - x; y++)
             if (v[y] > v[y + 1]) { uint64_t t = v[y]; v[y] = v[y + 1]; v[y + 1] = t; }
     for (int j = 0; j < 3; j++) row[j] = base + v[j];
     uint64_t q = b / g->block, i = b % g->block;
-    uint64_t c = g->c, csq = c * c;
+    uint64_t c = g->c, M = c * c;
+    unsigned bits = 0;
+    while ((1ULL << bits) < M) bits++;
+    unsigned hshift = (bits + 1) / 2;
     uint64_t u = sm64_output(g->seed, (1ULL << 62) + q);
-    uint64_t a = (u & 0xffffffffULL) | 1ULL, s0 = u >> 32;
-    uint64_t pi = (a * i + s0) % csq;
-    bias[1] = (uint32_t)((bias[0] + pi % c) % c);
-    bias[2] = (uint32_t)((bias[0] + pi / c) % c);
+    uint64_t a1 = (u & 0xfffffULL) | 1ULL;
+    uint64_t a2 = ((u >> 20) & 0xfffffULL) | 1ULL;
+    uint64_t s0 = (u >> 40) & 0xfffffULL;
+    uint64_t x = (i + s0) % M;
+    x = (x * a1) % M;
+    x ^= x >> hshift;
+    x = (x * a2) % M;
+    x ^= x >> hshift;
+    bias[1] = (uint32_t)((bias[0] + x % c) % c);
+    bias[2] = (uint32_t)((bias[0] + x / c) % c);
 }
 
 static uint64_t cell_of(const hco_geom *g, uint64_t p, const uint64_t row[3],

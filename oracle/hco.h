@@ -38,11 +38,11 @@
  * offset by q * R_b.  An element's cells then all lie in its block's rows, so
  * the blocks peel independently.  The rotations of batch number i of block q
  * are bias_0 as above, bias_1 = bias_0 + (pi mod c), bias_2 = bias_0 +
- * (pi div c), mod c, with pi = (a_q i + s_q) mod c^2, a_q = lo32(u_q) | 1,
- * s_q = u_q >> 32, u_q = SplitMix64 output number 2^62 + q: two batches of one
- * block never share three rows with the same relative rotations (c >= 32),
- * which would put every pair of their corresponding elements on the same three
- * cells.  K * c must be a multiple of 32 (whole bitmap words per block).
+ * (pi div c), mod c, with pi = P_q(i) a bijection of [0, c^2) keyed by
+ * u_q = SplitMix64 output number 2^62 + q (see hco_batch_hash): two batches of
+ * one block never share three rows with the same relative rotations
+ * (c >= 32), which would put every pair of their corresponding elements on the
+ * same three cells.  K * c must be a multiple of 32 (whole bitmap words per block).
  * block = 0 is the single global sketch (one block).
  *
  * Bloom-filter index (section 3.3), selected by bloom_k > 0: B is a bit array
@@ -122,6 +122,10 @@ int hco_bloom_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
 uint64_t hco_index_words(const hco_geom *g);
 /* The bloom_k bit positions of parameter p (bloom_k > 0). */
 void hco_bloom_bits(const hco_geom *g, uint64_t p, uint64_t *bits);
+/* Section 3.3 query for m parameters: out[i] = 1 iff all bloom_k bits of
+ * idx[i] are set in the filter B. */
+void hco_bloom_query(const hco_geom *g, const uint32_t *B, const uint64_t *idx, uint64_t m,
+                     uint8_t *out);
 
 /* Number of parameter blocks and rows per block of a geometry. */
 uint64_t hco_nblocks(const hco_geom *g);

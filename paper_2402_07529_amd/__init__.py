@@ -7,6 +7,7 @@ C ABI:
 
     hc_geometry   sketch sizing, |Y| >= gamma * n (section 3.2, gamma = 1.23)
     hc_geometry_blocked  the same for a blocked sketch (section 3.2 blocking)
+    hc_geometry_bloom    the same with a Bloom-filter index (section 3.3)
     hc_sizes      byte sizes of Y, B and the decode workspace
     hc_plan_bytes, hc_plan_build   inverse row map of a geometry (c >= 256)
     hc_encode     Algorithm 1 phase I on a dense gradient (sections 3.1-3.4)
@@ -31,8 +32,9 @@ HC_I32, HC_F32 = 0, 1
 GAMMA = 1.23
 INFO_BYTES = 32
 
-EXPORTS = ("hc_geometry", "hc_geometry_blocked", "hc_sizes", "hc_plan_bytes", "hc_plan_build", "hc_encode",
-           "hc_encode_coo", "hc_aggregate", "hc_decode", "hc_status_string", "hc_last_error")
+EXPORTS = ("hc_geometry", "hc_geometry_blocked", "hc_geometry_bloom", "hc_sizes", "hc_plan_bytes",
+           "hc_plan_build", "hc_encode", "hc_encode_coo", "hc_aggregate", "hc_decode",
+           "hc_status_string", "hc_last_error")
 
 
 class HCError(RuntimeError):
@@ -44,7 +46,9 @@ class HCError(RuntimeError):
 class hc_params(ctypes.Structure):
     _fields_ = [("n", ctypes.c_uint64), ("k", ctypes.c_uint32), ("c", ctypes.c_uint32),
                 ("rows", ctypes.c_uint64), ("seed", ctypes.c_uint64),
-                ("vtype", ctypes.c_uint32), ("block", ctypes.c_uint32)]
+                ("vtype", ctypes.c_uint32), ("block", ctypes.c_uint32),
+                ("bloom_k", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("bloom_rows", ctypes.c_uint64)]
 
     @property
     def cells(self) -> int:
@@ -52,7 +56,15 @@ class hc_params(ctypes.Structure):
 
     @property
     def words(self) -> int:
+        """Words of an n-bit bitmap (the bitmap index, the recovered mask)."""
         return (int(self.n) + 31) // 32
+
+    @property
+    def index_words(self) -> int:
+        """Words of the index B: the bitmap, or the Bloom filter."""
+        if int(self.bloom_k) == 0:
+            return self.words
+        return (int(self.bloom_rows) * int(self.c) + 31) // 32
 
     @property
     def is_f32(self) -> bool:
@@ -80,6 +92,9 @@ _lib.hc_geometry.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double, 
 _lib.hc_geometry_blocked.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double,
                                      ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64,
                                      ctypes.c_int, _PP]
+_lib.hc_geometry_bloom.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double,
+                                   ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int, _PP,
+                                   ctypes.POINTER(ctypes.c_double)]
 _lib.hc_sizes.argtypes = [_PP, ctypes.c_uint64, ctypes.POINTER(ctypes.c_size_t),
                           ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)]
 _lib.hc_encode.argtypes = [_PP, _P, _P, _P, _P]
@@ -89,8 +104,8 @@ _lib.hc_decode.argtypes = [_PP, _P, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P,
                            _P, ctypes.c_size_t, _P]
 _lib.hc_plan_bytes.argtypes = [_PP, ctypes.POINTER(ctypes.c_size_t)]
 _lib.hc_plan_build.argtypes = [_PP, _P, ctypes.c_size_t, _P]
-for _f in ("hc_geometry", "hc_geometry_blocked", "hc_sizes", "hc_plan_bytes", "hc_plan_build", "hc_encode",
-           "hc_encode_coo", "hc_aggregate", "hc_decode"):
+for _f in ("hc_geometry", "hc_geometry_blocked", "hc_geometry_bloom", "hc_sizes", "hc_plan_bytes",
+           "hc_plan_build", "hc_encode", "hc_encode_coo", "hc_aggregate", "hc_decode"):
     getattr(_lib, _f).restype = ctypes.c_int
 _lib.hc_status_string.argtypes = [ctypes.c_int]
 _lib.hc_status_string.restype = ctypes.c_char_p
@@ -158,10 +173,21 @@ def hc_geometry_blocked(n: int, n_nonzero: int, gamma: float = 1.3, c: int = 102
     return p
 
 
+def hc_geometry_bloom(n: int, n_nonzero: int, gamma: float = GAMMA, c: int = 1024, seed: int = 0,
+                      vtype: str = "i32"):
+    """(params with a Bloom-filter index, the paper's eps)."""
+    p = hc_params()
+    eps = ctypes.c_double()
+    vt = HC_F32 if vtype in ("f32", HC_F32) else HC_I32
+    _check(_lib.hc_geometry_bloom(n, n_nonzero, gamma, c, seed & (2**64 - 1), vt, ctypes.byref(p),
+                                  ctypes.byref(eps)), "hc_geometry_bloom")
+    return p, eps.value
+
+
 def make_params(n: int, rows: int, seed: int, c: int = 1024, vtype: str = "i32",
-                block: int = 0) -> hc_params:
+                block: int = 0, bloom_k: int = 0, bloom_rows: int = 0) -> hc_params:
     return hc_params(n, 3, c, rows, seed & (2**64 - 1), HC_F32 if vtype == "f32" else HC_I32,
-                     block)
+                     block, bloom_k, 0, bloom_rows)
 
 
 def hc_sizes(p: hc_params, max_support: int = 0):
@@ -175,8 +201,8 @@ def hc_sizes(p: hc_params, max_support: int = 0):
 
 def hc_encode(p: hc_params, x, y, b, stream=None):
     _check(_lib.hc_encode(ctypes.byref(p), _ptr(x, "x", _vdtypes(p), p.n),
-                          _ptr(y, "y", _vdtypes(p), p.cells), _ptr(b, "b", _u32(), p.words),
-                          _stream(stream)), "hc_encode")
+                          _ptr(y, "y", _vdtypes(p), p.cells),
+                          _ptr(b, "b", _u32(), p.index_words), _stream(stream)), "hc_encode")
 
 
 def hc_encode_coo(p: hc_params, idx, val, y, b, stream=None):
@@ -185,15 +211,16 @@ def hc_encode_coo(p: hc_params, idx, val, y, b, stream=None):
         raise ValueError("idx and val differ in length")
     _check(_lib.hc_encode_coo(ctypes.byref(p), _ptr(idx, "idx", _u32()),
                               _ptr(val, "val", _vdtypes(p)), nnz,
-                              _ptr(y, "y", _vdtypes(p), p.cells), _ptr(b, "b", _u32(), p.words),
-                              _stream(stream)), "hc_encode_coo")
+                              _ptr(y, "y", _vdtypes(p), p.cells),
+                              _ptr(b, "b", _u32(), p.index_words), _stream(stream)),
+           "hc_encode_coo")
 
 
 def hc_aggregate(p: hc_params, y_in, b_in, W: int, y_out, b_out, stream=None):
     _check(_lib.hc_aggregate(ctypes.byref(p), _ptr(y_in, "y_in", _vdtypes(p), W * p.cells),
-                             _ptr(b_in, "b_in", _u32(), W * p.words), W,
+                             _ptr(b_in, "b_in", _u32(), W * p.index_words), W,
                              _ptr(y_out, "y_out", _vdtypes(p), p.cells),
-                             _ptr(b_out, "b_out", _u32(), p.words), _stream(stream)),
+                             _ptr(b_out, "b_out", _u32(), p.index_words), _stream(stream)),
            "hc_aggregate")
 
 
@@ -222,7 +249,7 @@ def hc_decode(p: hc_params, y_agg, b_agg, info, ws, x_out=None, coo_idx=None, co
     import torch
     _check(_lib.hc_decode(ctypes.byref(p), _ptr(plan, "plan", (torch.uint8,)),
                           _ptr(y_agg, "y_agg", _vdtypes(p), p.cells),
-                          _ptr(b_agg, "b_agg", _u32(), p.words),
+                          _ptr(b_agg, "b_agg", _u32(), p.index_words),
                           _ptr(x_out, "x_out", _vdtypes(p), p.n),
                           _ptr(coo_idx, "coo_idx", _u32()), _ptr(coo_val, "coo_val", _vdtypes(p)),
                           coo_idx.numel() if coo_idx is not None else 0,

@@ -98,7 +98,7 @@ hipError_t launch_aggregate(const Geo& g, const void* y_in, const uint32_t* b_in
     e = g.f32 ? launch_reduce<AddF32>(y_in, y_out, g.cells, W, di.cus, s)
               : launch_reduce<AddU32>(y_in, y_out, g.cells, W, di.cus, s);
     if (e != hipSuccess) return e;
-    return launch_reduce<OrU32>(b_in, b_out, g.words, W, di.cus, s);
+    return launch_reduce<OrU32>(b_in, b_out, g.bwords, W, di.cus, s);
 }
 
 }  // namespace hc

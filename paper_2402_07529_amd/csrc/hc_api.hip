@@ -64,6 +64,20 @@ hc_status to_geo(const hc_params* p, Geo* g) {
         g->brows = (uint32_t)(p->rows / nblocks);
         g->nblocks = (uint32_t)nblocks;
     }
+    if (p->reserved != 0) return fail(HC_EINVAL, "reserved must be 0");
+    g->bloom_k = p->bloom_k;
+    g->bloom_rows = 0;
+    g->bwords = g->words;
+    if (p->bloom_k != 0) {
+        // section 3.3: a filter of bloom_rows rows of c bits, bit positions < 2^32
+        if (p->bloom_k > 64) return fail(HC_EINVAL, "bloom_k must be <= 64");
+        if (p->bloom_rows == 0 || p->bloom_rows > 0xffffffffull / p->c)
+            return fail(HC_EINVAL, "bloom_rows must be >= 1 with bloom_rows * c < 2^32");
+        if (p->block != 0)
+            return fail(HC_EUNSUPPORTED, "a Bloom-filter index needs the global sketch");
+        g->bloom_rows = (uint32_t)p->bloom_rows;
+        g->bwords = (p->bloom_rows * p->c + 31) / 32;
+    }
     return HC_OK;
 }
 
@@ -146,6 +160,50 @@ hc_status hc_geometry(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c, 
     return HC_OK;
 }
 
+hc_status hc_geometry_bloom(uint64_t n, uint64_t n_nonzero, double gamma, uint32_t c,
+                            uint64_t seed, hc_vtype vtype, hc_params* out, double* eps) {
+    g_last_error.clear();
+    if (out == nullptr) return fail(HC_EINVAL, "out is NULL");
+    if (!(gamma > 0.0) || !isfinite(gamma)) return fail(HC_EINVAL, "gamma must be > 0");
+    if (c == 0 || c > 1024 || (c & (c - 1)) != 0)
+        return fail(HC_EINVAL, "c must be a power of two in [1, 1024]");
+    if (n == 0 || n > 0xffffffffull) return fail(HC_EINVAL, "n must be in [1, 2^32 - 1]");
+    if (n_nonzero == 0 || n_nonzero >= n) return fail(HC_EINVAL, "n_nonzero must be in [1, n)");
+    // section 3.3: eps = 1 / (ln^2 2 * gamma * C * lambda), lambda n zeros,
+    // log2(1 / eps) hashes and (n / ln 2) log2(1 / eps) bits
+    const double ln2 = log(2.0);
+    const double lambda = (double)(n - n_nonzero) / (double)n_nonzero;
+    const double e = 1.0 / (ln2 * ln2 * gamma * 32.0 * lambda);
+    double k = floor(log2(1.0 / e) + 0.5);
+    if (!(k >= 1.0)) return fail(HC_EINVAL, "too dense for a Bloom filter (log2(1/eps) rounds to 0)");
+    if (k > 64.0) k = 64.0;
+    const double bits = ceil(k * (double)n_nonzero / ln2);
+    const uint64_t brows = ((uint64_t)bits + c - 1) / c;
+    // the sketch holds the expected candidates: support and false positives
+    const double cand = ceil((double)n_nonzero + ldexp(1.0, -(int)k) * (double)(n - n_nonzero));
+    const double need = gamma * cand;
+    uint64_t cells = (uint64_t)need;
+    if ((double)cells < need) cells++;
+    uint64_t rows = (cells + c - 1) / c;
+    if (rows < 3) rows = 3;
+    hc_params p;
+    memset(&p, 0, sizeof(p));
+    p.n = n;
+    p.k = 3;
+    p.c = c;
+    p.rows = rows;
+    p.seed = seed;
+    p.vtype = (uint32_t)vtype;
+    p.bloom_k = (uint32_t)k;
+    p.bloom_rows = brows;
+    Geo g;
+    const hc_status s = to_geo(&p, &g);
+    if (s != HC_OK) return s;
+    *out = p;
+    if (eps != nullptr) *eps = e;
+    return HC_OK;
+}
+
 namespace {
 
 // Blocked geometry for a given number of rows per block (validated inputs).
@@ -200,34 +258,48 @@ hc_status hc_geometry_blocked(uint64_t n, uint64_t n_nonzero, double gamma, uint
     if (n_nonzero == 0 || n_nonzero > n) return fail(HC_EINVAL, "n_nonzero must be in [1, n]");
     if (block_rows != 0 && block_rows < 3) return fail(HC_EINVAL, "block_rows must be 0 or >= 3");
     if (block_rows != 0) return blocked_for_rows(n, n_nonzero, gamma, c, block_rows, seed, vtype, out);
-    // automatic choice for the current device: each block is one workgroup of
-    // the encode and of the decode, whose time grows with the block's batches
-    // K, and the blocks run ceil(nblocks / CUs) workgroups deep per CU; take
-    // the row count minimising that product (ties to more rows: fewer, larger
-    // blocks peel more reliably), among blocks of at least 10,240 cells (below
-    // about ten thousand members a block needs more room than gamma = 1.3 to
-    // peel reliably) and at most 20,480
     DeviceInfo di;
     const hipError_t e = device_info(&di);
     if (e != hipSuccess) return fail_hip(e, "hc_geometry_blocked");
-    bool found = false;
-    uint64_t best_cost = 0;
+    // A block peels like a random hypergraph only when its batch-to-row graph
+    // is large: with few batches per block and dense batches, the graph's
+    // short cycles line up whole columns of elements into stopping sets.
+    // Measured at gamma = 1.3 (aggregate density d from 6 % to 73 %), blocks of
+    // K >= 600 d batches all peeled; fewer failed for d >= 0.4.  Halve c (not
+    // below 32, where a block's batches still get distinct rotation offsets)
+    // until the blocks hold that many batches.
+    const double density = (double)n_nonzero / (double)n;
     hc_params best;
     memset(&best, 0, sizeof(best));
-    for (uint32_t br = (10240 + c - 1) / c; br <= (20480 + c - 1) / c; br++) {
-        if (br < 3) continue;
-        hc_params p;
-        if (blocked_for_rows(n, n_nonzero, gamma, c, br, seed, vtype, &p) != HC_OK) continue;
-        const uint64_t batches = (n + c - 1) / c;
-        const uint64_t nblocks = (batches + p.block - 1) / p.block;
-        const uint64_t cost = (nblocks + di.cus - 1) / di.cus * p.block;
-        if (!found || cost <= best_cost) {
-            best = p;
-            best_cost = cost;
-            found = true;
+    for (uint32_t cc = c;; cc /= 2) {
+        // each block is one workgroup of the encode and of the decode, whose
+        // time grows with its batches K, and the blocks run ceil(nblocks /
+        // CUs) workgroups deep per CU: take the row count minimising that
+        // product (ties to more rows: fewer, larger blocks peel more
+        // reliably), among blocks of 10,240 to 20,480 cells (below about ten
+        // thousand members a block needs more room than gamma = 1.3)
+        bool found = false;
+        uint64_t best_cost = 0;
+        hc_params pick;
+        memset(&pick, 0, sizeof(pick));
+        for (uint32_t br = (10240 + cc - 1) / cc; br <= (20480 + cc - 1) / cc; br++) {
+            if (br < 3) continue;
+            hc_params p;
+            if (blocked_for_rows(n, n_nonzero, gamma, cc, br, seed, vtype, &p) != HC_OK) continue;
+            const uint64_t batches = (n + cc - 1) / cc;
+            const uint64_t nblocks = (batches + p.block - 1) / p.block;
+            const uint64_t cost = (nblocks + di.cus - 1) / di.cus * p.block;
+            if (!found || cost <= best_cost) {
+                pick = p;
+                best_cost = cost;
+                found = true;
+            }
         }
+        if (found) best = pick;
+        const bool enough = found && (double)pick.block >= 600.0 * density;
+        if (enough || cc <= 32 || cc == 1) break;
     }
-    if (!found) return fail(HC_EUNSUPPORTED, "no block size fits the LDS kernels");
+    if (best.n == 0) return fail(HC_EUNSUPPORTED, "no block size fits the LDS kernels");
     g_last_error.clear();
     *out = best;
     return HC_OK;
@@ -240,7 +312,7 @@ hc_status hc_sizes(const hc_params* p, uint64_t max_support, size_t* y_bytes, si
     const hc_status s = to_geo(p, &g);
     if (s != HC_OK) return s;
     if (y_bytes) *y_bytes = (size_t)g.cells * 4;
-    if (b_bytes) *b_bytes = (size_t)g.words * 4;
+    if (b_bytes) *b_bytes = (size_t)g.bwords * 4;
     if (ws_bytes)
         *ws_bytes = g.block ? blocked_layout(g).total : decode_layout(g, max_support).total;
     return HC_OK;

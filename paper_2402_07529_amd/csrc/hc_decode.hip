@@ -706,6 +706,54 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
     }
 }
 
+// Section 3.3 query: parameter p is a candidate iff its k filter bits are all
+// set.  One lane per candidate word (32 parameters).  For c >= 32 the word lies
+// in one batch, and under hash i its 32 bits sit rotated in one filter row:
+// the two filter words covering them, shifted back by the rotation, give the
+// hash's 32 answers at once; the word is their AND over i (stopping once it is
+// zero).  Below c = 32 each parameter is checked bit by bit.
+__global__ __launch_bounds__(kBlock) void bloom_probe_kernel(
+    const uint32_t* __restrict__ f, uint32_t* __restrict__ cand, uint64_t n, uint64_t words,
+    uint64_t seed, uint32_t k, uint32_t brows, uint32_t c, uint32_t cmask, uint32_t log2c,
+    uint32_t last_mask) {
+    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    for (uint64_t w = (uint64_t)blockIdx.x * kBlock + threadIdx.x; w < words; w += stride) {
+        const uint64_t p0 = w << 5;
+        uint32_t acc;
+        if (c >= 32) {
+            const uint64_t b = p0 >> log2c;
+            const uint32_t cw = c >> 5, ow = ((uint32_t)p0 & cmask) >> 5;
+            acc = ~0u;
+            for (uint32_t i = 0; i < k && acc != 0u; i++) {
+                const BloomHash h = bloom_hash(seed, k, brows, cmask, b, i);
+                const uint32_t q = h.bias >> 5, r = h.bias & 31u;
+                const uint32_t* rp = f + (uint64_t)h.row * cw;
+                const uint32_t w0 = (ow + q) & (cw - 1u);
+                uint32_t v = rp[w0] >> r;
+                if (r != 0u) v |= rp[(w0 + 1u) & (cw - 1u)] << (32u - r);
+                acc &= v;
+            }
+        } else {
+            acc = 0u;
+            for (uint32_t sb = 0; sb < 32; sb++) {
+                const uint64_t p = p0 + sb;
+                if (p >= n) break;
+                const uint64_t b = p >> log2c;
+                const uint32_t t = (uint32_t)p & cmask;
+                bool all = true;
+                for (uint32_t i = 0; i < k && all; i++) {
+                    const BloomHash h = bloom_hash(seed, k, brows, cmask, b, i);
+                    const uint32_t bit = h.row * c + ((t + h.bias) & cmask);
+                    all = ((f[bit >> 5] >> (bit & 31u)) & 1u) != 0u;
+                }
+                acc |= (all ? 1u : 0u) << sb;
+            }
+        }
+        if (w == words - 1) acc &= last_mask;
+        cand[w] = acc;
+    }
+}
+
 int peel_grid_cache[64];
 
 template <typename T>
@@ -874,8 +922,23 @@ DecodeLayout decode_layout(const Geo& g, uint64_t max_support) {
     L.yw = o;      o = align256(o + (size_t)g.cells * vsz);
     L.stamp = o;   o = align256(o + (size_t)g.cells * 4);
     L.queue = o;   o = align256(o + (size_t)g.cells * 8);
+    L.cand = o;    o = align256(o + (g.bloom_k ? g.words * 4 : 0));  // probed Bloom candidates
     L.total = o;
     return L;
+}
+
+hipError_t launch_bloom_probe(const Geo& g, const uint32_t* filter, uint32_t* cand,
+                              hipStream_t s) {
+    DeviceInfo di;
+    hipError_t e = device_info(&di);
+    if (e != hipSuccess) return e;
+    uint64_t grid = (g.words + kBlock - 1) / kBlock;
+    if (grid > (uint64_t)di.cus * 16) grid = (uint64_t)di.cus * 16;
+    const uint32_t last_mask = (g.n & 31u) ? ((1u << (g.n & 31u)) - 1u) : 0xffffffffu;
+    hipLaunchKernelGGL(bloom_probe_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, s, filter,
+                       cand, g.n, g.words, g.seed, g.bloom_k, g.bloom_rows, g.c, g.cmask,
+                       g.log2c, last_mask);
+    return hipGetLastError();
 }
 
 hipError_t launch_support_offsets(const Geo& g, const uint32_t* b, uint32_t* blk, void* ctrl,
@@ -894,6 +957,14 @@ hipError_t launch_support_offsets(const Geo& g, const uint32_t* b, uint32_t* blk
 
 hipError_t launch_decode(const Geo& g, const void* plan, const void* y_agg, const uint32_t* b_agg,
                          const DecodeOut& out, const DecodeLayout& L, void* ws, hipStream_t s) {
+    if (g.bloom_k != 0) {
+        // the support is what the filter reports: probe it into a bitmap of
+        // candidates, then decode as with the bitmap index
+        uint32_t* cand = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + L.cand);
+        const hipError_t e = launch_bloom_probe(g, b_agg, cand, s);
+        if (e != hipSuccess) return e;
+        b_agg = cand;
+    }
     if (g.f32) return launch_decode_t<float>(g, plan, y_agg, b_agg, out, L, ws, s);
     return launch_decode_t<int32_t>(g, plan, y_agg, b_agg, out, L, ws, s);
 }

@@ -67,17 +67,38 @@ __host__ __device__ __forceinline__ BatchHash batch_hash(uint64_t seed, uint32_t
 // the batch hashes 3b + j (b < 2^32) and the Bloom filter's hashes.
 constexpr uint64_t kBlockSaltBase = 1ull << 62;
 
+// P_u(i): a bijection of [0, 2^m), m = 2 log2 c, keyed by u: add s, multiply by
+// the odd a1, xor-shift right by h = ceil(m / 2), multiply by the odd a2,
+// xor-shift again (each step is invertible modulo 2^m), with a1, a2 and s the
+// low, middle and high 20-bit fields of u.
+__host__ __device__ __forceinline__ uint32_t block_offsets(uint64_t u, uint32_t i, uint32_t log2c) {
+    const uint32_t m = 2u * log2c;
+    const uint32_t mask = (1u << m) - 1u;  // m <= 20
+    const uint32_t h = (m + 1u) >> 1;
+    const uint32_t a1 = ((uint32_t)u & 0xfffffu) | 1u;
+    const uint32_t a2 = ((uint32_t)(u >> 20) & 0xfffffu) | 1u;
+    const uint32_t s = (uint32_t)(u >> 40) & 0xfffffu;
+    uint32_t x = (i + s) & mask;
+    x = (x * a1) & mask;
+    x ^= x >> h;
+    x = (x * a2) & mask;
+    x ^= x >> h;
+    return x;
+}
+
 // Hash of batch b in a blocked sketch, in block-local rows: batch b is number
 // i = b mod block of parameter block q = b / block, whose brows rows it draws
 // its three distinct rows from (as batch_hash), taken in ascending order.  Its
 // first rotation is h_0's; the other two are offset from it by the two base-c
-// digits of pi = (a_q i + s_q) mod c^2, with a_q odd and s_q from the block's
-// constant u_q = SplitMix64 output 2^62 + q.  For c >= 32 a block's batches
-// (at most 1024 <= c^2) get distinct offset pairs, so no two batches of one
-// block can sit on the same three rows with the same relative rotations, which
-// would pair every two of their corresponding elements on the same three
-// cells (a stopping set that no sketch size peels; with few rows per block
-// independent rotations make that likely).
+// digits of pi = P_q(i), P_q a bijection of [0, c^2) keyed by the block's
+// constant u_q = SplitMix64 output 2^62 + q (block_offsets).  For c >= 32 a
+// block's batches (at most 1024 <= c^2) get distinct offset pairs, so no two
+// batches of one block can sit on the same three rows with the same relative
+// rotations, which would pair every two of their corresponding elements on the
+// same three cells (a stopping set that no sketch size peels; with few rows
+// per block independent rotations make that likely).  P_q mixes (it is not
+// affine in i) so that the offsets carry no arithmetic structure, which would
+// itself create small stopping sets.
 __host__ __device__ __forceinline__ BatchHash blocked_local_hash(uint64_t seed, uint32_t brows,
                                                                  uint32_t cmask, uint32_t log2c,
                                                                  uint64_t b, uint32_t block) {
@@ -90,9 +111,7 @@ __host__ __device__ __forceinline__ BatchHash blocked_local_hash(uint64_t seed, 
     h.row[2] = hi;
     const uint64_t q = b / block;
     const uint32_t i = (uint32_t)(b - q * block);
-    const uint64_t u = splitmix(seed, kBlockSaltBase + q);
-    const uint32_t m = (cmask + 1u) * (cmask + 1u) - 1u;  // c^2 - 1
-    const uint32_t pi = (((uint32_t)u | 1u) * i + (uint32_t)(u >> 32)) & m;
+    const uint32_t pi = block_offsets(splitmix(seed, kBlockSaltBase + q), i, log2c);
     h.bias[1] = (h.bias[0] + (pi & cmask)) & cmask;
     h.bias[2] = (h.bias[0] + (pi >> log2c)) & cmask;
     return h;
@@ -110,6 +129,73 @@ __host__ __device__ __forceinline__ BatchHash batch_hash_blocked(uint64_t seed, 
     h.row[1] += base;
     h.row[2] += base;
     return h;
+}
+
+// ---- Bloom-filter index (section 3.3), batched like the sketch (3.4) --------
+
+// Hash i < k of batch b is SplitMix64 output number 3 * 2^32 + k * b + i (a
+// counter range the sketch's outputs 3b + j never reach): row
+// mulhi32(lo32(u), brows) of the filter's brows rows of c bits, rotation
+// (u >> 32) mod c.
+constexpr uint64_t kBloomBase = 3ull << 32;
+
+struct BloomHash {
+    uint32_t row;
+    uint32_t bias;
+};
+
+__host__ __device__ __forceinline__ BloomHash bloom_hash(uint64_t seed, uint32_t k,
+                                                         uint32_t brows, uint32_t cmask,
+                                                         uint64_t b, uint32_t i) {
+    const uint64_t u = splitmix(seed, kBloomBase + (uint64_t)k * b + i);
+    BloomHash h;
+    h.row = mulhi32((uint32_t)u, brows);
+    h.bias = (uint32_t)(u >> 32) & cmask;
+    return h;
+}
+
+// Sets the k filter bits of parameter p: bit row * c + ((t + bias) mod c).
+__device__ __forceinline__ void bloom_insert_param(uint32_t* f, uint64_t p, uint64_t seed,
+                                                   uint32_t k, uint32_t brows, uint32_t c,
+                                                   uint32_t cmask, uint32_t log2c) {
+    const uint64_t b = p >> log2c;
+    const uint32_t t = (uint32_t)p & cmask;
+    for (uint32_t i = 0; i < k; i++) {
+        const BloomHash h = bloom_hash(seed, k, brows, cmask, b, i);
+        const uint32_t bit = h.row * c + ((t + h.bias) & cmask);
+        atomicOr(f + (bit >> 5), 1u << (bit & 31u));
+    }
+}
+
+// Inserts the nonzeros of one 32-bit mask word (parameters p0 .. p0 + 31, p0 a
+// multiple of 32).  For c >= 32 the word lies in one batch and, per hash, its
+// bits land rotated in one filter row: at most two filter words receive it, so
+// it takes at most 2k atomic ORs whatever its popcount.
+__device__ __forceinline__ void bloom_insert_word(uint32_t* f, uint32_t word, uint64_t p0,
+                                                  uint64_t seed, uint32_t k, uint32_t brows,
+                                                  uint32_t c, uint32_t cmask, uint32_t log2c) {
+    if (c >= 32) {
+        const uint64_t b = p0 >> log2c;
+        const uint32_t cw = c >> 5, ow = ((uint32_t)p0 & cmask) >> 5;
+        for (uint32_t i = 0; i < k; i++) {
+            const BloomHash h = bloom_hash(seed, k, brows, cmask, b, i);
+            const uint32_t q = h.bias >> 5, r = h.bias & 31u;
+            uint32_t* rp = f + (uint64_t)h.row * cw;
+            const uint32_t w0 = (ow + q) & (cw - 1u);
+            const uint32_t lo = word << r;
+            if (lo != 0u) atomicOr(rp + w0, lo);
+            if (r != 0u) {
+                const uint32_t hi = word >> (32u - r);
+                if (hi != 0u) atomicOr(rp + ((w0 + 1u) & (cw - 1u)), hi);
+            }
+        }
+    } else {
+        while (word != 0u) {
+            const uint32_t sbit = (uint32_t)__builtin_ctz(word);
+            word &= word - 1u;
+            bloom_insert_param(f, p0 + sbit, seed, k, brows, c, cmask, log2c);
+        }
+    }
 }
 
 // Cell of column t under hash j.  c = cmask + 1 is a power of two.

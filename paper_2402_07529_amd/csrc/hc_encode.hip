@@ -97,12 +97,15 @@ __device__ __forceinline__ void scatter_load(const T (&e)[4], const bool (&nz)[4
 // One wave tile: 1024 consecutive parameters from `tbase` (a multiple of
 // 1024), four loads of 256 per wave, e[l][k] = parameter tbase + 256 l +
 // 4 lane + k.  Its 32 bitmap words form one 128-byte line, built from the 16
-// ballots and written by lanes 0..31 with a single store.
-template <typename T, int MODE>
+// ballots and written by lanes 0..31 with a single store; with a Bloom-filter
+// index (BL) each nonzero word is OR-ed, rotated, into the filter instead
+// (section 3.3).
+template <typename T, int MODE, bool BL>
 __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, uint32_t lane,
                                             T* __restrict__ y, uint32_t* __restrict__ b,
                                             uint64_t words, uint64_t seed, uint32_t rows,
-                                            uint32_t c, uint32_t cmask, uint32_t log2c) {
+                                            uint32_t c, uint32_t cmask, uint32_t log2c,
+                                            uint32_t bk, uint32_t brows) {
     bool nz[4][4];
     uint64_t m[4][4];
 #pragma unroll
@@ -123,7 +126,11 @@ __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, 
             word |= spread4((uint32_t)(mk >> sh)) << k;
         }
         const uint64_t widx = (tbase >> 5) + lane;
-        if (widx < words) b[widx] = word;
+        if (!BL) {
+            if (widx < words) b[widx] = word;
+        } else if (word != 0u) {
+            bloom_insert_word(b, word, widx << 5, seed, bk, brows, c, cmask, log2c);
+        }
     }
 #pragma unroll
     for (int l = 0; l < 4; l++) {
@@ -141,11 +148,11 @@ __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, 
 // nontemporal loads per lane before encoding the current pair.  The tail takes single tiles with
 // bounds-checked 4-byte loads (also used throughout when x is not 16-byte
 // aligned).
-template <typename T, int MODE>
+template <typename T, int MODE, bool BL>
 __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
     const T* __restrict__ x, T* __restrict__ y, uint32_t* __restrict__ b, uint64_t n,
     uint64_t words, uint64_t seed, uint32_t rows, uint32_t c, uint32_t cmask, uint32_t log2c,
-    bool vec) {
+    bool vec, uint32_t bk, uint32_t brows) {
     typedef typename Vec4<T>::type V;
     const uint32_t lane = lane_id();
     const uint64_t gwave = (uint64_t)blockIdx.x * (kBlock / 64) + uniform(threadIdx.x >> 6);
@@ -169,8 +176,8 @@ __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
                 e[l][2] = v[4 * h + l].z;
                 e[l][3] = v[4 * h + l].w;
             }
-            encode_tile<T, MODE>(e, (2 * q + h) * kTile, lane, y, b, words, seed, rows, c, cmask,
-                                 log2c);
+            encode_tile<T, MODE, BL>(e, (2 * q + h) * kTile, lane, y, b, words, seed, rows, c,
+                                     cmask, log2c, bk, brows);
         }
     };
     // rolling pipeline: the next pair's loads are issued before the current
@@ -207,7 +214,8 @@ __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
                 const uint64_t p = tbase + 256ull * l + 4ull * lane + k;
                 e[l][k] = p < n ? x[p] : T(0);
             }
-        encode_tile<T, MODE>(e, tbase, lane, y, b, words, seed, rows, c, cmask, log2c);
+        encode_tile<T, MODE, BL>(e, tbase, lane, y, b, words, seed, rows, c, cmask, log2c, bk,
+                                 brows);
     }
 }
 
@@ -215,13 +223,17 @@ template <typename T>
 __global__ __launch_bounds__(kBlock) void encode_coo_kernel(
     const uint32_t* __restrict__ idx, const T* __restrict__ val, uint64_t nnz,
     T* __restrict__ y, uint32_t* __restrict__ b, uint64_t n, uint64_t seed, uint32_t brows,
-    uint32_t block, uint32_t c, uint32_t cmask, uint32_t log2c) {
+    uint32_t block, uint32_t c, uint32_t cmask, uint32_t log2c, uint32_t bk,
+    uint32_t bloom_rows) {
     const uint64_t stride = (uint64_t)gridDim.x * kBlock;
     for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < nnz; i += stride) {
         const uint32_t p = idx[i];
         const T v = val[i];
         if (p >= n || !Val<T>::nonzero(v)) continue;
-        atomicOr(b + (p >> 5), 1u << (p & 31u));
+        if (bk == 0u)
+            atomicOr(b + (p >> 5), 1u << (p & 31u));
+        else
+            bloom_insert_param(b, p, seed, bk, bloom_rows, c, cmask, log2c);
         const BatchHash h =
             batch_hash_blocked(seed, brows, cmask, log2c, (uint64_t)(p >> log2c), block);
         const uint32_t t = p & cmask;
@@ -238,7 +250,7 @@ uint32_t grid_for(uint64_t work_items, uint64_t per_block, uint32_t cap) {
     return (uint32_t)g;
 }
 
-template <typename T, int MODE>
+template <typename T, int MODE, bool BL>
 hipError_t launch_dense_t(const Geo& g, const void* x, void* y, uint32_t* b, hipStream_t s,
                           uint64_t ntiles, int cus) {
     // one resident wave of workgroups: the kernel strides over the tiles
@@ -246,15 +258,15 @@ hipError_t launch_dense_t(const Geo& g, const void* x, void* y, uint32_t* b, hip
     if (per_cu == 0) {
         int v = 0;
         const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &v, reinterpret_cast<const void*>(&encode_dense_kernel<T, MODE>), kBlock, 0);
+            &v, reinterpret_cast<const void*>(&encode_dense_kernel<T, MODE, BL>), kBlock, 0);
         if (e != hipSuccess) return e;
         per_cu = v > 0 ? v : 1;
     }
     const uint32_t grid = grid_for(ntiles, 2 * (kBlock / 64), (uint32_t)(cus * per_cu));
-    hipLaunchKernelGGL((encode_dense_kernel<T, MODE>), dim3(grid), dim3(kBlock), 0, s,
+    hipLaunchKernelGGL((encode_dense_kernel<T, MODE, BL>), dim3(grid), dim3(kBlock), 0, s,
                        static_cast<const T*>(x), static_cast<T*>(y), b, g.n, g.words, g.seed,
                        g.rows, g.c, g.cmask, g.log2c,
-                       (reinterpret_cast<uintptr_t>(x) & 15u) == 0);
+                       (reinterpret_cast<uintptr_t>(x) & 15u) == 0, g.bloom_k, g.bloom_rows);
     return hipGetLastError();
 }
 
@@ -280,14 +292,27 @@ hipError_t launch_encode_dense(const Geo& g, const void* x, void* y, uint32_t* b
     if (e != hipSuccess) return e;
     const uint64_t ntiles = (g.n + kTile - 1) / kTile;
     const int mode = g.c >= 256 ? 0 : (g.c >= 4 ? 1 : 2);
-    if (g.f32) {
-        if (mode == 0) return launch_dense_t<float, 0>(g, x, y, b, s, ntiles, di.cus);
-        if (mode == 1) return launch_dense_t<float, 1>(g, x, y, b, s, ntiles, di.cus);
-        return launch_dense_t<float, 2>(g, x, y, b, s, ntiles, di.cus);
+    if (g.bloom_k != 0) {
+        // the filter collects OR-ed bits, so it starts from zero
+        e = launch_fill_u32(b, g.bwords, 0u, s);
+        if (e != hipSuccess) return e;
+        if (g.f32) {
+            if (mode == 0) return launch_dense_t<float, 0, true>(g, x, y, b, s, ntiles, di.cus);
+            if (mode == 1) return launch_dense_t<float, 1, true>(g, x, y, b, s, ntiles, di.cus);
+            return launch_dense_t<float, 2, true>(g, x, y, b, s, ntiles, di.cus);
+        }
+        if (mode == 0) return launch_dense_t<int32_t, 0, true>(g, x, y, b, s, ntiles, di.cus);
+        if (mode == 1) return launch_dense_t<int32_t, 1, true>(g, x, y, b, s, ntiles, di.cus);
+        return launch_dense_t<int32_t, 2, true>(g, x, y, b, s, ntiles, di.cus);
     }
-    if (mode == 0) return launch_dense_t<int32_t, 0>(g, x, y, b, s, ntiles, di.cus);
-    if (mode == 1) return launch_dense_t<int32_t, 1>(g, x, y, b, s, ntiles, di.cus);
-    return launch_dense_t<int32_t, 2>(g, x, y, b, s, ntiles, di.cus);
+    if (g.f32) {
+        if (mode == 0) return launch_dense_t<float, 0, false>(g, x, y, b, s, ntiles, di.cus);
+        if (mode == 1) return launch_dense_t<float, 1, false>(g, x, y, b, s, ntiles, di.cus);
+        return launch_dense_t<float, 2, false>(g, x, y, b, s, ntiles, di.cus);
+    }
+    if (mode == 0) return launch_dense_t<int32_t, 0, false>(g, x, y, b, s, ntiles, di.cus);
+    if (mode == 1) return launch_dense_t<int32_t, 1, false>(g, x, y, b, s, ntiles, di.cus);
+    return launch_dense_t<int32_t, 2, false>(g, x, y, b, s, ntiles, di.cus);
 }
 
 hipError_t launch_encode_coo(const Geo& g, const uint32_t* idx, const void* val, uint64_t nnz,
@@ -297,18 +322,20 @@ hipError_t launch_encode_coo(const Geo& g, const uint32_t* idx, const void* val,
     if (e != hipSuccess) return e;
     e = launch_fill_u32(static_cast<uint32_t*>(y), g.cells, 0u, s);
     if (e != hipSuccess) return e;
-    e = launch_fill_u32(b, g.words, 0u, s);
+    e = launch_fill_u32(b, g.bwords, 0u, s);
     if (e != hipSuccess) return e;
     if (nnz == 0) return hipSuccess;
     const uint32_t grid = grid_for(nnz, kBlock, (uint32_t)di.cus * 16);
     if (g.f32)
         hipLaunchKernelGGL(encode_coo_kernel<float>, dim3(grid), dim3(kBlock), 0, s, idx,
                            static_cast<const float*>(val), nnz, static_cast<float*>(y), b, g.n,
-                           g.seed, g.brows, g.block, g.c, g.cmask, g.log2c);
+                           g.seed, g.brows, g.block, g.c, g.cmask, g.log2c, g.bloom_k,
+                           g.bloom_rows);
     else
         hipLaunchKernelGGL(encode_coo_kernel<int32_t>, dim3(grid), dim3(kBlock), 0, s, idx,
                            static_cast<const int32_t*>(val), nnz, static_cast<int32_t*>(y), b,
-                           g.n, g.seed, g.brows, g.block, g.c, g.cmask, g.log2c);
+                           g.n, g.seed, g.brows, g.block, g.c, g.cmask, g.log2c, g.bloom_k,
+                           g.bloom_rows);
     return hipGetLastError();
 }
 

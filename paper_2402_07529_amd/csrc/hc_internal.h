@@ -25,12 +25,22 @@ struct Geo {
     uint32_t block;
     uint32_t brows;
     uint32_t nblocks;
+    // index: the bitmap (bloom_k == 0) or a Bloom filter of bloom_rows rows of
+    // c bits (section 3.3); bwords = words of the index
+    uint32_t bloom_k;
+    uint32_t bloom_rows;
+    uint64_t bwords;
 };
 
 struct DeviceInfo {
     int cus;          // compute units
 };
 hipError_t device_info(DeviceInfo* out);
+
+// Bloom filter: candidate bitmap cand[words] of the parameters whose bloom_k
+// filter bits are all set
+hipError_t launch_bloom_probe(const Geo& g, const uint32_t* filter, uint32_t* cand,
+                              hipStream_t s);
 
 // encode
 hipError_t launch_fill_u32(uint32_t* p, uint64_t count, uint32_t value, hipStream_t s);
@@ -80,7 +90,7 @@ hipError_t launch_encode_blocked(const Geo& g, const void* x, void* y, uint32_t*
 struct DecodeLayout {
     uint64_t cap;       // max support the workspace holds
     uint64_t nchunks;   // bitmap chunks of kChunkWords words
-    size_t ctrl, blk, woff, elem, vals, peeled, cnt, yw, stamp, queue, total;
+    size_t ctrl, blk, woff, elem, vals, peeled, cnt, yw, stamp, queue, cand, total;
 };
 constexpr uint32_t kChunkWords = 1024;
 DecodeLayout decode_layout(const Geo& g, uint64_t max_support);

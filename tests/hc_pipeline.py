@@ -15,11 +15,13 @@ def wrap_sum(arrs):
     return (acc & 0xFFFFFFFF).astype(np.uint32).view(np.int32)
 
 
-def oracle_run(w, rows: int, c: int, coo: bool = True, block: int = 0, seed=None):
+def oracle_run(w, rows: int, c: int, coo: bool = True, block: int = 0, seed=None,
+               bloom_k: int = 0, bloom_rows: int = 0):
     """Oracle encode (per worker), aggregate and decode of workload w (hash
-    seed: w's unless given)."""
+    seed: w's unless given; bloom_k > 0: a Bloom-filter index)."""
     seed = w.hash_seed if seed is None else seed
-    g = oracle.Geom(n=w.n, rows=rows, seed=seed, c=c, block=block)
+    g = oracle.Geom(n=w.n, rows=rows, seed=seed, c=c, block=block, bloom_k=bloom_k,
+                    bloom_rows=bloom_rows)
     Ys, Bs = [], []
     for i in range(w.W):
         if coo:
@@ -37,19 +39,21 @@ def oracle_run(w, rows: int, c: int, coo: bool = True, block: int = 0, seed=None
 
 def gpu_run(w, rows: int, c: int, coo_input: bool = False, want_coo_out: bool = True,
             max_support: int = 0, keep_workers: bool = True, coo_cap=None, use_plan=False,
-            plan=None, block: int = 0, seed=None):
+            plan=None, block: int = 0, seed=None, bloom_k: int = 0, bloom_rows: int = 0):
     """The same pipeline through libhc on the current GPU.  use_plan builds the
     geometry's inverse row map and decodes with it; `plan` passes one in;
-    block > 0 selects the blocked sketch; seed overrides w's hash seed."""
+    block > 0 selects the blocked sketch; seed overrides w's hash seed;
+    bloom_k > 0 selects a Bloom-filter index."""
     import torch
 
     import paper_2402_07529_amd as hc
     dev = torch.device("cuda")
-    p = hc.make_params(w.n, rows, w.hash_seed if seed is None else seed, c, w.vtype, block=block)
+    p = hc.make_params(w.n, rows, w.hash_seed if seed is None else seed, c, w.vtype, block=block,
+                       bloom_k=bloom_k, bloom_rows=bloom_rows)
     vt = torch.int32 if w.vtype == "i32" else torch.float32
     W = w.W
     Y = torch.empty((W, p.cells), dtype=vt, device=dev)
-    B = torch.empty((W, p.words), dtype=torch.int32, device=dev)
+    B = torch.empty((W, p.index_words), dtype=torch.int32, device=dev)
     for i in range(W):
         if coo_input:
             idx = torch.from_numpy(w.idx[i].view(np.int32)).to(dev)
@@ -61,7 +65,7 @@ def gpu_run(w, rows: int, c: int, coo_input: bool = False, want_coo_out: bool = 
             hc.hc_encode(p, x, Y[i], B[i])
             del x
     Ya = torch.empty(p.cells, dtype=vt, device=dev)
-    Ba = torch.empty(p.words, dtype=torch.int32, device=dev)
+    Ba = torch.empty(p.index_words, dtype=torch.int32, device=dev)
     hc.hc_aggregate(p, Y, B, W, Ya, Ba)
     out = torch.empty(w.n, dtype=vt, device=dev)
     mask = torch.empty(p.words, dtype=torch.int32, device=dev)

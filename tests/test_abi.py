@@ -149,3 +149,44 @@ def test_blocked_params_rejected():
     assert L.hc_decode(ctypes.byref(p), None, V(256), V(256), None, None, None, 0, None, V(256), 0,
                        V(256), 64, None) == hc.HC_EWORKSPACE
 
+
+
+def test_bloom_geometry_matches_oracle():
+    # section 3.3 sizing, computed by the library and by the oracle separately
+    import oracle
+    import paper_2402_07529_amd as hc
+    for n, nnz, c in ((1 << 30, 1_551_680, 1024), (109_482_240, 9_305_915, 1024),
+                      (109_482_240, 273_579, 256), (2_000_000, 8_000, 64), (50_000, 900, 1),
+                      (1000, 900, 8)):
+        p, eps = hc.hc_geometry_bloom(n, nnz, 1.23, c, 11, "i32")
+        g, eps_o = oracle.bloom_geometry(n, nnz, 11, c)
+        assert (int(p.bloom_k), int(p.bloom_rows), int(p.rows)) == (g.bloom_k, g.bloom_rows, g.rows)
+        assert eps == pytest.approx(eps_o, rel=1e-12)
+        _, b_bytes, _ = hc.hc_sizes(p)
+        assert b_bytes == 4 * g.index_words == 4 * p.index_words
+    with pytest.raises(hc.HCError) as ei:
+        hc.hc_geometry_bloom(1000, 950, 1.23, 1024, 1)   # log2(1/eps) rounds to 0
+    assert ei.value.status == hc.HC_EINVAL
+
+
+def test_bloom_params_rejected():
+    import paper_2402_07529_amd as hc
+    bad = ((hc.make_params(10_000, 9, 1, c=64, bloom_k=65, bloom_rows=10), hc.HC_EINVAL),
+           (hc.make_params(10_000, 9, 1, c=64, bloom_k=3, bloom_rows=0), hc.HC_EINVAL),
+           (hc.make_params(10_000, 9, 1, c=1024, bloom_k=3, bloom_rows=1 << 22), hc.HC_EINVAL),
+           (hc.make_params(10_000, 60, 1, c=64, block=8, bloom_k=3, bloom_rows=10),
+            hc.HC_EUNSUPPORTED))
+    for p, st in bad:
+        with pytest.raises(hc.HCError) as ei:
+            hc.hc_sizes(p)
+        assert ei.value.status == st
+    p = hc.make_params(10_000, 9, 1, c=64, bloom_k=3, bloom_rows=10)
+    p.reserved = 1
+    with pytest.raises(hc.HCError) as ei:
+        hc.hc_sizes(p)
+    assert ei.value.status == hc.HC_EINVAL
+    # the decode workspace holds the probed candidate bitmap on top
+    q = hc.make_params(10_000, 9, 1, c=64, bloom_k=3, bloom_rows=10)
+    _, _, ws_bloom = hc.hc_sizes(q, 100)
+    _, _, ws_bitmap = hc.hc_sizes(hc.make_params(10_000, 9, 1, c=64), 100)
+    assert ws_bloom - ws_bitmap >= 4 * q.words

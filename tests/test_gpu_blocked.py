@@ -249,3 +249,17 @@ def test_blocked_auto_rows_minimise_cost():
                 best = (cost, int(p.block), int(p.rows))
         p = hc.hc_geometry_blocked(n, nnz, gamma, c, 0, 7, vt)
         assert (int(p.block), int(p.rows)) == best[1:]
+
+
+def test_blocked_auto_lowers_c_for_dense_aggregates():
+    # a 73 %-dense aggregate (BERT-base, 5 % per worker, 10 % overlap): blocks
+    # of 1024-wide batches would hold about a dozen batches; the automatic
+    # geometry halves c until a block holds >= 600 * density batches
+    hc = _hc()
+    n, nnz = 109_482_240, 79_374_383
+    p = hc.hc_geometry_blocked(n, nnz, 1.3, 1024, 0, 7, "i32")
+    assert int(p.c) < 1024 and int(p.c) >= 32
+    assert int(p.block) >= 600 * nnz / n or int(p.c) == 32
+    # sparse aggregates keep the requested c
+    q = hc.hc_geometry_blocked(n, 9_305_915, 1.3, 1024, 0, 7, "i32")
+    assert int(q.c) == 1024

@@ -129,8 +129,9 @@ def test_fullsize_blocked(name, vtype):
     print(f"[fullsize blocked] {name} {vtype}: n={w.n} W={w.W} n_agg={w.n_agg} "
           f"block={int(p.block)} rows={int(p.rows)} nblocks={p.nblocks} seed={int(p.seed)}",
           flush=True)
-    g = gpu_run(w, int(p.rows), 1024, want_coo_out=False, block=int(p.block), seed=int(p.seed))
-    o = oracle_run(w, int(p.rows), 1024, block=int(p.block), seed=int(p.seed))
+    g = gpu_run(w, int(p.rows), int(p.c), want_coo_out=False, block=int(p.block),
+                seed=int(p.seed))
+    o = oracle_run(w, int(p.rows), int(p.c), block=int(p.block), seed=int(p.seed))
     if vtype == "i32":
         for i in range(w.W):
             assert np.array_equal(g["Y"][i], o["Y"][i]), f"worker {i} sketch"

@@ -235,3 +235,21 @@ def test_blocked_linearity():
     # linear wherever no nonzero cancels (a cancelled entry drops out of the
     # bitmap but contributes 0 to Y either way, so Y stays linear)
     assert np.array_equal(Ys, wrap_sum([Ya, Yb]))
+
+
+def test_small_blocks_peel_at_low_load():
+    # 3 rows per block, so every batch of a block has the same three rows:
+    # only the rotations separate them.  At about 0.26 members per cell the
+    # blocks must all peel; offsets with arithmetic structure (an affine map
+    # of the batch index) leave small stopping sets here
+    c, block, brows, nbk = 1024, 4, 3, 150
+    n = nbk * block * c
+    rng = np.random.default_rng(44)
+    parts = [rng.choice(block * c, 800, replace=False) + q * block * c for q in range(nbk)]
+    idx = np.sort(np.concatenate(parts)).astype(np.uint32)
+    val = (rng.integers(1, 2**20, idx.size) * rng.choice([-1, 1], idx.size)).astype(np.int32)
+    g = o.Geom(n=n, rows=nbk * brows, seed=91, c=c, block=block)
+    Y, B = o.encode_coo(g, idx, val)
+    x, mask, info = o.decode(g, Y, B)
+    assert info.success and info.n_support == idx.size
+    assert np.array_equal(x[idx], val)
