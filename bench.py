@@ -53,8 +53,11 @@ def parse():
                     help="rows per block of the blocked sketch (default: the library's choice "
                          "for this device, hc_geometry_blocked with block_rows = 0)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--sweep", action="store_true",
-                    help="BERT-base density/overlap grid and sketch-width sweep (one JSON object)")
+    ap.add_argument("--sweep", nargs="?", const="bert", choices=["bert", "compressed"],
+                    help="bert: BERT-base density/overlap grid and sketch-width sweep; "
+                         "compressed: one worker's compress + decompress over sketch sizes of 2 %% "
+                         "to 200 %% of a VGG19-shaped gradient at its natural 69.6 %% density "
+                         "(section 4.1's microbenchmark); one JSON object")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 10 times (the known-size kernel "
                          "against which the HBM byte counters are scaled)")
@@ -267,6 +270,46 @@ class Runner:
                     exact=exact, plan_ms=plan_ms)
 
 
+# sketch sizes (cells / n) of section 4.1's microbenchmark, 2 % to 200 %, with
+# the threshold 1.23 x 0.696 = 85.6 % among them
+COMPRESSED_SIZES = (0.02, 0.05, 0.1, 0.2, 0.3, 0.4, 0.5, 0.6, 0.7, 0.8, 0.856, 0.9, 1.0, 1.2,
+                    1.5, 2.0)
+
+
+def sweep_compressed(a, dev):
+    """Section 4.1's microbenchmark on one worker: a VGG19-shaped gradient at
+    its natural density (69.6 % nonzero, Table 1) compressed to sketches of 2 %
+    to 200 % of its size and decompressed at once.  Per size: the average
+    relative error |x_hat - x| / |x| over the nonzeros, the recovery rate
+    (fraction recovered by peeling), the recovery iterations (rounds), and the
+    compress + decompress throughput of the single worker (the paper's
+    single-worker, single-GPU aggregation throughput)."""
+    import workloads as wl
+    w = wl.make("vgg19", vtype=a.vtype, W=1, density=0.696)
+    r = Runner(w, 1024, dev)
+    x = r.x[0].double()
+    nz = x != 0
+    absx = x[nz].abs()
+    points = []
+    for frac in COMPRESSED_SIZES:
+        m = r.run(frac * w.n / r.n_agg, 3, 1, check=False)
+        inf = m["info"]
+        err = ((r.out.double()[nz] - x[nz]).abs() / absx).mean().item()
+        t = m["enc_ms"] + m["dec_ms"]  # W = 1: the aggregate of one sketch is a copy
+        pt = dict(compressed_size=frac, cells=m["p"].cells,
+                  index_bytes_frac=round(4 * m["p"].index_words / (4 * w.n), 4),
+                  avg_relative_error=err,
+                  recovery_rate=round(inf.n_recovered / max(inf.n_support, 1), 6),
+                  recovery_iterations=inf.rounds, success=inf.success,
+                  encode_ms=round(m["enc_ms"], 4), decode_ms=round(m["dec_ms"], 4),
+                  compress_decompress_gbs=round(4 * w.n / (t * 1e-3) / 1e9, 2))
+        log(f"[sweep] {pt}")
+        points.append(pt)
+    print(json.dumps({"sweep": "compressed-size", "workload": "vgg19 natural density",
+                      "n": w.n, "nonzeros": r.n_agg, "dtype": "int32" if w.vtype == "i32" else "fp32",
+                      "points": points}), flush=True)
+
+
 def sweep(a, dev):
     """BERT-base: density x overlap grid at gamma = 1.23, then sketch widths
     around gamma at 1 % / 50 % overlap, to chart the decode-failure boundary
@@ -318,6 +361,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if a.sweep == "compressed":
+        sweep_compressed(a, dev)
+        return
     if a.sweep:
         sweep(a, dev)
         return

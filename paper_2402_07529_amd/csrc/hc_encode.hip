@@ -4,7 +4,10 @@
 // four coalesced 16-byte nontemporal loads per lane (the gradient is read
 // once, so it should not evict the sketch from L2/MALL).  Per tile:
 //   - sixteen ballots of "x != 0" become the tile's 32 bitmap words (section
-//     3.2), one full 128-byte line written by a single store;
+//     3.2); only the nonzero words are stored, into a bitmap zero-filled by a
+//     pure write pass before the kernel (on MI355X, bitmap stores interleaved
+//     with the 4n-byte read stream cost about 0.18 ms per 2^30 parameters
+//     however they are shaped, against 0.02 ms for the separate fill);
 //   - every nonzero adds g_j * x to its three cells (section 3.1) with
 //     fire-and-forget global atomics.  Within one batch the cells of a hash
 //     are one sketch row rotated by a bias (section 3.4), so the atomics of a
@@ -96,10 +99,10 @@ __device__ __forceinline__ void scatter_load(const T (&e)[4], const bool (&nz)[4
 
 // One wave tile: 1024 consecutive parameters from `tbase` (a multiple of
 // 1024), four loads of 256 per wave, e[l][k] = parameter tbase + 256 l +
-// 4 lane + k.  Its 32 bitmap words form one 128-byte line, built from the 16
-// ballots and written by lanes 0..31 with a single store; with a Bloom-filter
-// index (BL) each nonzero word is OR-ed, rotated, into the filter instead
-// (section 3.3).
+// 4 lane + k.  Its 32 bitmap words are built from the 16 ballots in lanes
+// 0..31, which store the nonzero ones (the bitmap was zero-filled); with a
+// Bloom-filter index (BL) each nonzero word is OR-ed, rotated, into the filter
+// instead (section 3.3).
 template <typename T, int MODE, bool BL>
 __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, uint32_t lane,
                                             T* __restrict__ y, uint32_t* __restrict__ b,
@@ -127,7 +130,7 @@ __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, 
         }
         const uint64_t widx = (tbase >> 5) + lane;
         if (!BL) {
-            if (widx < words) b[widx] = word;
+            if (word != 0u && widx < words) b[widx] = word;
         } else if (word != 0u) {
             bloom_insert_word(b, word, widx << 5, seed, bk, brows, c, cmask, log2c);
         }
@@ -292,10 +295,11 @@ hipError_t launch_encode_dense(const Geo& g, const void* x, void* y, uint32_t* b
     if (e != hipSuccess) return e;
     const uint64_t ntiles = (g.n + kTile - 1) / kTile;
     const int mode = g.c >= 256 ? 0 : (g.c >= 4 ? 1 : 2);
+    // the index starts from zero: the kernel stores only the bitmap's nonzero
+    // words, and a filter collects OR-ed bits
+    e = launch_fill_u32(b, g.bwords, 0u, s);
+    if (e != hipSuccess) return e;
     if (g.bloom_k != 0) {
-        // the filter collects OR-ed bits, so it starts from zero
-        e = launch_fill_u32(b, g.bwords, 0u, s);
-        if (e != hipSuccess) return e;
         if (g.f32) {
             if (mode == 0) return launch_dense_t<float, 0, true>(g, x, y, b, s, ntiles, di.cus);
             if (mode == 1) return launch_dense_t<float, 1, true>(g, x, y, b, s, ntiles, di.cus);

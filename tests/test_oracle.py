@@ -570,3 +570,21 @@ def test_decode_bound_simple_chain():
     bnd = o.decode_bound(g, dY, B)
     cl, _ = o.cells(g, [7])
     assert bnd[7] == float(cl[0][0])  # all three cells pure: the j = 0 one is used
+
+
+def test_compressed_size_recovery_rate_closed_form():
+    # section 4.1: one worker at 69.6 % density, sketches of f * n cells;
+    # the fraction left unpeeled is the 2-core fraction of the 3-uniform
+    # hypergraph with lambda = 0.696 / f edges per cell (c = 1, where the
+    # random-hypergraph model is exact); complete from 1.23 x 0.696 on
+    n = 300_000
+    rng = np.random.default_rng(4)
+    S = np.sort(rng.choice(n, int(0.696 * n), replace=False))
+    x = np.zeros(n, np.int32)
+    x[S] = rng.integers(1, 2**20, S.size)
+    for f in (0.5, 0.7, 0.8, 0.9):
+        g = o.Geom(n=n, rows=int(f * n), seed=17, c=1)
+        _, _, info = o.decode(g, *o.encode(g, x))
+        unpeeled = 1 - info.n_recovered / info.n_support
+        assert abs(unpeeled - core_fraction(S.size / g.cells)) < 0.01, f
+    assert core_fraction(0.696 / 0.856) == 0.0
