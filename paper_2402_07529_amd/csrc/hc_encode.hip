@@ -32,21 +32,34 @@ template <typename T> struct Vec4;
 template <> struct Vec4<int32_t> { typedef v4i type; };
 template <> struct Vec4<float> { typedef v4f type; };
 
-// vec: p is 16-byte aligned (else plain 4-byte stores throughout).
-__global__ __launch_bounds__(kBlock) void fill_u32_kernel(uint32_t* __restrict__ p,
-                                                          uint64_t count, uint32_t value,
-                                                          bool vec) {
+// Sets p[0, count) to value; vec: p is 16-byte aligned (else plain 4-byte
+// stores throughout).  Workgroups [0, g0) fill p, the rest fill p2[0, count2)
+// (p2 may be null): one launch clears both of an encode's outputs.
+__device__ __forceinline__ void fill_range(uint32_t* __restrict__ p, uint64_t count,
+                                           uint32_t value, bool vec, uint32_t blk,
+                                           uint32_t nblk) {
     const uint64_t nvec = vec ? count / 4 : 0;
-    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    const uint64_t stride = (uint64_t)nblk * kBlock;
     if (!vec) {
-        for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < count; i += stride)
+        for (uint64_t i = (uint64_t)blk * kBlock + threadIdx.x; i < count; i += stride)
             p[i] = value;
         return;
     }
     const v4u v = {value, value, value, value};
-    for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < nvec; i += stride)
+    for (uint64_t i = (uint64_t)blk * kBlock + threadIdx.x; i < nvec; i += stride)
         reinterpret_cast<v4u*>(p)[i] = v;
-    if (blockIdx.x == 0 && threadIdx.x < count - nvec * 4) p[nvec * 4 + threadIdx.x] = value;
+    if (blk == 0 && threadIdx.x < count - nvec * 4) p[nvec * 4 + threadIdx.x] = value;
+}
+
+__global__ __launch_bounds__(kBlock) void fill_u32_kernel(uint32_t* __restrict__ p,
+                                                          uint64_t count, bool vec,
+                                                          uint32_t* __restrict__ p2,
+                                                          uint64_t count2, bool vec2,
+                                                          uint32_t g0, uint32_t value) {
+    if (blockIdx.x < g0)
+        fill_range(p, count, value, vec, blockIdx.x, g0);
+    else
+        fill_range(p2, count2, value, vec2, blockIdx.x - g0, gridDim.x - g0);
 }
 
 // Sketch updates for the parameters of one load: e[k] is parameter p0 + k of
@@ -275,15 +288,24 @@ hipError_t launch_dense_t(const Geo& g, const void* x, void* y, uint32_t* b, hip
 
 }  // namespace
 
-hipError_t launch_fill_u32(uint32_t* p, uint64_t count, uint32_t value, hipStream_t s) {
-    if (count == 0) return hipSuccess;
+hipError_t launch_fill2_u32(uint32_t* p, uint64_t count, uint32_t* p2, uint64_t count2,
+                            uint32_t value, hipStream_t s) {
+    if (count == 0 && count2 == 0) return hipSuccess;
     DeviceInfo di;
     hipError_t e = device_info(&di);
     if (e != hipSuccess) return e;
-    const uint32_t grid = grid_for(count / 4 + 1, kBlock, (uint32_t)di.cus * 16);
-    hipLaunchKernelGGL(fill_u32_kernel, dim3(grid), dim3(kBlock), 0, s, p, count, value,
-                       (reinterpret_cast<uintptr_t>(p) & 15u) == 0);
+    // workgroups in proportion to the two ranges' sizes
+    const uint32_t cap = (uint32_t)di.cus * 16;
+    const uint32_t g0 = count ? grid_for(count / 4 + 1, kBlock, cap) : 0;
+    const uint32_t g1 = count2 ? grid_for(count2 / 4 + 1, kBlock, cap) : 0;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3(g0 + g1), dim3(kBlock), 0, s, p, count,
+                       (reinterpret_cast<uintptr_t>(p) & 15u) == 0, p2, count2,
+                       (reinterpret_cast<uintptr_t>(p2) & 15u) == 0, g0, value);
     return hipGetLastError();
+}
+
+hipError_t launch_fill_u32(uint32_t* p, uint64_t count, uint32_t value, hipStream_t s) {
+    return launch_fill2_u32(p, count, nullptr, 0, value, s);
 }
 
 hipError_t launch_encode_dense(const Geo& g, const void* x, void* y, uint32_t* b,
@@ -291,14 +313,12 @@ hipError_t launch_encode_dense(const Geo& g, const void* x, void* y, uint32_t* b
     DeviceInfo di;
     hipError_t e = device_info(&di);
     if (e != hipSuccess) return e;
-    e = launch_fill_u32(static_cast<uint32_t*>(y), g.cells, 0u, s);
+    // the sketch and the index start from zero: the kernel adds into the
+    // sketch, stores only the bitmap's nonzero words, and ORs into a filter
+    e = launch_fill2_u32(static_cast<uint32_t*>(y), g.cells, b, g.bwords, 0u, s);
     if (e != hipSuccess) return e;
     const uint64_t ntiles = (g.n + kTile - 1) / kTile;
     const int mode = g.c >= 256 ? 0 : (g.c >= 4 ? 1 : 2);
-    // the index starts from zero: the kernel stores only the bitmap's nonzero
-    // words, and a filter collects OR-ed bits
-    e = launch_fill_u32(b, g.bwords, 0u, s);
-    if (e != hipSuccess) return e;
     if (g.bloom_k != 0) {
         if (g.f32) {
             if (mode == 0) return launch_dense_t<float, 0, true>(g, x, y, b, s, ntiles, di.cus);
@@ -324,9 +344,7 @@ hipError_t launch_encode_coo(const Geo& g, const uint32_t* idx, const void* val,
     DeviceInfo di;
     hipError_t e = device_info(&di);
     if (e != hipSuccess) return e;
-    e = launch_fill_u32(static_cast<uint32_t*>(y), g.cells, 0u, s);
-    if (e != hipSuccess) return e;
-    e = launch_fill_u32(b, g.bwords, 0u, s);
+    e = launch_fill2_u32(static_cast<uint32_t*>(y), g.cells, b, g.bwords, 0u, s);
     if (e != hipSuccess) return e;
     if (nnz == 0) return hipSuccess;
     const uint32_t grid = grid_for(nnz, kBlock, (uint32_t)di.cus * 16);
