@@ -9,7 +9,7 @@
 //
 // encode  the workgroup zeroes the block's sketch in LDS, streams the block's
 //         gradient once (wave tiles of 1024 parameters, four coalesced 16-byte
-//         loads per lane, the next tile in flight while one is encoded), writes
+//         loads per lane, two blocks per CU), writes
 //         each tile's 32 bitmap words with one 128-byte store (at the workloads'
 //         block densities a third of the words or more are nonzero, and a
 //         zero-fill pass plus nonzero-only stores measured slower), adds every
@@ -183,13 +183,23 @@ struct EncArgs {
     uint32_t* b;
     uint64_t n, seed;
     uint32_t block, brows, bcells, c, cmask, log2c, y_vec, x_vec;
+    uint32_t stage_b;  // the block's bitmap words go through LDS (written at the end)
 };
 
-template <typename T>
-__global__ __launch_bounds__(kEncThreads) void encode_blocked_kernel(EncArgs<T> a) {
+// PF = false: two workgroups (blocks) per CU, i.e. eight waves per SIMD (the
+// launch bound's second argument) and so at most 64 VGPRs, one tile in flight
+// per wave; one block's setup and sketch write-back then overlap the other's
+// gradient stream.  PF = true: one block per CU, each wave prefetching its next
+// tile while it encodes the current one.  Measured on MI355X, the first is
+// about 10 % faster when there are more than two blocks per CU to run (BERT-base
+// and VGG19 at 1 % density, about 990 blocks), the second 10-25 % faster with
+// fewer (LSTM, 497 blocks; sparse BERT-base, 105).
+template <typename T, bool PF>
+__global__ __launch_bounds__(kEncThreads, PF ? 4 : 8) void encode_blocked_kernel(EncArgs<T> a) {
     extern __shared__ __align__(16) unsigned char lds_raw[];
     T* s_y = reinterpret_cast<T*>(lds_raw);
     uint32_t* s_tab = reinterpret_cast<uint32_t*>(lds_raw + (size_t)a.bcells * sizeof(T));
+    uint32_t* s_bm = s_tab + ((3 * a.block + 3) & ~3u);  // staged bitmap words (16-byte aligned)
     const uint32_t q = blockIdx.x;
     const BlockRange r = block_range(q, a.block, a.log2c, a.cmask, a.n);
     for (uint32_t i = threadIdx.x; i < a.bcells; i += kEncThreads) s_y[i] = T(0);
@@ -197,20 +207,21 @@ __global__ __launch_bounds__(kEncThreads) void encode_blocked_kernel(EncArgs<T> 
     __syncthreads();
 
     const uint32_t lane = lane_id();
-    const uint32_t wave = threadIdx.x >> 6;
+    const uint32_t wave = uniform(threadIdx.x >> 6);
     const uint32_t ntiles = (uint32_t)((r.p1 - r.p0 + kWaveTile - 1) / kWaveTile);
     constexpr uint32_t kWaves = kEncThreads / 64;
     typedef T V4 __attribute__((ext_vector_type(4)));
     // A tile is read as four 16-byte loads per lane: e[l][k] = parameter
     // tp + 256 l + 4 lane + k.  Tiles wholly inside the block (and a 16-byte
-    // aligned gradient) take the vector loads with no branch, so the waits of
-    // the pipelined loop below count exactly the loads they need; the block's
-    // last, partial tile reads element by element, zero past the block's end.
+    // aligned gradient) take vector loads through one buffer resource over the
+    // block's gradient (at most 4 MiB; the tile's offset is scalar, the lane's
+    // fixed); the block's last, partial tile reads element by element, zero
+    // past the block's end.
+    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(a.x + r.p0, (uint32_t)((r.p1 - r.p0) * sizeof(T)));
     auto load_full = [&](uint32_t tile, T (&e)[4][4]) {
-        const V4* src = reinterpret_cast<const V4*>(a.x + r.p0 + (uint64_t)tile * kWaveTile) + lane;
 #pragma unroll
         for (int l = 0; l < 4; l++) {
-            const V4 v = __builtin_nontemporal_load(src + 64 * l);
+            const V4 v = buffer_load16_nt<V4>(rs, 16u * lane + 1024u * l, tile * (uint32_t)(kWaveTile * sizeof(T)));
             e[l][0] = v.x;
             e[l][1] = v.y;
             e[l][2] = v.z;
@@ -244,7 +255,10 @@ __global__ __launch_bounds__(kEncThreads) void encode_blocked_kernel(EncArgs<T> 
                 const uint64_t mk = l == 0 ? m[0][k] : l == 1 ? m[1][k] : l == 2 ? m[2][k] : m[3][k];
                 word |= spread4((uint32_t)(mk >> sh)) << k;
             }
-            a.b[(tp >> 5) + lane] = word;
+            if (a.stage_b)
+                s_bm[((tp - r.p0) >> 5) + lane] = word;
+            else
+                a.b[(tp >> 5) + lane] = word;
         }
         // sketch: three LDS atomics per nonzero
 #pragma unroll
@@ -281,37 +295,59 @@ __global__ __launch_bounds__(kEncThreads) void encode_blocked_kernel(EncArgs<T> 
             }
         }
     };
-    // rolling pipeline over the full tiles: the next tile's loads are issued
-    // before the current tile is encoded, so a wave keeps memory in flight
-    // while it works.  The prefetch is never conditional on its own, so every
-    // wait has one known count of younger loads to leave in flight.
     const uint32_t nfull = a.x_vec ? (uint32_t)((r.p1 - r.p0) / kWaveTile) : 0u;
-    T ea[4][4], eb[4][4];
-    uint32_t tile = wave;
-    if (tile < nfull) {
-        load_full(tile, ea);
-        for (;;) {
-            if (tile + kWaves >= nfull) {
-                encode_tile(tile, ea);
-                break;
-            }
-            load_full(tile + kWaves, eb);
+    T ea[4][4];
+    if (!PF) {
+        for (uint32_t tile = wave; tile < nfull; tile += kWaves) {
+            load_full(tile, ea);
             encode_tile(tile, ea);
-            tile += kWaves;
-            if (tile + kWaves >= nfull) {
+        }
+    } else {
+        // rolling pipeline: the next tile's loads are issued before the
+        // current tile is encoded (never conditionally on their own)
+        T eb[4][4];
+        uint32_t tile = wave;
+        if (tile < nfull) {
+            load_full(tile, ea);
+            for (;;) {
+                if (tile + kWaves >= nfull) {
+                    encode_tile(tile, ea);
+                    break;
+                }
+                load_full(tile + kWaves, eb);
+                encode_tile(tile, ea);
+                tile += kWaves;
+                if (tile + kWaves >= nfull) {
+                    encode_tile(tile, eb);
+                    break;
+                }
+                load_full(tile + kWaves, ea);
                 encode_tile(tile, eb);
-                break;
+                tile += kWaves;
             }
-            load_full(tile + kWaves, ea);
-            encode_tile(tile, eb);
-            tile += kWaves;
         }
     }
-    for (tile = nfull + wave; tile < ntiles; tile += kWaves) {
+    for (uint32_t tile = nfull + wave; tile < ntiles; tile += kWaves) {
         load_part(tile, ea);
         encode_tile(tile, ea);
     }
     __syncthreads();
+
+    if (a.stage_b) {
+        // the block's bitmap in one coalesced pass: a global store inside the
+        // streaming loop would sit in the memory counter ahead of the next
+        // tile's loads, so every iteration would wait for its acknowledgement
+        const uint32_t nw = (uint32_t)((r.p1 - r.p0 + 31) >> 5);
+        uint32_t* bb = a.b + (r.p0 >> 5);
+        if (((reinterpret_cast<uintptr_t>(bb) & 15u) == 0)) {
+            const uint32_t nv = nw / 4;
+            for (uint32_t i = threadIdx.x; i < nv; i += kEncThreads)
+                reinterpret_cast<v4u32*>(bb)[i] = reinterpret_cast<const v4u32*>(s_bm)[i];
+            for (uint32_t i = 4 * nv + threadIdx.x; i < nw; i += kEncThreads) bb[i] = s_bm[i];
+        } else {
+            for (uint32_t i = threadIdx.x; i < nw; i += kEncThreads) bb[i] = s_bm[i];
+        }
+    }
 
     T* yb = a.y + (uint64_t)q * a.bcells;
     if (a.y_vec) {
@@ -713,12 +749,17 @@ hipError_t allow_lds(K kernel, std::once_flag& flag) {
     return e;
 }
 
-std::once_flag g_enc_i32, g_enc_f32, g_dec_i32, g_dec_f32;
+std::once_flag g_enc_i32[2], g_enc_f32[2], g_dec_i32, g_dec_f32;
 
 template <typename T>
 hipError_t launch_encode_blocked_t(const Geo& g, const void* x, void* y, uint32_t* b,
-                                   hipStream_t s, std::once_flag& flag) {
-    hipError_t e = allow_lds(&encode_blocked_kernel<T>, flag);
+                                   hipStream_t s, std::once_flag (&flags)[2]) {
+    DeviceInfo di;
+    hipError_t e = device_info(&di);
+    if (e != hipSuccess) return e;
+    const bool pf = g.nblocks <= 2u * (uint32_t)di.cus;
+    e = pf ? allow_lds(&encode_blocked_kernel<T, true>, flags[1])
+           : allow_lds(&encode_blocked_kernel<T, false>, flags[0]);
     if (e != hipSuccess) return e;
     EncArgs<T> a;
     a.x = static_cast<const T*>(x);
@@ -734,8 +775,16 @@ hipError_t launch_encode_blocked_t(const Geo& g, const void* x, void* y, uint32_
     a.log2c = g.log2c;
     a.y_vec = (reinterpret_cast<uintptr_t>(y) & 15u) == 0 && (a.bcells & 3u) == 0;
     a.x_vec = (reinterpret_cast<uintptr_t>(x) & 15u) == 0;
-    hipLaunchKernelGGL(encode_blocked_kernel<T>, dim3(g.nblocks), dim3(kEncThreads),
-                       blocked_encode_lds(g), s, a);
+    // stage the bitmap in LDS when two blocks per CU still fit
+    const size_t lds = blocked_encode_lds(g);
+    const size_t staged = lds + 16 + (size_t)g.block * g.c / 8;
+    a.stage_b = staged + kLdsReserve <= kLdsBytes / 2 ? 1u : 0u;
+    if (pf)
+        hipLaunchKernelGGL((encode_blocked_kernel<T, true>), dim3(g.nblocks), dim3(kEncThreads),
+                           a.stage_b ? staged : lds, s, a);
+    else
+        hipLaunchKernelGGL((encode_blocked_kernel<T, false>), dim3(g.nblocks), dim3(kEncThreads),
+                           a.stage_b ? staged : lds, s, a);
     return hipGetLastError();
 }
 

@@ -249,6 +249,29 @@ __device__ __forceinline__ T median3(T a, T b, T c) {
     return c < lo ? lo : (c > hi ? hi : c);
 }
 
+// ---- streaming loads through buffer resources --------------------------------
+
+typedef unsigned int v4u32 __attribute__((ext_vector_type(4)));
+
+// Buffer resource over [base, base + bytes), bytes < 2^31 (word 3 as the
+// gfx9 family takes it for untyped loads).  Loads through it take a scalar
+// base, a scalar offset and a fixed per-lane offset, so the loop that streams
+// a gradient keeps no address arithmetic in the vector registers its loads
+// write (which would force a full wait on the memory counter at every
+// iteration).  Out-of-range addresses read as 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+// 16 bytes at byte offset voff + soff, nontemporal (read once).
+template <typename V>
+__device__ __forceinline__ V buffer_load16_nt(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                              uint32_t soff) {
+    const v4u32 raw = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 2);
+    return __builtin_bit_cast(V, raw);
+}
+
 // ---- wave64 utilities --------------------------------------------------------
 
 __device__ __forceinline__ uint32_t lane_id() {
