@@ -51,21 +51,35 @@ constexpr unsigned long long kOne = 1ull << 32;  // one incidence in a packed co
 constexpr uint64_t kChunkBits = (uint64_t)kChunkWords * 32;
 constexpr uint64_t kBarrierTimeoutTicks = 500000000ull;  // 5 s at the 100 MHz real-time clock
 
+// Statistics and flags (one 64-byte line; the support scan writes it too).
 struct Ctrl {
     unsigned long long n_support;
     unsigned long long recovered;
-    unsigned int tail;      // queue length
-    unsigned int fend;      // end of the current frontier in the queue
     unsigned int rounds;
     unsigned int overflow;  // |S| > capacity
     unsigned int abort;     // barrier timeout
-    unsigned int bar_count;
-    unsigned int bar_gen;
     unsigned int done;      // workgroups finished
     unsigned int bad_plan;  // the plan was built for another geometry
-    unsigned int pad[3];
+    unsigned int pad[7];
 };
 static_assert(sizeof(Ctrl) == 64, "control block layout");
+
+// Queue and barrier state of the peel.  Every word that many workgroups hit
+// in the same few microseconds has a 128-byte line of its own: appends to the
+// queue, barrier arrivals and the polls of the waiting workgroups would
+// otherwise queue up behind each other on one line (measured on MI355X: a
+// barrier of 256 workgroups took about 20 us with the queue length in the
+// barrier's line, under 7 us with separate lines and two-level arrival).
+constexpr uint32_t kBarGroups = 8;
+struct alignas(128) SyncLine {
+    unsigned int v[32];
+};
+struct PeelSync {
+    SyncLine tail;                // v[0]: queue length
+    SyncLine top;                 // v[0]: arrivals of the group leaders
+    SyncLine gen;                 // v[0]: barrier generation; v[1]: end of the current frontier
+    SyncLine group[kBarGroups];   // v[0]: arrivals within group g
+};
 
 // device mirror of hc_decode_info
 struct InfoDev {
@@ -108,9 +122,13 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(const T* __restrict__ y_ag
                                                       unsigned long long* __restrict__ cnt,
                                                       uint32_t* __restrict__ stamp,
                                                       uint32_t cells, bool planned,
-                                                      Ctrl* __restrict__ ctrl) {
-    if (blockIdx.x == 0 && threadIdx.x < sizeof(Ctrl) / 4)
-        reinterpret_cast<uint32_t*>(ctrl)[threadIdx.x] = 0u;
+                                                      Ctrl* __restrict__ ctrl,
+                                                      PeelSync* __restrict__ sync) {
+    if (blockIdx.x == 0) {
+        if (threadIdx.x < sizeof(Ctrl) / 4) reinterpret_cast<uint32_t*>(ctrl)[threadIdx.x] = 0u;
+        for (uint32_t k = threadIdx.x; k < sizeof(PeelSync) / 4; k += kBlock)
+            reinterpret_cast<uint32_t*>(sync)[k] = 0u;
+    }
     const uint64_t step = (uint64_t)gridDim.x * kBlock;
     for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < cells; i += step) {
         yw[i] = (typename Acc<T>::type)y_agg[i];
@@ -147,22 +165,48 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const uint32_t* __restric
     }
 }
 
-// One workgroup of 1024 lanes: chunk counts -> exclusive offsets.
+// One workgroup of 1024 lanes: chunk counts -> exclusive offsets.  Lane t
+// owns a run of consecutive counts whose length is a multiple of 4, read and
+// written as 16-byte vectors (the counts start 256-byte aligned).
+__device__ __forceinline__ uint4 load_counts4(const uint32_t* blk, uint64_t i, uint64_t nchunks) {
+    if (i + 4 <= nchunks) return *reinterpret_cast<const uint4*>(blk + i);
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (i < nchunks) v.x = blk[i];
+    if (i + 1 < nchunks) v.y = blk[i + 1];
+    if (i + 2 < nchunks) v.z = blk[i + 2];
+    return v;
+}
+
 __global__ __launch_bounds__(1024) void scan_kernel(uint32_t* __restrict__ blk, uint64_t nchunks,
                                                     Ctrl* __restrict__ ctrl, uint64_t cap,
                                                     uint32_t* __restrict__ woff, uint64_t words) {
     __shared__ uint32_t s_tmp[16];
-    const uint64_t per = (nchunks + 1023) / 1024;
+    const uint64_t per = ((nchunks + 1023) / 1024 + 3) & ~3ull;
     const uint64_t lo = (uint64_t)threadIdx.x * per;
-    const uint64_t hi = lo + per < nchunks ? lo + per : nchunks;
     uint32_t s = 0;
-    for (uint64_t i = lo; i < hi; i++) s += blk[i];
+#pragma unroll 8
+    for (uint64_t i = lo; i < lo + per; i += 4) {
+        const uint4 v = load_counts4(blk, i, nchunks);
+        s += v.x + v.y + v.z + v.w;
+    }
     uint32_t total;
     uint32_t off = block_exclusive_scan(s, s_tmp, &total);
-    for (uint64_t i = lo; i < hi; i++) {
-        const uint32_t v = blk[i];
-        blk[i] = off;
-        off += v;
+#pragma unroll 8
+    for (uint64_t i = lo; i < lo + per && i < nchunks; i += 4) {
+        const uint4 v = load_counts4(blk, i, nchunks);
+        uint4 o;
+        o.x = off;
+        o.y = o.x + v.x;
+        o.z = o.y + v.y;
+        o.w = o.z + v.z;
+        off = o.w + v.w;
+        if (i + 4 <= nchunks) {
+            *reinterpret_cast<uint4*>(blk + i) = o;
+        } else {
+            blk[i] = o.x;
+            if (i + 1 < nchunks) blk[i + 1] = o.y;
+            if (i + 2 < nchunks) blk[i + 2] = o.z;
+        }
     }
     if (threadIdx.x == 0) {
         ctrl->n_support = total;
@@ -251,13 +295,13 @@ __device__ __forceinline__ void lds_push(PushBuf& q, bool pred, uint32_t cell, u
 // Called by every lane of the workgroup with the same arguments.  Appends the
 // staged pairs to the global queue if `force` or if the buffer could not take
 // another `room` pushes.
-__device__ void flush_pushes(PushBuf& q, bool force, uint32_t room, Ctrl* ctrl, uint2* queue,
-                             uint32_t cells) {
+__device__ void flush_pushes(PushBuf& q, bool force, uint32_t room, unsigned int* tail,
+                             uint2* queue, uint32_t cells) {
     __syncthreads();
     const uint32_t n = q.count;
     __syncthreads();  // every lane has read n before any lane pushes again
     if (n == 0 || (!force && n + room <= kPushCap)) return;
-    if (threadIdx.x == 0) q.base = atomicAdd(&ctrl->tail, n);
+    if (threadIdx.x == 0) q.base = atomicAdd(tail, n);
     __syncthreads();
     const uint32_t base = q.base;
     for (uint32_t k = threadIdx.x; k < n; k += blockDim.x)
@@ -279,6 +323,7 @@ struct CounterArgs {
     uint32_t* stamp;
     uint2* queue;
     Ctrl* ctrl;
+    PeelSync* sync;
     uint64_t n, seed, words, nb;
     uint32_t rows, c, cmask, cells, last_mask;
 };
@@ -367,9 +412,9 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
             a.stamp[cell] = pure ? 0u : kNever;
             lds_push(q, pure, cell, (uint32_t)acc, 0u, nullptr);
         }
-        flush_pushes(q, false, C, a.ctrl, a.queue, a.cells);
+        flush_pushes(q, false, C, &a.sync->tail.v[0], a.queue, a.cells);
     }
-    flush_pushes(q, true, 0, a.ctrl, a.queue, a.cells);
+    flush_pushes(q, true, 0, &a.sync->tail.v[0], a.queue, a.cells);
 }
 
 // ---- peel ------------------------------------------------------------------------
@@ -377,6 +422,7 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
 template <typename T>
 struct PeelArgs {  // T: the decode-side arithmetic type
     Ctrl* ctrl;
+    PeelSync* sync;
     const uint32_t* elem;
     T* vals;
     uint8_t* peeled;
@@ -390,45 +436,61 @@ struct PeelArgs {  // T: the decode-side arithmetic type
     bool planned;   // the round-0 frontier is already queued
 };
 
-// Grid-wide barrier.  The last block to arrive publishes the end of the next
-// frontier.  Each block makes its writes visible with one release fence
-// before arriving and picks up everyone else's with one acquire fence after
-// the wait; the wait itself polls with relaxed loads, so spinning blocks do
-// not keep invalidating their caches.  Returns false if the wait timed out
-// (then ctrl->abort is set).
-__device__ bool grid_barrier(Ctrl* ctrl, uint32_t nblocks) {
+// Grid-wide barrier in two levels: the workgroups of group g (blockIdx % G)
+// arrive on the group's counter, the last of each group on the top counter,
+// and the last of those publishes the end of the next frontier and bumps the
+// generation that everyone polls.  Each workgroup makes its writes visible
+// with one release fence before arriving and picks up everyone else's with
+// one acquire fence after the wait; group leaders pass their group's writes on
+// with an acquire-release fence.  The wait polls with relaxed loads, so
+// spinning workgroups do not keep invalidating their caches.  Returns false
+// if the wait timed out (then ctrl->abort is set).
+__device__ __forceinline__ uint32_t ld_agent(const unsigned int* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent(unsigned int* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t add_agent(unsigned int* p, uint32_t v) {
+    return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks) {
     __shared__ uint32_t s_ok;
     __syncthreads();
     if (threadIdx.x == 0) {
         uint32_t ok = 1;
-        const uint32_t gen =
-            __hip_atomic_load(&ctrl->bar_gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint32_t groups = nblocks < kBarGroups ? nblocks : kBarGroups;
+        const uint32_t grp = blockIdx.x % groups;
+        const uint32_t gsize = (nblocks - grp + groups - 1u) / groups;  // blocks in the group
+        const uint32_t gen = ld_agent(&sy->gen.v[0]);
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        const uint32_t arrived = __hip_atomic_fetch_add(&ctrl->bar_count, 1u, __ATOMIC_RELAXED,
-                                                        __HIP_MEMORY_SCOPE_AGENT);
-        if (arrived == nblocks - 1u) {
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-            const uint32_t t =
-                __hip_atomic_load(&ctrl->tail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&ctrl->fend, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&ctrl->bar_count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&ctrl->bar_gen, gen + 1u, __ATOMIC_RELEASE,
-                               __HIP_MEMORY_SCOPE_AGENT);
-        } else {
+        bool wait = true;
+        if (add_agent(&sy->group[grp].v[0], 1u) == gsize - 1u) {
+            st_agent(&sy->group[grp].v[0], 0u);
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "agent");
+            if (add_agent(&sy->top.v[0], 1u) == groups - 1u) {
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                st_agent(&sy->gen.v[1], ld_agent(&sy->tail.v[0]));
+                st_agent(&sy->top.v[0], 0u);
+                __hip_atomic_store(&sy->gen.v[0], gen + 1u, __ATOMIC_RELEASE,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+                wait = false;
+            }
+        }
+        if (wait) {
             const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-            while (__hip_atomic_load(&ctrl->bar_gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-                   gen) {
+            while (ld_agent(&sy->gen.v[0]) == gen) {
                 __builtin_amdgcn_s_sleep(2);
                 if (__builtin_amdgcn_s_memrealtime() - t0 > kBarrierTimeoutTicks) {
-                    __hip_atomic_store(&ctrl->abort, 1u, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
+                    st_agent(&ctrl->abort, 1u);
                     ok = 0;
                     break;
                 }
             }
         }
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        if (__hip_atomic_load(&ctrl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) ok = 0;
+        if (ld_agent(&ctrl->abort)) ok = 0;
         s_ok = ok;
     }
     __syncthreads();
@@ -440,6 +502,7 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
     __shared__ PushBuf q;
     __shared__ uint32_t s_red[2];
     Ctrl* ctrl = a.ctrl;
+    PeelSync* sync = a.sync;
     const uint32_t lane = lane_id();
     const uint32_t waves_per_block = kPeelBlock / 64;
     // wave-sized chunks of work go round-robin over the workgroups, so small
@@ -471,16 +534,15 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                     pure = (v >> 32) == 1ull;
                 }
                 lds_push(q, pure, cidx, (uint32_t)v, 0u, a.stamp);
-                flush_pushes(q, false, kPeelBlock, ctrl, a.queue, a.cells);
+                flush_pushes(q, false, kPeelBlock, &sync->tail.v[0], a.queue, a.cells);
             }
-            flush_pushes(q, true, 0, ctrl, a.queue, a.cells);
+            flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
         }
-        ok = grid_barrier(ctrl, gridDim.x);
+        ok = grid_barrier(ctrl, sync, gridDim.x);
 
         uint32_t qs = 0;
         for (uint32_t r = 0; ok; r++) {
-            uint32_t qe =
-                __hip_atomic_load(&ctrl->fend, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            uint32_t qe = ld_agent(&sync->gen.v[1]);
             if (qe > a.cells) qe = a.cells;  // the queue holds each cell at most once
             if (qe <= qs) break;
             const uint32_t nsweep = (qe - qs + nwaves * 64u - 1u) / (nwaves * 64u);
@@ -532,11 +594,11 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                 }
                 lds_push(q, push_a, cell_a, pos_a, r + 1u, a.stamp);
                 lds_push(q, push_b, cell_b, pos_b, r + 1u, a.stamp);
-                flush_pushes(q, false, 2u * kPeelBlock, ctrl, a.queue, a.cells);
+                flush_pushes(q, false, 2u * kPeelBlock, &sync->tail.v[0], a.queue, a.cells);
             }
-            flush_pushes(q, true, 0, ctrl, a.queue, a.cells);
+            flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
             qs = qe;
-            ok = grid_barrier(ctrl, gridDim.x);
+            ok = grid_barrier(ctrl, sync, gridDim.x);
         }
 
         // leftovers: Count Sketch median estimate from the residual sketch
@@ -763,6 +825,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     char* base = static_cast<char*>(ws);
     typedef typename Acc<T>::type A;
     Ctrl* ctrl = reinterpret_cast<Ctrl*>(base + L.ctrl);
+    PeelSync* sync = reinterpret_cast<PeelSync*>(base + L.sync);
     uint32_t* blk = reinterpret_cast<uint32_t*>(base + L.blk);
     uint32_t* woff = plan ? reinterpret_cast<uint32_t*>(base + L.woff) : nullptr;
     uint32_t* elem = reinterpret_cast<uint32_t*>(base + L.elem);
@@ -782,7 +845,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     uint64_t grid = ((uint64_t)g.cells + kBlock - 1) / kBlock;
     if (grid > (uint64_t)di.cus * 16) grid = (uint64_t)di.cus * 16;
     hipLaunchKernelGGL(prep_kernel<T>, dim3((uint32_t)grid), dim3(kBlock), 0, s, y_agg, yw, cnt,
-                       stamp, g.cells, planned, ctrl);
+                       stamp, g.cells, planned, ctrl, sync);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const uint32_t last_mask = (g.n & 31u) ? ((1u << (g.n & 31u)) - 1u) : 0xffffffffu;
     hipLaunchKernelGGL(count_kernel, dim3((uint32_t)L.nchunks), dim3(kBlock), 0, s, b, g.words,
@@ -809,6 +872,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
         ca.stamp = stamp;
         ca.queue = queue;
         ca.ctrl = ctrl;
+        ca.sync = sync;
         ca.n = g.n;
         ca.seed = g.seed;
         ca.words = g.words;
@@ -848,6 +912,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     }
     PeelArgs<A> pa;
     pa.ctrl = ctrl;
+    pa.sync = sync;
     pa.elem = elem;
     pa.vals = vals;
     pa.peeled = peeled;
@@ -913,6 +978,7 @@ DecodeLayout decode_layout(const Geo& g, uint64_t max_support) {
     const size_t vsz = g.f32 ? 8 : 4;  // decode-side values: int32, or fp64 for fp32
     size_t o = 0;
     L.ctrl = o;    o = align256(o + sizeof(Ctrl));
+    L.sync = o;    o = align256(o + sizeof(PeelSync));
     L.blk = o;     o = align256(o + L.nchunks * 4);
     L.woff = o;    o = align256(o + (g.words + 1) * 4);
     L.elem = o;    o = align256(o + cap * 4);
