@@ -682,7 +682,8 @@ int hco_decode_f64(const hco_geom *g, const double *Y, const uint32_t *B,
 /* Error bound carried through the schedule of hco_decode_f64 (see hco.h).
  * The schedule (which cells are pure in which round) depends only on B and
  * the hashes, so this repeats it with absolute-value accumulation in place
- * of subtraction. */
+ * of subtraction, taking for each peeled element the largest bound among its
+ * pure cells. */
 int hco_decode_bound_f64(const hco_geom *g, const double *dY, const uint32_t *B,
                          double *bound)
 {
@@ -719,11 +720,13 @@ int hco_decode_bound_f64(const hco_geom *g, const double *dY, const uint32_t *B,
             pick[i] = -1;
             if (!get_bit(bits, ps[i])) continue;
             for (int j = 0; j < 3; j++) {
-                if (deg[cell[3 * i + j]] == 1) {
+                if (deg[cell[3 * i + j]] != 1) continue;
+                if (pick[i] < 0) {
                     pick[i] = (int8_t)j;
                     eb[i] = Eb[cell[3 * i + j]];
                     peeled++;
-                    break;
+                } else if (Eb[cell[3 * i + j]] > eb[i]) {
+                    eb[i] = Eb[cell[3 * i + j]];
                 }
             }
         }

@@ -178,7 +178,10 @@ int hco_decode_f64(const hco_geom *g, const double *Y, const uint32_t *B,
  * linear in Y for a fixed schedule: x = g_j * (Y[c] - sum of g' x' over the
  * earlier-peeled members of c), so |dx| <= dY[c] + sum of |dx'|; a leftover
  * estimate is a median, which moves by at most the largest of its three
- * cells' errors.  Returns 0 or -1. */
+ * cells' errors.  Section 3.2 does not fix which of an element's pure cells
+ * supplies its value (in exact arithmetic they all hold it), so the bound of
+ * a peeled element is the largest over all its cells pure in that round:
+ * it holds whichever of them a decoder reads.  Returns 0 or -1. */
 int hco_decode_bound_f64(const hco_geom *g, const double *dY, const uint32_t *B,
                          double *bound);
 

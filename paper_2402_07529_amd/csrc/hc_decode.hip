@@ -3,7 +3,7 @@
 // Stages (one stream, no host round trips):
 //   prep     copy the aggregated sketch into a residual Yw (fp64 for fp32
 //            gradients), clear the control block (and, without a plan, the
-//            per-cell counters and round stamps);
+//            per-cell counters);
 //   count    popcount of the bitmap per chunk of 1024 words;
 //   scan     exclusive scan of the chunk counts (one workgroup) -> offsets and
 //            the support size |S|;
@@ -23,12 +23,15 @@
 //            (section 3.2, parallel peeling).  The frontier of round r is the
 //            list of (cell, element) pairs whose cell became pure during round
 //            r-1, kept in one append-only queue.  An element owning several
-//            frontier cells is claimed through the one with the smallest j; a
-//            per-cell stamp (the round in whose frontier the cell sits) tells
-//            which of its cells were pure at the round start without racing
-//            with the round's own updates.  The claimer recovers x = g_j * Y,
-//            and subtracts g * x and the element from its other two cells with
-//            atomics; a cell whose count drops to one joins the next frontier.
+//            frontier cells is claimed by an atomic exchange on its flag: the
+//            first of its frontier entries to get there recovers x = g_j * Y
+//            from its cell (every pure cell of the element holds the same
+//            value, exactly so in integer arithmetic), and subtracts g * x and
+//            the element from its other two cells with atomics; a cell whose
+//            count drops to one joins the next frontier.  Entries whose element
+//            is already taken (in this round or an earlier one) do nothing, so
+//            the elements peeled in round r are exactly those with a cell in
+//            its frontier that were still live when it began.
 //            One grid barrier per round; rounds end when a frontier is empty.
 //            Elements never peeled get the Count Sketch median estimate from
 //            the residual sketch (Algorithm 1, last recovery step);
@@ -46,7 +49,6 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kPeelBlock = 1024;  // lanes per workgroup of the persistent peel kernel
-constexpr uint32_t kNever = 0xffffffffu;
 constexpr unsigned long long kOne = 1ull << 32;  // one incidence in a packed counter
 constexpr uint64_t kChunkBits = (uint64_t)kChunkWords * 32;
 constexpr uint64_t kBarrierTimeoutTicks = 500000000ull;  // 5 s at the 100 MHz real-time clock
@@ -120,7 +122,6 @@ template <typename T>
 __global__ __launch_bounds__(kBlock) void prep_kernel(const T* __restrict__ y_agg,
                                                       typename Acc<T>::type* __restrict__ yw,
                                                       unsigned long long* __restrict__ cnt,
-                                                      uint32_t* __restrict__ stamp,
                                                       uint32_t cells, bool planned,
                                                       Ctrl* __restrict__ ctrl,
                                                       PeelSync* __restrict__ sync) {
@@ -132,10 +133,7 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(const T* __restrict__ y_ag
     const uint64_t step = (uint64_t)gridDim.x * kBlock;
     for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < cells; i += step) {
         yw[i] = (typename Acc<T>::type)y_agg[i];
-        if (!planned) {
-            cnt[i] = 0ull;
-            stamp[i] = kNever;
-        }
+        if (!planned) cnt[i] = 0ull;
     }
 }
 
@@ -219,7 +217,7 @@ __global__ __launch_bounds__(1024) void scan_kernel(uint32_t* __restrict__ blk, 
 // offsets (planned) or the per-cell counters by atomics (unplanned).
 __global__ __launch_bounds__(kBlock) void compact_kernel(
     const uint32_t* __restrict__ b, uint64_t words, uint32_t last_mask,
-    const uint32_t* __restrict__ blk, uint32_t* __restrict__ elem, uint8_t* __restrict__ peeled,
+    const uint32_t* __restrict__ blk, uint32_t* __restrict__ elem, uint32_t* __restrict__ peeled,
     uint32_t* __restrict__ woff, unsigned long long* __restrict__ cnt,
     const Ctrl* __restrict__ ctrl, uint64_t seed, uint32_t rows, uint32_t c, uint32_t cmask,
     uint32_t log2c) {
@@ -277,8 +275,7 @@ struct PushBuf {
     uint2 item[kPushCap];
 };
 
-__device__ __forceinline__ void lds_push(PushBuf& q, bool pred, uint32_t cell, uint32_t pos,
-                                         uint32_t round_stamp, uint32_t* stamp) {
+__device__ __forceinline__ void lds_push(PushBuf& q, bool pred, uint32_t cell, uint32_t pos) {
     const uint64_t m = __ballot(pred);
     if (m == 0) return;
     const uint32_t lane = lane_id();
@@ -286,10 +283,7 @@ __device__ __forceinline__ void lds_push(PushBuf& q, bool pred, uint32_t cell, u
     uint32_t off = 0;
     if (lane == leader) off = atomicAdd(&q.count, (unsigned int)__popcll(m));
     off = __shfl(off, leader);
-    if (pred) {
-        q.item[off + lanes_below(m)] = make_uint2(cell, pos);
-        if (stamp != nullptr) stamp[cell] = round_stamp;
-    }
+    if (pred) q.item[off + lanes_below(m)] = make_uint2(cell, pos);
 }
 
 // Called by every lane of the workgroup with the same arguments.  Appends the
@@ -320,7 +314,6 @@ struct CounterArgs {
     const uint32_t* b;
     const uint32_t* woff;   // words + 1 entries
     unsigned long long* cnt;
-    uint32_t* stamp;
     uint2* queue;
     Ctrl* ctrl;
     PeelSync* sync;
@@ -337,7 +330,7 @@ struct CounterArgs {
 // only the batches that have one: lanes 0..C/32-1 load the batch's bitmap
 // words and rank offsets, every lane takes the (at most two) words covering
 // its C/64 consecutive cells by shuffle, and adds into the row's counters in
-// LDS.  The row is then written once, with its stamps, and its pure cells
+// LDS.  The row is then written once, and its pure cells
 // become the round-0 frontier.
 template <int C>
 __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
@@ -409,8 +402,7 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
             const uint32_t cell = row * C + k;
             const bool pure = (acc >> 32) == 1ull;
             a.cnt[cell] = acc;
-            a.stamp[cell] = pure ? 0u : kNever;
-            lds_push(q, pure, cell, (uint32_t)acc, 0u, nullptr);
+            lds_push(q, pure, cell, (uint32_t)acc);
         }
         flush_pushes(q, false, C, &a.sync->tail.v[0], a.queue, a.cells);
     }
@@ -425,10 +417,9 @@ struct PeelArgs {  // T: the decode-side arithmetic type
     PeelSync* sync;
     const uint32_t* elem;
     T* vals;
-    uint8_t* peeled;
+    uint32_t* peeled;
     unsigned long long* cnt;
     T* yw;
-    uint32_t* stamp;
     uint2* queue;
     InfoDev* info;
     uint64_t seed;
@@ -533,7 +524,7 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                     v = a.cnt[cidx];
                     pure = (v >> 32) == 1ull;
                 }
-                lds_push(q, pure, cidx, (uint32_t)v, 0u, a.stamp);
+                lds_push(q, pure, cidx, (uint32_t)v);
                 flush_pushes(q, false, kPeelBlock, &sync->tail.v[0], a.queue, a.cells);
             }
             flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
@@ -551,26 +542,27 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                 bool push_a = false, push_b = false;
                 uint32_t cell_a = 0, cell_b = 0, pos_a = 0, pos_b = 0;
                 if (i < qe) {
-                    // the cell was pure with element pos when queued; pos is dead
-                    // if it was peeled through another cell since
+                    // the cell was pure with element pos when queued.  The first
+                    // frontier entry of the element to take its flag recovers it;
+                    // the flag is already set if it was recovered through another
+                    // cell, in this round or an earlier one.  The element and the
+                    // cell's residual are read alongside the claim: once claimed,
+                    // nothing else changes that cell this round.
                     const uint2 it = a.queue[i];
                     const uint32_t cidx = it.x, pos = it.y;
-                    if (pos < nsup && !a.peeled[pos]) {
+                    if (pos < nsup) {
+                        const uint32_t taken = atomicExch(a.peeled + pos, 1u);
                         const uint32_t p = a.elem[pos];
+                        const T ycell = a.yw[cidx];
                         const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p >> a.log2c);
                         const uint32_t t = p & a.cmask;
                         uint32_t cl[3];
 #pragma unroll
                         for (int j = 0; j < 3; j++) cl[j] = cell_of(h, j, t, a.c, a.cmask);
                         const int j = cl[0] == cidx ? 0 : (cl[1] == cidx ? 1 : 2);
-                        // claimed by the smallest j among its cells pure at the round start
-                        bool mine = cl[j] == cidx;
-                        if (j >= 1 && a.stamp[cl[0]] == r) mine = false;
-                        if (j == 2 && mine && a.stamp[cl[1]] == r) mine = false;
-                        if (mine) {
-                            const T val = Val<T>::sign(a.yw[cidx], (h.neg >> j) & 1u);
+                        if (taken == 0u && cl[j] == cidx) {
+                            const T val = Val<T>::sign(ycell, (h.neg >> j) & 1u);
                             a.vals[pos] = val;
-                            a.peeled[pos] = 1;
                             my_recovered++;
                             my_last_round = r + 1u;
                             const int ja = j == 0 ? 1 : 0;
@@ -592,8 +584,8 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                         }
                     }
                 }
-                lds_push(q, push_a, cell_a, pos_a, r + 1u, a.stamp);
-                lds_push(q, push_b, cell_b, pos_b, r + 1u, a.stamp);
+                lds_push(q, push_a, cell_a, pos_a);
+                lds_push(q, push_b, cell_b, pos_b);
                 flush_pushes(q, false, 2u * kPeelBlock, &sync->tail.v[0], a.queue, a.cells);
             }
             flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
@@ -660,7 +652,7 @@ struct EmitArgs {  // T: the gradient type; values are kept in Acc<T>
     const uint32_t* blk;
     const uint32_t* elem;
     const typename Acc<T>::type* vals;
-    const uint8_t* peeled;
+    const uint32_t* peeled;
     const T* y_agg;
     const Ctrl* ctrl;
     T* x_out;
@@ -830,10 +822,9 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     uint32_t* woff = plan ? reinterpret_cast<uint32_t*>(base + L.woff) : nullptr;
     uint32_t* elem = reinterpret_cast<uint32_t*>(base + L.elem);
     A* vals = reinterpret_cast<A*>(base + L.vals);
-    uint8_t* peeled = reinterpret_cast<uint8_t*>(base + L.peeled);
+    uint32_t* peeled = reinterpret_cast<uint32_t*>(base + L.peeled);
     unsigned long long* cnt = reinterpret_cast<unsigned long long*>(base + L.cnt);
     A* yw = reinterpret_cast<A*>(base + L.yw);
-    uint32_t* stamp = reinterpret_cast<uint32_t*>(base + L.stamp);
     uint2* queue = reinterpret_cast<uint2*>(base + L.queue);
     const T* y_agg = static_cast<const T*>(y_agg_v);
     const bool planned = plan != nullptr;
@@ -845,7 +836,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     uint64_t grid = ((uint64_t)g.cells + kBlock - 1) / kBlock;
     if (grid > (uint64_t)di.cus * 16) grid = (uint64_t)di.cus * 16;
     hipLaunchKernelGGL(prep_kernel<T>, dim3((uint32_t)grid), dim3(kBlock), 0, s, y_agg, yw, cnt,
-                       stamp, g.cells, planned, ctrl, sync);
+                       g.cells, planned, ctrl, sync);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const uint32_t last_mask = (g.n & 31u) ? ((1u << (g.n & 31u)) - 1u) : 0xffffffffu;
     hipLaunchKernelGGL(count_kernel, dim3((uint32_t)L.nchunks), dim3(kBlock), 0, s, b, g.words,
@@ -869,7 +860,6 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
         ca.b = b;
         ca.woff = woff;
         ca.cnt = cnt;
-        ca.stamp = stamp;
         ca.queue = queue;
         ca.ctrl = ctrl;
         ca.sync = sync;
@@ -918,7 +908,6 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     pa.peeled = peeled;
     pa.cnt = cnt;
     pa.yw = yw;
-    pa.stamp = stamp;
     pa.queue = queue;
     pa.info = static_cast<InfoDev*>(out.info);
     pa.seed = g.seed;
@@ -983,10 +972,9 @@ DecodeLayout decode_layout(const Geo& g, uint64_t max_support) {
     L.woff = o;    o = align256(o + (g.words + 1) * 4);
     L.elem = o;    o = align256(o + cap * 4);
     L.vals = o;    o = align256(o + cap * vsz);
-    L.peeled = o;  o = align256(o + cap);
+    L.peeled = o;  o = align256(o + cap * 4);
     L.cnt = o;     o = align256(o + (size_t)g.cells * 8);
     L.yw = o;      o = align256(o + (size_t)g.cells * vsz);
-    L.stamp = o;   o = align256(o + (size_t)g.cells * 4);
     L.queue = o;   o = align256(o + (size_t)g.cells * 8);
     L.cand = o;    o = align256(o + (g.bloom_k ? g.words * 4 : 0));  // probed Bloom candidates
     L.total = o;

@@ -90,7 +90,7 @@ hipError_t launch_encode_blocked(const Geo& g, const void* x, void* y, uint32_t*
 struct DecodeLayout {
     uint64_t cap;       // max support the workspace holds
     uint64_t nchunks;   // bitmap chunks of kChunkWords words
-    size_t ctrl, sync, blk, woff, elem, vals, peeled, cnt, yw, stamp, queue, cand, total;
+    size_t ctrl, sync, blk, woff, elem, vals, peeled, cnt, yw, queue, cand, total;
 };
 constexpr uint32_t kChunkWords = 1024;
 DecodeLayout decode_layout(const Geo& g, uint64_t max_support);
