@@ -267,15 +267,16 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(
 // workgroup and appended to the global queue with one atomic per flush (a
 // single global counter bumped by every wave would serialize the whole grid
 // on one cache line).
-constexpr uint32_t kPushCap = 4 * kPeelBlock;
-
+template <uint32_t CAP>
 struct PushBuf {
+    static constexpr uint32_t kCap = CAP;
     uint32_t count;
     uint32_t base;
-    uint2 item[kPushCap];
+    uint2 item[CAP];
 };
 
-__device__ __forceinline__ void lds_push(PushBuf& q, bool pred, uint32_t cell, uint32_t pos) {
+template <typename Q>
+__device__ __forceinline__ void lds_push(Q& q, bool pred, uint32_t cell, uint32_t pos) {
     const uint64_t m = __ballot(pred);
     if (m == 0) return;
     const uint32_t lane = lane_id();
@@ -289,12 +290,13 @@ __device__ __forceinline__ void lds_push(PushBuf& q, bool pred, uint32_t cell, u
 // Called by every lane of the workgroup with the same arguments.  Appends the
 // staged pairs to the global queue if `force` or if the buffer could not take
 // another `room` pushes.
-__device__ void flush_pushes(PushBuf& q, bool force, uint32_t room, unsigned int* tail,
+template <typename Q>
+__device__ void flush_pushes(Q& q, bool force, uint32_t room, unsigned int* tail,
                              uint2* queue, uint32_t cells) {
     __syncthreads();
     const uint32_t n = q.count;
     __syncthreads();  // every lane has read n before any lane pushes again
-    if (n == 0 || (!force && n + room <= kPushCap)) return;
+    if (n == 0 || (!force && n + room <= Q::kCap)) return;
     if (threadIdx.x == 0) q.base = atomicAdd(tail, n);
     __syncthreads();
     const uint32_t base = q.base;
@@ -325,19 +327,31 @@ struct CounterArgs {
 // every (batch b, hash j) in the row's plan entry list, the parameter
 // t = (k - bias_j(b)) mod c of batch b: if its bit is set it adds 2^32 + its
 // rank in the support.  Integer sums, so the result equals the atomic build
-// exactly whatever the order.  Each wave screens 64 entries at a time (one
-// lane each: is any member of the support in that batch?) and then visits
-// only the batches that have one: lanes 0..C/32-1 load the batch's bitmap
-// words and rank offsets, every lane takes the (at most two) words covering
-// its C/64 consecutive cells by shuffle, and adds into the row's counters in
-// LDS.  The row is then written once, and its pure cells
-// become the round-0 frontier.
+// exactly whatever the order.  Every step issues its global loads together,
+// so a row costs a few memory latencies however many batches land on it:
+//   screen  each lane takes one plan entry (kBlock at a time) and checks
+//           whether any member of the support lies in that batch; the live
+//           entries are compacted into an LDS list;
+//   stage   the bitmap words and rank offsets of up to kStage live batches
+//           are copied into LDS, all lanes loading at once;
+//   add     wave w takes staged batches w, w + 4, ...: each lane covers C/64
+//           consecutive cells, finds their parameters' bits in the staged
+//           words and adds into the row's counters in LDS.
+// The row is then written once, and its pure cells become the round-0
+// frontier.
+constexpr uint32_t kStage = 64;  // live batches staged in LDS at a time
+
 template <int C>
 __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
     constexpr uint32_t WPB = C / 32;  // bitmap words per batch
     constexpr uint32_t CPL = C / 64;  // cells per lane
+    constexpr uint32_t kWaves = kBlock / 64;
     __shared__ unsigned long long s_acc[C];
-    __shared__ PushBuf q;
+    __shared__ uint32_t s_word[kStage * WPB];
+    __shared__ uint32_t s_off[kStage * WPB];
+    __shared__ uint2 s_live[kBlock];
+    __shared__ uint32_t s_tmp[kWaves];
+    __shared__ PushBuf<C> q;
     const PlanHeader* hdr = a.hdr;
     const bool ok = hdr->magic == kPlanMagic && hdr->n == a.n && hdr->seed == a.seed &&
                     hdr->c == a.c && hdr->rows == a.rows;
@@ -348,14 +362,13 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
     if (a.ctrl->overflow) return;
     const uint32_t lane = lane_id();
     const uint32_t wave = threadIdx.x >> 6;
-    constexpr uint32_t kWaves = kBlock / 64;
     if (threadIdx.x == 0) q.count = 0;
     for (uint32_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
         for (uint32_t k = threadIdx.x; k < C; k += kBlock) s_acc[k] = 0ull;
-        __syncthreads();
         const uint32_t e0 = a.rowoff[row], e1 = a.rowoff[row + 1];
-        for (uint32_t base = e0 + wave * 64u; base < e1; base += kWaves * 64u) {
-            const uint32_t e = base + lane;
+        for (uint32_t base = e0; base < e1; base += kBlock) {
+            // screen
+            const uint32_t e = base + threadIdx.x;
             uint2 ent = make_uint2(0xffffffffu, 0u);
             bool live = false;
             if (e < e1) {
@@ -366,37 +379,47 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
                     live = a.woff[we] != a.woff[ws];
                 }
             }
-            uint64_t m = __ballot(live);
-            while (m) {
-                const uint32_t src = (uint32_t)__ffsll((unsigned long long)m) - 1u;
-                m &= m - 1ull;
-                const uint32_t bidx = __shfl(ent.x, src);
-                const uint32_t bias = __shfl(ent.y, src) & 0xffffu;
-                const uint64_t ws = (uint64_t)bidx * WPB;
-                uint32_t myword = 0, myoff = 0;
-                if (lane < WPB && ws + lane < a.words) {
-                    myword = load_word(a.b, ws + lane, a.words, a.last_mask);
-                    myoff = a.woff[ws + lane];
+            uint32_t nlive;
+            const uint32_t slot = block_exclusive_scan(live ? 1u : 0u, s_tmp, &nlive);
+            if (live) s_live[slot] = ent;
+            __syncthreads();
+            for (uint32_t g0 = 0; g0 < nlive; g0 += kStage) {
+                const uint32_t ng = nlive - g0 < kStage ? nlive - g0 : kStage;
+                // stage
+                for (uint32_t k = threadIdx.x; k < ng * WPB; k += kBlock) {
+                    const uint64_t w = (uint64_t)s_live[g0 + k / WPB].x * WPB + (k % WPB);
+                    uint32_t word = 0, off = 0;
+                    if (w < a.words) {
+                        word = load_word(a.b, w, a.words, a.last_mask);
+                        off = a.woff[w];
+                    }
+                    s_word[k] = word;
+                    s_off[k] = off;
                 }
-                const uint32_t t0 = (lane * CPL - bias) & (C - 1u);
-                const uint32_t wa = t0 >> 5, wb = ((t0 + CPL - 1u) & (C - 1u)) >> 5;
-                const uint32_t word_a = __shfl(myword, wa), off_a = __shfl(myoff, wa);
-                const uint32_t word_b = __shfl(myword, wb), off_b = __shfl(myoff, wb);
+                __syncthreads();
+                // add
+                for (uint32_t g = wave; g < ng; g += kWaves) {
+                    const uint32_t bias = s_live[g0 + g].y & 0xffffu;
+                    const uint32_t t0 = (lane * CPL - bias) & (C - 1u);
+                    const uint32_t wa = t0 >> 5, wb = ((t0 + CPL - 1u) & (C - 1u)) >> 5;
+                    const uint32_t word_a = s_word[g * WPB + wa], off_a = s_off[g * WPB + wa];
+                    const uint32_t word_b = s_word[g * WPB + wb], off_b = s_off[g * WPB + wb];
 #pragma unroll
-                for (uint32_t i = 0; i < CPL; i++) {
-                    const uint32_t t = (t0 + i) & (C - 1u);
-                    const bool first = (t >> 5) == wa;
-                    const uint32_t word = first ? word_a : word_b;
-                    const uint32_t bit = t & 31u;
-                    if ((word >> bit) & 1u) {
-                        const uint32_t rank = (first ? off_a : off_b) +
-                                              __popc(word & ((1u << bit) - 1u));
-                        atomicAdd(&s_acc[lane * CPL + i], kOne + rank);
+                    for (uint32_t i = 0; i < CPL; i++) {
+                        const uint32_t t = (t0 + i) & (C - 1u);
+                        const bool first = (t >> 5) == wa;
+                        const uint32_t word = first ? word_a : word_b;
+                        const uint32_t bit = t & 31u;
+                        if ((word >> bit) & 1u) {
+                            const uint32_t rank = (first ? off_a : off_b) +
+                                                  __popc(word & ((1u << bit) - 1u));
+                            atomicAdd(&s_acc[lane * CPL + i], kOne + rank);
+                        }
                     }
                 }
+                __syncthreads();  // the staging buffers are reused
             }
         }
-        __syncthreads();
         for (uint32_t k = threadIdx.x; k < C; k += kBlock) {
             const unsigned long long acc = s_acc[k];
             const uint32_t cell = row * C + k;
@@ -490,7 +513,7 @@ __device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks) {
 
 template <typename T>
 __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
-    __shared__ PushBuf q;
+    __shared__ PushBuf<4 * kPeelBlock> q;
     __shared__ uint32_t s_red[2];
     Ctrl* ctrl = a.ctrl;
     PeelSync* sync = a.sync;
@@ -738,7 +761,7 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
         if (a.x_out != nullptr && p0 < a.n) {
             if (a.x_vec && p0 + 4 <= a.n) {
                 V4 v = {out[0], out[1], out[2], out[3]};
-                __builtin_nontemporal_store(v, reinterpret_cast<V4*>(a.x_out + p0));
+                *reinterpret_cast<V4*>(a.x_out + p0) = v;
             } else {
                 for (int k = 0; k < 4; k++)
                     if (p0 + k < a.n) a.x_out[p0 + k] = out[k];
