@@ -52,6 +52,10 @@ def parse():
     ap.add_argument("--block-rows", type=int, default=None,
                     help="rows per block of the blocked sketch (default: the library's choice "
                          "for this device, hc_geometry_blocked with block_rows = 0)")
+    ap.add_argument("--encode", default="atomic", choices=["atomic", "gather"],
+                    help="atomic: hc_encode (each nonzero adds into its cells); gather: "
+                         "hc_encode_gather (each sketch row assembled through the plan; "
+                         "global sketch, bitmap index, c >= 256)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", nargs="?", const="bert", choices=["bert", "compressed"],
                     help="bert: BERT-base density/overlap grid and sketch-width sweep; "
@@ -192,9 +196,10 @@ class Runner:
         self.out = torch.empty(w.n, dtype=self.vt, device=dev)
         self.mask = torch.empty((w.n + 31) // 32, dtype=torch.int32, device=dev)
 
-    def run(self, ratio, steps, warmup, check=True, block_rows=None, bloom=False):
+    def run(self, ratio, steps, warmup, check=True, block_rows=None, bloom=False, gather=False):
         """block_rows: None for the global sketch, else the rows per block of
-        a blocked sketch; bloom: a Bloom-filter index instead of the bitmap."""
+        a blocked sketch; bloom: a Bloom-filter index instead of the bitmap;
+        gather: encode row by row through the plan (hc_encode_gather)."""
         import paper_2402_07529_amd as hc
         torch, w, dev, W = self.torch, self.w, self.dev, self.w.W
         max_support = self.n_agg
@@ -228,7 +233,10 @@ class Runner:
             if ev is not None:
                 ev[0].record(stream)
             for i in range(W):
-                hc.hc_encode(p, x[i], Y[i], B[i], stream)
+                if gather:
+                    hc.hc_encode_gather(p, plan, x[i], Y[i], B[i], stream)
+                else:
+                    hc.hc_encode(p, x[i], Y[i], B[i], stream)
             if ev is not None:
                 ev[1].record(stream)
             hc.hc_aggregate(p, Y, B, W, Ya, Ba, stream)
@@ -292,7 +300,10 @@ def sweep_compressed(a, dev):
     absx = x[nz].abs()
     points = []
     for frac in COMPRESSED_SIZES:
-        m = r.run(frac * w.n / r.n_agg, 3, 1, check=False)
+        # the atomic encode first, for its time alone; then the timed run with
+        # the encode gathered through the plan, which suits a dense gradient
+        atomic_ms = r.run(frac * w.n / r.n_agg, 3, 1, check=False)["enc_ms"]
+        m = r.run(frac * w.n / r.n_agg, 3, 1, check=False, gather=True)
         inf = m["info"]
         err = ((r.out.double()[nz] - x[nz]).abs() / absx).mean().item()
         t = m["enc_ms"] + m["dec_ms"]  # W = 1: the aggregate of one sketch is a copy
@@ -301,7 +312,8 @@ def sweep_compressed(a, dev):
                   avg_relative_error=err,
                   recovery_rate=round(inf.n_recovered / max(inf.n_support, 1), 6),
                   recovery_iterations=inf.rounds, success=inf.success,
-                  encode_ms=round(m["enc_ms"], 4), decode_ms=round(m["dec_ms"], 4),
+                  encode_ms=round(m["enc_ms"], 4), encode_atomic_ms=round(atomic_ms, 4),
+                  decode_ms=round(m["dec_ms"], 4),
                   compress_decompress_gbs=round(4 * w.n / (t * 1e-3) / 1e9, 2))
         log(f"[sweep] {pt}")
         points.append(pt)
@@ -380,7 +392,13 @@ def main():
     if a.index == "bloom" and a.blocked:
         print("bench.py: the Bloom-filter index needs the global sketch", file=sys.stderr)
         sys.exit(2)
-    m = r.run(ratio, a.steps, a.warmup, block_rows=block_rows, bloom=a.index == "bloom")
+    gather = a.encode == "gather"
+    if gather and (a.blocked or a.index == "bloom" or a.c < 256):
+        print("bench.py: --encode gather needs the global sketch, the bitmap index and c >= 256",
+              file=sys.stderr)
+        sys.exit(2)
+    m = r.run(ratio, a.steps, a.warmup, block_rows=block_rows, bloom=a.index == "bloom",
+              gather=gather)
     p, inf, W, n_agg = m["p"], m["info"], w.W, r.n_agg
     ms, enc_ms, agg_ms, dec_ms = m["ms"], m["enc_ms"], m["agg_ms"], m["dec_ms"]
     cells = p.cells
@@ -401,13 +419,15 @@ def main():
                               f"{p.nblocks} blocks") if a.blocked else "global",
                    "index": (f"bloom: {int(p.bloom_k)} hashes, {4 * p.index_words} bytes"
                              if a.index == "bloom" else "bitmap"),
+                   "encode": a.encode,
                    **{k: v for k, v in w.params.items() if k in ("density", "overlap", "rows_per_worker")}},
         "roofline": {"bound": "hbm",
                      "kernel": ("hc_encode (blocked LDS encode)" if a.blocked
+                                else "hc_encode_gather (rows through the plan)" if gather
                                 else "hc_encode (Y clear + dense encode)"),
                      "achieved": round(enc_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(enc_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": (None if a.blocked or a.index == "bloom"
+                     "traffic": (None if a.blocked or a.index == "bloom" or gather
                                  else measured_traffic(w.name, w.vtype)),
                      "bytes_per_launch": enc_b, "avg_launch_ms": round(enc_ms, 4)},
         "hbm_frac_iteration": round(iter_b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),

@@ -8,6 +8,8 @@
  * aggregation API; this library exposes one call per stage:
  *
  *   hc_encode / hc_encode_coo   Algorithm 1, phase I (sections 3.1, 3.2, 3.4)
+ *   hc_encode_gather            the same for dense gradients, row by row
+ *                               through a plan
  *   hc_aggregate                what the aggregation API does between the
  *                               phases: Y <- sum Y, B <- OR B (section 3)
  *   hc_decode                   Algorithm 1, phase II (section 3.2 peeling,
@@ -15,7 +17,8 @@
  *   hc_geometry / hc_sizes      sketch sizing, |Y| >= gamma * n (section 3.2)
  *   hc_geometry_bloom           the same with a Bloom-filter index (section 3.3)
  *   hc_plan_bytes / _build      the inverse row map of a geometry (section 3.4
- *                               batching), built once, used by the decode
+ *                               batching), built once, used by the decode and
+ *                               by hc_encode_gather
  *
  * Conventions for every call:
  *   - Buffer pointers are DEVICE pointers unless marked "host".  The caller
@@ -214,6 +217,23 @@ hc_status hc_plan_build(const hc_params *p, void *plan, size_t plan_bytes, hipSt
  * rounding order is not fixed. */
 hc_status hc_encode(const hc_params *p, const void *x, void *y, uint32_t *b,
                     hipStream_t stream);
+
+/* Phase I on a dense gradient, assembled row by row through a plan: the
+ * same outputs as hc_encode with a bitmap index (int32 bit-identical; fp32
+ * summed in another order).  hc_encode adds each nonzero into its three cells
+ * (section 3.1) with scattered atomics, which bound it when most parameters
+ * are nonzero, as in section 4.1's microbenchmark.  Here one workgroup per
+ * sketch row reads every batch that lands on the row (section 3.4: a batch
+ * lands on one whole row per hash, rotated) and sums the row in LDS: 12n
+ * bytes of reads whatever the density, no global atomics.  Unblocked sketch,
+ * bitmap index, c >= 256 (HC_EUNSUPPORTED otherwise).  plan: built by
+ * hc_plan_build for the same params, 256-byte aligned (HC_EINVAL), plan_bytes
+ * at least hc_plan_bytes (HC_EWORKSPACE).  A plan built for other params is
+ * detected on the device from its header: the call then writes a zero sketch
+ * and an all-ones bitmap, which a decode reports as a failure (success = 0)
+ * rather than as a gradient. */
+hc_status hc_encode_gather(const hc_params *p, const void *plan, size_t plan_bytes,
+                           const void *x, void *y, uint32_t *b, hipStream_t stream);
 
 /* Phase I on COO input: idx[nnz] (uint32, each < n, any order) and
  * val[nnz].  Zero values are skipped; repeated indices are summed.  Same

@@ -33,8 +33,8 @@ GAMMA = 1.23
 INFO_BYTES = 32
 
 EXPORTS = ("hc_geometry", "hc_geometry_blocked", "hc_geometry_bloom", "hc_sizes", "hc_plan_bytes",
-           "hc_plan_build", "hc_encode", "hc_encode_coo", "hc_aggregate", "hc_decode",
-           "hc_status_string", "hc_last_error")
+           "hc_plan_build", "hc_encode", "hc_encode_gather", "hc_encode_coo", "hc_aggregate",
+           "hc_decode", "hc_status_string", "hc_last_error")
 
 
 class HCError(RuntimeError):
@@ -98,6 +98,7 @@ _lib.hc_geometry_bloom.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_do
 _lib.hc_sizes.argtypes = [_PP, ctypes.c_uint64, ctypes.POINTER(ctypes.c_size_t),
                           ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)]
 _lib.hc_encode.argtypes = [_PP, _P, _P, _P, _P]
+_lib.hc_encode_gather.argtypes = [_PP, _P, ctypes.c_size_t, _P, _P, _P, _P]
 _lib.hc_encode_coo.argtypes = [_PP, _P, _P, ctypes.c_uint64, _P, _P, _P]
 _lib.hc_aggregate.argtypes = [_PP, _P, _P, ctypes.c_uint32, _P, _P, _P]
 _lib.hc_decode.argtypes = [_PP, _P, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, ctypes.c_uint64,
@@ -105,7 +106,8 @@ _lib.hc_decode.argtypes = [_PP, _P, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P,
 _lib.hc_plan_bytes.argtypes = [_PP, ctypes.POINTER(ctypes.c_size_t)]
 _lib.hc_plan_build.argtypes = [_PP, _P, ctypes.c_size_t, _P]
 for _f in ("hc_geometry", "hc_geometry_blocked", "hc_geometry_bloom", "hc_sizes", "hc_plan_bytes",
-           "hc_plan_build", "hc_encode", "hc_encode_coo", "hc_aggregate", "hc_decode"):
+           "hc_plan_build", "hc_encode", "hc_encode_gather", "hc_encode_coo", "hc_aggregate",
+           "hc_decode"):
     getattr(_lib, _f).restype = ctypes.c_int
 _lib.hc_status_string.argtypes = [ctypes.c_int]
 _lib.hc_status_string.restype = ctypes.c_char_p
@@ -203,6 +205,15 @@ def hc_encode(p: hc_params, x, y, b, stream=None):
     _check(_lib.hc_encode(ctypes.byref(p), _ptr(x, "x", _vdtypes(p), p.n),
                           _ptr(y, "y", _vdtypes(p), p.cells),
                           _ptr(b, "b", _u32(), p.index_words), _stream(stream)), "hc_encode")
+
+
+def hc_encode_gather(p: hc_params, plan, x, y, b, stream=None):
+    import torch
+    _check(_lib.hc_encode_gather(ctypes.byref(p), _ptr(plan, "plan", (torch.uint8,)), plan.numel(),
+                                 _ptr(x, "x", _vdtypes(p), p.n),
+                                 _ptr(y, "y", _vdtypes(p), p.cells),
+                                 _ptr(b, "b", _u32(), p.index_words), _stream(stream)),
+           "hc_encode_gather")
 
 
 def hc_encode_coo(p: hc_params, idx, val, y, b, stream=None):

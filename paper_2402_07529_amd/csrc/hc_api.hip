@@ -336,6 +336,24 @@ hc_status hc_encode(const hc_params* p, const void* x, void* y, uint32_t* b, hip
     return e == hipSuccess ? HC_OK : fail_hip(e, "hc_encode");
 }
 
+hc_status hc_encode_gather(const hc_params* p, const void* plan, size_t plan_bytes, const void* x,
+                           void* y, uint32_t* b, hipStream_t stream) {
+    g_last_error.clear();
+    Geo g;
+    const hc_status s = to_geo(p, &g);
+    if (s != HC_OK) return s;
+    if (g.block) return fail(HC_EUNSUPPORTED, "a blocked sketch is encoded by hc_encode");
+    if (g.bloom_k) return fail(HC_EUNSUPPORTED, "the gathered encode writes a bitmap index");
+    if (!plan_supported(g)) return fail(HC_EUNSUPPORTED, "plans need c >= 256");
+    if (!plan || !aligned(plan, 256)) return fail(HC_EINVAL, "plan must be non-NULL and 256-byte aligned");
+    if (plan_bytes < plan_layout(g).total) return fail(HC_EWORKSPACE, "plan smaller than hc_plan_bytes reports");
+    if (!x || !y || !b) return fail(HC_EINVAL, "x, y and b must be non-NULL");
+    if (!aligned(x, 4) || !aligned(y, 4) || !aligned(b, 4))
+        return fail(HC_EINVAL, "x, y and b must be 4-byte aligned");
+    const hipError_t e = launch_encode_gather(g, plan, x, y, b, stream);
+    return e == hipSuccess ? HC_OK : fail_hip(e, "hc_encode_gather");
+}
+
 hc_status hc_encode_coo(const hc_params* p, const uint32_t* idx, const void* val, uint64_t nnz,
                         void* y, uint32_t* b, hipStream_t stream) {
     g_last_error.clear();

@@ -124,10 +124,10 @@ __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* s_tmp) {
     const uint32_t lane = lane_id(), wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
     v = wave_sum_u32(v);
     if (lane == 0) s_tmp[wave] = v;
-    __syncthreads();
+    lds_barrier();
     uint32_t t = 0;
     for (uint32_t w = 0; w < nwaves; w++) t += s_tmp[w];
-    __syncthreads();
+    lds_barrier();
     return t;
 }
 
@@ -140,14 +140,14 @@ __device__ __forceinline__ uint32_t block_scan(uint32_t v, uint32_t* s_tmp, uint
         if (lane >= (uint32_t)d) x += y;
     }
     if (lane == 63) s_tmp[wave] = x;
-    __syncthreads();
+    lds_barrier();
     uint32_t off = 0, tot = 0;
     for (uint32_t w = 0; w < nwaves; w++) {
         const uint32_t s = s_tmp[w];
         if (w < wave) off += s;
         tot += s;
     }
-    __syncthreads();
+    lds_barrier();
     *total = tot;
     return off + x - v;
 }
@@ -204,7 +204,7 @@ __global__ __launch_bounds__(kEncThreads, PF ? 4 : 8) void encode_blocked_kernel
     const BlockRange r = block_range(q, a.block, a.log2c, a.cmask, a.n);
     for (uint32_t i = threadIdx.x; i < a.bcells; i += kEncThreads) s_y[i] = T(0);
     fill_table(s_tab, r, a.seed, a.brows, a.c, a.cmask, a.log2c, a.block);
-    __syncthreads();
+    lds_barrier();
 
     const uint32_t lane = lane_id();
     const uint32_t wave = uniform(threadIdx.x >> 6);
@@ -331,7 +331,7 @@ __global__ __launch_bounds__(kEncThreads, PF ? 4 : 8) void encode_blocked_kernel
         load_part(tile, ea);
         encode_tile(tile, ea);
     }
-    __syncthreads();
+    lds_barrier();
 
     if (a.stage_b) {
         // the block's bitmap in one coalesced pass: a global store inside the
@@ -480,7 +480,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
     }
     fill_table(s_tab, r, a.seed, a.brows, a.c, cmask, a.log2c, a.block);
     if (tid < 4) s_tmp[48 + tid] = 0u;
-    __syncthreads();
+    lds_barrier();
 
     // counters from the bitmap.  Wave w takes a contiguous range of groups of
     // 64 words (the output pass below takes the same range, so the support
@@ -520,7 +520,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
     }
     const uint32_t wave_support = wave_sum_u32(lane_support);
     if (lane == 0) s_tmp[32 + wave] = wave_support;
-    __syncthreads();
+    lds_barrier();
 
     // round-0 frontier: every cell of degree one, appended to the queue (one
     // LDS atomic per wave and step)
@@ -535,7 +535,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
         base = (uint32_t)__builtin_amdgcn_readlane((int)base, (int)leader);
         if (pure) s_q[base + lanes_below(m)] = (uint16_t)i;
     }
-    __syncthreads();
+    lds_barrier();
 
     // synchronous peeling rounds (section 3.2).  The frontier of a round is
     // the queue segment [qs, qe): the cells that became pure in the previous
@@ -560,7 +560,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
         }
         const bool wave_claims = __ballot(claims != 0u) != 0ull;  // every lane takes part
         if (lane == 0 && wave_claims) s_any[rounds & 1u] = 1u;
-        __syncthreads();
+        lds_barrier();
         if (s_any[rounds & 1u] == 0u) break;
         if (tid == 0) s_any[(rounds + 1u) & 1u] = 0u;
         rounds++;
@@ -583,7 +583,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
             }
             s_cnt[cell] = kClaimed | bl;  // keeps g_j * x in s_val[cell]
         }
-        __syncthreads();
+        lds_barrier();
         qs = qe;
         qe = *s_tail;
     }

@@ -106,14 +106,14 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
         if (lane >= (uint32_t)d) x += y;
     }
     if (lane == 63) s_tmp[wave] = x;
-    __syncthreads();
+    lds_barrier();
     uint32_t off = 0, tot = 0;
     for (uint32_t w = 0; w < nwaves; w++) {
         const uint32_t s = s_tmp[w];
         if (w < wave) off += s;
         tot += s;
     }
-    __syncthreads();
+    lds_barrier();
     *total = tot;
     return off + x - v;
 }
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const uint32_t* __restric
     for (int k = 0; k < 4; k++) c += __popc(load_word(b, w0 + k, words, last_mask));
     c = wave_sum(c);
     if (lane_id() == 0) s_tmp[threadIdx.x >> 6] = c;
-    __syncthreads();
+    lds_barrier();
     if (threadIdx.x == 0) {
         uint32_t t = 0;
         for (int w = 0; w < kBlock / 64; w++) t += s_tmp[w];
@@ -293,18 +293,18 @@ __device__ __forceinline__ void lds_push(Q& q, bool pred, uint32_t cell, uint32_
 template <typename Q>
 __device__ void flush_pushes(Q& q, bool force, uint32_t room, unsigned int* tail,
                              uint2* queue, uint32_t cells) {
-    __syncthreads();
+    lds_barrier();
     const uint32_t n = q.count;
-    __syncthreads();  // every lane has read n before any lane pushes again
+    lds_barrier();  // every lane has read n before any lane pushes again
     if (n == 0 || (!force && n + room <= Q::kCap)) return;
     if (threadIdx.x == 0) q.base = atomicAdd(tail, n);
-    __syncthreads();
+    lds_barrier();
     const uint32_t base = q.base;
     for (uint32_t k = threadIdx.x; k < n; k += blockDim.x)
         if (base + k < cells) queue[base + k] = q.item[k];  // a cell is pushed at most once
-    __syncthreads();
+    lds_barrier();
     if (threadIdx.x == 0) q.count = 0;
-    __syncthreads();
+    lds_barrier();
 }
 
 // ---- counters by row (planned path) --------------------------------------------
@@ -382,7 +382,7 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
             uint32_t nlive;
             const uint32_t slot = block_exclusive_scan(live ? 1u : 0u, s_tmp, &nlive);
             if (live) s_live[slot] = ent;
-            __syncthreads();
+            lds_barrier();
             for (uint32_t g0 = 0; g0 < nlive; g0 += kStage) {
                 const uint32_t ng = nlive - g0 < kStage ? nlive - g0 : kStage;
                 // stage
@@ -396,7 +396,7 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
                     s_word[k] = word;
                     s_off[k] = off;
                 }
-                __syncthreads();
+                lds_barrier();
                 // add
                 for (uint32_t g = wave; g < ng; g += kWaves) {
                     const uint32_t bias = s_live[g0 + g].y & 0xffffu;
@@ -417,7 +417,7 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
                         }
                     }
                 }
-                __syncthreads();  // the staging buffers are reused
+                lds_barrier();  // the staging buffers are reused
             }
         }
         for (uint32_t k = threadIdx.x; k < C; k += kBlock) {
@@ -471,7 +471,7 @@ __device__ __forceinline__ uint32_t add_agent(unsigned int* p, uint32_t v) {
 
 __device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks) {
     __shared__ uint32_t s_ok;
-    __syncthreads();
+    lds_barrier();
     if (threadIdx.x == 0) {
         uint32_t ok = 1;
         const uint32_t groups = nblocks < kBarGroups ? nblocks : kBarGroups;
@@ -507,7 +507,7 @@ __device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks) {
         if (ld_agent(&ctrl->abort)) ok = 0;
         s_ok = ok;
     }
-    __syncthreads();
+    lds_barrier();
     return s_ok != 0;
 }
 
@@ -533,7 +533,7 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
         s_red[0] = 0;
         s_red[1] = 0;
     }
-    __syncthreads();
+    lds_barrier();
 
     if (!skip) {
         const uint32_t nsup = (uint32_t)ctrl->n_support;
@@ -641,7 +641,7 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
         atomicAdd(&s_red[0], my_recovered);
         atomicMax(&s_red[1], wmax);
     }
-    __syncthreads();
+    lds_barrier();
     if (threadIdx.x == 0) {
         if (s_red[0]) atomicAdd(&ctrl->recovered, (unsigned long long)s_red[0]);
         if (s_red[1]) atomicMax(&ctrl->rounds, s_red[1]);
@@ -724,7 +724,7 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
         s_pref[4 * threadIdx.x + k] = run;
         run += __popc(w4[k]);
     }
-    __syncthreads();
+    lds_barrier();
     const uint64_t off = a.blk[chunk];
     // with no valid element list (support over capacity, or a plan for
     // another geometry) every member gets the estimate from the aggregate

@@ -284,6 +284,17 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
                                      __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
+// Workgroup barrier that first waits for all of this wave's LDS operations,
+// atomics without a return value included.  hipcc does not always emit that
+// wait before s_barrier after such atomics (seen on gfx950: a loop of LDS
+// float adds followed directly by the barrier), and another wave could then
+// read a cell before an add to it has landed.  s_waitcnt 0xc07f is
+// lgkmcnt(0) with the vector-memory and export counters left alone.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __syncthreads();
+}
+
 __device__ __forceinline__ uint32_t uniform(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
 }

@@ -286,6 +286,146 @@ hipError_t launch_dense_t(const Geo& g, const void* x, void* y, uint32_t* b, hip
     return hipGetLastError();
 }
 
+
+// ---- gathered encode (through the plan) ------------------------------------------
+//
+// One workgroup per sketch row (grid-stride) assembles the row in LDS from the
+// plan's list of (batch, hash) pairs landing on it: each wave takes one pair at
+// a time, reads the batch's c values (coalesced 16-byte loads, C/256 per lane)
+// and adds g_j * x_t into cell (t + bias_j) mod c of the row.  Within one pair
+// the cells are a rotation, so the LDS adds of a wave never collide; waves
+// working on different pairs of the row meet only through LDS atomics.  The
+// pair with j = 0 of each batch (there is exactly one) also writes the batch's
+// bitmap words, all of them, from the same loads.  Every batch is read once per
+// hash, 12n bytes in all whatever the density, and no global atomics are used.
+template <typename T>
+struct GatherArgs {
+    const PlanHeader* hdr;
+    const uint32_t* rowoff;
+    const uint2* entry;
+    const T* x;
+    T* y;
+    uint32_t* b;
+    uint64_t n, seed, words;
+    uint32_t rows;
+    bool vec;  // x is 16-byte aligned
+};
+
+template <typename T, int C>
+__global__ __launch_bounds__(kBlock) void encode_gather_kernel(GatherArgs<T> a) {
+    typedef typename Vec4<T>::type V;
+    constexpr uint32_t NV = C / 256;  // 16-byte loads per lane per batch
+    constexpr uint32_t WPB = C / 32;  // bitmap words per batch
+    constexpr uint32_t kWaves = kBlock / 64;
+    __shared__ T s_acc[C];
+    const PlanHeader* hdr = a.hdr;
+    const bool ok = hdr->magic == kPlanMagic && hdr->n == a.n && hdr->seed == a.seed &&
+                    hdr->c == (uint32_t)C && hdr->rows == a.rows;
+    if (!ok) {
+        // a plan of another geometry: a zero sketch and an all-ones bitmap,
+        // which no decode can mistake for a gradient
+        const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+        const uint64_t cells = (uint64_t)a.rows * C;
+        for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < cells; i += stride)
+            a.y[i] = T(0);
+        for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < a.words; i += stride)
+            a.b[i] = 0xffffffffu;
+        return;
+    }
+    const uint32_t lane = lane_id();
+    const uint32_t wave = uniform(threadIdx.x >> 6);
+    for (uint32_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
+        for (uint32_t k = threadIdx.x; k < (uint32_t)C; k += kBlock) s_acc[k] = T(0);
+        lds_barrier();
+        const uint32_t e0 = a.rowoff[row], e1 = a.rowoff[row + 1];
+        for (uint32_t e = e0 + wave; e < e1; e += kWaves) {
+            const uint2 ent = a.entry[e];
+            const uint32_t bias = ent.y & 0xffffu, j = (ent.y >> 16) & 3u;
+            const bool neg = (ent.y >> 31) != 0u;
+            const uint64_t base = (uint64_t)ent.x * C;
+            // value t = 256 u + 4 lane + k of the batch is v[u][k]
+            T v[NV][4];
+            if (a.vec && base + C <= a.n) {
+                const V* src = reinterpret_cast<const V*>(a.x + base) + lane;
+#pragma unroll
+                for (uint32_t u = 0; u < NV; u++) {
+                    const V q = __builtin_nontemporal_load(src + 64 * u);
+                    v[u][0] = q.x;
+                    v[u][1] = q.y;
+                    v[u][2] = q.z;
+                    v[u][3] = q.w;
+                }
+            } else {
+#pragma unroll
+                for (uint32_t u = 0; u < NV; u++)
+#pragma unroll
+                    for (uint32_t k = 0; k < 4; k++) {
+                        const uint64_t p = base + 256u * u + 4u * lane + k;
+                        v[u][k] = p < a.n ? a.x[p] : T(0);
+                    }
+            }
+            if (j == 0u) {
+                // word w of the batch holds t = 32 w .. 32 w + 31: lanes
+                // 8 (w mod 8) .. + 7 of load w / 8, parameter 4 lane' + k at
+                // bit 4 (lane' - 8 (w mod 8)) + k
+                uint64_t m[NV][4];
+#pragma unroll
+                for (uint32_t u = 0; u < NV; u++)
+#pragma unroll
+                    for (uint32_t k = 0; k < 4; k++) m[u][k] = __ballot(Val<T>::nonzero(v[u][k]));
+                if (lane < WPB) {
+                    const uint32_t u = lane >> 3, sh = 8u * (lane & 7u);
+                    uint32_t word = 0;
+#pragma unroll
+                    for (uint32_t k = 0; k < 4; k++) {
+                        uint64_t mk = m[0][k];
+#pragma unroll
+                        for (uint32_t uu = 1; uu < NV; uu++)
+                            if (u == uu) mk = m[uu][k];
+                        word |= spread4((uint32_t)(mk >> sh)) << k;
+                    }
+                    const uint64_t widx = (uint64_t)ent.x * WPB + lane;
+                    if (widx < a.words) a.b[widx] = word;
+                }
+            }
+#pragma unroll
+            for (uint32_t u = 0; u < NV; u++)
+#pragma unroll
+                for (uint32_t k = 0; k < 4; k++) {
+                    if (!Val<T>::nonzero(v[u][k])) continue;
+                    const uint32_t t = 256u * u + 4u * lane + k;
+                    const T add = Val<T>::sign(v[u][k], neg);
+                    atomicAdd(&s_acc[(t + bias) & (uint32_t)(C - 1)], add);
+                }
+        }
+        lds_barrier();
+        T* dst = a.y + (uint64_t)row * C;
+        for (uint32_t k = threadIdx.x; k < (uint32_t)C; k += kBlock) dst[k] = s_acc[k];
+    }
+}
+
+template <typename T, int C>
+hipError_t launch_gather_t(const Geo& g, const void* plan, const void* x, void* y, uint32_t* b,
+                           hipStream_t s, int cus) {
+    const PlanLayout L = plan_layout(g);
+    const char* base = static_cast<const char*>(plan);
+    GatherArgs<T> a;
+    a.hdr = reinterpret_cast<const PlanHeader*>(base + L.header);
+    a.rowoff = reinterpret_cast<const uint32_t*>(base + L.rowoff);
+    a.entry = reinterpret_cast<const uint2*>(base + L.entry);
+    a.x = static_cast<const T*>(x);
+    a.y = static_cast<T*>(y);
+    a.b = b;
+    a.n = g.n;
+    a.seed = g.seed;
+    a.words = g.words;
+    a.rows = g.rows;
+    a.vec = (reinterpret_cast<uintptr_t>(x) & 15u) == 0;
+    const uint32_t grid = g.rows < (uint32_t)cus * 8 ? g.rows : (uint32_t)cus * 8;
+    hipLaunchKernelGGL((encode_gather_kernel<T, C>), dim3(grid), dim3(kBlock), 0, s, a);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_fill2_u32(uint32_t* p, uint64_t count, uint32_t* p2, uint64_t count2,
@@ -337,6 +477,22 @@ hipError_t launch_encode_dense(const Geo& g, const void* x, void* y, uint32_t* b
     if (mode == 0) return launch_dense_t<int32_t, 0, false>(g, x, y, b, s, ntiles, di.cus);
     if (mode == 1) return launch_dense_t<int32_t, 1, false>(g, x, y, b, s, ntiles, di.cus);
     return launch_dense_t<int32_t, 2, false>(g, x, y, b, s, ntiles, di.cus);
+}
+
+
+hipError_t launch_encode_gather(const Geo& g, const void* plan, const void* x, void* y,
+                                uint32_t* b, hipStream_t s) {
+    DeviceInfo di;
+    hipError_t e = device_info(&di);
+    if (e != hipSuccess) return e;
+    if (g.f32) {
+        if (g.c == 1024) return launch_gather_t<float, 1024>(g, plan, x, y, b, s, di.cus);
+        if (g.c == 512) return launch_gather_t<float, 512>(g, plan, x, y, b, s, di.cus);
+        return launch_gather_t<float, 256>(g, plan, x, y, b, s, di.cus);
+    }
+    if (g.c == 1024) return launch_gather_t<int32_t, 1024>(g, plan, x, y, b, s, di.cus);
+    if (g.c == 512) return launch_gather_t<int32_t, 512>(g, plan, x, y, b, s, di.cus);
+    return launch_gather_t<int32_t, 256>(g, plan, x, y, b, s, di.cus);
 }
 
 hipError_t launch_encode_coo(const Geo& g, const uint32_t* idx, const void* val, uint64_t nnz,

@@ -48,6 +48,10 @@ hipError_t launch_encode_dense(const Geo& g, const void* x, void* y, uint32_t* b
                                hipStream_t s);
 hipError_t launch_encode_coo(const Geo& g, const uint32_t* idx, const void* val,
                              uint64_t nnz, void* y, uint32_t* b, hipStream_t s);
+// dense encode gathered row by row through a plan (c >= 256, bitmap index,
+// unblocked sketch)
+hipError_t launch_encode_gather(const Geo& g, const void* plan, const void* x, void* y,
+                                uint32_t* b, hipStream_t s);
 
 // aggregate
 hipError_t launch_aggregate(const Geo& g, const void* y_in, const uint32_t* b_in, uint32_t W,

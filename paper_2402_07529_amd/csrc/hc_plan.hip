@@ -56,14 +56,14 @@ __device__ __forceinline__ uint32_t block_scan_excl(uint32_t v, uint32_t* s_tmp,
         if (lane >= (uint32_t)d) x += y;
     }
     if (lane == 63) s_tmp[wave] = x;
-    __syncthreads();
+    lds_barrier();
     uint32_t off = 0, tot = 0;
     for (uint32_t w = 0; w < blockDim.x / 64; w++) {
         const uint32_t s = s_tmp[w];
         if (w < wave) off += s;
         tot += s;
     }
-    __syncthreads();
+    lds_barrier();
     *total = tot;
     return off + x - v;
 }

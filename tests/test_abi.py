@@ -190,3 +190,24 @@ def test_bloom_params_rejected():
     _, _, ws_bloom = hc.hc_sizes(q, 100)
     _, _, ws_bitmap = hc.hc_sizes(hc.make_params(10_000, 9, 1, c=64), 100)
     assert ws_bloom - ws_bitmap >= 4 * q.words
+
+
+def test_gather_encode_rejected_before_launch():
+    # hc_encode_gather: unblocked sketch, bitmap index, c >= 256, a 256-byte
+    # aligned plan of at least hc_plan_bytes
+    import paper_2402_07529_amd as hc
+    L = hc.lib()
+    V = ctypes.c_void_p
+    p = hc.hc_geometry(2_000_000, 20_000, 1.23, 1024, 3)
+    need = hc.hc_plan_bytes(p)
+    ok = (V(256), need, V(256), V(256), V(256), None)
+    assert L.hc_encode_gather(ctypes.byref(p), V(100), *ok[1:]) == hc.HC_EINVAL
+    assert L.hc_encode_gather(ctypes.byref(p), None, *ok[1:]) == hc.HC_EINVAL
+    assert L.hc_encode_gather(ctypes.byref(p), V(256), need - 1, *ok[2:]) == hc.HC_EWORKSPACE
+    assert L.hc_encode_gather(ctypes.byref(p), *ok[:2], None, V(256), V(256), None) == hc.HC_EINVAL
+    assert L.hc_encode_gather(ctypes.byref(p), *ok[:2], V(18), V(256), V(256), None) == hc.HC_EINVAL
+    for q in (hc.hc_geometry(2_000_000, 20_000, 1.23, 64, 3),                  # c < 256
+              hc.hc_geometry_blocked(109_482_240, 9_305_915, 1.3, 1024, 14, 3),  # blocked
+              hc.hc_geometry_bloom(2_000_000, 20_000, 1.23, 1024, 3)[0]):        # Bloom index
+        assert L.hc_encode_gather(ctypes.byref(q), *ok) == hc.HC_EUNSUPPORTED
+        assert L.hc_last_error()

@@ -85,8 +85,8 @@ def assert_same_info(gi, oi):
     assert gi.status == 0
 
 
-def check_int(w, rows, c, coo_input=False, use_plan=False):
-    g = gpu_run(w, rows, c, coo_input=coo_input, use_plan=use_plan)
+def check_int(w, rows, c, coo_input=False, use_plan=False, gather=False):
+    g = gpu_run(w, rows, c, coo_input=coo_input, use_plan=use_plan, gather=gather)
     o = oracle_run(w, rows, c)
     for i in range(w.W):
         assert np.array_equal(g["Y"][i], o["Y"][i]), f"worker {i} sketch"
@@ -185,14 +185,17 @@ def test_forced_failure_three_cells():
     assert g["info"].n_recovered == 0 and g["info"].rounds == 0
 
 
-def check_fp32(w, rows, c, use_plan=False):
-    g = gpu_run(w, rows, c, use_plan=use_plan)
+def check_fp32(w, rows, c, use_plan=False, gather=False):
+    g = gpu_run(w, rows, c, use_plan=use_plan, gather=gather)
     o = oracle_run(w, rows, c)
     wb, ab = fp32_cell_bounds(w, o["g"])
     for i in range(w.W):
         assert np.array_equal(g["B"][i], o["B"][i])
         err = np.abs(g["Y"][i].astype(np.float64) - o["Y"][i])
-        assert np.all(err <= wb[i] * (1 + 1e-6)), f"worker {i} sketch"
+        over = np.nonzero(err > wb[i] * (1 + 1e-6))[0]
+        assert over.size == 0, (f"worker {i} sketch: {over.size} cells over the bound, e.g. "
+                                f"{over[:4]} err {err[over[:4]]} bound {wb[i][over[:4]]} "
+                                f"gpu {g['Y'][i][over[:4]]} oracle {o['Y'][i][over[:4]]}")
     assert np.array_equal(g["Ba"], o["Ba"])
     assert np.all(np.abs(g["Ya"].astype(np.float64) - o["Ya"]) <= ab * (1 + 1e-6))
     assert np.array_equal(g["mask"], o["mask"])
