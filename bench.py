@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--vtype", default="i32", choices=["i32", "f32"])
     ap.add_argument("--density", type=float, default=None)
     ap.add_argument("--overlap", type=float, default=None)
+    ap.add_argument("--workers", type=int, default=None,
+                    help="simulated workers W (default: the configuration's)")
     ap.add_argument("--ratio", type=float, default=None,
                     help="sketch cells / aggregate nonzeros (default: gamma = 1.23)")
     ap.add_argument("--c", type=int, default=1024)
@@ -88,6 +90,8 @@ def make_workload(a):
         kw["density"] = a.density
     if a.overlap is not None:
         kw["overlap"] = a.overlap
+    if a.workers is not None:
+        kw["W"] = a.workers
     return wl.make(a.config, vtype=a.vtype, **kw)
 
 

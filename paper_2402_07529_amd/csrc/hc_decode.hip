@@ -24,11 +24,11 @@
 //            list of (cell, element) pairs whose cell became pure during round
 //            r-1, kept in one append-only queue.  An element owning several
 //            frontier cells is claimed by an atomic exchange on its flag: the
-//            first of its frontier entries to get there recovers x = g_j * Y
-//            from its cell (every pure cell of the element holds the same
-//            value, exactly so in integer arithmetic), and subtracts g * x and
-//            the element from its other two cells with atomics; a cell whose
-//            count drops to one joins the next frontier.  Entries whose element
+//            first of its frontier entries to get there recovers
+//            x = g_j * Y from its cell (every pure cell of the element holds the
+//            same value, exactly so in integer arithmetic), and subtracts g * x
+//            and the element from its other two cells with atomics; a cell
+//            whose count drops to one joins the next frontier.  Entries whose element
 //            is already taken (in this round or an earlier one) do nothing, so
 //            the elements peeled in round r are exactly those with a cell in
 //            its frontier that were still live when it began.
@@ -213,8 +213,12 @@ __global__ __launch_bounds__(1024) void scan_kernel(uint32_t* __restrict__ blk, 
     }
 }
 
-// Element list E (ascending), cleared peeled flags, and either the word rank
-// offsets (planned) or the per-cell counters by atomics (unplanned).
+// Element list E (ascending), cleared peeled flags, and either the word
+// rank offsets (planned) or the per-cell counters by atomics (unplanned).  The
+// chunk's words are taken kBlock at a time, one per lane: each lane writes the
+// parameters of its word's set bits into LDS at their rank, and the workgroup
+// then stores that run of E with consecutive lanes on consecutive elements (a
+// lane storing its own run would spread every wave store over 64 lines).
 __global__ __launch_bounds__(kBlock) void compact_kernel(
     const uint32_t* __restrict__ b, uint64_t words, uint32_t last_mask,
     const uint32_t* __restrict__ blk, uint32_t* __restrict__ elem, uint32_t* __restrict__ peeled,
@@ -222,42 +226,36 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(
     const Ctrl* __restrict__ ctrl, uint64_t seed, uint32_t rows, uint32_t c, uint32_t cmask,
     uint32_t log2c) {
     __shared__ uint32_t s_tmp[kBlock / 64];
+    __shared__ uint32_t s_p[kBlock * 32];
     if (ctrl->overflow) return;
-    const uint64_t w0 = (uint64_t)blockIdx.x * kChunkWords + 4ull * threadIdx.x;
-    uint32_t w4[4];
-    uint32_t mine = 0;
-#pragma unroll
-    for (int k = 0; k < 4; k++) {
-        w4[k] = load_word(b, w0 + k, words, last_mask);
-        mine += __popc(w4[k]);
-    }
-    uint32_t total;
-    uint32_t pos = blk[blockIdx.x] + block_exclusive_scan(mine, s_tmp, &total);
-    uint64_t cached_batch = ~0ull;
-    BatchHash h;
-#pragma unroll
-    for (int k = 0; k < 4; k++) {
-        if (woff != nullptr && w0 + k < words) woff[w0 + k] = pos;
-        uint32_t w = w4[k];
+    uint32_t base = blk[blockIdx.x];
+    for (uint32_t part = 0; part < kChunkWords / kBlock; part++) {
+        const uint64_t wi = (uint64_t)blockIdx.x * kChunkWords + part * kBlock + threadIdx.x;
+        const uint32_t word = load_word(b, wi, words, last_mask);
+        uint32_t total;
+        const uint32_t off = block_exclusive_scan(__popc(word), s_tmp, &total);
+        if (woff != nullptr && wi < words) woff[wi] = base + off;
+        uint32_t w = word, o = off;
         while (w) {
-            const uint32_t bit = __builtin_ctz(w);
+            s_p[o++] = (uint32_t)(wi * 32u) + (uint32_t)__builtin_ctz(w);
             w &= w - 1u;
-            const uint64_t p = (w0 + k) * 32ull + bit;
-            elem[pos] = (uint32_t)p;
-            peeled[pos] = 0;
+        }
+        lds_barrier();
+        for (uint32_t i = threadIdx.x; i < total; i += kBlock) {
+            const uint32_t p = s_p[i];
+            const uint32_t pos = base + i;
+            elem[pos] = p;
+            peeled[pos] = 0u;
             if (woff == nullptr) {
-                const uint64_t batch = p >> log2c;
-                if (batch != cached_batch) {
-                    h = batch_hash(seed, rows, cmask, batch);
-                    cached_batch = batch;
-                }
-                const uint32_t t = (uint32_t)p & cmask;
+                const BatchHash h = batch_hash(seed, rows, cmask, p >> log2c);
+                const uint32_t t = p & cmask;
                 const unsigned long long inc = kOne + pos;
 #pragma unroll
                 for (int j = 0; j < 3; j++) atomicAdd(cnt + cell_of(h, j, t, c, cmask), inc);
             }
-            pos++;
         }
+        lds_barrier();  // s_p is refilled by the next part
+        base += total;
     }
 }
 
@@ -340,6 +338,7 @@ struct CounterArgs {
 // The row is then written once, and its pure cells become the round-0
 // frontier.
 constexpr uint32_t kStage = 64;  // live batches staged in LDS at a time
+constexpr uint64_t kWaveRowsEntries = 8;  // plan entries per row up to which a wave takes a row
 
 template <int C>
 __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
@@ -430,6 +429,85 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
         flush_pushes(q, false, C, &a.sync->tail.v[0], a.queue, a.cells);
     }
     flush_pushes(q, true, 0, &a.sync->tail.v[0], a.queue, a.cells);
+}
+
+// Rows that few batches land on (a sketch much wider than the support): one
+// wave per row, no workgroup barriers.  Lane e screens entry e of the row; the
+// live batches are visited in turn: lanes 0..C/32-1 load the batch's bitmap
+// words and rank offsets, every lane takes the (at most two) words covering
+// its C/64 consecutive cells by shuffle and adds into its own cells of the
+// wave's copy of the row in LDS.  The row is written with plain stores and
+// nothing is queued: the peel kernel finds the round-0 frontier by scanning
+// the counters, which for such sketches costs less than one queue append per
+// row.
+template <int C>
+__global__ __launch_bounds__(kBlock) void counter_wave_kernel(CounterArgs a) {
+    constexpr uint32_t WPB = C / 32;  // bitmap words per batch
+    constexpr uint32_t CPL = C / 64;  // cells per lane
+    constexpr uint32_t kWaves = kBlock / 64;
+    __shared__ unsigned long long s_acc[kWaves * C];
+    const PlanHeader* hdr = a.hdr;
+    const bool ok = hdr->magic == kPlanMagic && hdr->n == a.n && hdr->seed == a.seed &&
+                    hdr->c == a.c && hdr->rows == a.rows;
+    if (!ok) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) a.ctrl->bad_plan = 1u;
+        return;
+    }
+    if (a.ctrl->overflow) return;
+    const uint32_t lane = lane_id();
+    const uint32_t wave = uniform(threadIdx.x >> 6);
+    unsigned long long* const acc = s_acc + wave * C;
+    const uint32_t nwaves = gridDim.x * kWaves;
+    for (uint32_t row = blockIdx.x * kWaves + wave; row < a.rows; row += nwaves) {
+#pragma unroll
+        for (uint32_t i = 0; i < CPL; i++) acc[lane * CPL + i] = 0ull;
+        const uint32_t e0 = a.rowoff[row], e1 = a.rowoff[row + 1];
+        for (uint32_t base = e0; base < e1; base += 64u) {
+            const uint32_t e = base + lane;
+            uint2 ent = make_uint2(0xffffffffu, 0u);
+            bool live = false;
+            if (e < e1) {
+                ent = a.entry[e];
+                if (ent.x < a.nb) {
+                    const uint64_t ws = (uint64_t)ent.x * WPB;
+                    const uint64_t we = ws + WPB < a.words ? ws + WPB : a.words;
+                    live = a.woff[we] != a.woff[ws];
+                }
+            }
+            uint64_t m = __ballot(live);
+            while (m) {
+                const uint32_t src = (uint32_t)__ffsll((unsigned long long)m) - 1u;
+                m &= m - 1ull;
+                const uint32_t bidx = __shfl(ent.x, src);
+                const uint32_t bias = __shfl(ent.y, src) & 0xffffu;
+                const uint64_t ws = (uint64_t)bidx * WPB;
+                uint32_t myword = 0, myoff = 0;
+                if (lane < WPB && ws + lane < a.words) {
+                    myword = load_word(a.b, ws + lane, a.words, a.last_mask);
+                    myoff = a.woff[ws + lane];
+                }
+                const uint32_t t0 = (lane * CPL - bias) & (C - 1u);
+                const uint32_t wa = t0 >> 5, wb = ((t0 + CPL - 1u) & (C - 1u)) >> 5;
+                const uint32_t word_a = __shfl(myword, wa), off_a = __shfl(myoff, wa);
+                const uint32_t word_b = __shfl(myword, wb), off_b = __shfl(myoff, wb);
+#pragma unroll
+                for (uint32_t i = 0; i < CPL; i++) {
+                    const uint32_t t = (t0 + i) & (C - 1u);
+                    const bool first = (t >> 5) == wa;
+                    const uint32_t word = first ? word_a : word_b;
+                    const uint32_t bit = t & 31u;
+                    if ((word >> bit) & 1u) {
+                        const uint32_t rank = (first ? off_a : off_b) +
+                                              __popc(word & ((1u << bit) - 1u));
+                        acc[lane * CPL + i] += kOne + rank;
+                    }
+                }
+            }
+        }
+        unsigned long long* dst = a.cnt + (uint64_t)row * C;
+#pragma unroll
+        for (uint32_t i = 0; i < CPL; i++) dst[i * 64u + lane] = acc[i * 64u + lane];
+    }
 }
 
 // ---- peel ------------------------------------------------------------------------
@@ -574,7 +652,9 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                     const uint2 it = a.queue[i];
                     const uint32_t cidx = it.x, pos = it.y;
                     if (pos < nsup) {
-                        const uint32_t taken = atomicExch(a.peeled + pos, 1u);
+                        // one word per element: claims of neighbouring elements
+                        // would otherwise queue up on a shared word
+                        const bool taken = atomicExch(a.peeled + pos, 1u) != 0u;
                         const uint32_t p = a.elem[pos];
                         const T ycell = a.yw[cidx];
                         const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p >> a.log2c);
@@ -583,7 +663,7 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
 #pragma unroll
                         for (int j = 0; j < 3; j++) cl[j] = cell_of(h, j, t, a.c, a.cmask);
                         const int j = cl[0] == cidx ? 0 : (cl[1] == cidx ? 1 : 2);
-                        if (taken == 0u && cl[j] == cidx) {
+                        if (!taken && cl[j] == cidx) {
                             const T val = Val<T>::sign(ycell, (h.neg >> j) & 1u);
                             a.vals[pos] = val;
                             my_recovered++;
@@ -747,7 +827,7 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
                 const uint32_t p = (uint32_t)(p0 + k);
                 if (!raw) {
                     out[k] = (T)a.vals[rank];
-                    rec[k] = a.peeled[rank] != 0;
+                    rec[k] = a.peeled[rank] != 0u;
                 } else {
                     out[k] = estimate_raw(a, p);
                 }
@@ -851,6 +931,9 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     uint2* queue = reinterpret_cast<uint2*>(base + L.queue);
     const T* y_agg = static_cast<const T*>(y_agg_v);
     const bool planned = plan != nullptr;
+    // few plan entries per row (a sketch much wider than the support): one
+    // wave per row, and the round-0 frontier from the peel kernel's scan
+    const bool wave_rows = planned && 3ull * ((g.n + g.c - 1) / g.c) <= kWaveRowsEntries * g.rows;
 
     DeviceInfo di;
     hipError_t e = device_info(&di);
@@ -895,13 +978,24 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
         ca.cmask = g.cmask;
         ca.cells = g.cells;
         ca.last_mask = last_mask;
-        uint32_t cgrid = g.rows < (uint32_t)di.cus * 8 ? g.rows : (uint32_t)di.cus * 8;
-        if (g.c == 1024)
-            hipLaunchKernelGGL(counter_kernel<1024>, dim3(cgrid), dim3(kBlock), 0, s, ca);
-        else if (g.c == 512)
-            hipLaunchKernelGGL(counter_kernel<512>, dim3(cgrid), dim3(kBlock), 0, s, ca);
-        else
-            hipLaunchKernelGGL(counter_kernel<256>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+        if (wave_rows) {
+            const uint64_t want = ((uint64_t)g.rows + 3) / 4;  // four waves per workgroup
+            const uint32_t cgrid = want < (uint64_t)di.cus * 8 ? (uint32_t)want : (uint32_t)di.cus * 8;
+            if (g.c == 1024)
+                hipLaunchKernelGGL(counter_wave_kernel<1024>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+            else if (g.c == 512)
+                hipLaunchKernelGGL(counter_wave_kernel<512>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+            else
+                hipLaunchKernelGGL(counter_wave_kernel<256>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+        } else {
+            const uint32_t cgrid = g.rows < (uint32_t)di.cus * 8 ? g.rows : (uint32_t)di.cus * 8;
+            if (g.c == 1024)
+                hipLaunchKernelGGL(counter_kernel<1024>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+            else if (g.c == 512)
+                hipLaunchKernelGGL(counter_kernel<512>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+            else
+                hipLaunchKernelGGL(counter_kernel<256>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+        }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
 
@@ -939,7 +1033,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     pa.cmask = g.cmask;
     pa.log2c = g.log2c;
     pa.cells = g.cells;
-    pa.planned = planned;
+    pa.planned = planned && !wave_rows;
     void* args[] = {&pa};
     e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&peel_kernel<A>),
                                    dim3((uint32_t)peel_grid_cache[slot]), dim3(kPeelBlock), args,

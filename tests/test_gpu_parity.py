@@ -132,6 +132,27 @@ def test_multi_tile_ragged_int32_planned(c):
     assert g["info"].success
 
 
+@pytest.mark.parametrize("c,frac", [(1024, 0.5), (512, 2.0), (256, 0.4)])
+def test_wide_sketch_planned(c, frac):
+    # a sketch of frac * n cells: at most 8 plan entries per row, so the
+    # counters are built one wave per row and the round-0 frontier comes from
+    # the peel kernel's scan; a dense support, so most rows are live
+    _hc()
+    w = wl.make("synthetic", n=600_011, W=2, density=0.3, overlap=0.2, data_seed=c + 11)
+    rows = max(3, int(frac * w.n / c))
+    assert 3 * ((w.n + c - 1) // c) <= 8 * rows
+    g, o = check_int(w, rows, c, use_plan=True)
+    assert g["info"].success == o["info"].success
+
+
+def test_wide_sketch_planned_fp32():
+    _hc()
+    w = wl.make("synthetic", n=400_009, W=2, density=0.3, overlap=0.2, vtype="f32", data_seed=31)
+    rows = int(0.8 * w.n / 1024)
+    g, o, bnd = check_fp32(w, rows, 1024, use_plan=True)
+    assert g["info"].success
+
+
 @pytest.mark.parametrize("ratio", [1.10, 0.8])
 def test_undersized_sketch_failure_parity_planned(ratio):
     _hc()
