@@ -214,46 +214,88 @@ __global__ __launch_bounds__(1024) void scan_kernel(uint32_t* __restrict__ blk, 
 }
 
 // Element list E (ascending), cleared peeled flags, and either the word
-// rank offsets (planned) or the per-cell counters by atomics (unplanned).  The
-// chunk's words are taken kBlock at a time, one per lane: each lane writes the
-// parameters of its word's set bits into LDS at their rank, and the workgroup
-// then stores that run of E with consecutive lanes on consecutive elements (a
-// lane storing its own run would spread every wave store over 64 lines).
+// rank offsets (planned) or the per-cell counters by atomics (unplanned).
+// Each lane writes the parameters of its words' set bits into LDS at their
+// rank, and the workgroup then stores that run of E with consecutive lanes on
+// consecutive elements (a lane storing its own run would spread every wave
+// store over 64 lines).  A chunk whose elements fit in the 8 KiB stage at once
+// is taken in one pass, four words per lane; a denser one 64 words at a time,
+// a quarter word (8 bits) per lane.  The small stage keeps five or more
+// workgroups per CU, which the sparse case, a pure bitmap stream, needs.
+__device__ __forceinline__ void compact_store(const uint32_t* s_p, uint32_t total, uint32_t base,
+                                              uint32_t* __restrict__ elem,
+                                              uint32_t* __restrict__ peeled, bool planned,
+                                              unsigned long long* __restrict__ cnt, uint64_t seed,
+                                              uint32_t rows, uint32_t c, uint32_t cmask,
+                                              uint32_t log2c) {
+    for (uint32_t i = threadIdx.x; i < total; i += kBlock) {
+        const uint32_t p = s_p[i];
+        const uint32_t pos = base + i;
+        elem[pos] = p;
+        peeled[pos] = 0u;
+        if (!planned) {
+            const BatchHash h = batch_hash(seed, rows, cmask, p >> log2c);
+            const uint32_t t = p & cmask;
+            const unsigned long long inc = kOne + pos;
+#pragma unroll
+            for (int j = 0; j < 3; j++) atomicAdd(cnt + cell_of(h, j, t, c, cmask), inc);
+        }
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void compact_kernel(
     const uint32_t* __restrict__ b, uint64_t words, uint32_t last_mask,
     const uint32_t* __restrict__ blk, uint32_t* __restrict__ elem, uint32_t* __restrict__ peeled,
     uint32_t* __restrict__ woff, unsigned long long* __restrict__ cnt,
     const Ctrl* __restrict__ ctrl, uint64_t seed, uint32_t rows, uint32_t c, uint32_t cmask,
     uint32_t log2c) {
+    constexpr uint32_t kCap = kBlock * 8;  // elements staged at once
     __shared__ uint32_t s_tmp[kBlock / 64];
-    __shared__ uint32_t s_p[kBlock * 32];
+    __shared__ uint32_t s_p[kCap];
     if (ctrl->overflow) return;
     uint32_t base = blk[blockIdx.x];
-    for (uint32_t part = 0; part < kChunkWords / kBlock; part++) {
-        const uint64_t wi = (uint64_t)blockIdx.x * kChunkWords + part * kBlock + threadIdx.x;
-        const uint32_t word = load_word(b, wi, words, last_mask);
+    const uint32_t end =
+        blockIdx.x + 1 < gridDim.x ? blk[blockIdx.x + 1] : (uint32_t)ctrl->n_support;
+    const bool planned = woff != nullptr;
+    const uint64_t c0 = (uint64_t)blockIdx.x * kChunkWords;
+    if (end - base <= kCap) {
+        const uint64_t w0 = c0 + 4ull * threadIdx.x;
+        uint32_t w4[4], mine = 0;
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            w4[k] = load_word(b, w0 + k, words, last_mask);
+            mine += __popc(w4[k]);
+        }
         uint32_t total;
-        const uint32_t off = block_exclusive_scan(__popc(word), s_tmp, &total);
-        if (woff != nullptr && wi < words) woff[wi] = base + off;
-        uint32_t w = word, o = off;
+        uint32_t o = block_exclusive_scan(mine, s_tmp, &total);
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            if (planned && w0 + k < words) woff[w0 + k] = base + o;
+            uint32_t w = w4[k];
+            while (w) {
+                s_p[o++] = (uint32_t)((w0 + k) * 32u) + (uint32_t)__builtin_ctz(w);
+                w &= w - 1u;
+            }
+        }
+        lds_barrier();
+        compact_store(s_p, total, base, elem, peeled, planned, cnt, seed, rows, c, cmask, log2c);
+        return;
+    }
+    constexpr uint32_t kPartWords = kBlock / 4;
+    for (uint32_t part = 0; part < kChunkWords / kPartWords; part++) {
+        const uint64_t wi = c0 + part * kPartWords + (threadIdx.x >> 2);
+        const uint32_t q = threadIdx.x & 3u;  // which byte of the word
+        const uint32_t byte = (load_word(b, wi, words, last_mask) >> (8u * q)) & 0xffu;
+        uint32_t total;
+        uint32_t o = block_exclusive_scan(__popc(byte), s_tmp, &total);
+        if (planned && q == 0 && wi < words) woff[wi] = base + o;
+        uint32_t w = byte;
         while (w) {
-            s_p[o++] = (uint32_t)(wi * 32u) + (uint32_t)__builtin_ctz(w);
+            s_p[o++] = (uint32_t)(wi * 32u) + 8u * q + (uint32_t)__builtin_ctz(w);
             w &= w - 1u;
         }
         lds_barrier();
-        for (uint32_t i = threadIdx.x; i < total; i += kBlock) {
-            const uint32_t p = s_p[i];
-            const uint32_t pos = base + i;
-            elem[pos] = p;
-            peeled[pos] = 0u;
-            if (woff == nullptr) {
-                const BatchHash h = batch_hash(seed, rows, cmask, p >> log2c);
-                const uint32_t t = p & cmask;
-                const unsigned long long inc = kOne + pos;
-#pragma unroll
-                for (int j = 0; j < 3; j++) atomicAdd(cnt + cell_of(h, j, t, c, cmask), inc);
-            }
-        }
+        compact_store(s_p, total, base, elem, peeled, planned, cnt, seed, rows, c, cmask, log2c);
         lds_barrier();  // s_p is refilled by the next part
         base += total;
     }
