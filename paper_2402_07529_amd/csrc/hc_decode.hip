@@ -807,7 +807,8 @@ struct EmitArgs {  // T: the gradient type; values are kept in Acc<T>
     uint32_t* mask;
     uint64_t n, words, seed;
     uint32_t rows, c, cmask, log2c, last_mask;
-    bool x_vec;  // x_out is 16-byte aligned
+    bool x_vec;     // x_out is 16-byte aligned
+    bool mask_vec;  // mask is 16-byte aligned
 };
 
 template <typename T>
@@ -827,6 +828,7 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
     typedef T V4 __attribute__((ext_vector_type(4)));
     __shared__ uint32_t s_words[kChunkWords];
     __shared__ uint32_t s_pref[kChunkWords];
+    __shared__ uint32_t s_mask[kChunkWords];  // the chunk's mask words, stored at the end
     __shared__ uint32_t s_tmp[kBlock / 64];
     const uint32_t lane = lane_id();
     const uint32_t wave = threadIdx.x >> 6;
@@ -898,9 +900,22 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
                                     (spread4((uint32_t)(m1 >> s8)) << 1) |
                                     (spread4((uint32_t)(m2 >> s8)) << 2) |
                                     (spread4((uint32_t)(m3 >> s8)) << 3);
-                const uint64_t widx = ((chunk_p + it * (4 * kBlock) + wave * 256u) >> 5) + lane;
-                if (widx < a.words) a.mask[widx] = mw;
+                s_mask[((it * (4 * kBlock) + wave * 256u) >> 5) + lane] = mw;
             }
+        }
+    }
+    if (a.mask != nullptr) {
+        // one 16-byte store per lane instead of a 4-byte store by 8 lanes per
+        // wave and iteration
+        lds_barrier();
+        const uint64_t mw0 = chunk * kChunkWords + 4ull * threadIdx.x;
+        if (a.mask_vec && mw0 + 4 <= a.words) {
+            *reinterpret_cast<uint4*>(a.mask + mw0) =
+                make_uint4(s_mask[4 * threadIdx.x], s_mask[4 * threadIdx.x + 1],
+                           s_mask[4 * threadIdx.x + 2], s_mask[4 * threadIdx.x + 3]);
+        } else {
+            for (uint32_t k = 0; k < 4; k++)
+                if (mw0 + k < a.words) a.mask[mw0 + k] = s_mask[4 * threadIdx.x + k];
         }
     }
 }
@@ -1106,6 +1121,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
         ea.log2c = g.log2c;
         ea.last_mask = last_mask;
         ea.x_vec = (reinterpret_cast<uintptr_t>(out.x_out) & 15u) == 0;
+        ea.mask_vec = (reinterpret_cast<uintptr_t>(out.mask) & 15u) == 0;
         hipLaunchKernelGGL(emit_kernel<T>, dim3((uint32_t)L.nchunks), dim3(kBlock), 0, s, ea);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
