@@ -125,14 +125,19 @@ __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, 
                                             uint32_t c, uint32_t cmask, uint32_t log2c,
                                             uint32_t bk, uint32_t brows) {
     bool nz[4][4];
-    uint64_t m[4][4];
+    uint64_t m[4][4], any = 0;
 #pragma unroll
     for (int l = 0; l < 4; l++)
 #pragma unroll
         for (int k = 0; k < 4; k++) {
             nz[l][k] = Val<T>::nonzero(e[l][k]);
             m[l][k] = __ballot(nz[l][k]);
+            any |= m[l][k];
         }
+    // an all-zero tile has nothing to store (the bitmap was zero-filled) and
+    // nothing to add: on a sparse gradient that is almost every tile, and
+    // skipping the word assembly keeps the wave's next loads coming sooner
+    if (any == 0) return;
     // word w = 8 l + i holds parameters 32 w .. 32 w + 31: lanes 8i..8i+7 of
     // load l, parameter 4 lane' + k at bit 4 (lane' - 8 i) + k
     if (lane < 32) {
