@@ -577,8 +577,10 @@ struct PeelArgs {  // T: the decode-side arithmetic type
 // with one release fence before arriving and picks up everyone else's with
 // one acquire fence after the wait; group leaders pass their group's writes on
 // with an acquire-release fence.  The wait polls with relaxed loads, so
-// spinning workgroups do not keep invalidating their caches.  Returns false
-// if the wait timed out (then ctrl->abort is set).
+// spinning workgroups do not keep invalidating their caches.  *fend gets the
+// next frontier's end.  Returns false if this workgroup's wait timed out (it
+// sets ctrl->abort for the summary; any other workgroup still waiting then
+// times out too, since the barrier can no longer complete).
 __device__ __forceinline__ uint32_t ld_agent(const unsigned int* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -589,8 +591,12 @@ __device__ __forceinline__ uint32_t add_agent(unsigned int* p, uint32_t v) {
     return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks) {
-    __shared__ uint32_t s_ok;
+__device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks, uint32_t* fend) {
+    __shared__ uint32_t s_ok, s_fend;
+    // generation (low word) and frontier end (high word), stored and polled
+    // as one 64-bit word: a workgroup learns the next frontier's end from the
+    // same load that ends its wait
+    unsigned long long* const genw = reinterpret_cast<unsigned long long*>(&sy->gen.v[0]);
     lds_barrier();
     if (threadIdx.x == 0) {
         uint32_t ok = 1;
@@ -600,21 +606,28 @@ __device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks) {
         const uint32_t gen = ld_agent(&sy->gen.v[0]);
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         bool wait = true;
+        uint32_t fe = 0;
         if (add_agent(&sy->group[grp].v[0], 1u) == gsize - 1u) {
             st_agent(&sy->group[grp].v[0], 0u);
             __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "agent");
             if (add_agent(&sy->top.v[0], 1u) == groups - 1u) {
                 __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-                st_agent(&sy->gen.v[1], ld_agent(&sy->tail.v[0]));
+                fe = ld_agent(&sy->tail.v[0]);
                 st_agent(&sy->top.v[0], 0u);
-                __hip_atomic_store(&sy->gen.v[0], gen + 1u, __ATOMIC_RELEASE,
-                                   __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(genw, ((unsigned long long)fe << 32) | (gen + 1u),
+                                   __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
                 wait = false;
             }
         }
         if (wait) {
             const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-            while (ld_agent(&sy->gen.v[0]) == gen) {
+            for (;;) {
+                const unsigned long long gw =
+                    __hip_atomic_load(genw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if ((uint32_t)gw != gen) {
+                    fe = (uint32_t)(gw >> 32);
+                    break;
+                }
                 __builtin_amdgcn_s_sleep(2);
                 if (__builtin_amdgcn_s_memrealtime() - t0 > kBarrierTimeoutTicks) {
                     st_agent(&ctrl->abort, 1u);
@@ -624,10 +637,11 @@ __device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks) {
             }
         }
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        if (ld_agent(&ctrl->abort)) ok = 0;
         s_ok = ok;
+        s_fend = fe;
     }
     lds_barrier();
+    *fend = s_fend;
     return s_ok != 0;
 }
 
@@ -672,11 +686,12 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
             }
             flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
         }
-        ok = grid_barrier(ctrl, sync, gridDim.x);
+        uint32_t fend = 0;
+        ok = grid_barrier(ctrl, sync, gridDim.x, &fend);
 
         uint32_t qs = 0;
         for (uint32_t r = 0; ok; r++) {
-            uint32_t qe = ld_agent(&sync->gen.v[1]);
+            uint32_t qe = fend;
             if (qe > a.cells) qe = a.cells;  // the queue holds each cell at most once
             if (qe <= qs) break;
             const uint32_t nsweep = (qe - qs + nwaves * 64u - 1u) / (nwaves * 64u);
@@ -735,7 +750,7 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
             }
             flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
             qs = qe;
-            ok = grid_barrier(ctrl, sync, gridDim.x);
+            ok = grid_barrier(ctrl, sync, gridDim.x, &fend);
         }
 
         // leftovers: Count Sketch median estimate from the residual sketch
