@@ -577,7 +577,9 @@ struct PeelArgs {  // T: the decode-side arithmetic type
 // with one release fence before arriving and picks up everyone else's with
 // one acquire fence after the wait; group leaders pass their group's writes on
 // with an acquire-release fence.  The wait polls with relaxed loads, so
-// spinning workgroups do not keep invalidating their caches.  *fend gets the
+// spinning workgroups do not keep invalidating their caches.  gen is the
+// number of barriers the grid has passed (every workgroup counts them, and the
+// control block starts at zero), so arriving needs no load.  *fend gets the
 // next frontier's end.  Returns false if this workgroup's wait timed out (it
 // sets ctrl->abort for the summary; any other workgroup still waiting then
 // times out too, since the barrier can no longer complete).
@@ -591,7 +593,8 @@ __device__ __forceinline__ uint32_t add_agent(unsigned int* p, uint32_t v) {
     return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks, uint32_t* fend) {
+__device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks, uint32_t gen,
+                             uint32_t* fend) {
     __shared__ uint32_t s_ok, s_fend;
     // generation (low word) and frontier end (high word), stored and polled
     // as one 64-bit word: a workgroup learns the next frontier's end from the
@@ -603,7 +606,6 @@ __device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks, uint32_
         const uint32_t groups = nblocks < kBarGroups ? nblocks : kBarGroups;
         const uint32_t grp = blockIdx.x % groups;
         const uint32_t gsize = (nblocks - grp + groups - 1u) / groups;  // blocks in the group
-        const uint32_t gen = ld_agent(&sy->gen.v[0]);
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         bool wait = true;
         uint32_t fe = 0;
@@ -686,8 +688,8 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
             }
             flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
         }
-        uint32_t fend = 0;
-        ok = grid_barrier(ctrl, sync, gridDim.x, &fend);
+        uint32_t fend = 0, gen = 0;
+        ok = grid_barrier(ctrl, sync, gridDim.x, gen++, &fend);
 
         uint32_t qs = 0;
         for (uint32_t r = 0; ok; r++) {
@@ -750,7 +752,7 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
             }
             flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
             qs = qe;
-            ok = grid_barrier(ctrl, sync, gridDim.x, &fend);
+            ok = grid_barrier(ctrl, sync, gridDim.x, gen++, &fend);
         }
 
         // leftovers: Count Sketch median estimate from the residual sketch
