@@ -36,8 +36,6 @@
 //            Elements never peeled get the Count Sketch median estimate from
 //            the residual sketch (Algorithm 1, last recovery step);
 //   emit     dense output, recovered mask and COO from E and the values.
-#include <stdlib.h>
-
 #include <type_traits>
 
 #include "hc_device.h"
@@ -1085,11 +1083,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
         if (per_cu < 1) return hipErrorInvalidConfiguration;
         // one resident workgroup per CU: enough lanes for the largest
         // frontiers while keeping the barrier's arrival count low
-        int want = 1;
-        if (const char* env = getenv("HC_PEEL_BLOCKS_PER_CU")) want = atoi(env);
-        if (want < 1) want = 1;
-        if (want > per_cu) want = per_cu;
-        peel_grid_cache[slot] = want * di.cus;
+        peel_grid_cache[slot] = di.cus;
     }
     PeelArgs<A> pa;
     pa.ctrl = ctrl;
