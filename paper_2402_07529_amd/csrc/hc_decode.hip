@@ -47,6 +47,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kPeelBlock = 1024;  // lanes per workgroup of the persistent peel kernel
+constexpr uint64_t kPeelHalfGridCells = 8ull << 20;  // below this many cells the peel uses half the CUs
 constexpr unsigned long long kOne = 1ull << 32;  // one incidence in a packed counter
 constexpr uint64_t kChunkBits = (uint64_t)kChunkWords * 32;
 constexpr uint64_t kBarrierTimeoutTicks = 500000000ull;  // 5 s at the 100 MHz real-time clock
@@ -1081,10 +1082,18 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
             &per_cu, reinterpret_cast<const void*>(&peel_kernel<A>), kPeelBlock, 0);
         if (e != hipSuccess) return e;
         if (per_cu < 1) return hipErrorInvalidConfiguration;
-        // one resident workgroup per CU: enough lanes for the largest
-        // frontiers while keeping the barrier's arrival count low
         peel_grid_cache[slot] = di.cus;
     }
+    // At most one resident workgroup per CU.  A round costs a fixed barrier
+    // time that grows with the number of workgroups arriving (about 6.9 us at
+    // one per CU, 4.9 us at one per two CUs on MI355X) plus a per-entry time
+    // bound by the atomics the CUs can keep in flight (about 10 % higher on
+    // half the CUs).  Rounds are about 50-65 at the default sketch ratio, so
+    // a small sketch, with few entries per round, peels faster on half the
+    // CUs and a large one on all of them; the two meet near 8 M cells.
+    const uint32_t peel_grid = g.cells < kPeelHalfGridCells && peel_grid_cache[slot] >= 2
+                                   ? (uint32_t)peel_grid_cache[slot] / 2u
+                                   : (uint32_t)peel_grid_cache[slot];
     PeelArgs<A> pa;
     pa.ctrl = ctrl;
     pa.sync = sync;
@@ -1104,7 +1113,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     pa.planned = planned && !wave_rows;
     void* args[] = {&pa};
     e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&peel_kernel<A>),
-                                   dim3((uint32_t)peel_grid_cache[slot]), dim3(kPeelBlock), args,
+                                   dim3(peel_grid), dim3(kPeelBlock), args,
                                    0, s);
     if (e != hipSuccess) return e;
 
