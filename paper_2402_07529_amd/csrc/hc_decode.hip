@@ -4,12 +4,13 @@
 //   prep     copy the aggregated sketch into a residual Yw (fp64 for fp32
 //            gradients), clear the control block (and, without a plan, the
 //            per-cell counters);
-//   count    popcount of the bitmap per chunk of 1024 words;
-//   scan     exclusive scan of the chunk counts (one workgroup) -> offsets and
+//   count    popcount of the bitmap per tile of 16 chunks of 1024 words, and
+//            each chunk's offset within its tile;
+//   scan     exclusive scan of the tile counts (one workgroup) -> offsets and
 //            the support size |S|;
-//   compact  the set bits become the ascending element list E ("we know the
-//            indexes of all non-zero parameters", section 3.2) and, with a
-//            plan, every bitmap word's rank offset;
+//   support  one wave per chunk: the set bits become the ascending element
+//            list E ("we know the indexes of all non-zero parameters", section
+//            3.2) and, with a plan, every batch's rank offset;
 //   counters per cell  cnt = deg * 2^32 + (sum of member positions):  a cell
 //            is pure (one live element) exactly when cnt >> 32 == 1, and then
 //            its low word is that element's position.  With a plan (the
@@ -175,8 +176,7 @@ __device__ __forceinline__ uint4 load_counts4(const uint32_t* blk, uint64_t i, u
 }
 
 __global__ __launch_bounds__(1024) void scan_kernel(uint32_t* __restrict__ blk, uint64_t nchunks,
-                                                    Ctrl* __restrict__ ctrl, uint64_t cap,
-                                                    uint32_t* __restrict__ woff, uint64_t words) {
+                                                    Ctrl* __restrict__ ctrl, uint64_t cap) {
     __shared__ uint32_t s_tmp[16];
     const uint64_t per = ((nchunks + 1023) / 1024 + 3) & ~3ull;
     const uint64_t lo = (uint64_t)threadIdx.x * per;
@@ -208,96 +208,193 @@ __global__ __launch_bounds__(1024) void scan_kernel(uint32_t* __restrict__ blk, 
     if (threadIdx.x == 0) {
         ctrl->n_support = total;
         ctrl->overflow = (uint64_t)total > cap ? 1u : 0u;
-        if (woff != nullptr) woff[words] = total;
     }
 }
 
-// Element list E (ascending), cleared peeled flags, and either the word
-// rank offsets (planned) or the per-cell counters by atomics (unplanned).
-// Each lane writes the parameters of its words' set bits into LDS at their
-// rank, and the workgroup then stores that run of E with consecutive lanes on
-// consecutive elements (a lane storing its own run would spread every wave
-// store over 64 lines).  A chunk whose elements fit in the 8 KiB stage at once
-// is taken in one pass, four words per lane; a denser one 64 words at a time,
-// a quarter word (8 bits) per lane.  The small stage keeps five or more
-// workgroups per CU, which the sparse case, a pure bitmap stream, needs.
-__device__ __forceinline__ void compact_store(const uint32_t* s_p, uint32_t total, uint32_t base,
-                                              uint32_t* __restrict__ elem,
-                                              uint32_t* __restrict__ peeled, bool planned,
-                                              unsigned long long* __restrict__ cnt, uint64_t seed,
-                                              uint32_t rows, uint32_t c, uint32_t cmask,
-                                              uint32_t log2c) {
-    for (uint32_t i = threadIdx.x; i < total; i += kBlock) {
-        const uint32_t p = s_p[i];
-        const uint32_t pos = base + i;
-        elem[pos] = p;
-        peeled[pos] = 0u;
-        if (!planned) {
-            const BatchHash h = batch_hash(seed, rows, cmask, p >> log2c);
-            const uint32_t t = p & cmask;
-            const unsigned long long inc = kOne + pos;
+// ---- support: the element list from the index ------------------------------------
+//
+// The bitmap is counted in tiles of kTileChunks chunks (one workgroup each,
+// 64 KiB: long enough to stream at full rate), writing each tile's count and
+// each chunk's offset within its tile; one workgroup scans the tile counts;
+// then one wave per chunk writes the chunk offset the emit kernel reads, the
+// chunk's run of the ascending element list E ("we know the indexes of all
+// non-zero parameters", section 3.2), cleared peeled flags, and either the
+// rank offset of every batch of c parameters (with a plan) or the per-cell
+// counters by atomics (without).  A wave per chunk needs no workgroup
+// barriers, so a sparse chunk costs little more than its loads, and dense
+// bitmaps, whose chunks hold thousands of elements, still spread over the chip.
+constexpr uint32_t kTileChunks = 16;
+
+// Words k..k+3 of the bitmap (k a multiple of 4) as load_word reads them; one
+// 16-byte load when b is 16-byte aligned and the four lie before the last word.
+__device__ __forceinline__ uint4 load_words4(const uint32_t* b, uint64_t k, uint64_t words,
+                                             uint32_t last_mask, bool vec) {
+    if (vec && k + 4 < words) return *reinterpret_cast<const uint4*>(b + k);
+    return make_uint4(load_word(b, k, words, last_mask), load_word(b, k + 1, words, last_mask),
+                      load_word(b, k + 2, words, last_mask), load_word(b, k + 3, words, last_mask));
+}
+
+__global__ __launch_bounds__(kBlock) void tile_count_kernel(const uint32_t* __restrict__ b,
+                                                            uint64_t words, uint32_t last_mask,
+                                                            bool vec, uint64_t nchunks,
+                                                            uint32_t* __restrict__ cpre,
+                                                            uint32_t* __restrict__ tcnt) {
+    __shared__ uint32_t s_cnt[kBlock / 64][kTileChunks];
+    const uint32_t lane = lane_id();
+    const uint32_t wave = threadIdx.x >> 6;
+    const uint64_t ch0 = (uint64_t)blockIdx.x * kTileChunks;
+    const uint64_t w0 = ch0 * kChunkWords + 4ull * threadIdx.x;
+    uint4 v[kTileChunks];
 #pragma unroll
-            for (int j = 0; j < 3; j++) atomicAdd(cnt + cell_of(h, j, t, c, cmask), inc);
+    for (uint32_t q = 0; q < kTileChunks; q++)
+        v[q] = load_words4(b, w0 + q * kChunkWords, words, last_mask, vec);
+#pragma unroll
+    for (uint32_t q = 0; q < kTileChunks; q++) {
+        const uint32_t c = wave_sum(__popc(v[q].x) + __popc(v[q].y) + __popc(v[q].z) +
+                                    __popc(v[q].w));
+        if (lane == 0) s_cnt[wave][q] = c;
+    }
+    lds_barrier();
+    if (wave == 0) {
+        // lanes 0..kTileChunks-1: chunk counts -> offsets within the tile
+        uint32_t c = 0;
+        if (lane < kTileChunks)
+            for (uint32_t w = 0; w < kBlock / 64; w++) c += s_cnt[w][lane];
+        uint32_t x = c;
+#pragma unroll
+        for (uint32_t d = 1; d < kTileChunks; d <<= 1) {
+            const uint32_t y = __shfl_up(x, d);
+            if (lane >= d) x += y;
         }
+        if (lane < kTileChunks && ch0 + lane < nchunks) cpre[ch0 + lane] = x - c;
+        if (lane == kTileChunks - 1) tcnt[blockIdx.x] = x;
     }
 }
 
-__global__ __launch_bounds__(kBlock) void compact_kernel(
-    const uint32_t* __restrict__ b, uint64_t words, uint32_t last_mask,
-    const uint32_t* __restrict__ blk, uint32_t* __restrict__ elem, uint32_t* __restrict__ peeled,
-    uint32_t* __restrict__ woff, unsigned long long* __restrict__ cnt,
-    const Ctrl* __restrict__ ctrl, uint64_t seed, uint32_t rows, uint32_t c, uint32_t cmask,
-    uint32_t log2c) {
-    constexpr uint32_t kCap = kBlock * 8;  // elements staged at once
-    __shared__ uint32_t s_tmp[kBlock / 64];
-    __shared__ uint32_t s_p[kCap];
-    if (ctrl->overflow) return;
-    uint32_t base = blk[blockIdx.x];
-    const uint32_t end =
-        blockIdx.x + 1 < gridDim.x ? blk[blockIdx.x + 1] : (uint32_t)ctrl->n_support;
-    const bool planned = woff != nullptr;
-    const uint64_t c0 = (uint64_t)blockIdx.x * kChunkWords;
-    if (end - base <= kCap) {
-        const uint64_t w0 = c0 + 4ull * threadIdx.x;
-        uint32_t w4[4], mine = 0;
+struct SupportArgs {
+    const uint32_t* b;
+    const uint32_t* cpre;        // set bits before each chunk within its tile
+    const uint32_t* toff;        // set bits before each tile
+    uint32_t* blk;               // set bits before each chunk
+    uint32_t* woffb;             // with a plan: set bits before each batch (nb + 1 entries)
+    uint32_t* elem;
+    uint32_t* peeled;
+    unsigned long long* cnt;     // without a plan: counters built by atomics
+    Ctrl* ctrl;
+    uint64_t words, nchunks, cap, seed;
+    uint32_t last_mask, log2wpb, nb, rows, c, cmask, log2c;
+    bool vec;  // b is 16-byte aligned
+};
+
+// Element pos of E is parameter p: its list entry, its cleared flag and,
+// without a plan, its three counter increments.  Positions past the capacity
+// are dropped (the decode then reports overflow).
+__device__ __forceinline__ void support_put(const SupportArgs& a, uint32_t pos, uint32_t p) {
+    if (pos >= a.cap) return;
+    a.elem[pos] = p;
+    a.peeled[pos] = 0u;
+    if (a.woffb == nullptr) {
+        const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p >> a.log2c);
+        const uint32_t t = p & a.cmask;
+        const unsigned long long inc = kOne + pos;
 #pragma unroll
-        for (int k = 0; k < 4; k++) {
-            w4[k] = load_word(b, w0 + k, words, last_mask);
-            mine += __popc(w4[k]);
+        for (int j = 0; j < 3; j++) atomicAdd(a.cnt + cell_of(h, j, t, a.c, a.cmask), inc);
+    }
+}
+
+constexpr uint32_t kWaveStage = 1024;  // elements one wave stages in LDS at a time
+
+// The wave stores stage[0, total) as E[base + j], consecutive lanes on
+// consecutive elements.  Every lane has written its stage entries.
+__device__ __forceinline__ void support_flush(const SupportArgs& a, uint32_t* stage,
+                                              uint32_t total, uint32_t base, uint32_t lane) {
+    if (total == 0) return;
+    // the wave's LDS writes are complete before any lane reads them back
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_wave_barrier();
+    for (uint32_t j = lane; j < total; j += 64) support_put(a, base + j, stage[j]);
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_wave_barrier();  // the stage is refilled next
+}
+
+// One wave, one chunk, in four segments of 256 words; lane l holds words
+// 4l..4l+3 of each.  A lane's set bits go to LDS at their rank within the
+// segment and the wave then stores the run with consecutive lanes on
+// consecutive elements (a lane storing its own run would spread every store
+// over 64 lines); a segment with more than kWaveStage elements (over 1/8
+// dense) is staged in eight parts.
+__global__ __launch_bounds__(kBlock) void support_kernel(SupportArgs a) {
+    __shared__ uint32_t s_stage[kBlock / 64][kWaveStage];
+    const uint32_t lane = lane_id();
+    const uint32_t wave = uniform(threadIdx.x >> 6);
+    const uint64_t chunk = (uint64_t)blockIdx.x * (kBlock / 64) + wave;
+    if (chunk >= a.nchunks) return;
+    uint32_t* const stage = s_stage[wave];
+    const uint64_t c0 = chunk * kChunkWords;
+    uint4 v[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+        v[i] = load_words4(a.b, c0 + 256u * i + 4u * lane, a.words, a.last_mask, a.vec);
+    uint32_t base = a.toff[chunk / kTileChunks] + a.cpre[chunk];
+    if (lane == 0) a.blk[chunk] = base;
+    const uint64_t wmask = (1ull << a.log2wpb) - 1ull;
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        const uint32_t w4[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+        const uint32_t mine = __popc(w4[0]) + __popc(w4[1]) + __popc(w4[2]) + __popc(w4[3]);
+        uint32_t x = mine;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const uint32_t y = __shfl_up(x, d);
+            if (lane >= (uint32_t)d) x += y;
         }
-        uint32_t total;
-        uint32_t o = block_exclusive_scan(mine, s_tmp, &total);
+        const uint32_t total = __shfl(x, 63);
+        uint32_t o = x - mine;  // rank of this lane's first element in the segment
+        const uint64_t s0 = c0 + 256u * i;
+        const uint64_t w0 = s0 + 4u * lane;
+        const bool staged = total <= kWaveStage;
 #pragma unroll
         for (int k = 0; k < 4; k++) {
-            if (planned && w0 + k < words) woff[w0 + k] = base + o;
-            uint32_t w = w4[k];
-            while (w) {
-                s_p[o++] = (uint32_t)((w0 + k) * 32u) + (uint32_t)__builtin_ctz(w);
-                w &= w - 1u;
+            const uint64_t w = w0 + k;
+            if (a.woffb != nullptr && w < a.words && (w & wmask) == 0)
+                a.woffb[w >> a.log2wpb] = base + o;
+            uint32_t bits = staged ? w4[k] : 0u;
+            while (bits) {
+                stage[o++] = (uint32_t)(w * 32u) + (uint32_t)__builtin_ctz(bits);
+                bits &= bits - 1u;
+            }
+            if (!staged) o += __popc(w4[k]);
+        }
+        if (staged) {
+            support_flush(a, stage, total, base, lane);
+        } else {
+            // over 1/8 dense: eight passes of 32 words, two lanes per word
+            // (16 bits each), at most 1024 elements a pass
+            uint32_t pbase = base;
+            for (uint32_t part = 0; part < 8; part++) {
+                const uint64_t w = s0 + part * 32u + (lane >> 1);
+                const uint32_t half = lane & 1u;
+                uint32_t bits = (load_word(a.b, w, a.words, a.last_mask) >> (16u * half)) & 0xffffu;
+                const uint32_t pc = __popc(bits);
+                uint32_t y = pc;
+#pragma unroll
+                for (int d = 1; d < 64; d <<= 1) {
+                    const uint32_t z = __shfl_up(y, d);
+                    if (lane >= (uint32_t)d) y += z;
+                }
+                const uint32_t ptotal = __shfl(y, 63);
+                uint32_t q = y - pc;
+                while (bits) {
+                    stage[q++] = (uint32_t)(w * 32u) + 16u * half + (uint32_t)__builtin_ctz(bits);
+                    bits &= bits - 1u;
+                }
+                support_flush(a, stage, ptotal, pbase, lane);
+                pbase += ptotal;
             }
         }
-        lds_barrier();
-        compact_store(s_p, total, base, elem, peeled, planned, cnt, seed, rows, c, cmask, log2c);
-        return;
-    }
-    constexpr uint32_t kPartWords = kBlock / 4;
-    for (uint32_t part = 0; part < kChunkWords / kPartWords; part++) {
-        const uint64_t wi = c0 + part * kPartWords + (threadIdx.x >> 2);
-        const uint32_t q = threadIdx.x & 3u;  // which byte of the word
-        const uint32_t byte = (load_word(b, wi, words, last_mask) >> (8u * q)) & 0xffu;
-        uint32_t total;
-        uint32_t o = block_exclusive_scan(__popc(byte), s_tmp, &total);
-        if (planned && q == 0 && wi < words) woff[wi] = base + o;
-        uint32_t w = byte;
-        while (w) {
-            s_p[o++] = (uint32_t)(wi * 32u) + 8u * q + (uint32_t)__builtin_ctz(w);
-            w &= w - 1u;
-        }
-        lds_barrier();
-        compact_store(s_p, total, base, elem, peeled, planned, cnt, seed, rows, c, cmask, log2c);
-        lds_barrier();  // s_p is refilled by the next part
         base += total;
     }
+    if (chunk + 1 == a.nchunks && lane == 0 && a.woffb != nullptr) a.woffb[a.nb] = base;
 }
 
 // ---- frontier staging ----------------------------------------------------------
@@ -348,12 +445,27 @@ __device__ void flush_pushes(Q& q, bool force, uint32_t room, unsigned int* tail
 
 // ---- counters by row (planned path) --------------------------------------------
 
+// Lane l < WPB holds word l of a batch (other lanes hold 0): the set bits in
+// words 0..l-1, i.e. the word's rank offset within the batch.
+template <uint32_t WPB>
+__device__ __forceinline__ uint32_t batch_word_offset(uint32_t word) {
+    const uint32_t lane = lane_id();
+    const uint32_t pc = __popc(word);
+    uint32_t x = pc;
+#pragma unroll
+    for (uint32_t d = 1; d < WPB; d <<= 1) {
+        const uint32_t y = __shfl_up(x, d);
+        if (lane >= d) x += y;
+    }
+    return x - pc;
+}
+
 struct CounterArgs {
     const PlanHeader* hdr;
     const uint32_t* rowoff;
     const uint2* entry;
     const uint32_t* b;
-    const uint32_t* woff;   // words + 1 entries
+    const uint32_t* woffb;  // set bits before each batch (nb + 1 entries)
     unsigned long long* cnt;
     uint2* queue;
     Ctrl* ctrl;
@@ -388,7 +500,7 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
     constexpr uint32_t kWaves = kBlock / 64;
     __shared__ unsigned long long s_acc[C];
     __shared__ uint32_t s_word[kStage * WPB];
-    __shared__ uint32_t s_off[kStage * WPB];
+    __shared__ uint32_t s_boff[kStage];
     __shared__ uint2 s_live[kBlock];
     __shared__ uint32_t s_tmp[kWaves];
     __shared__ PushBuf<C> q;
@@ -413,11 +525,7 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
             bool live = false;
             if (e < e1) {
                 ent = a.entry[e];
-                if (ent.x < a.nb) {
-                    const uint64_t ws = (uint64_t)ent.x * WPB;
-                    const uint64_t we = ws + WPB < a.words ? ws + WPB : a.words;
-                    live = a.woff[we] != a.woff[ws];
-                }
+                if (ent.x < a.nb) live = a.woffb[ent.x + 1] != a.woffb[ent.x];
             }
             uint32_t nlive;
             const uint32_t slot = block_exclusive_scan(live ? 1u : 0u, s_tmp, &nlive);
@@ -428,22 +536,20 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
                 // stage
                 for (uint32_t k = threadIdx.x; k < ng * WPB; k += kBlock) {
                     const uint64_t w = (uint64_t)s_live[g0 + k / WPB].x * WPB + (k % WPB);
-                    uint32_t word = 0, off = 0;
-                    if (w < a.words) {
-                        word = load_word(a.b, w, a.words, a.last_mask);
-                        off = a.woff[w];
-                    }
-                    s_word[k] = word;
-                    s_off[k] = off;
+                    s_word[k] = load_word(a.b, w, a.words, a.last_mask);
                 }
+                for (uint32_t k = threadIdx.x; k < ng; k += kBlock)
+                    s_boff[k] = a.woffb[s_live[g0 + k].x];
                 lds_barrier();
                 // add
                 for (uint32_t g = wave; g < ng; g += kWaves) {
                     const uint32_t bias = s_live[g0 + g].y & 0xffffu;
                     const uint32_t t0 = (lane * CPL - bias) & (C - 1u);
                     const uint32_t wa = t0 >> 5, wb = ((t0 + CPL - 1u) & (C - 1u)) >> 5;
-                    const uint32_t word_a = s_word[g * WPB + wa], off_a = s_off[g * WPB + wa];
-                    const uint32_t word_b = s_word[g * WPB + wb], off_b = s_off[g * WPB + wb];
+                    const uint32_t myoff = s_boff[g] + batch_word_offset<WPB>(
+                                               lane < WPB ? s_word[g * WPB + lane] : 0u);
+                    const uint32_t word_a = s_word[g * WPB + wa], off_a = __shfl(myoff, wa);
+                    const uint32_t word_b = s_word[g * WPB + wb], off_b = __shfl(myoff, wb);
 #pragma unroll
                     for (uint32_t i = 0; i < CPL; i++) {
                         const uint32_t t = (t0 + i) & (C - 1u);
@@ -509,11 +615,7 @@ __global__ __launch_bounds__(kBlock) void counter_wave_kernel(CounterArgs a) {
             bool live = false;
             if (e < e1) {
                 ent = a.entry[e];
-                if (ent.x < a.nb) {
-                    const uint64_t ws = (uint64_t)ent.x * WPB;
-                    const uint64_t we = ws + WPB < a.words ? ws + WPB : a.words;
-                    live = a.woff[we] != a.woff[ws];
-                }
+                if (ent.x < a.nb) live = a.woffb[ent.x + 1] != a.woffb[ent.x];
             }
             uint64_t m = __ballot(live);
             while (m) {
@@ -522,11 +624,9 @@ __global__ __launch_bounds__(kBlock) void counter_wave_kernel(CounterArgs a) {
                 const uint32_t bidx = __shfl(ent.x, src);
                 const uint32_t bias = __shfl(ent.y, src) & 0xffffu;
                 const uint64_t ws = (uint64_t)bidx * WPB;
-                uint32_t myword = 0, myoff = 0;
-                if (lane < WPB && ws + lane < a.words) {
-                    myword = load_word(a.b, ws + lane, a.words, a.last_mask);
-                    myoff = a.woff[ws + lane];
-                }
+                const uint32_t boff = a.woffb[bidx];
+                const uint32_t myword = lane < WPB ? load_word(a.b, ws + lane, a.words, a.last_mask) : 0u;
+                const uint32_t myoff = boff + batch_word_offset<WPB>(myword);
                 const uint32_t t0 = (lane * CPL - bias) & (C - 1u);
                 const uint32_t wa = t0 >> 5, wb = ((t0 + CPL - 1u) & (C - 1u)) >> 5;
                 const uint32_t word_a = __shfl(myword, wa), off_a = __shfl(myoff, wa);
@@ -995,7 +1095,9 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     Ctrl* ctrl = reinterpret_cast<Ctrl*>(base + L.ctrl);
     PeelSync* sync = reinterpret_cast<PeelSync*>(base + L.sync);
     uint32_t* blk = reinterpret_cast<uint32_t*>(base + L.blk);
-    uint32_t* woff = plan ? reinterpret_cast<uint32_t*>(base + L.woff) : nullptr;
+    uint32_t* tcnt = reinterpret_cast<uint32_t*>(base + L.tcnt);
+    uint32_t* cpre = reinterpret_cast<uint32_t*>(base + L.cpre);
+    uint32_t* woffb = plan ? reinterpret_cast<uint32_t*>(base + L.woffb) : nullptr;
     uint32_t* elem = reinterpret_cast<uint32_t*>(base + L.elem);
     A* vals = reinterpret_cast<A*>(base + L.vals);
     uint32_t* peeled = reinterpret_cast<uint32_t*>(base + L.peeled);
@@ -1018,15 +1120,36 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
                        g.cells, planned, ctrl, sync);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const uint32_t last_mask = (g.n & 31u) ? ((1u << (g.n & 31u)) - 1u) : 0xffffffffu;
-    hipLaunchKernelGGL(count_kernel, dim3((uint32_t)L.nchunks), dim3(kBlock), 0, s, b, g.words,
-                       last_mask, blk);
+    const bool bvec = (reinterpret_cast<uintptr_t>(b) & 15u) == 0;
+    hipLaunchKernelGGL(tile_count_kernel, dim3((uint32_t)L.ntiles), dim3(kBlock), 0, s, b,
+                       g.words, last_mask, bvec, L.nchunks, cpre, tcnt);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, s, blk, L.nchunks, ctrl, L.cap, woff,
-                       g.words);
+    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, s, tcnt, L.ntiles, ctrl, L.cap);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(compact_kernel, dim3((uint32_t)L.nchunks), dim3(kBlock), 0, s, b, g.words,
-                       last_mask, blk, elem, peeled, woff, cnt, ctrl, g.seed, g.rows, g.c,
-                       g.cmask, g.log2c);
+    SupportArgs sa;
+    sa.b = b;
+    sa.cpre = cpre;
+    sa.toff = tcnt;
+    sa.blk = blk;
+    sa.woffb = woffb;
+    sa.elem = elem;
+    sa.peeled = peeled;
+    sa.cnt = cnt;
+    sa.ctrl = ctrl;
+    sa.words = g.words;
+    sa.nchunks = L.nchunks;
+    sa.cap = L.cap;
+    sa.seed = g.seed;
+    sa.last_mask = last_mask;
+    sa.log2wpb = planned ? g.log2c - 5u : 0u;  // planned sketches have c >= 256
+    sa.nb = (uint32_t)((g.n + g.c - 1) / g.c);
+    sa.rows = g.rows;
+    sa.c = g.c;
+    sa.cmask = g.cmask;
+    sa.log2c = g.log2c;
+    sa.vec = bvec;
+    hipLaunchKernelGGL(support_kernel, dim3((uint32_t)((L.nchunks + kBlock / 64 - 1) / (kBlock / 64))),
+                       dim3(kBlock), 0, s, sa);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     if (planned) {
@@ -1037,7 +1160,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
         ca.rowoff = reinterpret_cast<const uint32_t*>(pb + PL.rowoff);
         ca.entry = reinterpret_cast<const uint2*>(pb + PL.entry);
         ca.b = b;
-        ca.woff = woff;
+        ca.woffb = woffb;
         ca.cnt = cnt;
         ca.queue = queue;
         ca.ctrl = ctrl;
@@ -1163,8 +1286,12 @@ DecodeLayout decode_layout(const Geo& g, uint64_t max_support) {
     size_t o = 0;
     L.ctrl = o;    o = align256(o + sizeof(Ctrl));
     L.sync = o;    o = align256(o + sizeof(PeelSync));
+    L.ntiles = (L.nchunks + kTileChunks - 1) / kTileChunks;
     L.blk = o;     o = align256(o + L.nchunks * 4);
-    L.woff = o;    o = align256(o + (g.words + 1) * 4);
+    L.cpre = o;    o = align256(o + L.nchunks * 4);
+    L.tcnt = o;    o = align256(o + L.ntiles * 4);
+    // rank offsets per batch of c parameters, used with a plan (c >= 256)
+    L.woffb = o;   o = align256(o + (g.c >= 256 ? ((g.n + g.c - 1) / g.c + 1) * 4 : 0));
     L.elem = o;    o = align256(o + cap * 4);
     L.vals = o;    o = align256(o + cap * vsz);
     L.peeled = o;  o = align256(o + cap * 4);
@@ -1199,8 +1326,7 @@ hipError_t launch_support_offsets(const Geo& g, const uint32_t* b, uint32_t* blk
                        last_mask, blk);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, s, blk, nchunks, c, g.n,
-                       static_cast<uint32_t*>(nullptr), g.words);
+    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, s, blk, nchunks, c, g.n);
     return hipGetLastError();
 }
 

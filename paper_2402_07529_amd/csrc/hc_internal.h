@@ -94,7 +94,8 @@ hipError_t launch_encode_blocked(const Geo& g, const void* x, void* y, uint32_t*
 struct DecodeLayout {
     uint64_t cap;       // max support the workspace holds
     uint64_t nchunks;   // bitmap chunks of kChunkWords words
-    size_t ctrl, sync, blk, woff, elem, vals, peeled, cnt, yw, queue, cand, total;
+    uint64_t ntiles;    // tiles of the support passes (a few chunks each)
+    size_t ctrl, sync, blk, cpre, tcnt, woffb, elem, vals, peeled, cnt, yw, queue, cand, total;
 };
 constexpr uint32_t kChunkWords = 1024;
 DecodeLayout decode_layout(const Geo& g, uint64_t max_support);
