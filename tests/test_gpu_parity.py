@@ -335,3 +335,37 @@ def test_coo_capacity_truncates():
     sup = np.nonzero(np.unpackbits(o["Ba"].view(np.uint8), bitorder="little")[:w.n])[0]
     assert np.array_equal(g["coo_idx"], sup[:100].astype(np.uint32))
     assert np.array_equal(g["coo_val"], o["x"][sup[:100]])
+
+
+@pytest.mark.parametrize("use_plan,density", [(False, 0.01), (True, 0.01), (True, 0.12)])
+def test_decode_unaligned_views(use_plan, density):
+    # the decode reads the aggregate and writes its outputs through views 4
+    # bytes past a 16-byte boundary (the ABI asks for 4-byte alignment): the
+    # index is then read word by word, and the result must not change.  At
+    # 0.12 per worker the aggregate is about 0.4 dense, so the support pass
+    # takes its dense-segment path.
+    import torch
+    hc = _hc()
+    w = wl.make("synthetic", n=1_000_003, W=4, density=density, overlap=0.1,
+                data_seed=int(density * 1000) + use_plan)
+    rows = oracle.rows_for(w.n_agg)
+    a = gpu_run(w, rows, 1024, keep_workers=False, want_coo_out=False, use_plan=use_plan)
+    assert a["info"].success
+    p = a["p"]
+    dev = torch.device("cuda")
+    vt = torch.int32
+    Ya = torch.zeros(p.cells + 1, dtype=vt, device=dev)
+    Ba = torch.zeros(p.index_words + 1, dtype=torch.int32, device=dev)
+    Ya[1:] = torch.from_numpy(a["Ya"]).to(dev)
+    Ba[1:] = torch.from_numpy(a["Ba"].view(np.int32)).to(dev)
+    out = torch.empty(w.n + 1, dtype=vt, device=dev)
+    mask = torch.empty(p.words + 1, dtype=torch.int32, device=dev)
+    info = hc.alloc_info(dev)
+    ws = hc.alloc_workspace(p, 0, dev)
+    plan = hc.make_plan(p, dev) if use_plan else None
+    hc.hc_decode(p, Ya[1:], Ba[1:], info, ws, x_out=out[1:], mask=mask[1:], plan=plan)
+    torch.cuda.synchronize()
+    assert hc.read_info(info) == a["info"]
+    assert np.array_equal(out[1:].cpu().numpy(), a["x"])
+    assert np.array_equal(mask[1:].cpu().numpy().view(np.uint32), a["mask"])
+    assert np.array_equal(a["x"], wrap_sum([w.dense(i) for i in range(w.W)]))
