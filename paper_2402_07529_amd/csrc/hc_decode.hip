@@ -50,6 +50,21 @@ constexpr int kBlock = 256;
 constexpr int kPeelBlock = 1024;  // lanes per workgroup of the persistent peel kernel
 constexpr uint64_t kPeelHalfGridCells = 8ull << 20;  // below this many cells the peel uses half the CUs
 constexpr unsigned long long kOne = 1ull << 32;  // one incidence in a packed counter
+
+// The int32 peel can carry a cell's residual in its counter word: value in
+// the high 32 bits, deg * 2^k + (sum of member positions) in the low 32, with
+// every position below 2^k.  An element leaving the cell subtracts
+// (g x) * 2^32 + 2^k + pos: the low part holds the member's own terms, so it
+// never borrows from the value, and the value wraps mod 2^32 as the sketch
+// does.  One atomic then updates degree, identity and residual together.  It
+// needs deg * 2^k + sum < 2^32 in every cell at the start (the low part only
+// shrinks); the counter kernels flag any cell where that fails.
+__device__ __forceinline__ uint32_t pack_bits(uint64_t nsup) {
+    return nsup <= 1 ? 1u : 64u - (uint32_t)__builtin_clzll(nsup - 1);  // nsup <= 2^k
+}
+__device__ __forceinline__ bool fits_packed(unsigned long long acc, uint32_t k) {
+    return ((acc >> 32) << k) + (acc & 0xffffffffull) < (1ull << 32);
+}
 constexpr uint64_t kChunkBits = (uint64_t)kChunkWords * 32;
 constexpr uint64_t kBarrierTimeoutTicks = 500000000ull;  // 5 s at the 100 MHz real-time clock
 
@@ -62,7 +77,8 @@ struct Ctrl {
     unsigned int abort;     // barrier timeout
     unsigned int done;      // workgroups finished
     unsigned int bad_plan;  // the plan was built for another geometry
-    unsigned int pad[7];
+    unsigned int nopack;    // some cell's counter does not fit the packed form
+    unsigned int pad[6];
 };
 static_assert(sizeof(Ctrl) == 64, "control block layout");
 
@@ -512,6 +528,7 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
         return;
     }
     if (a.ctrl->overflow) return;
+    const uint32_t kpack = pack_bits(a.ctrl->n_support);
     const uint32_t lane = lane_id();
     const uint32_t wave = threadIdx.x >> 6;
     if (threadIdx.x == 0) q.count = 0;
@@ -571,6 +588,7 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
             const uint32_t cell = row * C + k;
             const bool pure = (acc >> 32) == 1ull;
             a.cnt[cell] = acc;
+            if (!fits_packed(acc, kpack)) atomicOr(&a.ctrl->nopack, 1u);
             lds_push(q, pure, cell, (uint32_t)acc);
         }
         flush_pushes(q, false, C, &a.sync->tail.v[0], a.queue, a.cells);
@@ -601,6 +619,7 @@ __global__ __launch_bounds__(kBlock) void counter_wave_kernel(CounterArgs a) {
         return;
     }
     if (a.ctrl->overflow) return;
+    const uint32_t kpack = pack_bits(a.ctrl->n_support);
     const uint32_t lane = lane_id();
     const uint32_t wave = uniform(threadIdx.x >> 6);
     unsigned long long* const acc = s_acc + wave * C;
@@ -646,8 +665,14 @@ __global__ __launch_bounds__(kBlock) void counter_wave_kernel(CounterArgs a) {
             }
         }
         unsigned long long* dst = a.cnt + (uint64_t)row * C;
+        bool fits = true;
 #pragma unroll
-        for (uint32_t i = 0; i < CPL; i++) dst[i * 64u + lane] = acc[i * 64u + lane];
+        for (uint32_t i = 0; i < CPL; i++) {
+            const unsigned long long v = acc[i * 64u + lane];
+            dst[i * 64u + lane] = v;
+            fits = fits && fits_packed(v, kpack);
+        }
+        if (!fits) atomicOr(&a.ctrl->nopack, 1u);
     }
 }
 
@@ -667,7 +692,63 @@ struct PeelArgs {  // T: the decode-side arithmetic type
     uint64_t seed;
     uint32_t rows, c, cmask, log2c, cells;
     bool planned;   // the round-0 frontier is already queued
+    bool counted;   // a counter kernel built the counters (and checked their packing)
 };
+
+// One frontier entry (cell cidx, element position pos), for the kernel below.
+// PACKED: int32 residuals ride in the counter words (kp position bits).
+// Sets the (at most two) cells that became pure, with their elements.
+template <typename T, bool PACKED>
+__device__ __forceinline__ void peel_entry(const PeelArgs<T>& a, uint32_t cidx, uint32_t pos,
+                                           uint32_t kp, uint32_t r, uint32_t& recovered,
+                                           uint32_t& last_round, bool (&push)[2],
+                                           uint32_t (&pcell)[2], uint32_t (&ppos)[2]) {
+    // one word per element: claims of neighbouring elements would otherwise
+    // queue up on a shared word
+    const bool taken = atomicExch(a.peeled + pos, 1u) != 0u;
+    const uint32_t p = a.elem[pos];
+    unsigned long long wcell = 0;
+    T ycell = T(0);
+    if (PACKED) wcell = a.cnt[cidx];
+    else ycell = a.yw[cidx];
+    const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p >> a.log2c);
+    const uint32_t t = p & a.cmask;
+    uint32_t cl[3];
+#pragma unroll
+    for (int j = 0; j < 3; j++) cl[j] = cell_of(h, j, t, a.c, a.cmask);
+    const int j = cl[0] == cidx ? 0 : (cl[1] == cidx ? 1 : 2);
+    if (taken || cl[j] != cidx) return;
+    if (PACKED) ycell = (T)(int32_t)(uint32_t)(wcell >> 32);
+    const T val = Val<T>::sign(ycell, (h.neg >> j) & 1u);
+    a.vals[pos] = val;
+    recovered++;
+    last_round = r + 1u;
+    const int jo[2] = {j == 0 ? 1 : 0, j == 2 ? 1 : 2};
+    unsigned long long old[2], inc[2];
+#pragma unroll
+    for (int u = 0; u < 2; u++) {
+        const T gx = Val<T>::sign(val, !((h.neg >> jo[u]) & 1u));  // -g * x
+        if (PACKED)
+            inc[u] = ((unsigned long long)(uint32_t)(int32_t)gx << 32) - ((1ull << kp) + pos);
+        else
+            inc[u] = 0ull - (kOne + pos);
+        old[u] = atomicAdd(a.cnt + cl[jo[u]], inc[u]);
+        if (!PACKED) Val<T>::atomic_add(a.yw + cl[jo[u]], gx);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; u++) {
+        const unsigned long long nw = old[u] + inc[u];
+        pcell[u] = cl[jo[u]];
+        if (PACKED) {
+            const uint32_t low = (uint32_t)nw;
+            push[u] = (low >> kp) == 1u;
+            ppos[u] = low & ((1u << kp) - 1u);
+        } else {
+            push[u] = (nw >> 32) == 1ull;
+            ppos[u] = (uint32_t)nw;
+        }
+    }
+}
 
 // Grid-wide barrier in two levels: the workgroups of group g (blockIdx % G)
 // arrive on the group's counter, the last of each group on the top counter,
@@ -772,8 +853,12 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
 
     if (!skip) {
         const uint32_t nsup = (uint32_t)ctrl->n_support;
-        if (!a.planned) {
-            // round-0 frontier: every cell with exactly one element
+        const uint32_t kp = pack_bits(nsup);
+        const bool packed = std::is_same<T, int32_t>::value && a.counted && ctrl->nopack == 0;
+        if (packed || !a.planned) {
+            // packed: each counter takes its cell's residual in its high
+            // word; without a queued frontier, round 0's is every cell with
+            // exactly one element
             for (uint32_t base = 0; base < a.cells; base += nthreads) {
                 const uint32_t cidx = base + gtid;
                 bool pure = false;
@@ -781,11 +866,18 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                 if (cidx < a.cells) {
                     v = a.cnt[cidx];
                     pure = (v >> 32) == 1ull;
+                    if constexpr (std::is_same<T, int32_t>::value) {
+                        if (packed)
+                            a.cnt[cidx] = ((unsigned long long)(uint32_t)a.yw[cidx] << 32) |
+                                          (((v >> 32) << kp) + (v & 0xffffffffull));
+                    }
                 }
-                lds_push(q, pure, cidx, (uint32_t)v);
-                flush_pushes(q, false, kPeelBlock, &sync->tail.v[0], a.queue, a.cells);
+                if (!a.planned) {
+                    lds_push(q, pure, cidx, (uint32_t)v);
+                    flush_pushes(q, false, kPeelBlock, &sync->tail.v[0], a.queue, a.cells);
+                }
             }
-            flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
+            if (!a.planned) flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
         }
         uint32_t fend = 0, gen = 0;
         ok = grid_barrier(ctrl, sync, gridDim.x, gen++, &fend);
@@ -798,8 +890,8 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
             const uint32_t nsweep = (qe - qs + nwaves * 64u - 1u) / (nwaves * 64u);
             for (uint32_t sw = 0; sw < nsweep; sw++) {
                 const uint32_t i = qs + (sw * nwaves + gwave) * 64u + lane;
-                bool push_a = false, push_b = false;
-                uint32_t cell_a = 0, cell_b = 0, pos_a = 0, pos_b = 0;
+                bool push[2] = {false, false};
+                uint32_t pcell[2] = {0u, 0u}, ppos[2] = {0u, 0u};
                 if (i < qe) {
                     // the cell was pure with element pos when queued.  The first
                     // frontier entry of the element to take its flag recovers it;
@@ -808,45 +900,22 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                     // cell's residual are read alongside the claim: once claimed,
                     // nothing else changes that cell this round.
                     const uint2 it = a.queue[i];
-                    const uint32_t cidx = it.x, pos = it.y;
-                    if (pos < nsup) {
-                        // one word per element: claims of neighbouring elements
-                        // would otherwise queue up on a shared word
-                        const bool taken = atomicExch(a.peeled + pos, 1u) != 0u;
-                        const uint32_t p = a.elem[pos];
-                        const T ycell = a.yw[cidx];
-                        const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p >> a.log2c);
-                        const uint32_t t = p & a.cmask;
-                        uint32_t cl[3];
-#pragma unroll
-                        for (int j = 0; j < 3; j++) cl[j] = cell_of(h, j, t, a.c, a.cmask);
-                        const int j = cl[0] == cidx ? 0 : (cl[1] == cidx ? 1 : 2);
-                        if (!taken && cl[j] == cidx) {
-                            const T val = Val<T>::sign(ycell, (h.neg >> j) & 1u);
-                            a.vals[pos] = val;
-                            my_recovered++;
-                            my_last_round = r + 1u;
-                            const int ja = j == 0 ? 1 : 0;
-                            const int jb = j == 2 ? 1 : 2;
-                            const unsigned long long dec = 0ull - (kOne + pos);
-                            const unsigned long long old_a = atomicAdd(a.cnt + cl[ja], dec);
-                            const unsigned long long old_b = atomicAdd(a.cnt + cl[jb], dec);
-                            Val<T>::atomic_add(a.yw + cl[ja],
-                                               Val<T>::sign(val, !((h.neg >> ja) & 1u)));
-                            Val<T>::atomic_add(a.yw + cl[jb],
-                                               Val<T>::sign(val, !((h.neg >> jb) & 1u)));
-                            const unsigned long long new_a = old_a + dec, new_b = old_b + dec;
-                            push_a = (new_a >> 32) == 1ull;
-                            push_b = (new_b >> 32) == 1ull;
-                            cell_a = cl[ja];
-                            cell_b = cl[jb];
-                            pos_a = (uint32_t)new_a;
-                            pos_b = (uint32_t)new_b;
+                    if (it.y < nsup) {
+                        bool done = false;
+                        if constexpr (std::is_same<T, int32_t>::value) {
+                            if (packed) {
+                                peel_entry<T, true>(a, it.x, it.y, kp, r, my_recovered,
+                                                    my_last_round, push, pcell, ppos);
+                                done = true;
+                            }
                         }
+                        if (!done)
+                            peel_entry<T, false>(a, it.x, it.y, kp, r, my_recovered,
+                                                 my_last_round, push, pcell, ppos);
                     }
                 }
-                lds_push(q, push_a, cell_a, pos_a);
-                lds_push(q, push_b, cell_b, pos_b);
+                lds_push(q, push[0], pcell[0], ppos[0]);
+                lds_push(q, push[1], pcell[1], ppos[1]);
                 flush_pushes(q, false, 2u * kPeelBlock, &sync->tail.v[0], a.queue, a.cells);
             }
             flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
@@ -863,8 +932,11 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                 const uint32_t t = p & a.cmask;
                 T e3[3];
 #pragma unroll
-                for (int j = 0; j < 3; j++)
-                    e3[j] = Val<T>::sign(a.yw[cell_of(h, j, t, a.c, a.cmask)], (h.neg >> j) & 1u);
+                for (int j = 0; j < 3; j++) {
+                    const uint32_t cell = cell_of(h, j, t, a.c, a.cmask);
+                    const T y = packed ? (T)(int32_t)(uint32_t)(a.cnt[cell] >> 32) : a.yw[cell];
+                    e3[j] = Val<T>::sign(y, (h.neg >> j) & 1u);
+                }
                 a.vals[pos] = median3(e3[0], e3[1], e3[2]);
             }
         }
@@ -1234,6 +1306,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     pa.log2c = g.log2c;
     pa.cells = g.cells;
     pa.planned = planned && !wave_rows;
+    pa.counted = planned;
     void* args[] = {&pa};
     e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&peel_kernel<A>),
                                    dim3(peel_grid), dim3(kPeelBlock), args,
