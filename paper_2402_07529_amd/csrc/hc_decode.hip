@@ -49,6 +49,7 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kPeelBlock = 1024;  // lanes per workgroup of the persistent peel kernel
 constexpr uint64_t kPeelHalfGridCells = 8ull << 20;  // below this many cells the peel uses half the CUs
+constexpr uint64_t kPeelHalfGridCellsInt = 32ull << 20;  // the same with residuals in the counters
 constexpr unsigned long long kOne = 1ull << 32;  // one incidence in a packed counter
 
 // The int32 peel can carry a cell's residual in its counter word: value in
@@ -1285,8 +1286,15 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     // bound by the atomics the CUs can keep in flight (about 10 % higher on
     // half the CUs).  Rounds are about 50-65 at the default sketch ratio, so
     // a small sketch, with few entries per round, peels faster on half the
-    // CUs and a large one on all of them; the two meet near 8 M cells.
-    const uint32_t peel_grid = g.cells < kPeelHalfGridCells && peel_grid_cache[slot] >= 2
+    // CUs and a large one on all of them; with five atomics per element the
+    // two meet near 8 M cells.  The int32 peel with a plan (residuals in the
+    // counters, three atomics per element) measured faster on half the CUs up
+    // to 11 M cells, and slower at 97 M (BERT-base at 5 %: 16.1 against
+    // 18.3 ms).
+    const bool fewer_atomics = std::is_same<T, int32_t>::value && planned;
+    const uint64_t half_below = fewer_atomics ? kPeelHalfGridCellsInt : kPeelHalfGridCells;
+    const uint32_t peel_grid = g.cells < half_below &&
+                                       peel_grid_cache[slot] >= 2
                                    ? (uint32_t)peel_grid_cache[slot] / 2u
                                    : (uint32_t)peel_grid_cache[slot];
     PeelArgs<A> pa;
