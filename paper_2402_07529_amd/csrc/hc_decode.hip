@@ -16,10 +16,9 @@
 //            its low word is that element's position.  With a plan (the
 //            inverse row map of hc_plan.hip) one workgroup per sketch row
 //            gathers its counters from the bitmap words of the batches that
-//            land on it -- no atomics -- and seeds the round-0 frontier with the
-//            row's pure cells.  Without a plan every element adds itself to its
-//            three cells with 64-bit atomics and the peel kernel finds the
-//            pure cells by a scan;
+//            land on it -- no atomics.  Without a plan every element adds
+//            itself to its three cells with 64-bit atomics.  Either way the
+//            peel kernel finds the round-0 frontier, the pure cells, by a scan;
 //   peel     one cooperative persistent kernel running synchronous rounds
 //            (section 3.2, parallel peeling).  The frontier of round r is the
 //            list of (cell, element) pairs whose cell became pure during round
@@ -48,6 +47,8 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kPeelBlock = 1024;  // lanes per workgroup of the persistent peel kernel
+constexpr uint32_t kScanCells = 4;  // cells a lane takes per pass of the round-0 scan
+constexpr uint32_t kPeelPushCap = 8 * kPeelBlock;  // staged frontier entries per workgroup (64 KiB)
 constexpr uint64_t kPeelHalfGridCells = 8ull << 20;  // below this many cells the peel uses half the CUs
 constexpr uint64_t kPeelHalfGridCellsInt = 32ull << 20;  // the same with residuals in the counters
 constexpr unsigned long long kOne = 1ull << 32;  // one incidence in a packed counter
@@ -484,9 +485,7 @@ struct CounterArgs {
     const uint32_t* b;
     const uint32_t* woffb;  // set bits before each batch (nb + 1 entries)
     unsigned long long* cnt;
-    uint2* queue;
     Ctrl* ctrl;
-    PeelSync* sync;
     uint64_t n, seed, words, nb;
     uint32_t rows, c, cmask, cells, last_mask;
 };
@@ -505,8 +504,9 @@ struct CounterArgs {
 //   add     wave w takes staged batches w, w + 4, ...: each lane covers C/64
 //           consecutive cells, finds their parameters' bits in the staged
 //           words and adds into the row's counters in LDS.
-// The row is then written once, and its pure cells become the round-0
-// frontier.
+// The row is then written once.  Its pure cells are left for the peel
+// kernel's scan: queuing them here took one append on the shared queue tail
+// per row (VGG19: 10 K rows, about 0.15 ms of contended atomics).
 constexpr uint32_t kStage = 64;  // live batches staged in LDS at a time
 constexpr uint64_t kWaveRowsEntries = 8;  // plan entries per row up to which a wave takes a row
 
@@ -520,7 +520,6 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
     __shared__ uint32_t s_boff[kStage];
     __shared__ uint2 s_live[kBlock];
     __shared__ uint32_t s_tmp[kWaves];
-    __shared__ PushBuf<C> q;
     const PlanHeader* hdr = a.hdr;
     const bool ok = hdr->magic == kPlanMagic && hdr->n == a.n && hdr->seed == a.seed &&
                     hdr->c == a.c && hdr->rows == a.rows;
@@ -532,7 +531,6 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
     const uint32_t kpack = pack_bits(a.ctrl->n_support);
     const uint32_t lane = lane_id();
     const uint32_t wave = threadIdx.x >> 6;
-    if (threadIdx.x == 0) q.count = 0;
     for (uint32_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
         for (uint32_t k = threadIdx.x; k < C; k += kBlock) s_acc[k] = 0ull;
         const uint32_t e0 = a.rowoff[row], e1 = a.rowoff[row + 1];
@@ -586,15 +584,11 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
         }
         for (uint32_t k = threadIdx.x; k < C; k += kBlock) {
             const unsigned long long acc = s_acc[k];
-            const uint32_t cell = row * C + k;
-            const bool pure = (acc >> 32) == 1ull;
-            a.cnt[cell] = acc;
+            a.cnt[row * C + k] = acc;
             if (!fits_packed(acc, kpack)) atomicOr(&a.ctrl->nopack, 1u);
-            lds_push(q, pure, cell, (uint32_t)acc);
         }
-        flush_pushes(q, false, C, &a.sync->tail.v[0], a.queue, a.cells);
+        lds_barrier();  // s_acc is cleared for the next row
     }
-    flush_pushes(q, true, 0, &a.sync->tail.v[0], a.queue, a.cells);
 }
 
 // Rows that few batches land on (a sketch much wider than the support): one
@@ -602,10 +596,7 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
 // live batches are visited in turn: lanes 0..C/32-1 load the batch's bitmap
 // words and rank offsets, every lane takes the (at most two) words covering
 // its C/64 consecutive cells by shuffle and adds into its own cells of the
-// wave's copy of the row in LDS.  The row is written with plain stores and
-// nothing is queued: the peel kernel finds the round-0 frontier by scanning
-// the counters, which for such sketches costs less than one queue append per
-// row.
+// wave's copy of the row in LDS.  The row is written with plain stores.
 template <int C>
 __global__ __launch_bounds__(kBlock) void counter_wave_kernel(CounterArgs a) {
     constexpr uint32_t WPB = C / 32;  // bitmap words per batch
@@ -692,7 +683,6 @@ struct PeelArgs {  // T: the decode-side arithmetic type
     InfoDev* info;
     uint64_t seed;
     uint32_t rows, c, cmask, log2c, cells;
-    bool planned;   // the round-0 frontier is already queued
     bool counted;   // a counter kernel built the counters (and checked their packing)
 };
 
@@ -830,7 +820,7 @@ __device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks, uint32_
 
 template <typename T>
 __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
-    __shared__ PushBuf<4 * kPeelBlock> q;
+    __shared__ PushBuf<kPeelPushCap> q;
     __shared__ uint32_t s_red[2];
     Ctrl* ctrl = a.ctrl;
     PeelSync* sync = a.sync;
@@ -856,30 +846,29 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
         const uint32_t nsup = (uint32_t)ctrl->n_support;
         const uint32_t kp = pack_bits(nsup);
         const bool packed = std::is_same<T, int32_t>::value && a.counted && ctrl->nopack == 0;
-        if (packed || !a.planned) {
-            // packed: each counter takes its cell's residual in its high
-            // word; without a queued frontier, round 0's is every cell with
-            // exactly one element
-            for (uint32_t base = 0; base < a.cells; base += nthreads) {
-                const uint32_t cidx = base + gtid;
-                bool pure = false;
-                unsigned long long v = 0;
-                if (cidx < a.cells) {
-                    v = a.cnt[cidx];
-                    pure = (v >> 32) == 1ull;
-                    if constexpr (std::is_same<T, int32_t>::value) {
-                        if (packed)
-                            a.cnt[cidx] = ((unsigned long long)(uint32_t)a.yw[cidx] << 32) |
-                                          (((v >> 32) << kp) + (v & 0xffffffffull));
-                    }
-                }
-                if (!a.planned) {
-                    lds_push(q, pure, cidx, (uint32_t)v);
-                    flush_pushes(q, false, kPeelBlock, &sync->tail.v[0], a.queue, a.cells);
-                }
+        // round 0's frontier is every cell with exactly one element; packed,
+        // each counter also takes its cell's residual in its high word.  Four
+        // cells per lane and pass, loaded together, then staged.
+        for (uint32_t base = 0; base < a.cells; base += kScanCells * nthreads) {
+            unsigned long long v[kScanCells];
+#pragma unroll
+            for (uint32_t m = 0; m < kScanCells; m++) {
+                const uint32_t cidx = base + m * nthreads + gtid;
+                v[m] = cidx < a.cells ? a.cnt[cidx] : 0ull;
             }
-            if (!a.planned) flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
+#pragma unroll
+            for (uint32_t m = 0; m < kScanCells; m++) {
+                const uint32_t cidx = base + m * nthreads + gtid;
+                if constexpr (std::is_same<T, int32_t>::value) {
+                    if (packed && cidx < a.cells)
+                        a.cnt[cidx] = ((unsigned long long)(uint32_t)a.yw[cidx] << 32) |
+                                      (((v[m] >> 32) << kp) + (v[m] & 0xffffffffull));
+                }
+                lds_push(q, (v[m] >> 32) == 1ull, cidx, (uint32_t)v[m]);
+            }
+            flush_pushes(q, false, kScanCells * kPeelBlock, &sync->tail.v[0], a.queue, a.cells);
         }
+        flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
         uint32_t fend = 0, gen = 0;
         ok = grid_barrier(ctrl, sync, gridDim.x, gen++, &fend);
 
@@ -1200,7 +1189,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     const T* y_agg = static_cast<const T*>(y_agg_v);
     const bool planned = plan != nullptr;
     // few plan entries per row (a sketch much wider than the support): one
-    // wave per row, and the round-0 frontier from the peel kernel's scan
+    // wave per row
     const bool wave_rows = planned && 3ull * ((g.n + g.c - 1) / g.c) <= kWaveRowsEntries * g.rows;
 
     DeviceInfo di;
@@ -1255,9 +1244,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
         ca.b = b;
         ca.woffb = woffb;
         ca.cnt = cnt;
-        ca.queue = queue;
         ca.ctrl = ctrl;
-        ca.sync = sync;
         ca.n = g.n;
         ca.seed = g.seed;
         ca.words = g.words;
@@ -1333,7 +1320,6 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     pa.cmask = g.cmask;
     pa.log2c = g.log2c;
     pa.cells = g.cells;
-    pa.planned = planned && !wave_rows;
     pa.counted = planned;
     void* args[] = {&pa};
     e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&peel_kernel<A>),
