@@ -32,9 +32,10 @@
 //            is already taken (in this round or an earlier one) do nothing, so
 //            the elements peeled in round r are exactly those with a cell in
 //            its frontier that were still live when it began.
-//            One grid barrier per round; rounds end when a frontier is empty.
-//            Elements never peeled get the Count Sketch median estimate from
-//            the residual sketch (Algorithm 1, last recovery step);
+//            One grid barrier per round; rounds end when a frontier is empty;
+//   leftovers  elements never peeled get the Count Sketch median estimate
+//            from the residual sketch (Algorithm 1, last recovery step), on
+//            the whole chip: when decoding fails most of the support is left;
 //   emit     dense output, recovered mask and COO from E and the values.
 #include <type_traits>
 
@@ -463,6 +464,16 @@ __device__ void flush_pushes(Q& q, bool force, uint32_t room, unsigned int* tail
 
 // ---- counters by row (planned path) --------------------------------------------
 
+// Called by every lane of a wave: sets ctrl->nopack if some lane's cells do
+// not fit the packed form.  One lane of the wave, and only while the flag is
+// still clear: a sketch far narrower than its support fails in most cells,
+// and an atomic per cell on one word took milliseconds.
+__device__ __forceinline__ void flag_unpackable(Ctrl* ctrl, bool fits) {
+    if (__ballot(!fits) == 0ull || lane_id() != 0) return;
+    if (__hip_atomic_load(&ctrl->nopack, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u)
+        atomicOr(&ctrl->nopack, 1u);
+}
+
 // Lane l < WPB holds word l of a batch (other lanes hold 0): the set bits in
 // words 0..l-1, i.e. the word's rank offset within the batch.
 template <uint32_t WPB>
@@ -582,11 +593,13 @@ __global__ __launch_bounds__(kBlock) void counter_kernel(CounterArgs a) {
                 lds_barrier();  // the staging buffers are reused
             }
         }
+        bool fits = true;
         for (uint32_t k = threadIdx.x; k < C; k += kBlock) {
             const unsigned long long acc = s_acc[k];
             a.cnt[row * C + k] = acc;
-            if (!fits_packed(acc, kpack)) atomicOr(&a.ctrl->nopack, 1u);
+            fits = fits && fits_packed(acc, kpack);
         }
+        flag_unpackable(a.ctrl, fits);
         lds_barrier();  // s_acc is cleared for the next row
     }
 }
@@ -664,7 +677,7 @@ __global__ __launch_bounds__(kBlock) void counter_wave_kernel(CounterArgs a) {
             dst[i * 64u + lane] = v;
             fits = fits && fits_packed(v, kpack);
         }
-        if (!fits) atomicOr(&a.ctrl->nopack, 1u);
+        flag_unpackable(a.ctrl, fits);
     }
 }
 
@@ -913,23 +926,6 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
             ok = grid_barrier(ctrl, sync, gridDim.x, gen++, &fend);
         }
 
-        // leftovers: Count Sketch median estimate from the residual sketch
-        if (ok) {
-            for (uint32_t pos = gtid; pos < nsup; pos += nthreads) {
-                if (a.peeled[pos]) continue;
-                const uint32_t p = a.elem[pos];
-                const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p >> a.log2c);
-                const uint32_t t = p & a.cmask;
-                T e3[3];
-#pragma unroll
-                for (int j = 0; j < 3; j++) {
-                    const uint32_t cell = cell_of(h, j, t, a.c, a.cmask);
-                    const T y = packed ? (T)(int32_t)(uint32_t)(a.cnt[cell] >> 32) : a.yw[cell];
-                    e3[j] = Val<T>::sign(y, (h.neg >> j) & 1u);
-                }
-                a.vals[pos] = median3(e3[0], e3[1], e3[2]);
-            }
-        }
     }
 
     // per-workgroup totals, one atomic each; the last workgroup to finish
@@ -964,6 +960,38 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
             a.info->success = (!skip && !aborted && rec == ns) ? 1u : 0u;
             a.info->status = bad_plan ? 3u : (overflow ? 1u : (aborted ? 2u : 0u));
         }
+    }
+}
+
+// ---- leftovers ---------------------------------------------------------------------
+
+// Algorithm 1's last recovery step for the elements the peel left: the Count
+// Sketch median estimate of each one's three cells in the residual sketch
+// (from the counters' high words when the peel packed the int32 residuals
+// there).  A kernel of its own over the whole chip, not the peel's workgroups:
+// when decoding fails most of the support is left, at three scattered loads
+// per element.
+template <typename T>
+__global__ __launch_bounds__(kBlock) void leftover_kernel(PeelArgs<T> a) {
+    const Ctrl* ctrl = a.ctrl;
+    if (ctrl->overflow != 0 || ctrl->bad_plan != 0) return;
+    const uint32_t nsup = (uint32_t)ctrl->n_support;
+    // the same test as the peel kernel's
+    const bool packed = std::is_same<T, int32_t>::value && a.counted && ctrl->nopack == 0;
+    const uint32_t stride = gridDim.x * kBlock;
+    for (uint32_t pos = blockIdx.x * kBlock + threadIdx.x; pos < nsup; pos += stride) {
+        if (a.peeled[pos]) continue;
+        const uint32_t p = a.elem[pos];
+        const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p >> a.log2c);
+        const uint32_t t = p & a.cmask;
+        T e3[3];
+#pragma unroll
+        for (int j = 0; j < 3; j++) {
+            const uint32_t cell = cell_of(h, j, t, a.c, a.cmask);
+            const T y = packed ? (T)(int32_t)(uint32_t)(a.cnt[cell] >> 32) : a.yw[cell];
+            e3[j] = Val<T>::sign(y, (h.neg >> j) & 1u);
+        }
+        a.vals[pos] = median3(e3[0], e3[1], e3[2]);
     }
 }
 
@@ -1328,6 +1356,8 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     if (e != hipSuccess) return e;
 
     if (out.x_out != nullptr || out.mask != nullptr || out.coo_idx != nullptr) {
+        hipLaunchKernelGGL(leftover_kernel<A>, dim3((uint32_t)di.cus * 8), dim3(kBlock), 0, s, pa);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
         EmitArgs<T> ea;
         ea.b = b;
         ea.blk = blk;
