@@ -369,3 +369,21 @@ def test_decode_unaligned_views(use_plan, density):
     assert np.array_equal(out[1:].cpu().numpy(), a["x"])
     assert np.array_equal(mask[1:].cpu().numpy().view(np.uint32), a["mask"])
     assert np.array_equal(a["x"], wrap_sum([w.dense(i) for i in range(w.W)]))
+
+
+def test_unpackable_counters_fall_back():
+    # 4.2 M elements on three rows: every cell holds about 1,400 of them, so
+    # deg * 2^k + (sum of positions) overflows 32 bits and the int32 peel keeps
+    # its residuals apart from the counters; nothing peels and every element
+    # gets the median estimate.  Exact against the oracle all the same.
+    _hc()
+    w = wl.make("synthetic", n=6_000_011, W=1, density=0.7, data_seed=4242)
+    rows = 3
+    print(f"[unpackable] n={w.n} nonzeros={w.n_agg} rows={rows}", flush=True)
+    g = gpu_run(w, rows, 1024, want_coo_out=False, use_plan=True, max_support=w.n_agg)
+    o = oracle_run(w, rows, 1024)
+    assert np.array_equal(g["Ya"], o["Ya"])
+    assert np.array_equal(g["x"], o["x"])
+    assert np.array_equal(g["mask"], o["mask"])
+    assert_same_info(g["info"], o["info"])
+    assert g["info"].n_recovered == 0
