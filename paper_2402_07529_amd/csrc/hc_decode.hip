@@ -27,8 +27,9 @@
 //            first of its frontier entries to get there recovers
 //            x = g_j * Y from its cell (every pure cell of the element holds the
 //            same value, exactly so in integer arithmetic), and subtracts g * x
-//            and the element from its other two cells with atomics; a cell
-//            whose count drops to one joins the next frontier.  Entries whose element
+//            and the element from its other two cells with atomics (int32 with
+//            a plan: one per cell, the residual riding in the counter word); a
+//            cell whose count drops to one joins the next frontier.  Entries whose element
 //            is already taken (in this round or an earlier one) do nothing, so
 //            the elements peeled in round r are exactly those with a cell in
 //            its frontier that were still live when it began.
