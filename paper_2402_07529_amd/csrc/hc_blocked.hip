@@ -43,7 +43,6 @@ namespace {
 constexpr int kEncThreads = 1024;
 constexpr int kDecThreads = 1024;
 constexpr uint32_t kWaveTile = 1024;          // parameters per wave tile (16 per lane)
-constexpr uint32_t kOutStep = 4 * kDecThreads;  // parameters per output iteration
 constexpr uint32_t kDegShift = 20;
 constexpr uint32_t kDegOne = 1u << kDegShift;
 constexpr uint32_t kSumMask = kDegOne - 1u;
@@ -129,27 +128,6 @@ __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* s_tmp) {
     for (uint32_t w = 0; w < nwaves; w++) t += s_tmp[w];
     lds_barrier();
     return t;
-}
-
-// Exclusive scan over the workgroup; *total gets the sum.
-__device__ __forceinline__ uint32_t block_scan(uint32_t v, uint32_t* s_tmp, uint32_t* total) {
-    const uint32_t lane = lane_id(), wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
-    uint32_t x = v;
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t y = __shfl_up(x, d);
-        if (lane >= (uint32_t)d) x += y;
-    }
-    if (lane == 63) s_tmp[wave] = x;
-    lds_barrier();
-    uint32_t off = 0, tot = 0;
-    for (uint32_t w = 0; w < nwaves; w++) {
-        const uint32_t s = s_tmp[w];
-        if (w < wave) off += s;
-        tot += s;
-    }
-    lds_barrier();
-    *total = tot;
-    return off + x - v;
 }
 
 // Position of the r-th (0-based) set bit of w; r < popcount(w).
