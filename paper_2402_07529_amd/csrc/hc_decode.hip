@@ -1034,7 +1034,9 @@ __device__ __forceinline__ T estimate_raw(const EmitArgs<T>& a, uint32_t p) {
 // flags are first copied into LDS with coalesced loads (when the run fits):
 // the output loop then has no global loads ahead of its stores.  A stage of
 // 2048 members measured best on MI355X: a 4096 one costs NCF's write stream
-// more occupancy than it saves on the denser workloads.
+// more occupancy than it saves on the denser workloads.  The dense output
+// goes out with nontemporal stores (measured 1-2 % faster here, though plain
+// stores win for a pure write stream).
 constexpr uint32_t kEmitStage = 2048;  // members staged per chunk (1/16 of its parameters)
 
 template <typename T>
@@ -1112,7 +1114,7 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
         if (a.x_out != nullptr && p0 < a.n) {
             if (a.x_vec && p0 + 4 <= a.n) {
                 V4 v = {out[0], out[1], out[2], out[3]};
-                *reinterpret_cast<V4*>(a.x_out + p0) = v;
+                __builtin_nontemporal_store(v, reinterpret_cast<V4*>(a.x_out + p0));
             } else {
                 for (int k = 0; k < 4; k++)
                     if (p0 + k < a.n) a.x_out[p0 + k] = out[k];
