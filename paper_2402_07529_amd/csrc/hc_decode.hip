@@ -17,10 +17,12 @@
 //            inverse row map of hc_plan.hip) one workgroup per sketch row
 //            gathers its counters from the bitmap words of the batches that
 //            land on it -- no atomics.  Without a plan every element adds
-//            itself to its three cells with 64-bit atomics.  Either way the
-//            peel kernel finds the round-0 frontier, the pure cells, by a scan;
-//   peel     one cooperative persistent kernel running synchronous rounds
-//            (section 3.2, parallel peeling).  The frontier of round r is the
+//            itself to its three cells with 64-bit atomics;
+//   round 0  a scan queues the pure cells (round 0's frontier) and, for large
+//            sketches, round 0 is peeled, both as ordinary launches over the
+//            whole chip; for smaller ones the peel kernel does both itself;
+//   peel     one cooperative persistent kernel running the later synchronous
+//            rounds (section 3.2, parallel peeling).  The frontier of round r is the
 //            list of (cell, element) pairs whose cell became pure during round
 //            r-1, kept in one append-only queue.  An element owning several
 //            frontier cells is claimed by an atomic exchange on its flag: the
@@ -100,6 +102,7 @@ struct PeelSync {
     SyncLine tail;                // v[0]: queue length
     SyncLine top;                 // v[0]: arrivals of the group leaders
     SyncLine gen;                 // v[0]: barrier generation; v[1]: end of the current frontier
+    SyncLine round0;              // v[0]: end of round 0's frontier in the queue
     SyncLine group[kBarGroups];   // v[0]: arrivals within group g
 };
 
@@ -698,6 +701,7 @@ struct PeelArgs {  // T: the decode-side arithmetic type
     uint64_t seed;
     uint32_t rows, c, cmask, log2c, cells;
     bool counted;   // a counter kernel built the counters (and checked their packing)
+    bool split0;    // round 0 ran before the peel kernel, as whole-chip launches
 };
 
 // One frontier entry (cell cidx, element position pos), for the kernel below.
@@ -844,8 +848,6 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
     // frontiers still spread over every CU
     const uint32_t gwave = (threadIdx.x >> 6) * gridDim.x + blockIdx.x;
     const uint32_t nwaves = gridDim.x * waves_per_block;
-    const uint32_t nthreads = gridDim.x * kPeelBlock;
-    const uint32_t gtid = gwave * 64u + lane;
     const bool skip = ctrl->overflow != 0 || ctrl->bad_plan != 0;
     bool ok = true;
     uint32_t my_recovered = 0, my_last_round = 0;
@@ -860,34 +862,42 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
         const uint32_t nsup = (uint32_t)ctrl->n_support;
         const uint32_t kp = pack_bits(nsup);
         const bool packed = std::is_same<T, int32_t>::value && a.counted && ctrl->nopack == 0;
-        // round 0's frontier is every cell with exactly one element; packed,
-        // each counter also takes its cell's residual in its high word.  Four
-        // cells per lane and pass, loaded together, then staged.
-        for (uint32_t base = 0; base < a.cells; base += kScanCells * nthreads) {
-            unsigned long long v[kScanCells];
+        if (!a.split0) {
+            // round 0's frontier is every cell with exactly one element;
+            // packed, each counter also takes its cell's residual in its high
+            // word.  Four cells per lane and pass, loaded together, then staged.
+            const uint32_t nthreads = gridDim.x * kPeelBlock;
+            const uint32_t gtid = gwave * 64u + lane;
+            for (uint32_t base = 0; base < a.cells; base += kScanCells * nthreads) {
+                unsigned long long v[kScanCells];
 #pragma unroll
-            for (uint32_t m = 0; m < kScanCells; m++) {
-                const uint32_t cidx = base + m * nthreads + gtid;
-                v[m] = cidx < a.cells ? a.cnt[cidx] : 0ull;
-            }
-#pragma unroll
-            for (uint32_t m = 0; m < kScanCells; m++) {
-                const uint32_t cidx = base + m * nthreads + gtid;
-                if constexpr (std::is_same<T, int32_t>::value) {
-                    if (packed && cidx < a.cells)
-                        a.cnt[cidx] = ((unsigned long long)(uint32_t)a.yw[cidx] << 32) |
-                                      (((v[m] >> 32) << kp) + (v[m] & 0xffffffffull));
+                for (uint32_t m = 0; m < kScanCells; m++) {
+                    const uint32_t cidx = base + m * nthreads + gtid;
+                    v[m] = cidx < a.cells ? a.cnt[cidx] : 0ull;
                 }
-                lds_push(q, (v[m] >> 32) == 1ull, cidx, (uint32_t)v[m]);
+#pragma unroll
+                for (uint32_t m = 0; m < kScanCells; m++) {
+                    const uint32_t cidx = base + m * nthreads + gtid;
+                    if constexpr (std::is_same<T, int32_t>::value) {
+                        if (packed && cidx < a.cells)
+                            a.cnt[cidx] = ((unsigned long long)(uint32_t)a.yw[cidx] << 32) |
+                                          (((v[m] >> 32) << kp) + (v[m] & 0xffffffffull));
+                    }
+                    lds_push(q, (v[m] >> 32) == 1ull, cidx, (uint32_t)v[m]);
+                }
+                flush_pushes(q, false, kScanCells * kPeelBlock, &sync->tail.v[0], a.queue,
+                             a.cells);
             }
-            flush_pushes(q, false, kScanCells * kPeelBlock, &sync->tail.v[0], a.queue, a.cells);
+            flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
         }
-        flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
+        // split: round 0 ran before this kernel and the queue holds round 1's
+        // frontier after round 0's
         uint32_t fend = 0, gen = 0;
         ok = grid_barrier(ctrl, sync, gridDim.x, gen++, &fend);
 
-        uint32_t qs = 0;
-        for (uint32_t r = 0; ok; r++) {
+        uint32_t qs = a.split0 ? sync->round0.v[0] : 0u;
+        if (qs > a.cells) qs = a.cells;
+        for (uint32_t r = a.split0 ? 1u : 0u; ok; r++) {
             uint32_t qe = fend;
             if (qe > a.cells) qe = a.cells;  // the queue holds each cell at most once
             if (qe <= qs) break;
@@ -961,6 +971,119 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
             a.info->success = (!skip && !aborted && rec == ns) ? 1u : 0u;
             a.info->status = bad_plan ? 3u : (overflow ? 1u : (aborted ? 2u : 0u));
         }
+    }
+}
+
+// ---- round 0 ---------------------------------------------------------------------
+//
+// For large sketches round 0 runs as ordinary launches over the whole chip,
+// the kernel boundaries serving as its barriers: its frontier is large (2.2 M
+// entries for VGG19), and the whole chip took it 15-20 % faster than the
+// persistent kernel's half grid, which the later, smaller rounds run faster on.
+//   scan0    every cell with exactly one element joins round 0's frontier;
+//            packed, each counter also takes its cell's residual in its high
+//            word.  Four cells per lane and pass, loaded together, then staged;
+//   snap0    records where round 0's frontier ends;
+//   round0   peels round 0's frontier, appending round 1's to the queue.
+constexpr uint32_t kRound0Push = 2048;  // staged entries per workgroup of 256 lanes
+// Below this many cells round 0 stays in the persistent kernel: NCF (1.9 M
+// cells) and LSTM (6.2 M) lost 16-49 us to the three extra launches, VGG19
+// (10.4 M) and BERT-base (11 M) gained about 60 us.
+constexpr uint64_t kRound0SplitCells = 8ull << 20;
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void scan0_kernel(PeelArgs<T> a) {
+    __shared__ PushBuf<kRound0Push> q;
+    const Ctrl* ctrl = a.ctrl;
+    if (ctrl->overflow != 0 || ctrl->bad_plan != 0) return;
+    if (threadIdx.x == 0) q.count = 0;
+    lds_barrier();
+    const uint32_t kp = pack_bits((uint32_t)ctrl->n_support);
+    const bool packed = std::is_same<T, int32_t>::value && a.counted && ctrl->nopack == 0;
+    const uint32_t nthreads = gridDim.x * kBlock;
+    const uint32_t gtid = blockIdx.x * kBlock + threadIdx.x;
+    for (uint32_t base = 0; base < a.cells; base += kScanCells * nthreads) {
+        unsigned long long v[kScanCells];
+#pragma unroll
+        for (uint32_t m = 0; m < kScanCells; m++) {
+            const uint32_t cidx = base + m * nthreads + gtid;
+            v[m] = cidx < a.cells ? a.cnt[cidx] : 0ull;
+        }
+#pragma unroll
+        for (uint32_t m = 0; m < kScanCells; m++) {
+            const uint32_t cidx = base + m * nthreads + gtid;
+            if constexpr (std::is_same<T, int32_t>::value) {
+                if (packed && cidx < a.cells)
+                    a.cnt[cidx] = ((unsigned long long)(uint32_t)a.yw[cidx] << 32) |
+                                  (((v[m] >> 32) << kp) + (v[m] & 0xffffffffull));
+            }
+            lds_push(q, (v[m] >> 32) == 1ull, cidx, (uint32_t)v[m]);
+        }
+        flush_pushes(q, false, kScanCells * kBlock, &a.sync->tail.v[0], a.queue, a.cells);
+    }
+    flush_pushes(q, true, 0, &a.sync->tail.v[0], a.queue, a.cells);
+}
+
+__global__ void snap0_kernel(PeelSync* sync) {
+    if (threadIdx.x == 0) sync->round0.v[0] = sync->tail.v[0];
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void round0_kernel(PeelArgs<T> a) {
+    __shared__ PushBuf<kRound0Push> q;
+    __shared__ uint32_t s_red[2];
+    Ctrl* ctrl = a.ctrl;
+    if (ctrl->overflow != 0 || ctrl->bad_plan != 0) return;
+    if (threadIdx.x == 0) {
+        q.count = 0;
+        s_red[0] = 0;
+        s_red[1] = 0;
+    }
+    lds_barrier();
+    const uint32_t nsup = (uint32_t)ctrl->n_support;
+    const uint32_t kp = pack_bits(nsup);
+    const bool packed = std::is_same<T, int32_t>::value && a.counted && ctrl->nopack == 0;
+    uint32_t qe = a.sync->round0.v[0];
+    if (qe > a.cells) qe = a.cells;
+    uint32_t my_recovered = 0, my_last_round = 0;
+    const uint32_t stride = gridDim.x * kBlock;
+    for (uint32_t base = 0; base < qe; base += stride) {
+        const uint32_t i = base + blockIdx.x * kBlock + threadIdx.x;
+        bool push[2] = {false, false};
+        uint32_t pcell[2] = {0u, 0u}, ppos[2] = {0u, 0u};
+        if (i < qe) {
+            const uint2 it = a.queue[i];
+            if (it.y < nsup) {
+                bool done = false;
+                if constexpr (std::is_same<T, int32_t>::value) {
+                    if (packed) {
+                        peel_entry<T, true>(a, it.x, it.y, kp, 0u, my_recovered, my_last_round,
+                                            push, pcell, ppos);
+                        done = true;
+                    }
+                }
+                if (!done)
+                    peel_entry<T, false>(a, it.x, it.y, kp, 0u, my_recovered, my_last_round,
+                                         push, pcell, ppos);
+            }
+        }
+        lds_push(q, push[0], pcell[0], ppos[0]);
+        lds_push(q, push[1], pcell[1], ppos[1]);
+        flush_pushes(q, false, 2u * kBlock, &a.sync->tail.v[0], a.queue, a.cells);
+    }
+    flush_pushes(q, true, 0, &a.sync->tail.v[0], a.queue, a.cells);
+    // per-workgroup totals into the control block, summed with the peel's
+    my_recovered = wave_sum(my_recovered);
+    uint32_t wmax = my_last_round;
+    for (int d = 32; d >= 1; d >>= 1) wmax = max(wmax, (uint32_t)__shfl_xor(wmax, d));
+    if (lane_id() == 0) {
+        atomicAdd(&s_red[0], my_recovered);
+        atomicMax(&s_red[1], wmax);
+    }
+    lds_barrier();
+    if (threadIdx.x == 0) {
+        if (s_red[0]) atomicAdd(&ctrl->recovered, (unsigned long long)s_red[0]);
+        if (s_red[1]) atomicMax(&ctrl->rounds, s_red[1]);
     }
 }
 
@@ -1352,6 +1475,17 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     pa.log2c = g.log2c;
     pa.cells = g.cells;
     pa.counted = planned;
+    // large sketches (large round-0 frontiers) take round 0 on the whole chip
+    pa.split0 = g.cells >= kRound0SplitCells;
+    if (pa.split0) {
+        const uint32_t grid0 = (uint32_t)di.cus * 8;
+        hipLaunchKernelGGL(scan0_kernel<A>, dim3(grid0), dim3(kBlock), 0, s, pa);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(snap0_kernel, dim3(1), dim3(64), 0, s, sync);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(round0_kernel<A>, dim3(grid0), dim3(kBlock), 0, s, pa);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     void* args[] = {&pa};
     e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&peel_kernel<A>),
                                    dim3(peel_grid), dim3(kPeelBlock), args,
