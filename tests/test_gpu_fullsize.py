@@ -38,6 +38,26 @@ def sparse_direct_sum(w):
 
 
 @pytest.mark.timeout(900)
+def test_fullsize_vgg19_int32_without_plan():
+    # no plan: the support kernel builds the counters with atomics and the
+    # peel keeps separate residuals; at this sketch size (10.4 M cells) the
+    # scan and round 0 run as whole-chip launches before the persistent peel
+    _hc()
+    w = wl.make("vgg19")
+    n_agg = w.n_agg
+    rows = oracle.rows_for(n_agg)
+    print(f"[fullsize] vgg19 without plan: n={w.n} W={w.W} n_agg={n_agg} rows={rows}", flush=True)
+    g = gpu_run(w, rows, 1024, want_coo_out=False, max_support=n_agg, use_plan=False,
+                keep_workers=False)
+    o = oracle_run(w, rows, 1024)
+    assert np.array_equal(g["Ya"], o["Ya"])
+    assert_same_info(g["info"], o["info"])
+    assert np.array_equal(g["mask"], o["mask"])
+    assert np.array_equal(g["x"], o["x"])
+    assert g["info"].success
+
+
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", ["tiny", "ncf", "lstm", "vgg19", "bert"])
 def test_fullsize_int32(name):
     _hc()
