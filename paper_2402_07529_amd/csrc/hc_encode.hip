@@ -280,7 +280,10 @@ uint32_t grid_for(uint64_t work_items, uint64_t per_block, uint32_t cap) {
 template <typename T, int MODE, bool BL>
 hipError_t launch_dense_t(const Geo& g, const void* x, void* y, uint32_t* b, hipStream_t s,
                           uint64_t ntiles, int cus) {
-    // one resident wave of workgroups: the kernel strides over the tiles
+    // the workgroups that are resident at once stride over the tiles; when
+    // that leaves each wave fewer than 64 tiles, four times as many, so the
+    // dispatcher evens out the last ones (measured on MI355X: VGG19- and
+    // BERT-base-sized gradients 4 % faster; at 2^30 parameters no change)
     static int per_cu = 0;  // resident workgroups per CU (same on every device here)
     if (per_cu == 0) {
         int v = 0;
@@ -289,7 +292,9 @@ hipError_t launch_dense_t(const Geo& g, const void* x, void* y, uint32_t* b, hip
         if (e != hipSuccess) return e;
         per_cu = v > 0 ? v : 1;
     }
-    const uint32_t grid = grid_for(ntiles, 2 * (kBlock / 64), (uint32_t)(cus * per_cu));
+    const uint64_t resident = (uint64_t)cus * per_cu;
+    const uint64_t mult = ntiles < 64 * resident * (kBlock / 64) ? 4 : 1;
+    const uint32_t grid = grid_for(ntiles, 2 * (kBlock / 64), (uint32_t)(resident * mult));
     hipLaunchKernelGGL((encode_dense_kernel<T, MODE, BL>), dim3(grid), dim3(kBlock), 0, s,
                        static_cast<const T*>(x), static_cast<T*>(y), b, g.n, g.words, g.seed,
                        g.rows, g.c, g.cmask, g.log2c,
