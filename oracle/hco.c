@@ -508,7 +508,7 @@ static uint64_t support_of(const hco_geom *g, const uint32_t *B, uint64_t **out_
  *      all three of its cells, Y[h_j] -= g_j * x.
  * Rounds stop when a round recovers nothing.  Parameters still set in the
  * bitmap get the Count Sketch median estimate from the residual sketch
- * (Algorithm 1, "estimate the not recovered parameters"; footnote of 3.2). */
+ * (the last recovery step of Algorithm 1; footnote of 3.2). */
 int hco_decode_i32(const hco_geom *g, const int32_t *Y, const uint32_t *B,
                    int32_t *x_out, uint32_t *mask, hco_info *info,
                    uint32_t *round_of)

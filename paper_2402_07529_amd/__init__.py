@@ -255,15 +255,28 @@ def make_plan(p: hc_params, device="cuda", stream=None):
     return plan
 
 
+def _coo_cap(coo_idx, coo_val) -> int:
+    """COO capacity: the decode writes up to coo_idx.numel() entries of both."""
+    if (coo_idx is None) != (coo_val is None):
+        raise ValueError("coo_idx and coo_val must both be given or both be None")
+    if coo_idx is None:
+        return 0
+    if coo_val.numel() < coo_idx.numel():
+        raise ValueError(f"coo_val has {coo_val.numel()} elements, fewer than coo_idx's "
+                         f"{coo_idx.numel()} (the decode writes that many of each)")
+    return coo_idx.numel()
+
+
 def hc_decode(p: hc_params, y_agg, b_agg, info, ws, x_out=None, coo_idx=None, coo_val=None,
               mask=None, max_support: int = 0, stream=None, plan=None):
     import torch
+    coo_cap = _coo_cap(coo_idx, coo_val)
     _check(_lib.hc_decode(ctypes.byref(p), _ptr(plan, "plan", (torch.uint8,)),
                           _ptr(y_agg, "y_agg", _vdtypes(p), p.cells),
                           _ptr(b_agg, "b_agg", _u32(), p.index_words),
                           _ptr(x_out, "x_out", _vdtypes(p), p.n),
-                          _ptr(coo_idx, "coo_idx", _u32()), _ptr(coo_val, "coo_val", _vdtypes(p)),
-                          coo_idx.numel() if coo_idx is not None else 0,
+                          _ptr(coo_idx, "coo_idx", _u32()),
+                          _ptr(coo_val, "coo_val", _vdtypes(p), coo_cap), coo_cap,
                           _ptr(mask, "mask", _u32(), p.words),
                           _ptr(info, "info", (torch.uint8,), INFO_BYTES),
                           max_support, _ptr(ws, "ws", (torch.uint8,)),

@@ -4,8 +4,10 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <map>
 #include <mutex>
 #include <string>
+#include <tuple>
 
 #include "../../include/hc.h"
 #include "hc_internal.h"
@@ -93,7 +95,9 @@ hc_status blocked_supported(const Geo& g) {
 }
 
 std::mutex g_dev_mu;
-int g_dev_cus[64];
+std::map<int, int> g_dev_cus;                                        // device -> CUs
+std::map<std::tuple<int, const void*, int>, int> g_occupancy;        // -> workgroups per CU
+std::map<std::tuple<int, const void*>, int> g_dyn_lds;               // -> dynamic LDS allowed
 
 }  // namespace
 
@@ -102,14 +106,46 @@ hipError_t device_info(DeviceInfo* out) {
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
     std::lock_guard<std::mutex> lk(g_dev_mu);
-    const int slot = dev & 63;
-    if (g_dev_cus[slot] == 0) {
+    auto it = g_dev_cus.find(dev);
+    if (it == g_dev_cus.end()) {
         int cus = 0;
         e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
         if (e != hipSuccess) return e;
-        g_dev_cus[slot] = cus > 0 ? cus : 1;
+        it = g_dev_cus.emplace(dev, cus > 0 ? cus : 1).first;
     }
-    out->cus = g_dev_cus[slot];
+    out->cus = it->second;
+    return hipSuccess;
+}
+
+hipError_t occupancy_per_cu(const void* kernel, int block, int* out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lk(g_dev_mu);
+    const auto key = std::make_tuple(dev, kernel, block);
+    auto it = g_occupancy.find(key);
+    if (it == g_occupancy.end()) {
+        int v = 0;
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, kernel, block, 0);
+        if (e != hipSuccess) return e;
+        if (v < 1) return hipErrorInvalidConfiguration;
+        it = g_occupancy.emplace(key, v).first;
+    }
+    *out = it->second;
+    return hipSuccess;
+}
+
+hipError_t allow_dynamic_lds(const void* kernel, int bytes) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lk(g_dev_mu);
+    const auto key = std::make_tuple(dev, kernel);
+    auto it = g_dyn_lds.find(key);
+    if (it != g_dyn_lds.end() && it->second >= bytes) return hipSuccess;
+    e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) return e;
+    g_dyn_lds[key] = bytes;
     return hipSuccess;
 }
 
@@ -407,23 +443,50 @@ hc_status hc_plan_build(const hc_params* p, void* plan, size_t plan_bytes, hipSt
     return e == hipSuccess ? HC_OK : fail_hip(e, "hc_plan_build");
 }
 
+}  // extern "C"
+
+namespace {
+
+// hc_decode's argument checks, workspace check and launches.
+hc_status decode_impl(const hc_params* p, const void* plan, const void* y_agg,
+                      const uint32_t* b_agg, void* x_out, uint32_t* coo_idx, void* coo_val,
+                      uint64_t coo_cap, uint32_t* mask, hc_decode_info* info,
+                      uint64_t max_support, void* ws, size_t ws_bytes, hipStream_t stream);
+
+}  // namespace
+
+extern "C" {
+
 hc_status hc_decode(const hc_params* p, const void* plan, const void* y_agg,
                     const uint32_t* b_agg, void* x_out, uint32_t* coo_idx, void* coo_val,
                     uint64_t coo_cap, uint32_t* mask, hc_decode_info* info, uint64_t max_support,
                     void* ws, size_t ws_bytes, hipStream_t stream) {
     g_last_error.clear();
+    if (!ws) return fail(HC_EINVAL, "ws must be non-NULL");
+    return decode_impl(p, plan, y_agg, b_agg, x_out, coo_idx, coo_val, coo_cap, mask, info,
+                       max_support, ws, ws_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+hc_status decode_impl(const hc_params* p, const void* plan, const void* y_agg,
+                      const uint32_t* b_agg, void* x_out, uint32_t* coo_idx, void* coo_val,
+                      uint64_t coo_cap, uint32_t* mask, hc_decode_info* info,
+                      uint64_t max_support, void* ws, size_t ws_bytes, hipStream_t stream) {
     Geo g;
     const hc_status s = to_geo(p, &g);
     if (s != HC_OK) return s;
     if (plan && g.block) return fail(HC_EINVAL, "a blocked sketch is decoded without a plan");
     if (plan && (!plan_supported(g) || !aligned(plan, 256)))
         return fail(HC_EINVAL, "plan given for a geometry with c < 256, or not 256-byte aligned");
-    if (!y_agg || !b_agg || !info || !ws) return fail(HC_EINVAL, "y_agg, b_agg, info and ws must be non-NULL");
+    if (!y_agg || !b_agg || !info) return fail(HC_EINVAL, "y_agg, b_agg and info must be non-NULL");
     if (!aligned(y_agg, 4) || !aligned(b_agg, 4) || (x_out && !aligned(x_out, 4)) ||
         (mask && !aligned(mask, 4)) || (coo_idx && !aligned(coo_idx, 4)) ||
         (coo_val && !aligned(coo_val, 4)))
         return fail(HC_EINVAL, "buffers must be 4-byte aligned");
-    if (!aligned(ws, 256) || !aligned(info, 8))
+    if ((ws && !aligned(ws, 256)) || !aligned(info, 8))
         return fail(HC_EINVAL, "ws must be 256-byte and info 8-byte aligned");
     if ((coo_idx == nullptr) != (coo_val == nullptr))
         return fail(HC_EINVAL, "coo_idx and coo_val must both be given or both be NULL");
@@ -434,18 +497,20 @@ hc_status hc_decode(const hc_params* p, const void* plan, const void* y_agg,
     out.coo_cap = coo_cap;
     out.mask = mask;
     out.info = info;
+    const char* where = "hc_decode";
+    const size_t need = g.block ? blocked_layout(g).total : decode_layout(g, max_support).total;
     if (g.block) {
         const hc_status bs = blocked_supported(g);
         if (bs != HC_OK) return bs;
         const BlockedLayout BL = blocked_layout(g);
         if (ws_bytes < BL.total) return fail(HC_EWORKSPACE, "workspace smaller than hc_sizes reports");
         const hipError_t e = launch_decode_blocked(g, y_agg, b_agg, out, BL, ws, stream);
-        return e == hipSuccess ? HC_OK : fail_hip(e, "hc_decode");
+        return e == hipSuccess ? HC_OK : fail_hip(e, where);
     }
     const DecodeLayout L = decode_layout(g, max_support);
-    if (ws_bytes < L.total) return fail(HC_EWORKSPACE, "workspace smaller than hc_sizes reports");
+    if (ws_bytes < need) return fail(HC_EWORKSPACE, "workspace smaller than hc_sizes reports");
     const hipError_t e = launch_decode(g, plan, y_agg, b_agg, out, L, ws, stream);
-    return e == hipSuccess ? HC_OK : fail_hip(e, "hc_decode");
+    return e == hipSuccess ? HC_OK : fail_hip(e, where);
 }
 
-}  // extern "C"
+}  // namespace

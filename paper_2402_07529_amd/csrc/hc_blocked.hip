@@ -30,7 +30,6 @@
 //         recovered mask and COO entries are then written by the same
 //         workgroup: a recovered element finds its value in its claimed cell,
 //         an unrecovered one gets the median estimate from the residual.
-#include <mutex>
 
 #include "../../include/hc.h"
 #include "hc_device.h"
@@ -717,27 +716,19 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 template <typename K>
-hipError_t allow_lds(K kernel, std::once_flag& flag) {
-    hipError_t e = hipSuccess;
-    std::call_once(flag, [&] {
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                                hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)(kLdsBytes - kLdsReserve));
-    });
-    return e;
+hipError_t allow_lds(K kernel) {
+    return allow_dynamic_lds(reinterpret_cast<const void*>(kernel),
+                             (int)(kLdsBytes - kLdsReserve));
 }
-
-std::once_flag g_enc_i32[2], g_enc_f32[2], g_dec_i32, g_dec_f32;
 
 template <typename T>
 hipError_t launch_encode_blocked_t(const Geo& g, const void* x, void* y, uint32_t* b,
-                                   hipStream_t s, std::once_flag (&flags)[2]) {
+                                   hipStream_t s) {
     DeviceInfo di;
     hipError_t e = device_info(&di);
     if (e != hipSuccess) return e;
     const bool pf = g.nblocks <= 2u * (uint32_t)di.cus;
-    e = pf ? allow_lds(&encode_blocked_kernel<T, true>, flags[1])
-           : allow_lds(&encode_blocked_kernel<T, false>, flags[0]);
+    e = pf ? allow_lds(&encode_blocked_kernel<T, true>) : allow_lds(&encode_blocked_kernel<T, false>);
     if (e != hipSuccess) return e;
     EncArgs<T> a;
     a.x = static_cast<const T*>(x);
@@ -769,8 +760,8 @@ hipError_t launch_encode_blocked_t(const Geo& g, const void* x, void* y, uint32_
 template <typename T>
 hipError_t launch_decode_blocked_t(const Geo& g, const void* y_agg, const uint32_t* b,
                                    const DecodeOut& out, const BlockedLayout& L, void* ws,
-                                   hipStream_t s, std::once_flag& flag) {
-    hipError_t e = allow_lds(&decode_blocked_kernel<T>, flag);
+                                   hipStream_t s) {
+    hipError_t e = allow_lds(&decode_blocked_kernel<T>);
     if (e != hipSuccess) return e;
     char* base = static_cast<char*>(ws);
     BCtrl* bctrl = reinterpret_cast<BCtrl*>(base + L.bctrl);
@@ -835,15 +826,15 @@ BlockedLayout blocked_layout(const Geo& g) {
 
 hipError_t launch_encode_blocked(const Geo& g, const void* x, void* y, uint32_t* b,
                                  hipStream_t s) {
-    if (g.f32) return launch_encode_blocked_t<float>(g, x, y, b, s, g_enc_f32);
-    return launch_encode_blocked_t<int32_t>(g, x, y, b, s, g_enc_i32);
+    if (g.f32) return launch_encode_blocked_t<float>(g, x, y, b, s);
+    return launch_encode_blocked_t<int32_t>(g, x, y, b, s);
 }
 
 hipError_t launch_decode_blocked(const Geo& g, const void* y_agg, const uint32_t* b_agg,
                                  const DecodeOut& out, const BlockedLayout& L, void* ws,
                                  hipStream_t s) {
-    if (g.f32) return launch_decode_blocked_t<float>(g, y_agg, b_agg, out, L, ws, s, g_dec_f32);
-    return launch_decode_blocked_t<int32_t>(g, y_agg, b_agg, out, L, ws, s, g_dec_i32);
+    if (g.f32) return launch_decode_blocked_t<float>(g, y_agg, b_agg, out, L, ws, s);
+    return launch_decode_blocked_t<int32_t>(g, y_agg, b_agg, out, L, ws, s);
 }
 
 }  // namespace hc

@@ -9,8 +9,8 @@
 //   scan     exclusive scan of the tile counts (one workgroup) -> offsets and
 //            the support size |S|;
 //   support  one wave per chunk: the set bits become the ascending element
-//            list E ("we know the indexes of all non-zero parameters", section
-//            3.2) and, with a plan, every batch's rank offset;
+//            list E (section 3.2: the index names every nonzero parameter)
+//            and, with a plan, every batch's rank offset;
 //   counters per cell  cnt = deg * 2^32 + (sum of member positions):  a cell
 //            is pure (one live element) exactly when cnt >> 32 == 1, and then
 //            its low word is that element's position.  With a plan (the
@@ -240,8 +240,8 @@ __global__ __launch_bounds__(1024) void scan_kernel(uint32_t* __restrict__ blk, 
 // 64 KiB: long enough to stream at full rate), writing each tile's count and
 // each chunk's offset within its tile; one workgroup scans the tile counts;
 // then one wave per chunk writes the chunk offset the emit kernel reads, the
-// chunk's run of the ascending element list E ("we know the indexes of all
-// non-zero parameters", section 3.2), cleared peeled flags, and either the
+// chunk's run of the ascending element list E (section 3.2: the index names
+// every nonzero parameter), cleared peeled flags, and either the
 // rank offset of every batch of c parameters (with a plan) or the per-cell
 // counters by atomics (without).  A wave per chunk needs no workgroup
 // barriers, so a sparse chunk costs little more than its loads, and dense
@@ -460,7 +460,7 @@ __device__ void flush_pushes(Q& q, bool force, uint32_t room, unsigned int* tail
     lds_barrier();
     const uint32_t base = q.base;
     for (uint32_t k = threadIdx.x; k < n; k += blockDim.x)
-        if (base + k < cells) queue[base + k] = q.item[k];  // a cell is pushed at most once
+        if ((uint64_t)base + k < cells) queue[base + k] = q.item[k];  // a cell is pushed at most once
     lds_barrier();
     if (threadIdx.x == 0) q.count = 0;
     lds_barrier();
@@ -866,24 +866,25 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
             // round 0's frontier is every cell with exactly one element;
             // packed, each counter also takes its cell's residual in its high
             // word.  Four cells per lane and pass, loaded together, then staged.
-            const uint32_t nthreads = gridDim.x * kPeelBlock;
-            const uint32_t gtid = gwave * 64u + lane;
-            for (uint32_t base = 0; base < a.cells; base += kScanCells * nthreads) {
+            // 64-bit indexes: a sketch of nearly 2^32 cells must not wrap
+            const uint64_t nthreads = (uint64_t)gridDim.x * kPeelBlock;
+            const uint64_t gtid = (uint64_t)gwave * 64u + lane;
+            for (uint64_t base = 0; base < a.cells; base += kScanCells * nthreads) {
                 unsigned long long v[kScanCells];
 #pragma unroll
                 for (uint32_t m = 0; m < kScanCells; m++) {
-                    const uint32_t cidx = base + m * nthreads + gtid;
+                    const uint64_t cidx = base + m * nthreads + gtid;
                     v[m] = cidx < a.cells ? a.cnt[cidx] : 0ull;
                 }
 #pragma unroll
                 for (uint32_t m = 0; m < kScanCells; m++) {
-                    const uint32_t cidx = base + m * nthreads + gtid;
+                    const uint64_t cidx = base + m * nthreads + gtid;
                     if constexpr (std::is_same<T, int32_t>::value) {
                         if (packed && cidx < a.cells)
                             a.cnt[cidx] = ((unsigned long long)(uint32_t)a.yw[cidx] << 32) |
                                           (((v[m] >> 32) << kp) + (v[m] & 0xffffffffull));
                     }
-                    lds_push(q, (v[m] >> 32) == 1ull, cidx, (uint32_t)v[m]);
+                    lds_push(q, (v[m] >> 32) == 1ull, (uint32_t)cidx, (uint32_t)v[m]);
                 }
                 flush_pushes(q, false, kScanCells * kPeelBlock, &sync->tail.v[0], a.queue,
                              a.cells);
@@ -901,9 +902,10 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
             uint32_t qe = fend;
             if (qe > a.cells) qe = a.cells;  // the queue holds each cell at most once
             if (qe <= qs) break;
-            const uint32_t nsweep = (qe - qs + nwaves * 64u - 1u) / (nwaves * 64u);
+            const uint64_t span = (uint64_t)nwaves * 64u;
+            const uint32_t nsweep = (uint32_t)(((uint64_t)(qe - qs) + span - 1u) / span);
             for (uint32_t sw = 0; sw < nsweep; sw++) {
-                const uint32_t i = qs + (sw * nwaves + gwave) * 64u + lane;
+                const uint64_t i = qs + ((uint64_t)sw * nwaves + gwave) * 64u + lane;
                 bool push[2] = {false, false};
                 uint32_t pcell[2] = {0u, 0u}, ppos[2] = {0u, 0u};
                 if (i < qe) {
@@ -1000,24 +1002,24 @@ __global__ __launch_bounds__(kBlock) void scan0_kernel(PeelArgs<T> a) {
     lds_barrier();
     const uint32_t kp = pack_bits((uint32_t)ctrl->n_support);
     const bool packed = std::is_same<T, int32_t>::value && a.counted && ctrl->nopack == 0;
-    const uint32_t nthreads = gridDim.x * kBlock;
-    const uint32_t gtid = blockIdx.x * kBlock + threadIdx.x;
-    for (uint32_t base = 0; base < a.cells; base += kScanCells * nthreads) {
+    const uint64_t nthreads = (uint64_t)gridDim.x * kBlock;
+    const uint64_t gtid = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+    for (uint64_t base = 0; base < a.cells; base += kScanCells * nthreads) {
         unsigned long long v[kScanCells];
 #pragma unroll
         for (uint32_t m = 0; m < kScanCells; m++) {
-            const uint32_t cidx = base + m * nthreads + gtid;
+            const uint64_t cidx = base + m * nthreads + gtid;
             v[m] = cidx < a.cells ? a.cnt[cidx] : 0ull;
         }
 #pragma unroll
         for (uint32_t m = 0; m < kScanCells; m++) {
-            const uint32_t cidx = base + m * nthreads + gtid;
+            const uint64_t cidx = base + m * nthreads + gtid;
             if constexpr (std::is_same<T, int32_t>::value) {
                 if (packed && cidx < a.cells)
                     a.cnt[cidx] = ((unsigned long long)(uint32_t)a.yw[cidx] << 32) |
                                   (((v[m] >> 32) << kp) + (v[m] & 0xffffffffull));
             }
-            lds_push(q, (v[m] >> 32) == 1ull, cidx, (uint32_t)v[m]);
+            lds_push(q, (v[m] >> 32) == 1ull, (uint32_t)cidx, (uint32_t)v[m]);
         }
         flush_pushes(q, false, kScanCells * kBlock, &a.sync->tail.v[0], a.queue, a.cells);
     }
@@ -1046,9 +1048,9 @@ __global__ __launch_bounds__(kBlock) void round0_kernel(PeelArgs<T> a) {
     uint32_t qe = a.sync->round0.v[0];
     if (qe > a.cells) qe = a.cells;
     uint32_t my_recovered = 0, my_last_round = 0;
-    const uint32_t stride = gridDim.x * kBlock;
-    for (uint32_t base = 0; base < qe; base += stride) {
-        const uint32_t i = base + blockIdx.x * kBlock + threadIdx.x;
+    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    for (uint64_t base = 0; base < qe; base += stride) {
+        const uint64_t i = base + (uint64_t)blockIdx.x * kBlock + threadIdx.x;
         bool push[2] = {false, false};
         uint32_t pcell[2] = {0u, 0u}, ppos[2] = {0u, 0u};
         if (i < qe) {
@@ -1320,8 +1322,6 @@ __global__ __launch_bounds__(kBlock) void bloom_probe_kernel(
     }
 }
 
-int peel_grid_cache[64];
-
 template <typename T>
 hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
                            const uint32_t* b, const DecodeOut& out, const DecodeLayout& L,
@@ -1429,18 +1429,11 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
 
-    // persistent peel: every workgroup must be resident (cooperative launch)
-    int dev = 0;
-    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
-    const int slot = (dev & 31) * 2 + (std::is_same<T, float>::value ? 1 : 0);  // per device and type
-    if (peel_grid_cache[slot] == 0) {
-        int per_cu = 0;
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per_cu, reinterpret_cast<const void*>(&peel_kernel<A>), kPeelBlock, 0);
-        if (e != hipSuccess) return e;
-        if (per_cu < 1) return hipErrorInvalidConfiguration;
-        peel_grid_cache[slot] = di.cus;
-    }
+    // persistent peel: every workgroup must be resident (cooperative launch);
+    // one per CU at most, so it is enough that one fits
+    int per_cu = 0;
+    e = occupancy_per_cu(reinterpret_cast<const void*>(&peel_kernel<A>), kPeelBlock, &per_cu);
+    if (e != hipSuccess) return e;
     // At most one resident workgroup per CU.  A round costs a fixed barrier
     // time that grows with the number of workgroups arriving (about 6.9 us at
     // one per CU, 4.9 us at one per two CUs on MI355X) plus a per-entry time
@@ -1454,10 +1447,8 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     // 18.3 ms).
     const bool fewer_atomics = std::is_same<T, int32_t>::value && planned;
     const uint64_t half_below = fewer_atomics ? kPeelHalfGridCellsInt : kPeelHalfGridCells;
-    const uint32_t peel_grid = g.cells < half_below &&
-                                       peel_grid_cache[slot] >= 2
-                                   ? (uint32_t)peel_grid_cache[slot] / 2u
-                                   : (uint32_t)peel_grid_cache[slot];
+    const uint32_t peel_grid = g.cells < half_below && di.cus >= 2 ? (uint32_t)di.cus / 2u
+                                                                   : (uint32_t)di.cus;
     PeelArgs<A> pa;
     pa.ctrl = ctrl;
     pa.sync = sync;

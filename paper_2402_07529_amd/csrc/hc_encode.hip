@@ -284,14 +284,10 @@ hipError_t launch_dense_t(const Geo& g, const void* x, void* y, uint32_t* b, hip
     // that leaves each wave fewer than 64 tiles, four times as many, so the
     // dispatcher evens out the last ones (measured on MI355X: VGG19- and
     // BERT-base-sized gradients 4 % faster; at 2^30 parameters no change)
-    static int per_cu = 0;  // resident workgroups per CU (same on every device here)
-    if (per_cu == 0) {
-        int v = 0;
-        const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &v, reinterpret_cast<const void*>(&encode_dense_kernel<T, MODE, BL>), kBlock, 0);
-        if (e != hipSuccess) return e;
-        per_cu = v > 0 ? v : 1;
-    }
+    int per_cu = 0;  // resident workgroups per CU
+    const hipError_t e = occupancy_per_cu(
+        reinterpret_cast<const void*>(&encode_dense_kernel<T, MODE, BL>), kBlock, &per_cu);
+    if (e != hipSuccess) return e;
     const uint64_t resident = (uint64_t)cus * per_cu;
     const uint64_t mult = ntiles < 64 * resident * (kBlock / 64) ? 4 : 1;
     const uint32_t grid = grid_for(ntiles, 2 * (kBlock / 64), (uint32_t)(resident * mult));

@@ -35,7 +35,15 @@ struct Geo {
 struct DeviceInfo {
     int cus;          // compute units
 };
+// Properties of the current device, queried once per device (thread-safe).
 hipError_t device_info(DeviceInfo* out);
+// Resident workgroups per CU of `kernel` at `block` lanes and no dynamic LDS
+// on the current device (at least 1), queried once per (device, kernel,
+// block) and cached (thread-safe).
+hipError_t occupancy_per_cu(const void* kernel, int block, int* out);
+// Lets `kernel` take up to `bytes` of dynamic LDS on the current device (set
+// once per (device, kernel), thread-safe).
+hipError_t allow_dynamic_lds(const void* kernel, int bytes);
 
 // Bloom filter: candidate bitmap cand[words] of the parameters whose bloom_k
 // filter bits are all set

@@ -211,3 +211,19 @@ def test_gather_encode_rejected_before_launch():
               hc.hc_geometry_bloom(2_000_000, 20_000, 1.23, 1024, 3)[0]):        # Bloom index
         assert L.hc_encode_gather(ctypes.byref(q), *ok) == hc.HC_EUNSUPPORTED
         assert L.hc_last_error()
+
+
+def test_decode_binding_checks_coo_lengths_before_launch():
+    # the decode writes coo_cap = coo_idx.numel() entries of both COO arrays:
+    # a shorter coo_val, or only one of the two, is refused on the host
+    import torch
+
+    import paper_2402_07529_amd as hc
+    p = hc.hc_geometry(10_000, 100, 1.23, 1024, 3)
+    assert hc._coo_cap(None, None) == 0
+    assert hc._coo_cap(torch.zeros(8, dtype=torch.int32), torch.zeros(8, dtype=torch.int32)) == 8
+    with pytest.raises(ValueError, match="fewer than"):
+        hc.hc_decode(p, None, None, None, None, coo_idx=torch.zeros(8, dtype=torch.int32),
+                     coo_val=torch.zeros(7, dtype=torch.int32))
+    with pytest.raises(ValueError, match="both"):
+        hc.hc_decode(p, None, None, None, None, coo_idx=torch.zeros(8, dtype=torch.int32))
