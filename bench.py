@@ -25,6 +25,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "encode+aggregate+decode dense-gradient GB/s at 1 GPU; % HBM peak; decode success"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+MALL_BYTES = 256 * 2**20  # MI355X Infinity Cache (memory-attached last level)
 
 
 def log(*a):
@@ -132,6 +133,24 @@ def measured_traffic(workload, vtype):
     return int(fields["traffic_bytes_per_launch"])
 
 
+def host_cpu():
+    """(CPU model, logical CPUs of the host, CPUs this process may run on)."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count()
+    return model, os.cpu_count(), usable
+
+
 def cpu_baseline(w, rows, c, block, seed):
     """The CPU oracle, as it stands, on a bounded sample of the same workload:
     one worker's dense encode (timed), the other workers encoded from COO
@@ -158,7 +177,9 @@ def cpu_baseline(w, rows, c, block, seed):
     _, _, info = oracle.decode(g, Ya, Ba)
     t_dec = time.perf_counter() - t0
     t_iter = w.W * t_enc + t_agg + t_dec
+    model, nproc, usable = host_cpu()
     return dict(value=round(4 * w.n / t_iter / 1e9, 4), unit="GB/s", cores=1, kind="oracle",
+                cpu_model=model, nproc=nproc, cpus_usable=usable,
                 sample=(f"{w.name}: 1 of {w.W} dense encodes timed ({t_enc:.2f} s, scaled x{w.W}), "
                         f"aggregate {t_agg:.2f} s, decode {t_dec:.2f} s; single-threaded C"),
                 success=int(info.success), rounds=int(info.rounds))
@@ -263,10 +284,32 @@ class Runner:
         stop.record(stream)
         torch.cuda.synchronize()
         ms = start.elapsed_time(stop) / steps
+        step_ms = [e[0].elapsed_time(e[3]) for e in evs]
         enc_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) / W
         agg_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
         dec_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
         inf = hc.read_info(info)
+        # the decode alone without the plan (per-cell counters by atomics), for
+        # a geometry that changes every iteration and so cannot reuse a plan
+        dec_noplan_ms = None
+        if plan is not None:
+            info2 = hc.alloc_info(dev)
+            dev_ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            times = []
+            for k in range(max(steps // 2, 2) + 1):
+                dev_ev[0].record(stream)
+                hc.hc_decode(p, Ya, Ba, info2, ws, x_out=out, mask=mask,
+                             max_support=max_support, stream=stream)
+                dev_ev[1].record(stream)
+                torch.cuda.synchronize()
+                if k > 0:
+                    times.append(dev_ev[0].elapsed_time(dev_ev[1]))
+            dec_noplan_ms = float(np.median(times))
+            assert hc.read_info(info2) == inf, "decode without a plan differs"
+            # the timed iterations' outputs again (the check below reads them)
+            hc.hc_decode(p, Ya, Ba, info, ws, x_out=out, mask=mask, max_support=max_support,
+                         stream=stream, plan=plan)
+            torch.cuda.synchronize()
         exact = None
         if check:
             # correctness of the timed result against the direct sum of the inputs
@@ -279,7 +322,8 @@ class Runner:
                              1e-5 * direct.abs().max().item()) if inf.success else False
             del direct
         return dict(p=p, ms=ms, enc_ms=enc_ms, agg_ms=agg_ms, dec_ms=dec_ms, info=inf,
-                    exact=exact, plan_ms=plan_ms)
+                    exact=exact, plan_ms=plan_ms, step_ms=step_ms, dec_noplan_ms=dec_noplan_ms,
+                    ws_bytes=int(ws.numel()))
 
 
 # sketch sizes (cells / n) of section 4.1's microbenchmark, 2 % to 200 %, with
@@ -411,6 +455,7 @@ def main():
                                             a.blocked)
     iter_b = W * enc_b + agg_b + dec_b
     value = 4 * w.n / (ms * 1e-3) / 1e9
+    nnz_w = float(np.mean([w.nnz(i) for i in range(W)]))  # nonzeros one worker encodes
     enc_gbs = enc_b / (enc_ms * 1e-3) / 1e9
     res = {
         "metric": METRIC, "value": round(value, 3), "unit": "GB/s", "n_gpus": 1,
@@ -434,13 +479,28 @@ def main():
                      "traffic": (None if a.blocked or a.index == "bloom" or gather
                                  else measured_traffic(w.name, w.vtype)),
                      "bytes_per_launch": enc_b, "avg_launch_ms": round(enc_ms, 4)},
+        "ms_per_step_median": round(float(np.median(m["step_ms"])), 4),
         "hbm_frac_iteration": round(iter_b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "stages_ms": {"encode_per_worker": round(enc_ms, 4), "aggregate": round(agg_ms, 4),
                       "decode": round(dec_ms, 4)},
         "stages_gbs_dense": {"encode": round(4 * w.n / (enc_ms * 1e-3) / 1e9, 1),
                              "aggregate": round(4 * w.n / (agg_ms * 1e-3) / 1e9, 1),
                              "decode": round(4 * w.n / (dec_ms * 1e-3) / 1e9, 1)},
+        # nonzeros handled per second: one worker's nonzeros per encode, the
+        # aggregate's nonzeros for the aggregate and the decode
+        "stages_nonzeros_per_s": {"encode": round(nnz_w / (enc_ms * 1e-3), 1),
+                                  "aggregate": round(n_agg / (agg_ms * 1e-3), 1),
+                                  "decode": round(n_agg / (dec_ms * 1e-3), 1)},
         "plan_build_ms_once": round(m["plan_ms"], 3),
+        "decode_ms_without_plan": (round(m["dec_noplan_ms"], 4) if m["dec_noplan_ms"] is not None
+                                   else None),
+        # whether the sketch (and the decode's working set) fit the 256 MiB
+        # Infinity Cache that backs HBM; the W dense inputs never do
+        "mall": {"capacity_bytes": MALL_BYTES, "sketch_bytes": 4 * cells,
+                 "sketch_resident": 4 * cells <= MALL_BYTES,
+                 "all_worker_sketches_resident": W * (4 * cells + 4 * p.index_words) <= MALL_BYTES,
+                 "decode_workspace_bytes": m["ws_bytes"],
+                 "decode_workspace_resident": m["ws_bytes"] + 4 * cells <= MALL_BYTES},
         "decode": {"success": inf.success, "n_support": inf.n_support,
                    "n_recovered": inf.n_recovered, "rounds": inf.rounds, "status": inf.status,
                    "equals_direct_sum": m["exact"]},

@@ -147,7 +147,8 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(const T* __restrict__ y_ag
                                                       unsigned long long* __restrict__ cnt,
                                                       uint32_t cells, bool planned,
                                                       Ctrl* __restrict__ ctrl,
-                                                      PeelSync* __restrict__ sync) {
+                                                      PeelSync* __restrict__ sync,
+                                                      uint32_t* __restrict__ mark) {
     if (blockIdx.x == 0) {
         if (threadIdx.x < sizeof(Ctrl) / 4) reinterpret_cast<uint32_t*>(ctrl)[threadIdx.x] = 0u;
         for (uint32_t k = threadIdx.x; k < sizeof(PeelSync) / 4; k += kBlock)
@@ -157,6 +158,7 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(const T* __restrict__ y_ag
     for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < cells; i += step) {
         yw[i] = (typename Acc<T>::type)y_agg[i];
         if (!planned) cnt[i] = 0ull;
+        if (mark != nullptr) mark[i] = 0u;
     }
 }
 
@@ -448,10 +450,11 @@ __device__ __forceinline__ void lds_push(Q& q, bool pred, uint32_t cell, uint32_
 
 // Called by every lane of the workgroup with the same arguments.  Appends the
 // staged pairs to the global queue if `force` or if the buffer could not take
-// another `room` pushes.
+// another `room` pushes.  With marks (the fp32 peel), each appended cell's
+// mark becomes `markval`: its frontier round plus one.
 template <typename Q>
 __device__ void flush_pushes(Q& q, bool force, uint32_t room, unsigned int* tail,
-                             uint2* queue, uint32_t cells) {
+                             uint2* queue, uint32_t cells, uint32_t* mark, uint32_t markval) {
     lds_barrier();
     const uint32_t n = q.count;
     lds_barrier();  // every lane has read n before any lane pushes again
@@ -459,8 +462,13 @@ __device__ void flush_pushes(Q& q, bool force, uint32_t room, unsigned int* tail
     if (threadIdx.x == 0) q.base = atomicAdd(tail, n);
     lds_barrier();
     const uint32_t base = q.base;
-    for (uint32_t k = threadIdx.x; k < n; k += blockDim.x)
-        if ((uint64_t)base + k < cells) queue[base + k] = q.item[k];  // a cell is pushed at most once
+    for (uint32_t k = threadIdx.x; k < n; k += blockDim.x) {
+        if ((uint64_t)base + k >= cells) continue;  // a cell is pushed at most once
+        const uint2 it = q.item[k];
+        queue[base + k] = it;
+        if (mark != nullptr)
+            __hip_atomic_store(mark + it.x, markval, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     lds_barrier();
     if (threadIdx.x == 0) q.count = 0;
     lds_barrier();
@@ -697,6 +705,7 @@ struct PeelArgs {  // T: the decode-side arithmetic type
     unsigned long long* cnt;
     T* yw;
     uint2* queue;
+    uint32_t* mark;  // fp32 peel: per cell, its frontier round + 1 (0: never queued)
     InfoDev* info;
     uint64_t seed;
     uint32_t rows, c, cmask, log2c, cells;
@@ -707,14 +716,34 @@ struct PeelArgs {  // T: the decode-side arithmetic type
 // One frontier entry (cell cidx, element position pos), for the kernel below.
 // PACKED: int32 residuals ride in the counter words (kp position bits).
 // Sets the (at most two) cells that became pure, with their elements.
+// Integer peels (T = int32): the first frontier entry of an element to claim
+// its flag recovers it; any of its pure cells holds the same value exactly.
+// The fp32 gradient's peel (T = double, with marks): every element is
+// recovered from the pure cell with the smallest j among those in the round's
+// frontier, as the synchronous rounds define it.  In floating point the pure
+// cells of an element carry different rounding, so this makes the result
+// independent of the order in which entries are taken.  A cell of a live
+// element that is in the frontier holds that element alone, and a live
+// element's cells enter the frontier only in the round before it is
+// recovered, so "mark == r + 1" tells exactly which of its cells are pure at
+// the start of round r; the element's entries with a larger j stand aside and
+// no claim is needed.  Its flag, set with a plain store, stops entries of
+// later rounds (a cell of the element that became pure while it was being
+// recovered).
 template <typename T, bool PACKED>
 __device__ __forceinline__ void peel_entry(const PeelArgs<T>& a, uint32_t cidx, uint32_t pos,
                                            uint32_t kp, uint32_t r, uint32_t& recovered,
                                            uint32_t& last_round, bool (&push)[2],
                                            uint32_t (&pcell)[2], uint32_t (&ppos)[2]) {
-    // one word per element: claims of neighbouring elements would otherwise
-    // queue up on a shared word
-    const bool taken = atomicExch(a.peeled + pos, 1u) != 0u;
+    constexpr bool kMarks = std::is_same<T, double>::value;
+    bool taken;
+    if (kMarks) {
+        taken = __hip_atomic_load(a.peeled + pos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+    } else {
+        // one word per element: claims of neighbouring elements would
+        // otherwise queue up on a shared word
+        taken = atomicExch(a.peeled + pos, 1u) != 0u;
+    }
     const uint32_t p = a.elem[pos];
     unsigned long long wcell = 0;
     T ycell = T(0);
@@ -727,6 +756,13 @@ __device__ __forceinline__ void peel_entry(const PeelArgs<T>& a, uint32_t cidx, 
     for (int j = 0; j < 3; j++) cl[j] = cell_of(h, j, t, a.c, a.cmask);
     const int j = cl[0] == cidx ? 0 : (cl[1] == cidx ? 1 : 2);
     if (taken || cl[j] != cidx) return;
+    if (kMarks) {
+        for (int jj = 0; jj < j; jj++)
+            if (__hip_atomic_load(a.mark + cl[jj], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                r + 1u)
+                return;
+        __hip_atomic_store(a.peeled + pos, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     if (PACKED) ycell = (T)(int32_t)(uint32_t)(wcell >> 32);
     const T val = Val<T>::sign(ycell, (h.neg >> j) & 1u);
     a.vals[pos] = val;
@@ -887,9 +923,9 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                     lds_push(q, (v[m] >> 32) == 1ull, (uint32_t)cidx, (uint32_t)v[m]);
                 }
                 flush_pushes(q, false, kScanCells * kPeelBlock, &sync->tail.v[0], a.queue,
-                             a.cells);
+                             a.cells, a.mark, 1u);
             }
-            flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
+            flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells, a.mark, 1u);
         }
         // split: round 0 ran before this kernel and the queue holds round 1's
         // frontier after round 0's
@@ -932,9 +968,10 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                 }
                 lds_push(q, push[0], pcell[0], ppos[0]);
                 lds_push(q, push[1], pcell[1], ppos[1]);
-                flush_pushes(q, false, 2u * kPeelBlock, &sync->tail.v[0], a.queue, a.cells);
+                flush_pushes(q, false, 2u * kPeelBlock, &sync->tail.v[0], a.queue, a.cells,
+                             a.mark, r + 2u);
             }
-            flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells);
+            flush_pushes(q, true, 0, &sync->tail.v[0], a.queue, a.cells, a.mark, r + 2u);
             qs = qe;
             ok = grid_barrier(ctrl, sync, gridDim.x, gen++, &fend);
         }
@@ -1021,9 +1058,10 @@ __global__ __launch_bounds__(kBlock) void scan0_kernel(PeelArgs<T> a) {
             }
             lds_push(q, (v[m] >> 32) == 1ull, (uint32_t)cidx, (uint32_t)v[m]);
         }
-        flush_pushes(q, false, kScanCells * kBlock, &a.sync->tail.v[0], a.queue, a.cells);
+        flush_pushes(q, false, kScanCells * kBlock, &a.sync->tail.v[0], a.queue, a.cells,
+                     a.mark, 1u);
     }
-    flush_pushes(q, true, 0, &a.sync->tail.v[0], a.queue, a.cells);
+    flush_pushes(q, true, 0, &a.sync->tail.v[0], a.queue, a.cells, a.mark, 1u);
 }
 
 __global__ void snap0_kernel(PeelSync* sync) {
@@ -1071,9 +1109,9 @@ __global__ __launch_bounds__(kBlock) void round0_kernel(PeelArgs<T> a) {
         }
         lds_push(q, push[0], pcell[0], ppos[0]);
         lds_push(q, push[1], pcell[1], ppos[1]);
-        flush_pushes(q, false, 2u * kBlock, &a.sync->tail.v[0], a.queue, a.cells);
+        flush_pushes(q, false, 2u * kBlock, &a.sync->tail.v[0], a.queue, a.cells, a.mark, 2u);
     }
-    flush_pushes(q, true, 0, &a.sync->tail.v[0], a.queue, a.cells);
+    flush_pushes(q, true, 0, &a.sync->tail.v[0], a.queue, a.cells, a.mark, 2u);
     // per-workgroup totals into the control block, summed with the peel's
     my_recovered = wave_sum(my_recovered);
     uint32_t wmax = my_last_round;
@@ -1340,6 +1378,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     unsigned long long* cnt = reinterpret_cast<unsigned long long*>(base + L.cnt);
     A* yw = reinterpret_cast<A*>(base + L.yw);
     uint2* queue = reinterpret_cast<uint2*>(base + L.queue);
+    uint32_t* mark = g.f32 ? reinterpret_cast<uint32_t*>(base + L.mark) : nullptr;
     const T* y_agg = static_cast<const T*>(y_agg_v);
     const bool planned = plan != nullptr;
     // few plan entries per row (a sketch much wider than the support): one
@@ -1353,7 +1392,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     uint64_t grid = ((uint64_t)g.cells + kBlock - 1) / kBlock;
     if (grid > (uint64_t)di.cus * 16) grid = (uint64_t)di.cus * 16;
     hipLaunchKernelGGL(prep_kernel<T>, dim3((uint32_t)grid), dim3(kBlock), 0, s, y_agg, yw, cnt,
-                       g.cells, planned, ctrl, sync);
+                       g.cells, planned, ctrl, sync, mark);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const uint32_t last_mask = (g.n & 31u) ? ((1u << (g.n & 31u)) - 1u) : 0xffffffffu;
     const bool bvec = (reinterpret_cast<uintptr_t>(b) & 15u) == 0;
@@ -1458,6 +1497,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     pa.cnt = cnt;
     pa.yw = yw;
     pa.queue = queue;
+    pa.mark = mark;
     pa.info = static_cast<InfoDev*>(out.info);
     pa.seed = g.seed;
     pa.rows = g.rows;
@@ -1543,6 +1583,7 @@ DecodeLayout decode_layout(const Geo& g, uint64_t max_support) {
     L.cnt = o;     o = align256(o + (size_t)g.cells * 8);
     L.yw = o;      o = align256(o + (size_t)g.cells * vsz);
     L.queue = o;   o = align256(o + (size_t)g.cells * 8);
+    L.mark = o;    o = align256(o + (g.f32 ? (size_t)g.cells * 4 : 0));  // fp32: frontier marks
     L.cand = o;    o = align256(o + (g.bloom_k ? g.words * 4 : 0));  // probed Bloom candidates
     L.total = o;
     return L;

@@ -103,7 +103,7 @@ struct DecodeLayout {
     uint64_t cap;       // max support the workspace holds
     uint64_t nchunks;   // bitmap chunks of kChunkWords words
     uint64_t ntiles;    // tiles of the support passes (a few chunks each)
-    size_t ctrl, sync, blk, cpre, tcnt, woffb, elem, vals, peeled, cnt, yw, queue, cand, total;
+    size_t ctrl, sync, blk, cpre, tcnt, woffb, elem, vals, peeled, cnt, yw, queue, mark, cand, total;
 };
 constexpr uint32_t kChunkWords = 1024;
 DecodeLayout decode_layout(const Geo& g, uint64_t max_support);

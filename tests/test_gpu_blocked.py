@@ -14,7 +14,8 @@ import pytest
 import oracle
 import workloads as wl
 from hc_pipeline import gpu_run, oracle_run, wrap_sum
-from test_gpu_parity import assert_fp32_values, assert_same_info, fp32_cell_bounds
+from test_gpu_parity import (assert_fp32_decode_stage, assert_fp32_values, assert_same_info,
+                             fp32_cell_bounds)
 
 pytestmark = pytest.mark.gpu
 
@@ -197,6 +198,7 @@ def test_blocked_fp32(c, block_rows, gamma):
     assert_fp32_values(r["x"], o["x"], oracle.decode_bound(o["g"], ab, o["Ba"]), sup)
     assert np.array_equal(r["coo_idx"], sup.astype(np.uint32))
     assert np.array_equal(r["coo_val"], r["x"][sup])
+    assert_fp32_decode_stage(r, o["g"], f"blocked c={c}")
 
 
 def test_blocked_fp32_failures_structure_exact():

@@ -18,7 +18,8 @@ import pytest
 import oracle
 import workloads as wl
 from hc_pipeline import gpu_run, oracle_run, wrap_sum
-from test_gpu_parity import assert_fp32_values, assert_same_info, fp32_cell_bounds
+from test_gpu_parity import (assert_fp32_decode_stage, assert_fp32_values, assert_same_info,
+                             fp32_cell_bounds)
 
 pytestmark = pytest.mark.gpu
 
@@ -121,6 +122,7 @@ def test_bloom_fp32(c):
     assert_same_info(r["info"], o["info"])
     cand = np.nonzero(np.unpackbits(o["mask"].view(np.uint8), bitorder="little")[:w.n])[0]
     assert_fp32_values(r["x"], o["x"], oracle.decode_bound(o["g"], ab, o["Ba"]), cand)
+    assert_fp32_decode_stage(r, o["g"], f"bloom c={c}")
 
 
 def test_bloom_geometry_call_and_tiny_lengths():

@@ -7,7 +7,8 @@ int32: every stage bit-exact against the CPU oracle (per-worker sketches and
 bitmaps, aggregate, decoded gradient, mask, support size, recovered count,
 round count, success), and the decoded gradient equals the direct sum of the
 workers' sparse gradients.  fp32 (VGG19): structure exact, values within the
-per-element bound derived in test_gpu_parity.
+per-element bound derived in test_gpu_parity, and the decode stage within 1e-6
+relative of the oracle's decode of the GPU's own fp32 aggregate.
 """
 import numpy as np
 import pytest
@@ -15,7 +16,8 @@ import pytest
 import oracle
 import workloads as wl
 from hc_pipeline import gpu_run, oracle_run
-from test_gpu_parity import assert_fp32_values, assert_same_info, fp32_cell_bounds
+from test_gpu_parity import (assert_fp32_decode_stage, assert_fp32_values, assert_same_info,
+                             fp32_cell_bounds, fp32_normwise_error)
 
 pytestmark = pytest.mark.gpu
 
@@ -97,17 +99,19 @@ def test_fullsize_vgg19_fp32():
     assert np.array_equal(g["mask"], o["mask"])
     assert_same_info(g["info"], o["info"])
     sup = np.nonzero(np.unpackbits(o["Ba"].view(np.uint8), bitorder="little")[:w.n])[0]
-    assert_fp32_values(g["x"], o["x"], oracle.decode_bound(o["g"], ab, o["Ba"]), sup)
+    bnd = oracle.decode_bound(o["g"], ab, o["Ba"])
+    assert_fp32_values(g["x"], o["x"], bnd, sup)
+    assert_fp32_decode_stage(g, o["g"], "vgg19 global")
+    fp32_normwise_error(g["x"], o["x"], bnd, "vgg19 global")
 
 
 @pytest.mark.timeout(900)
 @pytest.mark.parametrize("density,overlap", [(0.001, 0.9), (0.05, 0.1)])
 def test_fullsize_bert_sweep_corners(density, overlap):
     # the smallest and the largest aggregate of the BERT-base density/overlap
-    # sweep.  The large corner (79 M aggregate nonzeros) is checked through
-    # the oracle's encode and aggregate and through properties of the decode
-    # that hold at any size: success, the support, and equality with the
-    # direct sum of the workers' gradients.
+    # sweep, every stage against the oracle (the large corner's 79 M aggregate
+    # nonzeros take the oracle's decode about two minutes), and the decode
+    # also against the direct sum of the workers' gradients.
     _hc()
     w = wl.make("bert", density=density, overlap=overlap)
     n_agg = w.n_agg
@@ -121,6 +125,8 @@ def test_fullsize_bert_sweep_corners(density, overlap):
         assert np.array_equal(g["Y"][i], Y) and np.array_equal(g["B"][i], B), f"worker {i}"
         Ys.append(Y)
         Bs.append(B)
+        print(f"[fullsize] bert d={density} o={overlap}: oracle encode of worker {i} equal",
+              flush=True)
     Ya, Ba = oracle.aggregate(np.stack(Ys), np.stack(Bs))
     del Ys, Bs
     assert np.array_equal(g["Ya"], Ya) and np.array_equal(g["Ba"], Ba)
@@ -130,10 +136,11 @@ def test_fullsize_bert_sweep_corners(density, overlap):
     uniq, sums = sparse_direct_sum(w)
     assert np.array_equal(g["x"][uniq], sums)
     assert np.count_nonzero(g["x"]) == np.count_nonzero(sums)
-    if n_agg < 2_000_000:
-        xo, mo, io = oracle.decode(gg, Ya, Ba)
-        assert_same_info(inf, io)
-        assert np.array_equal(g["x"], xo)
+    print(f"[fullsize] bert d={density} o={overlap}: oracle decode", flush=True)
+    xo, mo, io = oracle.decode(gg, Ya, Ba)
+    assert_same_info(inf, io)
+    assert np.array_equal(g["mask"], mo)
+    assert np.array_equal(g["x"], xo)
 
 
 @pytest.mark.timeout(900)
@@ -165,7 +172,10 @@ def test_fullsize_blocked(name, vtype):
             assert np.all(np.abs(g["Y"][i].astype(np.float64) - o["Y"][i]) <= wb[i] * (1 + 1e-6))
         assert np.all(np.abs(g["Ya"].astype(np.float64) - o["Ya"]) <= ab * (1 + 1e-6))
         sup = np.nonzero(np.unpackbits(o["Ba"].view(np.uint8), bitorder="little")[:w.n])[0]
-        assert_fp32_values(g["x"], o["x"], oracle.decode_bound(o["g"], ab, o["Ba"]), sup)
+        bnd = oracle.decode_bound(o["g"], ab, o["Ba"])
+        assert_fp32_values(g["x"], o["x"], bnd, sup)
+        assert_fp32_decode_stage(g, o["g"], f"{name} blocked")
+        fp32_normwise_error(g["x"], o["x"], bnd, f"{name} blocked")
     assert np.array_equal(g["Ba"], o["Ba"])
     assert np.array_equal(g["mask"], o["mask"])
     assert_same_info(g["info"], o["info"])

@@ -16,9 +16,14 @@ tolerance derived from the arithmetic, element by element:
     cell bounds carried through the peeling schedule (oracle.decode_bound),
     plus one rounding to fp32 (u |x|) and fp64 noise (1e-12 of the largest
     value).
-A flat 1e-6 normwise tolerance is not attainable by any decoder of an fp32
-sketch: rounding the exact aggregate sketch to fp32 once already moves the
-exactly peeled result by about 1.3e-6 of its largest value on these inputs.
+A flat 1e-6 normwise tolerance against the exact sum is not attainable by any
+decoder of an fp32 sketch: rounding the exact aggregate sketch to fp32 once
+already moves the exactly peeled result by about 1.3e-6 of its largest value
+on these inputs (pinned on the CPU in test_oracle).  The decode stage alone
+meets the 1e-6 bar: the oracle decodes the GPU's own fp32 aggregate (widened
+to fp64, the same synchronous rounds, each element read from the pure cell of
+smallest j, as the GPU's fp32 peel does), and every decoded value agrees
+within 1e-6 of its own magnitude (plus 1e-12 of the largest value).
 """
 import math
 
@@ -69,6 +74,36 @@ def assert_fp32_values(x_gpu, x_oracle, bnd, support):
     other = np.ones(x_gpu.size, bool)
     other[support] = False
     assert not x_gpu[other].any()
+
+
+def assert_fp32_decode_stage(g, geom, label=""):
+    """The GPU's fp32 decode against the oracle's decode of the same fp32
+    aggregate: structure exact, values within 1e-6 relative.  Returns the
+    largest element-wise relative difference."""
+    xo, mo, io = oracle.decode(geom, g["Ya"].astype(np.float64), g["Ba"])
+    assert np.array_equal(g["mask"], mo), label
+    assert_same_info(g["info"], io)
+    err = np.abs(g["x"].astype(np.float64) - xo)
+    tol = 1e-6 * np.abs(xo) + 1e-12 * max(float(np.max(np.abs(xo))), 1e-300)
+    bad = np.nonzero(err > tol)[0]
+    assert bad.size == 0, (label, bad[:5], g["x"][bad[:5]], xo[bad[:5]])
+    rel = float(np.max(err / np.maximum(np.abs(xo), 1e-300), initial=0.0))
+    print(f"[fp32 decode stage] {label} max |gpu - oracle(gpu aggregate)| / |x| = {rel:.3e}",
+          flush=True)
+    return rel
+
+
+def fp32_normwise_error(x_gpu, truth, bnd=None, label=""):
+    """max |x - truth| / max |truth| (printed, with max error / bound)."""
+    t = truth.astype(np.float64)
+    err = np.abs(x_gpu.astype(np.float64) - t)
+    nw = float(np.max(err) / max(float(np.max(np.abs(t))), 1e-300))
+    msg = f"[fp32 vs exact sum] {label} normwise error {nw:.3e}"
+    if bnd is not None:
+        tol = bnd + U * np.abs(t) + 1e-12 * np.max(np.abs(t))
+        msg += f", max error / bound {float(np.max(err / np.maximum(tol, 1e-300))):.3f}"
+    print(msg, flush=True)
+    return nw
 
 
 def _hc():
@@ -226,6 +261,7 @@ def check_fp32(w, rows, c, use_plan=False, gather=False):
     assert_fp32_values(g["x"], o["x"], bnd, sup)
     assert np.array_equal(g["coo_idx"], sup.astype(np.uint32))
     assert np.array_equal(g["coo_val"], g["x"][sup])
+    assert_fp32_decode_stage(g, o["g"], f"n={w.n} c={c}")
     return g, o, bnd
 
 
@@ -241,6 +277,19 @@ def test_fp32_all_stages(use_plan):
     sup = np.nonzero(truth)[0]
     assert np.all(np.abs(g["x"] - truth) <= bnd * (1 + 1e-6) + U * np.abs(truth) +
                   1e-12 * np.max(np.abs(truth)))
+    # against the exact sum the fp32 sketch's own rounding sets the scale:
+    # the exact decode of the exact aggregate rounded once to fp32 misses by
+    # `floor` (about 1.3e-6 here); the GPU's worker sketches and aggregate
+    # round at every addition, so its error may be a few times that
+    Yr = o["Ya"].astype(np.float32).astype(np.float64)
+    xr, _, ir = oracle.decode(o["g"], Yr, o["Ba"])
+    assert ir.success
+    floor = float(np.max(np.abs(xr - truth)) / np.max(np.abs(truth)))
+    nw = fp32_normwise_error(g["x"], truth, bnd, f"use_plan={use_plan}")
+    print(f"[fp32 vs exact sum] single-rounding floor {floor:.3e}, gpu / floor {nw / floor:.2f}",
+          flush=True)
+    assert floor > 1e-6
+    assert nw <= 8 * floor
     # the tolerance is not vacuous: for the typical element it is a few
     # rounding units of the gradient's scale (it grows only along long
     # peeling chains, where worst-case errors add up)
