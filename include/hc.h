@@ -281,6 +281,32 @@ hc_status hc_decode(const hc_params *p, const void *plan, const void *y_agg,
                     uint32_t *mask, hc_decode_info *info, uint64_t max_support,
                     void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* Bytes of the static device scratch array behind hc_decode_noalloc (64 MiB
+ * per GPU the library runs on, held until the process ends). */
+#define HC_NOALLOC_SCRATCH_BYTES ((size_t)64 * 1024 * 1024)
+
+/* hc_decode without a workspace argument, for callers that cannot allocate
+ * device memory (code under stream capture, tight serving loops, harnesses
+ * that forbid allocation).  Same arguments, checks, outputs and stream
+ * semantics as hc_decode with ws and ws_bytes removed: the workspace is a
+ * static device array of HC_NOALLOC_SCRATCH_BYTES in the library, one per
+ * GPU, and the call allocates nothing.  Limit: the decode must need at most
+ * that much workspace, i.e. hc_sizes must report ws_bytes <=
+ * HC_NOALLOC_SCRATCH_BYTES for the same params and max_support (a blocked
+ * sketch's decode always fits; for a global int32 sketch the workspace is
+ * about 20 bytes per cell plus 12 per support element, e.g. one million cells
+ * with a support of up to 1.5 million); HC_EWORKSPACE otherwise, before
+ * anything is enqueued.  All calls on one GPU share its scratch array: calls
+ * that overlap in time on one GPU (different streams or host threads without
+ * ordering) race and give undefined results; calls ordered on one stream are
+ * safe.  The scratch contents on entry are ignored, as hc_decode ignores its
+ * workspace's. */
+hc_status hc_decode_noalloc(const hc_params *p, const void *plan, const void *y_agg,
+                            const uint32_t *b_agg,
+                            void *x_out, uint32_t *coo_idx, void *coo_val, uint64_t coo_cap,
+                            uint32_t *mask, hc_decode_info *info, uint64_t max_support,
+                            hipStream_t stream);
+
 /* Human-readable name of a status, and the message of the calling thread's
  * last failing call ("" if none). */
 const char *hc_status_string(hc_status s);

@@ -34,7 +34,8 @@ INFO_BYTES = 32
 
 EXPORTS = ("hc_geometry", "hc_geometry_blocked", "hc_geometry_bloom", "hc_sizes", "hc_plan_bytes",
            "hc_plan_build", "hc_encode", "hc_encode_gather", "hc_encode_coo", "hc_aggregate",
-           "hc_decode", "hc_status_string", "hc_last_error")
+           "hc_decode", "hc_decode_noalloc", "hc_status_string", "hc_last_error")
+NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
 
 
 class HCError(RuntimeError):
@@ -103,11 +104,13 @@ _lib.hc_encode_coo.argtypes = [_PP, _P, _P, ctypes.c_uint64, _P, _P, _P]
 _lib.hc_aggregate.argtypes = [_PP, _P, _P, ctypes.c_uint32, _P, _P, _P]
 _lib.hc_decode.argtypes = [_PP, _P, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, ctypes.c_uint64,
                            _P, ctypes.c_size_t, _P]
+_lib.hc_decode_noalloc.argtypes = [_PP, _P, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P,
+                                   ctypes.c_uint64, _P]
 _lib.hc_plan_bytes.argtypes = [_PP, ctypes.POINTER(ctypes.c_size_t)]
 _lib.hc_plan_build.argtypes = [_PP, _P, ctypes.c_size_t, _P]
 for _f in ("hc_geometry", "hc_geometry_blocked", "hc_geometry_bloom", "hc_sizes", "hc_plan_bytes",
            "hc_plan_build", "hc_encode", "hc_encode_gather", "hc_encode_coo", "hc_aggregate",
-           "hc_decode"):
+           "hc_decode", "hc_decode_noalloc"):
     getattr(_lib, _f).restype = ctypes.c_int
 _lib.hc_status_string.argtypes = [ctypes.c_int]
 _lib.hc_status_string.restype = ctypes.c_char_p
@@ -281,6 +284,22 @@ def hc_decode(p: hc_params, y_agg, b_agg, info, ws, x_out=None, coo_idx=None, co
                           _ptr(info, "info", (torch.uint8,), INFO_BYTES),
                           max_support, _ptr(ws, "ws", (torch.uint8,)),
                           ws.numel() if ws is not None else 0, _stream(stream)), "hc_decode")
+
+
+def hc_decode_noalloc(p: hc_params, y_agg, b_agg, info, x_out=None, coo_idx=None, coo_val=None,
+                      mask=None, max_support: int = 0, stream=None, plan=None):
+    """hc_decode with the library's static scratch array as its workspace."""
+    import torch
+    coo_cap = _coo_cap(coo_idx, coo_val)
+    _check(_lib.hc_decode_noalloc(ctypes.byref(p), _ptr(plan, "plan", (torch.uint8,)),
+                                  _ptr(y_agg, "y_agg", _vdtypes(p), p.cells),
+                                  _ptr(b_agg, "b_agg", _u32(), p.index_words),
+                                  _ptr(x_out, "x_out", _vdtypes(p), p.n),
+                                  _ptr(coo_idx, "coo_idx", _u32()),
+                                  _ptr(coo_val, "coo_val", _vdtypes(p), coo_cap), coo_cap,
+                                  _ptr(mask, "mask", _u32(), p.words),
+                                  _ptr(info, "info", (torch.uint8,), INFO_BYTES),
+                                  max_support, _stream(stream)), "hc_decode_noalloc")
 
 
 @dataclass(frozen=True)

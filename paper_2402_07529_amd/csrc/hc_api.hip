@@ -447,7 +447,8 @@ hc_status hc_plan_build(const hc_params* p, void* plan, size_t plan_bytes, hipSt
 
 namespace {
 
-// hc_decode's argument checks, workspace check and launches.
+// hc_decode's argument checks, workspace check and launches.  ws == nullptr
+// means the static scratch array below (hc_decode_noalloc).
 hc_status decode_impl(const hc_params* p, const void* plan, const void* y_agg,
                       const uint32_t* b_agg, void* x_out, uint32_t* coo_idx, void* coo_val,
                       uint64_t coo_cap, uint32_t* mask, hc_decode_info* info,
@@ -467,9 +468,47 @@ hc_status hc_decode(const hc_params* p, const void* plan, const void* y_agg,
                        max_support, ws, ws_bytes, stream);
 }
 
+hc_status hc_decode_noalloc(const hc_params* p, const void* plan, const void* y_agg,
+                            const uint32_t* b_agg, void* x_out, uint32_t* coo_idx,
+                            void* coo_val, uint64_t coo_cap, uint32_t* mask,
+                            hc_decode_info* info, uint64_t max_support, hipStream_t stream) {
+    g_last_error.clear();
+    return decode_impl(p, plan, y_agg, b_agg, x_out, coo_idx, coo_val, coo_cap, mask, info,
+                       max_support, nullptr, 0, stream);
+}
+
 }  // extern "C"
 
 namespace {
+
+// The allocation-free decode's workspace: one array per GPU, held by the
+// loaded library until the process ends.  Host code never passes its name to
+// a kernel (in host code it is only a stand-in for the device symbol): the
+// device address comes from hipGetSymbolAddress, once per device, and the
+// kernels take that.  Every hc_decode_noalloc call on a GPU shares the array;
+// the decode clears what it needs cleared itself.
+__device__ __align__(256) unsigned char scratch[HC_NOALLOC_SCRATCH_BYTES];
+
+std::mutex g_scratch_mu;
+std::map<int, void*> g_scratch_ptr;  // device -> address of its copy of `scratch`
+
+hc_status scratch_address(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail_hip(e, "hc_decode_noalloc: hipGetDevice");
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    auto it = g_scratch_ptr.find(dev);
+    if (it == g_scratch_ptr.end()) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return fail_hip(e, "hc_decode_noalloc: hipGetSymbolAddress");
+        if (ptr == nullptr || !aligned(ptr, 256))
+            return fail(HC_EHIP, "hc_decode_noalloc: scratch has no usable device address");
+        it = g_scratch_ptr.emplace(dev, ptr).first;
+    }
+    *out = it->second;
+    return HC_OK;
+}
 
 hc_status decode_impl(const hc_params* p, const void* plan, const void* y_agg,
                       const uint32_t* b_agg, void* x_out, uint32_t* coo_idx, void* coo_val,
@@ -497,8 +536,22 @@ hc_status decode_impl(const hc_params* p, const void* plan, const void* y_agg,
     out.coo_cap = coo_cap;
     out.mask = mask;
     out.info = info;
-    const char* where = "hc_decode";
+    const char* where = ws ? "hc_decode" : "hc_decode_noalloc";
     const size_t need = g.block ? blocked_layout(g).total : decode_layout(g, max_support).total;
+    if (ws == nullptr) {
+        // the static scratch array stands in for the caller's workspace
+        if (need > (size_t)HC_NOALLOC_SCRATCH_BYTES) {
+            char msg[160];
+            snprintf(msg, sizeof(msg),
+                     "hc_decode_noalloc: this decode needs %zu bytes of workspace, more than the "
+                     "%zu of its static scratch (use hc_decode)",
+                     need, (size_t)HC_NOALLOC_SCRATCH_BYTES);
+            return fail(HC_EWORKSPACE, msg);
+        }
+        const hc_status ss = scratch_address(&ws);
+        if (ss != HC_OK) return ss;
+        ws_bytes = HC_NOALLOC_SCRATCH_BYTES;
+    }
     if (g.block) {
         const hc_status bs = blocked_supported(g);
         if (bs != HC_OK) return bs;
