@@ -55,10 +55,16 @@ def parse():
     ap.add_argument("--block-rows", type=int, default=None,
                     help="rows per block of the blocked sketch (default: the library's choice "
                          "for this device, hc_geometry_blocked with block_rows = 0)")
-    ap.add_argument("--encode", default="atomic", choices=["atomic", "gather"],
-                    help="atomic: hc_encode (each nonzero adds into its cells); gather: "
-                         "hc_encode_gather (each sketch row assembled through the plan; "
-                         "global sketch, bitmap index, c >= 256)")
+    ap.add_argument("--encode", default="auto", choices=["auto", "atomic", "gather", "staged"],
+                    help="auto: staged for a global sketch with c >= 256 when a worker has at "
+                         "least one nonzero per two batches of c parameters (else the atomic "
+                         "encode, whose cost follows the nonzeros while the staged encode's "
+                         "second pass visits every batch); atomic: hc_encode (each nonzero adds "
+                         "into its cells); gather: "
+                         "hc_encode_gather (each sketch row assembled through the plan from "
+                         "the gradient; global sketch, bitmap index, c >= 256); staged: "
+                         "hc_encode_staged (nonzeros staged per batch, rows assembled through "
+                         "the plan; global sketch, c >= 256)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", nargs="?", const="bert", choices=["bert", "compressed"],
                     help="bert: BERT-base density/overlap grid and sketch-width sweep; "
@@ -221,10 +227,13 @@ class Runner:
         self.out = torch.empty(w.n, dtype=self.vt, device=dev)
         self.mask = torch.empty((w.n + 31) // 32, dtype=torch.int32, device=dev)
 
-    def run(self, ratio, steps, warmup, check=True, block_rows=None, bloom=False, gather=False):
+    def run(self, ratio, steps, warmup, check=True, block_rows=None, bloom=False, gather=False,
+            staged=False):
         """block_rows: None for the global sketch, else the rows per block of
         a blocked sketch; bloom: a Bloom-filter index instead of the bitmap;
-        gather: encode row by row through the plan (hc_encode_gather)."""
+        gather: encode row by row through the plan (hc_encode_gather);
+        staged: stage each batch's nonzeros, then assemble the rows through
+        the plan (hc_encode_staged)."""
         import paper_2402_07529_amd as hc
         torch, w, dev, W = self.torch, self.w, self.dev, self.w.W
         max_support = self.n_agg
@@ -252,6 +261,7 @@ class Runner:
         plan = hc.make_plan(p, dev) if self.c >= 256 and block_rows is None else None
         torch.cuda.synchronize()
         plan_ms = (time.perf_counter() - t_plan) * 1e3
+        stage_ws = hc.alloc_stage_workspace(p, dev) if staged else None
         x, out, mask = self.x, self.out, self.mask
 
         def step(ev=None):
@@ -260,6 +270,8 @@ class Runner:
             for i in range(W):
                 if gather:
                     hc.hc_encode_gather(p, plan, x[i], Y[i], B[i], stream)
+                elif staged:
+                    hc.hc_encode_staged(p, plan, stage_ws, x[i], Y[i], B[i], stream)
                 else:
                     hc.hc_encode(p, x[i], Y[i], B[i], stream)
             if ev is not None:
@@ -440,13 +452,23 @@ def main():
     if a.index == "bloom" and a.blocked:
         print("bench.py: the Bloom-filter index needs the global sketch", file=sys.stderr)
         sys.exit(2)
-    gather = a.encode == "gather"
+    encode = a.encode
+    if encode == "auto":
+        nnz_w = float(np.mean([w.nnz(i) for i in range(w.W)]))
+        batches = (w.n + a.c - 1) // a.c
+        encode = ("staged" if not a.blocked and a.c >= 256 and nnz_w >= 0.5 * batches
+                  else "atomic")
+    gather = encode == "gather"
+    staged = encode == "staged"
     if gather and (a.blocked or a.index == "bloom" or a.c < 256):
         print("bench.py: --encode gather needs the global sketch, the bitmap index and c >= 256",
               file=sys.stderr)
         sys.exit(2)
+    if staged and (a.blocked or a.c < 256):
+        print("bench.py: --encode staged needs the global sketch and c >= 256", file=sys.stderr)
+        sys.exit(2)
     m = r.run(ratio, a.steps, a.warmup, block_rows=block_rows, bloom=a.index == "bloom",
-              gather=gather)
+              gather=gather, staged=staged)
     p, inf, W, n_agg = m["p"], m["info"], w.W, r.n_agg
     ms, enc_ms, agg_ms, dec_ms = m["ms"], m["enc_ms"], m["agg_ms"], m["dec_ms"]
     cells = p.cells
@@ -468,15 +490,16 @@ def main():
                               f"{p.nblocks} blocks") if a.blocked else "global",
                    "index": (f"bloom: {int(p.bloom_k)} hashes, {4 * p.index_words} bytes"
                              if a.index == "bloom" else "bitmap"),
-                   "encode": a.encode,
+                   "encode": encode,
                    **{k: v for k, v in w.params.items() if k in ("density", "overlap", "rows_per_worker")}},
         "roofline": {"bound": "hbm",
                      "kernel": ("hc_encode (blocked LDS encode)" if a.blocked
                                 else "hc_encode_gather (rows through the plan)" if gather
-                                else "hc_encode (Y clear + dense encode)"),
+                                else "hc_encode_staged (staging pass + rows through the plan)"
+                                if staged else "hc_encode (Y clear + dense encode)"),
                      "achieved": round(enc_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(enc_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": (None if a.blocked or a.index == "bloom" or gather
+                     "traffic": (None if a.blocked or a.index == "bloom" or gather or staged
                                  else measured_traffic(w.name, w.vtype)),
                      "bytes_per_launch": enc_b, "avg_launch_ms": round(enc_ms, 4)},
         "ms_per_step_median": round(float(np.median(m["step_ms"])), 4),

@@ -10,6 +10,8 @@
  *   hc_encode / hc_encode_coo   Algorithm 1, phase I (sections 3.1, 3.2, 3.4)
  *   hc_encode_gather            the same for dense gradients, row by row
  *                               through a plan
+ *   hc_encode_staged            the same for sparse gradients: nonzeros staged
+ *                               per batch, rows assembled through a plan
  *   hc_aggregate                what the aggregation API does between the
  *                               phases: Y <- sum Y, B <- OR B (section 3)
  *   hc_decode                   Algorithm 1, phase II (section 3.2 peeling,
@@ -234,6 +236,30 @@ hc_status hc_encode(const hc_params *p, const void *x, void *y, uint32_t *b,
  * rather than as a gradient. */
 hc_status hc_encode_gather(const hc_params *p, const void *plan, size_t plan_bytes,
                            const void *x, void *y, uint32_t *b, hipStream_t stream);
+
+/* Phase I on a dense gradient, staged: the same outputs as hc_encode (int32
+ * bit-identical; fp32 summed in another order), without its three scattered
+ * atomics per nonzero (section 3.1), which bound hc_encode on sparse
+ * gradients.  A first pass streams x once, writes the index (bitmap or Bloom
+ * filter, as hc_encode) and compacts each batch's nonzeros (section 3.4's
+ * batches of c parameters) into a per-batch list of up to 64 (column, value)
+ * pairs in the workspace; a second pass builds every sketch row in LDS from
+ * the lists of the batches the plan lands on it (section 3.4: a batch lands on
+ * one whole row per hash, rotated) and stores it once.  A batch with more than
+ * 64 nonzeros is read from x itself by the second pass (once per hash), so any
+ * density is handled; below about 6 % (c = 1024) every batch fits its list.
+ * Unblocked sketch, c >= 256 (HC_EUNSUPPORTED otherwise).  plan: built by
+ * hc_plan_build for the same params, 256-byte aligned (HC_EINVAL), plan_bytes
+ * at least hc_plan_bytes (HC_EWORKSPACE); a plan built for other params is
+ * detected on the device and gives a zero sketch and an all-ones index (as
+ * hc_encode_gather).  ws: 256-byte aligned device workspace (HC_EINVAL) of at
+ * least hc_encode_staged_bytes (HC_EWORKSPACE), about n / 2 bytes at
+ * c = 1024; contents on entry are ignored.  hc_encode_staged_bytes writes the
+ * size to the HOST pointer `bytes`. */
+hc_status hc_encode_staged_bytes(const hc_params *p, size_t *bytes);
+hc_status hc_encode_staged(const hc_params *p, const void *plan, size_t plan_bytes, void *ws,
+                           size_t ws_bytes, const void *x, void *y, uint32_t *b,
+                           hipStream_t stream);
 
 /* Phase I on COO input: idx[nnz] (uint32, each < n, any order) and
  * val[nnz].  Zero values are skipped; repeated indices are summed.  Same

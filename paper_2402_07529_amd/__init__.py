@@ -11,6 +11,8 @@ C ABI:
     hc_sizes      byte sizes of Y, B and the decode workspace
     hc_plan_bytes, hc_plan_build   inverse row map of a geometry (c >= 256)
     hc_encode     Algorithm 1 phase I on a dense gradient (sections 3.1-3.4)
+    hc_encode_gather, hc_encode_staged  the same through a plan (dense or
+                  sparse gradients), without global atomics
     hc_encode_coo the same from COO input
     hc_aggregate  sum of sketches and OR of bitmaps over W workers (section 3)
     hc_decode     Algorithm 1 phase II: parallel peeling + median estimate
@@ -33,7 +35,8 @@ GAMMA = 1.23
 INFO_BYTES = 32
 
 EXPORTS = ("hc_geometry", "hc_geometry_blocked", "hc_geometry_bloom", "hc_sizes", "hc_plan_bytes",
-           "hc_plan_build", "hc_encode", "hc_encode_gather", "hc_encode_coo", "hc_aggregate",
+           "hc_plan_build", "hc_encode", "hc_encode_gather", "hc_encode_staged_bytes",
+           "hc_encode_staged", "hc_encode_coo", "hc_aggregate",
            "hc_decode", "hc_decode_noalloc", "hc_status_string", "hc_last_error")
 NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
 
@@ -100,6 +103,8 @@ _lib.hc_sizes.argtypes = [_PP, ctypes.c_uint64, ctypes.POINTER(ctypes.c_size_t),
                           ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)]
 _lib.hc_encode.argtypes = [_PP, _P, _P, _P, _P]
 _lib.hc_encode_gather.argtypes = [_PP, _P, ctypes.c_size_t, _P, _P, _P, _P]
+_lib.hc_encode_staged_bytes.argtypes = [_PP, ctypes.POINTER(ctypes.c_size_t)]
+_lib.hc_encode_staged.argtypes = [_PP, _P, ctypes.c_size_t, _P, ctypes.c_size_t, _P, _P, _P, _P]
 _lib.hc_encode_coo.argtypes = [_PP, _P, _P, ctypes.c_uint64, _P, _P, _P]
 _lib.hc_aggregate.argtypes = [_PP, _P, _P, ctypes.c_uint32, _P, _P, _P]
 _lib.hc_decode.argtypes = [_PP, _P, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, ctypes.c_uint64,
@@ -109,7 +114,8 @@ _lib.hc_decode_noalloc.argtypes = [_PP, _P, _P, _P, _P, _P, _P, ctypes.c_uint64,
 _lib.hc_plan_bytes.argtypes = [_PP, ctypes.POINTER(ctypes.c_size_t)]
 _lib.hc_plan_build.argtypes = [_PP, _P, ctypes.c_size_t, _P]
 for _f in ("hc_geometry", "hc_geometry_blocked", "hc_geometry_bloom", "hc_sizes", "hc_plan_bytes",
-           "hc_plan_build", "hc_encode", "hc_encode_gather", "hc_encode_coo", "hc_aggregate",
+           "hc_plan_build", "hc_encode", "hc_encode_gather", "hc_encode_staged_bytes",
+           "hc_encode_staged", "hc_encode_coo", "hc_aggregate",
            "hc_decode", "hc_decode_noalloc"):
     getattr(_lib, _f).restype = ctypes.c_int
 _lib.hc_status_string.argtypes = [ctypes.c_int]
@@ -217,6 +223,27 @@ def hc_encode_gather(p: hc_params, plan, x, y, b, stream=None):
                                  _ptr(y, "y", _vdtypes(p), p.cells),
                                  _ptr(b, "b", _u32(), p.index_words), _stream(stream)),
            "hc_encode_gather")
+
+
+def hc_encode_staged_bytes(p: hc_params) -> int:
+    b = ctypes.c_size_t()
+    _check(_lib.hc_encode_staged_bytes(ctypes.byref(p), ctypes.byref(b)), "hc_encode_staged_bytes")
+    return b.value
+
+
+def hc_encode_staged(p: hc_params, plan, ws, x, y, b, stream=None):
+    import torch
+    _check(_lib.hc_encode_staged(ctypes.byref(p), _ptr(plan, "plan", (torch.uint8,)), plan.numel(),
+                                 _ptr(ws, "ws", (torch.uint8,)), ws.numel(),
+                                 _ptr(x, "x", _vdtypes(p), p.n),
+                                 _ptr(y, "y", _vdtypes(p), p.cells),
+                                 _ptr(b, "b", _u32(), p.index_words), _stream(stream)),
+           "hc_encode_staged")
+
+
+def alloc_stage_workspace(p: hc_params, device="cuda"):
+    import torch
+    return torch.empty(hc_encode_staged_bytes(p), dtype=torch.uint8, device=device)
 
 
 def hc_encode_coo(p: hc_params, idx, val, y, b, stream=None):

@@ -390,6 +390,39 @@ hc_status hc_encode_gather(const hc_params* p, const void* plan, size_t plan_byt
     return e == hipSuccess ? HC_OK : fail_hip(e, "hc_encode_gather");
 }
 
+hc_status hc_encode_staged_bytes(const hc_params* p, size_t* bytes) {
+    g_last_error.clear();
+    Geo g;
+    const hc_status s = to_geo(p, &g);
+    if (s != HC_OK) return s;
+    if (!bytes) return fail(HC_EINVAL, "bytes is NULL");
+    if (g.block) return fail(HC_EUNSUPPORTED, "a blocked sketch is encoded by hc_encode");
+    if (!plan_supported(g)) return fail(HC_EUNSUPPORTED, "the staged encode needs c >= 256");
+    *bytes = stage_layout(g).total;
+    return HC_OK;
+}
+
+hc_status hc_encode_staged(const hc_params* p, const void* plan, size_t plan_bytes, void* ws,
+                           size_t ws_bytes, const void* x, void* y, uint32_t* b,
+                           hipStream_t stream) {
+    g_last_error.clear();
+    Geo g;
+    const hc_status s = to_geo(p, &g);
+    if (s != HC_OK) return s;
+    if (g.block) return fail(HC_EUNSUPPORTED, "a blocked sketch is encoded by hc_encode");
+    if (!plan_supported(g)) return fail(HC_EUNSUPPORTED, "the staged encode needs c >= 256");
+    if (!plan || !aligned(plan, 256)) return fail(HC_EINVAL, "plan must be non-NULL and 256-byte aligned");
+    if (plan_bytes < plan_layout(g).total) return fail(HC_EWORKSPACE, "plan smaller than hc_plan_bytes reports");
+    if (!ws || !aligned(ws, 256)) return fail(HC_EINVAL, "ws must be non-NULL and 256-byte aligned");
+    if (ws_bytes < stage_layout(g).total)
+        return fail(HC_EWORKSPACE, "ws smaller than hc_encode_staged_bytes reports");
+    if (!x || !y || !b) return fail(HC_EINVAL, "x, y and b must be non-NULL");
+    if (!aligned(x, 4) || !aligned(y, 4) || !aligned(b, 4))
+        return fail(HC_EINVAL, "x, y and b must be 4-byte aligned");
+    const hipError_t e = launch_encode_staged(g, plan, ws, x, y, b, stream);
+    return e == hipSuccess ? HC_OK : fail_hip(e, "hc_encode_staged");
+}
+
 hc_status hc_encode_coo(const hc_params* p, const uint32_t* idx, const void* val, uint64_t nnz,
                         void* y, uint32_t* b, hipStream_t stream) {
     g_last_error.clear();

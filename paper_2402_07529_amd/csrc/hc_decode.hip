@@ -117,30 +117,6 @@ __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
     return v;
 }
 
-// Exclusive scan over the lanes of a workgroup; *total gets the sum.
-__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s_tmp,
-                                                         uint32_t* total) {
-    const uint32_t lane = lane_id();
-    const uint32_t wave = threadIdx.x >> 6;
-    const uint32_t nwaves = blockDim.x >> 6;
-    uint32_t x = v;
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t y = __shfl_up(x, d);
-        if (lane >= (uint32_t)d) x += y;
-    }
-    if (lane == 63) s_tmp[wave] = x;
-    lds_barrier();
-    uint32_t off = 0, tot = 0;
-    for (uint32_t w = 0; w < nwaves; w++) {
-        const uint32_t s = s_tmp[w];
-        if (w < wave) off += s;
-        tot += s;
-    }
-    lds_barrier();
-    *total = tot;
-    return off + x - v;
-}
-
 template <typename T>
 __global__ __launch_bounds__(kBlock) void prep_kernel(const T* __restrict__ y_agg,
                                                       typename Acc<T>::type* __restrict__ yw,

@@ -116,18 +116,85 @@ __device__ __forceinline__ void scatter_load(const T (&e)[4], const bool (&nz)[4
     }
 }
 
+// Staged encode, first pass: the nonzeros of every batch of c >= 256
+// parameters go to the batch's list of kStageCap (column, value) entries in
+// the staging buffer, at ranks taken from the wave's ballots; count[b] gets
+// the batch's number of nonzeros (the lists keep the first kStageCap; a batch
+// with more is read from the gradient itself by the second pass).  No global
+// atomics: the sketch is assembled row by row afterwards.
+struct StageOut {
+    uint2* list;      // [nb * kStageCap]: .x = column t, .y = value bits
+    uint32_t* count;  // [nb]
+    uint64_t nb;      // batches: a tile past the gradient's end names batches >= nb
+};
+
+template <typename T>
+__device__ __forceinline__ uint32_t value_bits(T v) {
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// The wave's staged entries of batch b (cnt nonzeros, the first kStageCap in
+// stage[]) go to the batch's list with one store, lane r storing entry r.
+// Every batch's count is written, zero or not (the staged encode clears
+// nothing beforehand).
+static_assert(kStageCap == 64, "one staged entry per lane");
+__device__ __forceinline__ void flush_batch(const uint2* stage, uint32_t cnt, uint64_t b,
+                                            uint32_t lane, const StageOut& so) {
+    if (lane == 0 && b < so.nb) so.count[b] = cnt;
+    if (cnt == 0u) return;  // uniform over the wave (a batch >= nb has none)
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // the wave's LDS writes have landed
+    __builtin_amdgcn_wave_barrier();
+    if (lane < cnt) so.list[b * kStageCap + lane] = stage[lane];
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // read back before the stage is refilled
+    __builtin_amdgcn_wave_barrier();
+}
+
+// e[l][k] is parameter tbase + 256 l + 4 lane + k; a batch spans c / 256
+// loads.  Each nonzero's (column, value) goes to the wave's LDS stage at its
+// rank in the batch, and each batch's run is then stored whole.
+template <typename T>
+__device__ __forceinline__ void stage_tile(const T (&e)[4][4], const bool (&nz)[4][4],
+                                           const uint64_t (&m)[4][4], uint64_t tbase,
+                                           uint32_t lane, const StageOut& so, uint32_t log2c,
+                                           uint2* stage) {
+    const uint32_t cmask = (1u << log2c) - 1u;
+    uint32_t base = 0;  // nonzeros of the current batch before this load
+#pragma unroll
+    for (int l = 0; l < 4; l++) {
+        const uint64_t pl = tbase + 256ull * l;
+        if (l > 0 && (pl & cmask) == 0u) {  // load l starts a new batch
+            flush_batch(stage, base, (pl >> log2c) - 1u, lane, so);
+            base = 0;
+        }
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            const uint64_t mk = m[l][k];
+            if (mk == 0ull) continue;  // uniform over the wave
+            if (nz[l][k]) {
+                const uint32_t rank = base + lanes_below(mk);
+                if (rank < kStageCap)
+                    stage[rank] = make_uint2((256u * (uint32_t)l + 4u * lane + (uint32_t)k) & cmask,
+                                             value_bits(e[l][k]));
+            }
+            base += (uint32_t)__popcll(mk);
+        }
+    }
+    flush_batch(stage, base, (tbase + 768u) >> log2c, lane, so);
+}
+
 // One wave tile: 1024 consecutive parameters from `tbase` (a multiple of
 // 1024), four loads of 256 per wave, e[l][k] = parameter tbase + 256 l +
 // 4 lane + k.  Its 32 bitmap words are built from the 16 ballots in lanes
 // 0..31, which store the nonzero ones (the bitmap was zero-filled); with a
 // Bloom-filter index (BL) each nonzero word is OR-ed, rotated, into the filter
 // instead (section 3.3).
-template <typename T, int MODE, bool BL>
+template <typename T, int MODE, bool BL, bool STAGED>
 __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, uint32_t lane,
                                             T* __restrict__ y, uint32_t* __restrict__ b,
                                             uint64_t words, uint64_t seed, uint32_t rows,
                                             uint32_t c, uint32_t cmask, uint32_t log2c,
-                                            uint32_t bk, uint32_t brows) {
+                                            uint32_t bk, uint32_t brows, const StageOut& so,
+                                            uint2* stage) {
     bool nz[4][4];
     uint64_t m[4][4], any = 0;
 #pragma unroll
@@ -140,8 +207,10 @@ __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, 
         }
     // an all-zero tile has nothing to store (the bitmap was zero-filled) and
     // nothing to add: on a sparse gradient that is almost every tile, and
-    // skipping the word assembly keeps the wave's next loads coming sooner
-    if (any == 0) return;
+    // skipping the word assembly keeps the wave's next loads coming sooner.
+    // The staged encode clears nothing beforehand and stores every tile's
+    // words and counts, zero or not.
+    if (!STAGED && any == 0) return;
     // word w = 8 l + i holds parameters 32 w .. 32 w + 31: lanes 8i..8i+7 of
     // load l, parameter 4 lane' + k at bit 4 (lane' - 8 i) + k
     if (lane < 32) {
@@ -154,10 +223,15 @@ __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, 
         }
         const uint64_t widx = (tbase >> 5) + lane;
         if (!BL) {
-            if (word != 0u && widx < words) b[widx] = word;
+            // staged: all 32 words of every tile, one full 128-byte line
+            if ((STAGED || word != 0u) && widx < words) b[widx] = word;
         } else if (word != 0u) {
             bloom_insert_word(b, word, widx << 5, seed, bk, brows, c, cmask, log2c);
         }
+    }
+    if (STAGED) {
+        stage_tile<T>(e, nz, m, tbase, lane, so, log2c, stage);
+        return;
     }
 #pragma unroll
     for (int l = 0; l < 4; l++) {
@@ -175,12 +249,14 @@ __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, 
 // nontemporal loads per lane before encoding the current pair.  The tail takes single tiles with
 // bounds-checked 4-byte loads (also used throughout when x is not 16-byte
 // aligned).
-template <typename T, int MODE, bool BL>
+template <typename T, int MODE, bool BL, bool STAGED>
 __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
     const T* __restrict__ x, T* __restrict__ y, uint32_t* __restrict__ b, uint64_t n,
     uint64_t words, uint64_t seed, uint32_t rows, uint32_t c, uint32_t cmask, uint32_t log2c,
-    bool vec, uint32_t bk, uint32_t brows) {
+    bool vec, uint32_t bk, uint32_t brows, StageOut so) {
     typedef typename Vec4<T>::type V;
+    __shared__ uint2 s_stage[STAGED ? kBlock : 1];  // staged: kStageCap entries per wave
+    uint2* const stage = s_stage + (STAGED ? (threadIdx.x & ~63u) : 0u);
     const uint32_t lane = lane_id();
     const uint64_t gwave = (uint64_t)blockIdx.x * (kBlock / 64) + uniform(threadIdx.x >> 6);
     const uint64_t nwaves = (uint64_t)gridDim.x * (kBlock / 64);
@@ -203,8 +279,8 @@ __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
                 e[l][2] = v[4 * h + l].z;
                 e[l][3] = v[4 * h + l].w;
             }
-            encode_tile<T, MODE, BL>(e, (2 * q + h) * kTile, lane, y, b, words, seed, rows, c,
-                                     cmask, log2c, bk, brows);
+            encode_tile<T, MODE, BL, STAGED>(e, (2 * q + h) * kTile, lane, y, b, words, seed, rows,
+                                             c, cmask, log2c, bk, brows, so, stage);
         }
     };
     // rolling pipeline: the next pair's loads are issued before the current
@@ -241,8 +317,8 @@ __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
                 const uint64_t p = tbase + 256ull * l + 4ull * lane + k;
                 e[l][k] = p < n ? x[p] : T(0);
             }
-        encode_tile<T, MODE, BL>(e, tbase, lane, y, b, words, seed, rows, c, cmask, log2c, bk,
-                                 brows);
+        encode_tile<T, MODE, BL, STAGED>(e, tbase, lane, y, b, words, seed, rows, c, cmask, log2c,
+                                         bk, brows, so, stage);
     }
 }
 
@@ -277,24 +353,24 @@ uint32_t grid_for(uint64_t work_items, uint64_t per_block, uint32_t cap) {
     return (uint32_t)g;
 }
 
-template <typename T, int MODE, bool BL>
+template <typename T, int MODE, bool BL, bool STAGED = false>
 hipError_t launch_dense_t(const Geo& g, const void* x, void* y, uint32_t* b, hipStream_t s,
-                          uint64_t ntiles, int cus) {
+                          uint64_t ntiles, int cus, StageOut so = StageOut{nullptr, nullptr, 0}) {
     // the workgroups that are resident at once stride over the tiles; when
     // that leaves each wave fewer than 64 tiles, four times as many, so the
     // dispatcher evens out the last ones (measured on MI355X: VGG19- and
     // BERT-base-sized gradients 4 % faster; at 2^30 parameters no change)
     int per_cu = 0;  // resident workgroups per CU
     const hipError_t e = occupancy_per_cu(
-        reinterpret_cast<const void*>(&encode_dense_kernel<T, MODE, BL>), kBlock, &per_cu);
+        reinterpret_cast<const void*>(&encode_dense_kernel<T, MODE, BL, STAGED>), kBlock, &per_cu);
     if (e != hipSuccess) return e;
     const uint64_t resident = (uint64_t)cus * per_cu;
     const uint64_t mult = ntiles < 64 * resident * (kBlock / 64) ? 4 : 1;
     const uint32_t grid = grid_for(ntiles, 2 * (kBlock / 64), (uint32_t)(resident * mult));
-    hipLaunchKernelGGL((encode_dense_kernel<T, MODE, BL>), dim3(grid), dim3(kBlock), 0, s,
+    hipLaunchKernelGGL((encode_dense_kernel<T, MODE, BL, STAGED>), dim3(grid), dim3(kBlock), 0, s,
                        static_cast<const T*>(x), static_cast<T*>(y), b, g.n, g.words, g.seed,
                        g.rows, g.c, g.cmask, g.log2c,
-                       (reinterpret_cast<uintptr_t>(x) & 15u) == 0, g.bloom_k, g.bloom_rows);
+                       (reinterpret_cast<uintptr_t>(x) & 15u) == 0, g.bloom_k, g.bloom_rows, so);
     return hipGetLastError();
 }
 
@@ -454,7 +530,268 @@ hipError_t launch_gather_t(const Geo& g, const void* plan, const void* x, void* 
     return hipGetLastError();
 }
 
+// ---- staged encode, second pass: rows from the staged lists ----------------------
+//
+// One wave per sketch row (grid-stride) sums the row in its own LDS copy: for
+// every (batch, hash j) pair of the row's plan entries, g_j * value into cell
+// (t + bias_j) mod C for each nonzero (t, value) of the batch -- taken from the
+// batch's staged list when the list holds them all, else from the gradient
+// itself (the batch's C values, coalesced, as in the gathered encode).  The
+// entries are taken 64 at a time, one per lane, which loads it and its
+// batch's count; a wave prefix sum gives each listed nonzero a slot, and the
+// lanes take slots in turn with kAhead list loads in flight each.  Batches
+// past the list capacity go one at a time.  Within one pair the cells are a
+// rotation and never collide; different pairs of a row may, so the adds are
+// LDS atomics (int32 wraps; fp32 sums in an unspecified order, like
+// hc_encode's global atomics).  The row is then stored once, so the sketch
+// needs no clearing and takes no global atomics.  A wave per row, with no
+// workgroup barriers, keeps four times as many rows in flight as a workgroup
+// per row: a row is a few dependent memory latencies whatever its size.
+template <typename T>
+struct RowsArgs {
+    const PlanHeader* hdr;
+    const uint32_t* rowoff;
+    const uint2* entry;
+    const uint32_t* count;
+    const uint2* list;
+    const T* x;
+    T* y;
+    uint32_t* b;
+    uint64_t n, seed, words, nb;
+    uint32_t rows;
+    bool vec;    // x is 16-byte aligned
+    bool y_vec;  // y is 16-byte aligned
+};
+
+template <typename T>
+__device__ __forceinline__ T bits_value(uint32_t v) {
+    return __builtin_bit_cast(T, v);
+}
+
+template <typename T>
+__device__ __forceinline__ void lds_add(T* a, T v) {
+    if constexpr (std::is_same<T, int32_t>::value)
+        atomicAdd(reinterpret_cast<unsigned int*>(a), (unsigned int)v);
+    else
+        atomicAdd(a, v);
+}
+
+template <typename T, int C>
+__global__ __launch_bounds__(kBlock) void stage_rows_kernel(RowsArgs<T> a) {
+    typedef typename Vec4<T>::type V;
+    constexpr uint32_t NV = C / 256;  // 16-byte vectors per lane per row (and per batch)
+    constexpr uint32_t kWaves = kBlock / 64;
+    constexpr uint32_t kAhead = 4;    // listed nonzeros per lane with loads in flight
+    __shared__ __align__(16) T s_rows[kWaves * C];
+    const PlanHeader* hdr = a.hdr;
+    const bool ok = hdr->magic == kPlanMagic && hdr->n == a.n && hdr->seed == a.seed &&
+                    hdr->c == (uint32_t)C && hdr->rows == a.rows;
+    if (!ok) {
+        // a plan of another geometry: a zero sketch and an all-ones bitmap,
+        // which no decode can mistake for a gradient
+        const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+        const uint64_t cells = (uint64_t)a.rows * C;
+        for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < cells; i += stride)
+            a.y[i] = T(0);
+        for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < a.words; i += stride)
+            a.b[i] = 0xffffffffu;
+        return;
+    }
+    const uint32_t lane = lane_id();
+    const uint32_t wave = uniform(threadIdx.x >> 6);
+    T* const acc = s_rows + wave * C;
+    const uint32_t nwaves = gridDim.x * kWaves;
+    for (uint32_t row = blockIdx.x * kWaves + wave; row < a.rows; row += nwaves) {
+        // a wave's LDS operations complete in order: the previous row's reads
+        // are done before these stores
+#pragma unroll
+        for (uint32_t q = 0; q < NV; q++) {
+            const V z = {T(0), T(0), T(0), T(0)};
+            *reinterpret_cast<V*>(acc + 256u * q + 4u * lane) = z;
+        }
+        const uint32_t e0 = a.rowoff[row], e1 = a.rowoff[row + 1];
+        for (uint32_t cb = e0; cb < e1; cb += 64u) {
+            const uint32_t e = cb + lane;
+            uint2 ent = make_uint2(0u, 0u);
+            uint32_t m = 0;
+            if (e < e1) {
+                ent = a.entry[e];
+                if (ent.x < a.nb) m = a.count[ent.x];
+            }
+            const uint32_t lm = m <= kStageCap ? m : 0u;  // listed nonzeros of this lane's pair
+            uint32_t incl = lm;
+#pragma unroll
+            for (uint32_t d = 1; d < 64; d <<= 1) {
+                const uint32_t y = __shfl_up(incl, d);
+                if (lane >= d) incl += y;
+            }
+            const uint32_t total = __shfl(incl, 63);
+            for (uint32_t i0 = 0; i0 < total; i0 += 64u * kAhead) {
+                uint2 it[kAhead];
+                uint32_t eb[kAhead];
+#pragma unroll
+                for (uint32_t u = 0; u < kAhead; u++) {
+                    // slot i belongs to the first lane whose inclusive sum
+                    // exceeds it (every lane searches, so the shuffles see
+                    // the whole wave)
+                    const uint32_t i = i0 + 64u * u + lane;
+                    const uint32_t ic = i < total ? i : total - 1u;
+                    uint32_t pos = 0;
+#pragma unroll
+                    for (uint32_t step = 32; step >= 1; step >>= 1)
+                        if ((uint32_t)__shfl(incl, (int)(pos + step - 1u)) <= ic) pos += step;
+                    const uint32_t first = (uint32_t)__shfl(incl, (int)pos) -
+                                           (uint32_t)__shfl(lm, (int)pos);
+                    const uint32_t bx = (uint32_t)__shfl(ent.x, (int)pos);
+                    eb[u] = (uint32_t)__shfl(ent.y, (int)pos);
+                    it[u] = make_uint2(0u, 0u);
+                    if (i < total) it[u] = a.list[(uint64_t)bx * kStageCap + (ic - first)];
+                }
+#pragma unroll
+                for (uint32_t u = 0; u < kAhead; u++) {
+                    if (i0 + 64u * u + lane >= total) continue;
+                    const uint32_t cell = (it[u].x + (eb[u] & 0xffffu)) & (uint32_t)(C - 1);
+                    lds_add(&acc[cell], Val<T>::sign(bits_value<T>(it[u].y), (eb[u] >> 31) != 0u));
+                }
+            }
+            // batches past the list capacity: the batch's values from x
+            uint64_t big = __ballot(m > kStageCap);
+            while (big != 0ull) {
+                const uint32_t src = (uint32_t)__ffsll((unsigned long long)big) - 1u;
+                big &= big - 1ull;
+                const uint32_t bx = (uint32_t)__shfl(ent.x, (int)src);
+                const uint32_t ey = (uint32_t)__shfl(ent.y, (int)src);
+                const uint32_t bias = ey & 0xffffu;
+                const bool neg = (ey >> 31) != 0u;
+                const uint64_t bbase = (uint64_t)bx * C;
+                T v[NV][4];
+                if (a.vec && bbase + C <= a.n) {
+                    const V* src4 = reinterpret_cast<const V*>(a.x + bbase) + lane;
+#pragma unroll
+                    for (uint32_t u = 0; u < NV; u++) {
+                        const V q = __builtin_nontemporal_load(src4 + 64 * u);
+                        v[u][0] = q.x;
+                        v[u][1] = q.y;
+                        v[u][2] = q.z;
+                        v[u][3] = q.w;
+                    }
+                } else {
+#pragma unroll
+                    for (uint32_t u = 0; u < NV; u++)
+#pragma unroll
+                        for (uint32_t k = 0; k < 4; k++) {
+                            const uint64_t p = bbase + 256u * u + 4u * lane + k;
+                            v[u][k] = p < a.n ? a.x[p] : T(0);
+                        }
+                }
+#pragma unroll
+                for (uint32_t u = 0; u < NV; u++)
+#pragma unroll
+                    for (uint32_t k = 0; k < 4; k++) {
+                        if (!Val<T>::nonzero(v[u][k])) continue;
+                        const uint32_t t = 256u * u + 4u * lane + k;
+                        lds_add(&acc[(t + bias) & (uint32_t)(C - 1)], Val<T>::sign(v[u][k], neg));
+                    }
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // every lane's LDS adds have landed
+        __builtin_amdgcn_wave_barrier();
+        T* dst = a.y + (uint64_t)row * C;
+        if (a.y_vec) {
+#pragma unroll
+            for (uint32_t q = 0; q < NV; q++)
+                reinterpret_cast<V*>(dst)[64u * q + lane] =
+                    *reinterpret_cast<const V*>(acc + 256u * q + 4u * lane);
+        } else {
+#pragma unroll
+            for (uint32_t q = 0; q < 4 * NV; q++) dst[64u * q + lane] = acc[64u * q + lane];
+        }
+    }
+}
+
+template <typename T, int C>
+hipError_t launch_stage_rows_t(const Geo& g, const void* plan, const StageLayout& SL, void* ws,
+                               const void* x, void* y, uint32_t* b, hipStream_t s, int cus) {
+    const PlanLayout L = plan_layout(g);
+    const char* pb = static_cast<const char*>(plan);
+    char* wb = static_cast<char*>(ws);
+    RowsArgs<T> a;
+    a.hdr = reinterpret_cast<const PlanHeader*>(pb + L.header);
+    a.rowoff = reinterpret_cast<const uint32_t*>(pb + L.rowoff);
+    a.entry = reinterpret_cast<const uint2*>(pb + L.entry);
+    a.count = reinterpret_cast<const uint32_t*>(wb + SL.count);
+    a.list = reinterpret_cast<const uint2*>(wb + SL.list);
+    a.x = static_cast<const T*>(x);
+    a.y = static_cast<T*>(y);
+    a.b = b;
+    a.n = g.n;
+    a.seed = g.seed;
+    a.words = g.bwords;
+    a.nb = SL.nb;
+    a.rows = g.rows;
+    a.vec = (reinterpret_cast<uintptr_t>(x) & 15u) == 0;
+    a.y_vec = (reinterpret_cast<uintptr_t>(y) & 15u) == 0;
+    // one wave per row, four per workgroup, every row in flight at once when
+    // the chip holds that many workgroups
+    int per_cu = 0;
+    hipError_t e = occupancy_per_cu(reinterpret_cast<const void*>(&stage_rows_kernel<T, C>), kBlock,
+                                    &per_cu);
+    if (e != hipSuccess) return e;
+    const uint64_t want = ((uint64_t)g.rows + kBlock / 64 - 1) / (kBlock / 64);
+    const uint64_t cap = (uint64_t)cus * per_cu;
+    const uint32_t grid = (uint32_t)(want < cap ? want : cap);
+    hipLaunchKernelGGL((stage_rows_kernel<T, C>), dim3(grid), dim3(kBlock), 0, s, a);
+    return hipGetLastError();
+}
+
+template <typename T, bool BL>
+hipError_t launch_staged_t(const Geo& g, const void* plan, void* ws, const void* x, void* y,
+                           uint32_t* b, hipStream_t s, int cus) {
+    const StageLayout SL = stage_layout(g);
+    char* wb = static_cast<char*>(ws);
+    StageOut so;
+    so.list = reinterpret_cast<uint2*>(wb + SL.list);
+    so.count = reinterpret_cast<uint32_t*>(wb + SL.count);
+    so.nb = SL.nb;
+    const uint64_t ntiles = (g.n + kTile - 1) / kTile;
+    hipError_t e = launch_dense_t<T, 0, BL, true>(g, x, y, b, s, ntiles, cus, so);
+    if (e != hipSuccess) return e;
+    if (g.c == 1024) return launch_stage_rows_t<T, 1024>(g, plan, SL, ws, x, y, b, s, cus);
+    if (g.c == 512) return launch_stage_rows_t<T, 512>(g, plan, SL, ws, x, y, b, s, cus);
+    return launch_stage_rows_t<T, 256>(g, plan, SL, ws, x, y, b, s, cus);
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
 }  // namespace
+
+StageLayout stage_layout(const Geo& g) {
+    StageLayout L;
+    L.nb = (g.n + g.c - 1) / g.c;
+    size_t o = 0;
+    L.count = o;  o = align256(o + L.nb * 4);
+    L.list = o;   o = align256(o + L.nb * kStageCap * 8);
+    L.total = o;
+    return L;
+}
+
+hipError_t launch_encode_staged(const Geo& g, const void* plan, void* ws, const void* x, void* y,
+                                uint32_t* b, hipStream_t s) {
+    DeviceInfo di;
+    hipError_t e = device_info(&di);
+    if (e != hipSuccess) return e;
+    // nothing is cleared: the first pass writes every bitmap word and every
+    // batch count, the second every sketch cell; a Bloom filter, which the
+    // first pass ORs into, is cleared
+    if (g.bloom_k != 0) {
+        e = launch_fill_u32(b, g.bwords, 0u, s);
+        if (e != hipSuccess) return e;
+        if (g.f32) return launch_staged_t<float, true>(g, plan, ws, x, y, b, s, di.cus);
+        return launch_staged_t<int32_t, true>(g, plan, ws, x, y, b, s, di.cus);
+    }
+    if (g.f32) return launch_staged_t<float, false>(g, plan, ws, x, y, b, s, di.cus);
+    return launch_staged_t<int32_t, false>(g, plan, ws, x, y, b, s, di.cus);
+}
 
 hipError_t launch_fill2_u32(uint32_t* p, uint64_t count, uint32_t* p2, uint64_t count2,
                             uint32_t value, hipStream_t s) {

@@ -61,6 +61,21 @@ hipError_t launch_encode_coo(const Geo& g, const uint32_t* idx, const void* val,
 hipError_t launch_encode_gather(const Geo& g, const void* plan, const void* x, void* y,
                                 uint32_t* b, hipStream_t s);
 
+// staged dense encode (c >= 256, unblocked sketch): a first pass writes the
+// index and, per batch of c parameters, its nonzero count and up to kStageCap
+// of its (column, value) pairs into a caller workspace; a second pass builds
+// every sketch row in LDS through the plan
+constexpr uint32_t kStageCap = 64;
+struct StageLayout {
+    uint64_t nb;          // batches
+    size_t count, list, total;
+};
+StageLayout stage_layout(const Geo& g);
+hipError_t launch_encode_staged(const Geo& g, const void* plan, void* ws, const void* x, void* y,
+                                uint32_t* b, hipStream_t s);
+hipError_t launch_fill2_u32(uint32_t* p, uint64_t count, uint32_t* p2, uint64_t count2,
+                            uint32_t value, hipStream_t s);
+
 // aggregate
 hipError_t launch_aggregate(const Geo& g, const void* y_in, const uint32_t* b_in, uint32_t W,
                             void* y_out, uint32_t* b_out, hipStream_t s);

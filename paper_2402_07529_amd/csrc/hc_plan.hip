@@ -48,26 +48,6 @@ __global__ __launch_bounds__(kBlock) void plan_count_kernel(uint32_t* __restrict
     }
 }
 
-__device__ __forceinline__ uint32_t block_scan_excl(uint32_t v, uint32_t* s_tmp, uint32_t* total) {
-    const uint32_t lane = lane_id(), wave = threadIdx.x >> 6;
-    uint32_t x = v;
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t y = __shfl_up(x, d);
-        if (lane >= (uint32_t)d) x += y;
-    }
-    if (lane == 63) s_tmp[wave] = x;
-    lds_barrier();
-    uint32_t off = 0, tot = 0;
-    for (uint32_t w = 0; w < blockDim.x / 64; w++) {
-        const uint32_t s = s_tmp[w];
-        if (w < wave) off += s;
-        tot += s;
-    }
-    lds_barrier();
-    *total = tot;
-    return off + x - v;
-}
-
 // Three-pass exclusive scan of a uint32 array (sums fit in 32 bits).
 __global__ __launch_bounds__(kBlock) void scan_tiles_kernel(const uint32_t* __restrict__ in,
                                                             uint64_t len,
@@ -78,7 +58,7 @@ __global__ __launch_bounds__(kBlock) void scan_tiles_kernel(const uint32_t* __re
     for (uint32_t i = 0; i < kScanItems; i++)
         if (base + i < len) s += in[base + i];
     uint32_t total;
-    block_scan_excl(s, s_tmp, &total);
+    block_exclusive_scan(s, s_tmp, &total);
     if (threadIdx.x == 0) tile_sum[blockIdx.x] = total;
 }
 
@@ -93,7 +73,7 @@ __global__ __launch_bounds__(1024) void scan_tile_sums_kernel(uint32_t* __restri
     uint32_t s = 0;
     for (uint64_t i = lo; i < hi; i++) s += tile_sum[i];
     uint32_t total;
-    uint32_t off = block_scan_excl(s, s_tmp, &total);
+    uint32_t off = block_exclusive_scan(s, s_tmp, &total);
     for (uint64_t i = lo; i < hi; i++) {
         const uint32_t v = tile_sum[i];
         tile_sum[i] = off;
@@ -117,7 +97,7 @@ __global__ __launch_bounds__(kBlock) void scan_write_kernel(const uint32_t* __re
         s += v[i];
     }
     uint32_t total;
-    uint32_t off = tile_sum[blockIdx.x] + block_scan_excl(s, s_tmp, &total);
+    uint32_t off = tile_sum[blockIdx.x] + block_exclusive_scan(s, s_tmp, &total);
     for (uint32_t i = 0; i < kScanItems; i++) {
         if (base + i < len) {
             out[base + i] = off;

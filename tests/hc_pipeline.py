@@ -40,12 +40,14 @@ def oracle_run(w, rows: int, c: int, coo: bool = True, block: int = 0, seed=None
 def gpu_run(w, rows: int, c: int, coo_input: bool = False, want_coo_out: bool = True,
             max_support: int = 0, keep_workers: bool = True, coo_cap=None, use_plan=False,
             plan=None, block: int = 0, seed=None, bloom_k: int = 0, bloom_rows: int = 0,
-            gather: bool = False):
+            gather: bool = False, staged: bool = False):
     """The same pipeline through libhc on the current GPU.  use_plan builds the
     geometry's inverse row map and decodes with it; `plan` passes one in;
     block > 0 selects the blocked sketch; seed overrides w's hash seed;
     bloom_k > 0 selects a Bloom-filter index; gather encodes the dense
-    gradients row by row through a plan (hc_encode_gather)."""
+    gradients row by row through a plan (hc_encode_gather); staged stages
+    each batch's nonzeros and assembles the rows through a plan
+    (hc_encode_staged)."""
     import torch
 
     import paper_2402_07529_amd as hc
@@ -56,7 +58,8 @@ def gpu_run(w, rows: int, c: int, coo_input: bool = False, want_coo_out: bool = 
     W = w.W
     Y = torch.empty((W, p.cells), dtype=vt, device=dev)
     B = torch.empty((W, p.index_words), dtype=torch.int32, device=dev)
-    enc_plan = hc.make_plan(p, dev) if gather else None
+    enc_plan = hc.make_plan(p, dev) if gather or staged else None
+    stage_ws = hc.alloc_stage_workspace(p, dev) if staged else None
     for i in range(W):
         if coo_input:
             idx = torch.from_numpy(w.idx[i].view(np.int32)).to(dev)
@@ -67,6 +70,8 @@ def gpu_run(w, rows: int, c: int, coo_input: bool = False, want_coo_out: bool = 
             x[torch.from_numpy(w.idx[i].astype(np.int64)).to(dev)] = torch.from_numpy(w.val[i]).to(dev)
             if gather:
                 hc.hc_encode_gather(p, enc_plan, x, Y[i], B[i])
+            elif staged:
+                hc.hc_encode_staged(p, enc_plan, stage_ws, x, Y[i], B[i])
             else:
                 hc.hc_encode(p, x, Y[i], B[i])
             del x

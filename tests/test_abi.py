@@ -227,3 +227,29 @@ def test_decode_binding_checks_coo_lengths_before_launch():
                      coo_val=torch.zeros(7, dtype=torch.int32))
     with pytest.raises(ValueError, match="both"):
         hc.hc_decode(p, None, None, None, None, coo_idx=torch.zeros(8, dtype=torch.int32))
+
+
+def test_staged_encode_rejected_before_launch():
+    # hc_encode_staged: unblocked sketch, c >= 256, a 256-byte aligned plan of
+    # at least hc_plan_bytes and a 256-byte aligned workspace of at least
+    # hc_encode_staged_bytes
+    import paper_2402_07529_amd as hc
+    L = hc.lib()
+    V = ctypes.c_void_p
+    p = hc.hc_geometry(2_000_000, 20_000, 1.23, 1024, 3)
+    need = hc.hc_plan_bytes(p)
+    wsb = hc.hc_encode_staged_bytes(p)
+    assert wsb >= ((2_000_000 + 1023) // 1024) * (64 * 8 + 4)
+    ok = [V(256), need, V(512), wsb, V(256), V(256), V(256), None]
+    bad = [(0, V(100), hc.HC_EINVAL), (0, None, hc.HC_EINVAL), (1, need - 1, hc.HC_EWORKSPACE),
+           (2, V(520), hc.HC_EINVAL), (2, None, hc.HC_EINVAL), (3, wsb - 1, hc.HC_EWORKSPACE),
+           (4, None, hc.HC_EINVAL), (5, V(18), hc.HC_EINVAL)]
+    for k, v, st in bad:
+        args = list(ok)
+        args[k] = v
+        assert L.hc_encode_staged(ctypes.byref(p), *args) == st, (k, v)
+    for q in (hc.hc_geometry(2_000_000, 20_000, 1.23, 64, 3),                  # c < 256
+              hc.hc_geometry_blocked(109_482_240, 9_305_915, 1.3, 1024, 14, 3)):  # blocked
+        assert L.hc_encode_staged(ctypes.byref(q), *ok) == hc.HC_EUNSUPPORTED
+        with pytest.raises(hc.HCError):
+            hc.hc_encode_staged_bytes(q)

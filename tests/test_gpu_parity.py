@@ -120,8 +120,8 @@ def assert_same_info(gi, oi):
     assert gi.status == 0
 
 
-def check_int(w, rows, c, coo_input=False, use_plan=False, gather=False):
-    g = gpu_run(w, rows, c, coo_input=coo_input, use_plan=use_plan, gather=gather)
+def check_int(w, rows, c, coo_input=False, use_plan=False, gather=False, staged=False):
+    g = gpu_run(w, rows, c, coo_input=coo_input, use_plan=use_plan, gather=gather, staged=staged)
     o = oracle_run(w, rows, c)
     for i in range(w.W):
         assert np.array_equal(g["Y"][i], o["Y"][i]), f"worker {i} sketch"
@@ -241,8 +241,8 @@ def test_forced_failure_three_cells():
     assert g["info"].n_recovered == 0 and g["info"].rounds == 0
 
 
-def check_fp32(w, rows, c, use_plan=False, gather=False):
-    g = gpu_run(w, rows, c, use_plan=use_plan, gather=gather)
+def check_fp32(w, rows, c, use_plan=False, gather=False, staged=False):
+    g = gpu_run(w, rows, c, use_plan=use_plan, gather=gather, staged=staged)
     o = oracle_run(w, rows, c)
     wb, ab = fp32_cell_bounds(w, o["g"])
     for i in range(w.W):
