@@ -30,7 +30,8 @@ from dataclasses import dataclass
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "libhco.so")
+# HCO_LIB selects another build of hco.c (the sanitizer build in the tests)
+_LIB_PATH = os.environ.get("HCO_LIB") or os.path.join(_HERE, "libhco.so")
 _lib = None
 
 GAMMA = 1.23  # section 3.2

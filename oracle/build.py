@@ -5,11 +5,19 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
-def build(verbose: bool = False) -> str:
+SANITIZED = os.path.join(HERE, "libhco_san.so")
+
+
+def build(verbose: bool = False, sanitize: bool = False) -> str:
+    """sanitize: an AddressSanitizer + UndefinedBehaviorSanitizer build in
+    libhco_san.so (host code only; load it with the ASan runtime preloaded and
+    HCO_LIB pointing at it)."""
     src = os.path.join(HERE, "hco.c")
-    out = os.path.join(HERE, "libhco.so")
+    out = SANITIZED if sanitize else os.path.join(HERE, "libhco.so")
     tmp = out + ".tmp"
-    cmd = ["gcc", "-std=c99", "-O2", "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, src, "-lm"]
+    flags = (["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+              "-fno-sanitize-recover=undefined"] if sanitize else ["-O2"])
+    cmd = ["gcc", "-std=c99", *flags, "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, src, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
