@@ -191,6 +191,15 @@ def cpu_baseline(w, rows, c, block, seed):
                 success=int(info.success), rounds=int(info.rounds))
 
 
+def auto_encode(w, c, blocked):
+    """The encode 'auto' picks: staged for a global sketch with c >= 256 when a
+    worker has at least one nonzero per two batches of c parameters (its
+    second pass visits every batch), else the atomic encode."""
+    nnz_w = float(np.mean([w.nnz(i) for i in range(w.W)]))
+    batches = (w.n + c - 1) // c
+    return "staged" if not blocked and c >= 256 and nnz_w >= 0.5 * batches else "atomic"
+
+
 def core_fraction(lam):
     """Edges left in the 2-core of a random 3-uniform hypergraph with lam edges
     per vertex (x^3 for the largest root of x = 1 - exp(-3 lam x^2)); the
@@ -389,12 +398,14 @@ def sweep(a, dev):
     import workloads as wl
     points = []
     for density in (0.001, 0.01, 0.05):
-        for overlap in (0.1, 0.5, 0.9):
+        for overlap in (0.1, 0.3, 0.5, 0.7, 0.9):
             w = wl.make("bert", density=density, overlap=overlap)
             r = Runner(w, 1024, dev)
-            m = r.run(1.23, 3, 1)
+            enc = auto_encode(w, 1024, False)
+            m = r.run(1.23, 3, 1, staged=enc == "staged")
             inf = m["info"]
             pt = dict(kind="density_overlap", density=density, overlap=overlap, n_agg=r.n_agg,
+                      encode=enc,
                       ratio=round(m["p"].cells / r.n_agg, 4), value=round(4 * w.n / m["ms"] / 1e6, 2),
                       ms_per_step=round(m["ms"], 4), encode_ms=round(m["enc_ms"], 4),
                       aggregate_ms=round(m["agg_ms"], 4), decode_ms=round(m["dec_ms"], 4),
@@ -406,8 +417,9 @@ def sweep(a, dev):
             del r
     w = wl.make("bert", density=0.01, overlap=0.5)
     r = Runner(w, 1024, dev)
+    enc = auto_encode(w, 1024, False)
     for ratio in (1.10, 1.15, 1.20, 1.22, 1.23, 1.25, 1.30, 1.50, 2.00):
-        m = r.run(ratio, 2, 1, check=False)
+        m = r.run(ratio, 2, 1, check=False, staged=enc == "staged")
         inf = m["info"]
         lam = r.n_agg / m["p"].cells
         pt = dict(kind="width", density=0.01, overlap=0.5, ratio=round(m["p"].cells / r.n_agg, 4),
@@ -454,10 +466,7 @@ def main():
         sys.exit(2)
     encode = a.encode
     if encode == "auto":
-        nnz_w = float(np.mean([w.nnz(i) for i in range(w.W)]))
-        batches = (w.n + a.c - 1) // a.c
-        encode = ("staged" if not a.blocked and a.c >= 256 and nnz_w >= 0.5 * batches
-                  else "atomic")
+        encode = auto_encode(w, a.c, a.blocked)
     gather = encode == "gather"
     staged = encode == "staged"
     if gather and (a.blocked or a.index == "bloom" or a.c < 256):

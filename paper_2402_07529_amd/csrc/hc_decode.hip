@@ -669,6 +669,136 @@ __global__ __launch_bounds__(kBlock) void counter_wave_kernel(CounterArgs a) {
     }
 }
 
+// The live batches of one screened chunk (lanes with `live`, their batch,
+// rotation and rank offset in bidx, bias and boff) added into the wave's row
+// of counters acc: kGroup batches per wave-wide load (WPB lanes each, one
+// bitmap word per lane), kUnroll loads in flight together; each lane turns
+// its word's set bits into cells and ranks.
+template <int C>
+__device__ __forceinline__ void add_live_batches(const CounterArgs& a, bool live, uint32_t bidx,
+                                                 uint32_t bias, uint32_t boff,
+                                                 unsigned long long* acc) {
+    constexpr uint32_t WPB = C / 32;       // bitmap words per batch
+    constexpr uint32_t kGroup = 64 / WPB;  // batches per wave-wide load
+    constexpr uint32_t kUnroll = 4;        // wave-wide loads in flight
+    const uint32_t lane = lane_id();
+    const uint32_t seg = lane / WPB;  // which batch of a group this lane serves
+    const uint32_t wl = lane % WPB;   // which word of it
+    uint64_t m = __ballot(live);
+    while (m != 0ull) {
+        uint32_t word[kUnroll], gbias[kUnroll], goff[kUnroll];
+        bool have[kUnroll];
+#pragma unroll
+        for (uint32_t u = 0; u < kUnroll; u++) {
+            // this segment's batch: the seg-th live lane left, if any
+            uint64_t mm = m;
+#pragma unroll
+            for (uint32_t q = 0; q < kGroup; q++)
+                if (q < seg && mm != 0ull) mm &= mm - 1ull;
+            have[u] = mm != 0ull;
+            const uint32_t src = have[u] ? (uint32_t)__ffsll((unsigned long long)mm) - 1u : 0u;
+            const uint32_t gb = (uint32_t)__shfl(bidx, (int)src);
+            gbias[u] = (uint32_t)__shfl(bias, (int)src);
+            goff[u] = (uint32_t)__shfl(boff, (int)src);
+            word[u] = have[u] ? load_word(a.b, (uint64_t)gb * WPB + wl, a.words, a.last_mask) : 0u;
+#pragma unroll
+            for (uint32_t q = 0; q < kGroup; q++)  // the group's batches are taken
+                if (m != 0ull) m &= m - 1ull;
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < kUnroll; u++) {
+            // rank of the word's first bit: the batch's offset plus the
+            // popcounts of its earlier words (a scan within the segment)
+            const uint32_t pc = __popc(word[u]);
+            uint32_t x = pc;
+#pragma unroll
+            for (uint32_t d = 1; d < WPB; d <<= 1) {
+                const uint32_t y = __shfl_up(x, d);
+                if (wl >= d) x += y;
+            }
+            uint32_t rank = goff[u] + x - pc;
+            uint32_t w = have[u] ? word[u] : 0u;
+            while (w != 0u) {
+                const uint32_t bit = (uint32_t)__builtin_ctz(w);
+                w &= w - 1u;
+                atomicAdd(&acc[(32u * wl + bit + gbias[u]) & (uint32_t)(C - 1)], kOne + rank);
+                rank++;
+            }
+        }
+    }
+}
+
+// One wave per sketch row (grid-stride), its counters in the wave's LDS: the
+// same counters as counter_kernel, for sketches with rows to spare.  The
+// wave screens kScreen chunks of 64 plan entries with their loads in flight
+// (a lane per entry: is any member of the support in the batch?), then adds
+// the live batches' members bit by bit (add_live_batches).  The row is then
+// written once.  A wave per row needs no workgroup barriers and keeps four
+// times as many rows in flight as a workgroup per row (VGG19: 10 K rows, the
+// counters went from 178 to 101 us); with few long rows (NCF: 1.9 K rows of
+// 1.7 K entries, a few dense words per batch) it left SIMDs idle and ran
+// twice as long as counter_kernel.
+template <int C>
+__global__ __launch_bounds__(kBlock) void counter_rows_kernel(CounterArgs a) {
+    constexpr uint32_t kWaves = kBlock / 64;
+    constexpr uint32_t kScreen = 4;  // chunks of 64 plan entries screened together
+    __shared__ unsigned long long s_acc[kWaves * C];
+    const PlanHeader* hdr = a.hdr;
+    const bool ok = hdr->magic == kPlanMagic && hdr->n == a.n && hdr->seed == a.seed &&
+                    hdr->c == a.c && hdr->rows == a.rows;
+    if (!ok) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) a.ctrl->bad_plan = 1u;
+        return;
+    }
+    if (a.ctrl->overflow) return;
+    const uint32_t kpack = pack_bits(a.ctrl->n_support);
+    const uint32_t lane = lane_id();
+    const uint32_t wave = uniform(threadIdx.x >> 6);
+    unsigned long long* const acc = s_acc + wave * C;
+    const uint32_t nwaves = gridDim.x * kWaves;
+    for (uint32_t row = blockIdx.x * kWaves + wave; row < a.rows; row += nwaves) {
+        // a wave's LDS operations complete in order: the previous row's
+        // reads are done before these stores
+        for (uint32_t k = lane; k < (uint32_t)C; k += 64) acc[k] = 0ull;
+        const uint32_t e0 = a.rowoff[row], e1 = a.rowoff[row + 1];
+        for (uint32_t cs = e0; cs < e1; cs += 64u * kScreen) {
+            // screen: each lane one entry per chunk, all loads in flight
+            uint32_t bidx[kScreen], bias[kScreen], boff[kScreen];
+            bool live[kScreen];
+#pragma unroll
+            for (uint32_t h = 0; h < kScreen; h++) {
+                const uint32_t e = cs + 64u * h + lane;
+                uint2 ent = make_uint2(0xffffffffu, 0u);
+                if (e < e1) ent = a.entry[e];
+                bidx[h] = ent.x;
+                bias[h] = ent.y & 0xffffu;
+            }
+#pragma unroll
+            for (uint32_t h = 0; h < kScreen; h++) {
+                boff[h] = 0;
+                live[h] = false;
+                if (bidx[h] < a.nb) {
+                    boff[h] = a.woffb[bidx[h]];
+                    live[h] = a.woffb[bidx[h] + 1] != boff[h];
+                }
+            }
+#pragma unroll
+            for (uint32_t h = 0; h < kScreen; h++)
+                add_live_batches<C>(a, live[h], bidx[h], bias[h], boff[h], acc);
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // every lane's LDS adds have landed
+        __builtin_amdgcn_wave_barrier();
+        unsigned long long* dst = a.cnt + (uint64_t)row * C;
+        bool fits = true;
+        for (uint32_t k = lane; k < (uint32_t)C; k += 64) {
+            const unsigned long long v = acc[k];
+            dst[k] = v;
+            fits = fits && fits_packed(v, kpack);
+        }
+        flag_unpackable(a.ctrl, fits);
+    }
+}
+
 // ---- peel ------------------------------------------------------------------------
 
 template <typename T>
@@ -1073,8 +1203,8 @@ __global__ __launch_bounds__(kBlock) void round0_kernel(PeelArgs<T> a) {
                 bool done = false;
                 if constexpr (std::is_same<T, int32_t>::value) {
                     if (packed) {
-                        peel_entry<T, true>(a, it.x, it.y, kp, 0u, my_recovered, my_last_round,
-                                            push, pcell, ppos);
+                        peel_entry<T, true>(a, it.x, it.y, kp, 0u, my_recovered,
+                                            my_last_round, push, pcell, ppos);
                         done = true;
                     }
                 }
@@ -1357,9 +1487,6 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     uint32_t* mark = g.f32 ? reinterpret_cast<uint32_t*>(base + L.mark) : nullptr;
     const T* y_agg = static_cast<const T*>(y_agg_v);
     const bool planned = plan != nullptr;
-    // few plan entries per row (a sketch much wider than the support): one
-    // wave per row
-    const bool wave_rows = planned && 3ull * ((g.n + g.c - 1) / g.c) <= kWaveRowsEntries * g.rows;
 
     DeviceInfo di;
     hipError_t e = device_info(&di);
@@ -1423,7 +1550,26 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
         ca.cmask = g.cmask;
         ca.cells = g.cells;
         ca.last_mask = last_mask;
-        if (wave_rows) {
+        // Rows to spare (two or more per SIMD): one wave per row, its loads in
+        // flight together.  Fewer, longer rows (NCF: 1.9 K rows of 1.7 K plan
+        // entries) keep more waves busy as a workgroup per row, or, when a
+        // row has only a few entries, a wave per row walking them in turn.
+        if ((uint64_t)g.rows >= 8ull * (uint64_t)di.cus) {
+            int per_cu = 0;
+            const void* kfn = g.c == 1024 ? reinterpret_cast<const void*>(&counter_rows_kernel<1024>)
+                            : g.c == 512 ? reinterpret_cast<const void*>(&counter_rows_kernel<512>)
+                                         : reinterpret_cast<const void*>(&counter_rows_kernel<256>);
+            if ((e = occupancy_per_cu(kfn, kBlock, &per_cu)) != hipSuccess) return e;
+            const uint64_t want = ((uint64_t)g.rows + kBlock / 64 - 1) / (kBlock / 64);
+            const uint64_t cap = (uint64_t)di.cus * per_cu;
+            const uint32_t cgrid = (uint32_t)(want < cap ? want : cap);
+            if (g.c == 1024)
+                hipLaunchKernelGGL(counter_rows_kernel<1024>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+            else if (g.c == 512)
+                hipLaunchKernelGGL(counter_rows_kernel<512>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+            else
+                hipLaunchKernelGGL(counter_rows_kernel<256>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+        } else if (3ull * ((g.n + g.c - 1) / g.c) <= kWaveRowsEntries * g.rows) {
             const uint64_t want = ((uint64_t)g.rows + 3) / 4;  // four waves per workgroup
             const uint32_t cgrid = want < (uint64_t)di.cus * 8 ? (uint32_t)want : (uint32_t)di.cus * 8;
             if (g.c == 1024)

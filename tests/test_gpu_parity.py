@@ -436,3 +436,30 @@ def test_unpackable_counters_fall_back():
     assert np.array_equal(g["mask"], o["mask"])
     assert_same_info(g["info"], o["info"])
     assert g["info"].n_recovered == 0
+
+
+@pytest.mark.parametrize("n", [4096 * 32, 4098 * 32, 4094 * 32 + 5, 4097 * 32 + 1])
+@pytest.mark.parametrize("offset", [0, 1, 2])
+def test_aggregate_every_vector_width(n, offset):
+    # bitmap word counts that are multiples of 4, of 2 only, and odd, on
+    # buffers offset by 0, 1 or 2 words (16-, 8- and 4-byte aligned): the
+    # aggregate takes vectors of 4, 2 or 1 words accordingly, always exact
+    import torch
+    hc = _hc()
+    dev = torch.device("cuda")
+    p = hc.make_params(n, 3, 17, c=1)  # 3 cells: the sketch is odd-sized too
+    W = 3
+    rng = np.random.default_rng(n + offset)
+    Yh = rng.integers(-2**31, 2**31, (W, p.cells), dtype=np.int64).astype(np.int32)
+    Bh = rng.integers(0, 2**32, (W, p.words), dtype=np.uint64).astype(np.uint32)
+    Yb = torch.zeros(W * p.cells + offset, dtype=torch.int32, device=dev)
+    Bb = torch.zeros(W * p.words + offset, dtype=torch.int32, device=dev)
+    Yb[offset:] = torch.from_numpy(Yh.reshape(-1)).to(dev)
+    Bb[offset:] = torch.from_numpy(Bh.reshape(-1).view(np.int32)).to(dev)
+    Yo = torch.empty(p.cells + offset, dtype=torch.int32, device=dev)
+    Bo = torch.empty(p.words + offset, dtype=torch.int32, device=dev)
+    hc.hc_aggregate(p, Yb[offset:], Bb[offset:], W, Yo[offset:], Bo[offset:])
+    torch.cuda.synchronize()
+    assert np.array_equal(Yo[offset:].cpu().numpy(), wrap_sum(list(Yh)))
+    assert np.array_equal(Bo[offset:].cpu().numpy().view(np.uint32),
+                          np.bitwise_or.reduce(Bh, axis=0))
