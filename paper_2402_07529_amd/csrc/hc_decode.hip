@@ -131,8 +131,12 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(const T* __restrict__ y_ag
             reinterpret_cast<uint32_t*>(sync)[k] = 0u;
     }
     const uint64_t step = (uint64_t)gridDim.x * kBlock;
+    // int32 with a plan: the round-0 scan takes the residual from the
+    // aggregate itself (into the counters' high words, or into yw when they
+    // do not pack)
+    const bool copy = !(std::is_same<T, int32_t>::value && planned);
     for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < cells; i += step) {
-        yw[i] = (typename Acc<T>::type)y_agg[i];
+        if (copy) yw[i] = (typename Acc<T>::type)y_agg[i];
         if (!planned) cnt[i] = 0ull;
         if (mark != nullptr) mark[i] = 0u;
     }
@@ -279,7 +283,7 @@ struct SupportArgs {
     uint32_t* blk;               // set bits before each chunk
     uint32_t* woffb;             // with a plan: set bits before each batch (nb + 1 entries)
     uint32_t* elem;
-    uint32_t* peeled;
+    uint8_t* peeled;             // a byte per element
     unsigned long long* cnt;     // without a plan: counters built by atomics
     Ctrl* ctrl;
     uint64_t words, nchunks, cap, seed;
@@ -807,9 +811,10 @@ struct PeelArgs {  // T: the decode-side arithmetic type
     PeelSync* sync;
     const uint32_t* elem;
     T* vals;
-    uint32_t* peeled;
+    uint8_t* peeled;  // a byte per element, set and tested through its 32-bit word
     unsigned long long* cnt;
     T* yw;
+    const int32_t* y_agg;  // int32: the aggregated sketch (the residual before round 0)
     uint2* queue;
     uint32_t* mark;  // fp32 peel: per cell, its frontier round + 1 (0: never queued)
     InfoDev* info;
@@ -818,6 +823,22 @@ struct PeelArgs {  // T: the decode-side arithmetic type
     bool counted;   // a counter kernel built the counters (and checked their packing)
     bool split0;    // round 0 ran before the peel kernel, as whole-chip launches
 };
+
+// Round-0 scan of an int32 sketch with a plan: the residual starts as the
+// aggregate, in the counter's high word when packed (v: the counter as the
+// counter kernel built it), else in yw.
+template <typename T>
+__device__ __forceinline__ void scan_residual(const PeelArgs<T>& a, uint64_t cidx,
+                                              unsigned long long v, bool packed, uint32_t kp) {
+    if constexpr (std::is_same<T, int32_t>::value) {
+        if (!a.counted || cidx >= a.cells) return;
+        const uint32_t y = (uint32_t)a.y_agg[cidx];
+        if (packed)
+            a.cnt[cidx] = ((unsigned long long)y << 32) | (((v >> 32) << kp) + (v & 0xffffffffull));
+        else
+            a.yw[cidx] = (int32_t)y;
+    }
+}
 
 // One frontier entry (cell cidx, element position pos), for the kernel below.
 // PACKED: int32 residuals ride in the counter words (kp position bits).
@@ -842,14 +863,17 @@ __device__ __forceinline__ void peel_entry(const PeelArgs<T>& a, uint32_t cidx, 
                                            uint32_t& last_round, bool (&push)[2],
                                            uint32_t (&pcell)[2], uint32_t (&ppos)[2]) {
     constexpr bool kMarks = std::is_same<T, double>::value;
+    // the element's flag byte within its 32-bit word (the flags are 256-byte
+    // aligned): a byte rather than a word per element keeps the flags a
+    // quarter of the size in the caches; claims of four neighbouring
+    // elements share a word but rarely meet in time
+    unsigned int* const fword = reinterpret_cast<unsigned int*>(a.peeled + (pos & ~3u));
+    const uint32_t fbit = 1u << (8u * (pos & 3u));
     bool taken;
-    if (kMarks) {
-        taken = __hip_atomic_load(a.peeled + pos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
-    } else {
-        // one word per element: claims of neighbouring elements would
-        // otherwise queue up on a shared word
-        taken = atomicExch(a.peeled + pos, 1u) != 0u;
-    }
+    if (kMarks)
+        taken = (__hip_atomic_load(fword, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & fbit) != 0u;
+    else
+        taken = (atomicOr(fword, fbit) & fbit) != 0u;
     const uint32_t p = a.elem[pos];
     unsigned long long wcell = 0;
     T ycell = T(0);
@@ -867,7 +891,7 @@ __device__ __forceinline__ void peel_entry(const PeelArgs<T>& a, uint32_t cidx, 
             if (__hip_atomic_load(a.mark + cl[jj], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
                 r + 1u)
                 return;
-        __hip_atomic_store(a.peeled + pos, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        atomicOr(fword, fbit);  // neighbours' flags share the word
     }
     if (PACKED) ycell = (T)(int32_t)(uint32_t)(wcell >> 32);
     const T val = Val<T>::sign(ycell, (h.neg >> j) & 1u);
@@ -1021,11 +1045,7 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
 #pragma unroll
                 for (uint32_t m = 0; m < kScanCells; m++) {
                     const uint64_t cidx = base + m * nthreads + gtid;
-                    if constexpr (std::is_same<T, int32_t>::value) {
-                        if (packed && cidx < a.cells)
-                            a.cnt[cidx] = ((unsigned long long)(uint32_t)a.yw[cidx] << 32) |
-                                          (((v[m] >> 32) << kp) + (v[m] & 0xffffffffull));
-                    }
+                    scan_residual(a, cidx, v[m], packed, kp);
                     lds_push(q, (v[m] >> 32) == 1ull, (uint32_t)cidx, (uint32_t)v[m]);
                 }
                 flush_pushes(q, false, kScanCells * kPeelBlock, &sync->tail.v[0], a.queue,
@@ -1157,11 +1177,7 @@ __global__ __launch_bounds__(kBlock) void scan0_kernel(PeelArgs<T> a) {
 #pragma unroll
         for (uint32_t m = 0; m < kScanCells; m++) {
             const uint64_t cidx = base + m * nthreads + gtid;
-            if constexpr (std::is_same<T, int32_t>::value) {
-                if (packed && cidx < a.cells)
-                    a.cnt[cidx] = ((unsigned long long)(uint32_t)a.yw[cidx] << 32) |
-                                  (((v[m] >> 32) << kp) + (v[m] & 0xffffffffull));
-            }
+            scan_residual(a, cidx, v[m], packed, kp);
             lds_push(q, (v[m] >> 32) == 1ull, (uint32_t)cidx, (uint32_t)v[m]);
         }
         flush_pushes(q, false, kScanCells * kBlock, &a.sync->tail.v[0], a.queue, a.cells,
@@ -1273,7 +1289,7 @@ struct EmitArgs {  // T: the gradient type; values are kept in Acc<T>
     const uint32_t* blk;
     const uint32_t* elem;
     const typename Acc<T>::type* vals;
-    const uint32_t* peeled;
+    const uint8_t* peeled;
     const T* y_agg;
     const Ctrl* ctrl;
     T* x_out;
@@ -1480,7 +1496,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     uint32_t* woffb = plan ? reinterpret_cast<uint32_t*>(base + L.woffb) : nullptr;
     uint32_t* elem = reinterpret_cast<uint32_t*>(base + L.elem);
     A* vals = reinterpret_cast<A*>(base + L.vals);
-    uint32_t* peeled = reinterpret_cast<uint32_t*>(base + L.peeled);
+    uint8_t* peeled = reinterpret_cast<uint8_t*>(base + L.peeled);
     unsigned long long* cnt = reinterpret_cast<unsigned long long*>(base + L.cnt);
     A* yw = reinterpret_cast<A*>(base + L.yw);
     uint2* queue = reinterpret_cast<uint2*>(base + L.queue);
@@ -1618,6 +1634,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     pa.peeled = peeled;
     pa.cnt = cnt;
     pa.yw = yw;
+    pa.y_agg = g.f32 ? nullptr : static_cast<const int32_t*>(y_agg_v);
     pa.queue = queue;
     pa.mark = mark;
     pa.info = static_cast<InfoDev*>(out.info);
@@ -1701,7 +1718,7 @@ DecodeLayout decode_layout(const Geo& g, uint64_t max_support) {
     L.woffb = o;   o = align256(o + (g.c >= 256 ? ((g.n + g.c - 1) / g.c + 1) * 4 : 0));
     L.elem = o;    o = align256(o + cap * 4);
     L.vals = o;    o = align256(o + cap * vsz);
-    L.peeled = o;  o = align256(o + cap * 4);
+    L.peeled = o;  o = align256(o + cap);  // a byte per element
     L.cnt = o;     o = align256(o + (size_t)g.cells * 8);
     L.yw = o;      o = align256(o + (size_t)g.cells * vsz);
     L.queue = o;   o = align256(o + (size_t)g.cells * 8);
