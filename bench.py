@@ -57,7 +57,7 @@ def parse():
                          "for this device, hc_geometry_blocked with block_rows = 0)")
     ap.add_argument("--encode", default="auto", choices=["auto", "atomic", "gather", "staged"],
                     help="auto: staged for a global sketch with c >= 256 when a worker has at "
-                         "least one nonzero per two batches of c parameters (else the atomic "
+                         "least two nonzeros per batch of c parameters (else the atomic "
                          "encode, whose cost follows the nonzeros while the staged encode's "
                          "second pass visits every batch); atomic: hc_encode (each nonzero adds "
                          "into its cells); gather: "
@@ -117,13 +117,14 @@ def algorithmic_bytes(n, W, cells, n_sup, index_bytes, blocked=False):
     return enc, agg, dec
 
 
-def measured_traffic(workload, vtype):
-    """HBM bytes per encode launch from the committed rocprofv3 counter summary
-    (FETCH_SIZE and WRITE_SIZE runs scaled by a plain copy of known size),
-    or None if there is none for this workload or the encode kernel's sources
-    changed since the counters were taken."""
+def measured_traffic(tag, mode, vtype):
+    """HBM bytes per encode call (all of its kernels) from the committed
+    rocprofv3 counter summary profiles/hbm_counters_<line>_<mode>.md
+    (FETCH_SIZE and WRITE_SIZE runs scaled by a plain copy of known size), or
+    None if there is none for this line or the encode's sources changed since
+    the counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"encode_{workload}_hbm_counters.md")
+    path = os.path.join(ROOT, "profiles", f"hbm_counters_{tag}_{mode}.md")
     if vtype != "i32" or not os.path.exists(path):
         return None
     fields = {}
@@ -131,12 +132,28 @@ def measured_traffic(workload, vtype):
         if ":" in line and line.split(":")[0] in ("traffic_bytes_per_launch", "kernel_source_sha256"):
             k, v = line.split(":", 1)
             fields[k] = v.strip()
-    csrc = os.path.join(ROOT, "paper_2402_07529_amd", "csrc")
-    src = open(os.path.join(csrc, "hc_encode.hip"), "rb").read() + \
-        open(os.path.join(csrc, "hc_device.h"), "rb").read()
-    if fields.get("kernel_source_sha256") != hashlib.sha256(src).hexdigest():
+    if fields.get("kernel_source_sha256") != encode_source_sha256(mode):
         return None
     return int(fields["traffic_bytes_per_launch"])
+
+
+def line_tag(a, w):
+    """The workload's name, plus the density, overlap and worker count when
+    they were given on the command line (names the counter summaries)."""
+    tag = w.name
+    for flag, v in (("d", a.density), ("o", a.overlap), ("w", a.workers)):
+        if v is not None:
+            tag += f"_{flag}{v}"
+    return tag
+
+
+def encode_source_sha256(mode):
+    """sha256 of the sources an encode mode's kernels are built from."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2402_07529_amd", "csrc")
+    files = ["hc_blocked.hip"] if mode == "blocked" else ["hc_encode.hip"]
+    src = b"".join(open(os.path.join(csrc, f), "rb").read() for f in files + ["hc_device.h"])
+    return hashlib.sha256(src).hexdigest()
 
 
 def host_cpu():
@@ -193,11 +210,14 @@ def cpu_baseline(w, rows, c, block, seed):
 
 def auto_encode(w, c, blocked):
     """The encode 'auto' picks: staged for a global sketch with c >= 256 when a
-    worker has at least one nonzero per two batches of c parameters (its
-    second pass visits every batch), else the atomic encode."""
+    worker has at least two nonzeros per batch of c parameters (its second
+    pass visits every batch), else the atomic encode.  Measured on MI355X at
+    c = 1024 (per worker, BERT-base / VGG19 shapes): 2 per batch 0.098 / 0.126
+    ms atomic against 0.095 / 0.125 staged; 4 per batch 0.114 / 0.146 against
+    0.098 / 0.127; 1 per batch (BERT-base, Bloom index) 0.124 against 0.156."""
     nnz_w = float(np.mean([w.nnz(i) for i in range(w.W)]))
     batches = (w.n + c - 1) // c
-    return "staged" if not blocked and c >= 256 and nnz_w >= 0.5 * batches else "atomic"
+    return "staged" if not blocked and c >= 256 and nnz_w >= 2 * batches else "atomic"
 
 
 def core_fraction(lam):
@@ -508,8 +528,9 @@ def main():
                                 if staged else "hc_encode (Y clear + dense encode)"),
                      "achieved": round(enc_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(enc_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": (None if a.blocked or a.index == "bloom" or gather or staged
-                                 else measured_traffic(w.name, w.vtype)),
+                     "traffic": (None if a.index == "bloom" else
+                                 measured_traffic(line_tag(a, w), "blocked" if a.blocked
+                                                  else encode, w.vtype)),
                      "bytes_per_launch": enc_b, "avg_launch_ms": round(enc_ms, 4)},
         "ms_per_step_median": round(float(np.median(m["step_ms"])), 4),
         "hbm_frac_iteration": round(iter_b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
