@@ -354,6 +354,7 @@ struct DecArgs {
     hc_decode_info* info;
     uint64_t n, words, seed;
     uint32_t block, brows, bcells, c, cmask, log2c, last_mask, x_vec;
+    uint32_t claim_words;  // int32: words of per-parameter claim bits in LDS (0: none)
 };
 
 __global__ void zero_bctrl_kernel(BCtrl* c) {
@@ -426,8 +427,9 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
     uint16_t* s_q = reinterpret_cast<uint16_t*>(s_cnt + bcells);  // frontier queue of cells
     uint32_t* s_tab = reinterpret_cast<uint32_t*>(s_q + ((bcells + 1) & ~1u));
     uint32_t* s_tmp = s_tab + 3 * a.block;  // kScratchWords: reductions, wave totals, flags
-    uint32_t* s_any = s_tmp + 48;           // a claim was made, by round parity
-    uint32_t* s_tail = s_tmp + 50;          // queue length
+    uint32_t* s_any = s_tmp + 48;           // a claim was made, by round (parity, or mod 3)
+    uint32_t* s_tail = s_tmp + 51;          // queue length
+    uint32_t* s_claim = s_tmp + kScratchWords;  // int32 with claim bits: one per block parameter
 
     const uint32_t q = blockIdx.x;
     const uint32_t tid = threadIdx.x;
@@ -456,6 +458,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
         }
     }
     fill_table(s_tab, r, a.seed, a.brows, a.c, cmask, a.log2c, a.block);
+    for (uint32_t i = tid; i < a.claim_words; i += kDecThreads) s_claim[i] = 0u;
     if (tid < 4) s_tmp[48 + tid] = 0u;
     lds_barrier();
 
@@ -523,7 +526,51 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
     // applies them and appends the cells that became pure.
     uint32_t qs = 0, qe = *s_tail;
     uint32_t rounds = 0, recovered = 0;
-    while (qs < qe) {
+    // int32 with claim bits: one barrier per round.  Every pure cell of an
+    // element holds its value exactly, so whichever frontier entry of the
+    // element sets its claim bit first recovers it; the others stand aside,
+    // and the elements recovered in a round are still exactly those with a
+    // cell in its frontier.  An entry's cell can only lose its member during
+    // the round (when another pure cell of the member wins), so an entry that
+    // reads it as pure and then loses the claim is the only race, and it is
+    // harmless.  The flag of a round lives in slot round mod 3, cleared one
+    // round ahead.
+    bool single = false;
+    if constexpr (std::is_same<T, int32_t>::value) single = a.claim_words != 0u;
+    while (single && qs < qe) {
+        if (tid == 0) s_any[(rounds + 1u) % 3u] = 0u;
+        bool mine = false;
+        for (uint32_t idx = qs + tid; idx < qe; idx += kDecThreads) {
+            const uint32_t cell = s_q[idx];
+            const uint32_t cc = s_cnt[cell];
+            if ((cc >> kDegShift) != 1u) continue;  // its member left with another cell
+            const uint32_t bl = cc & kSumMask;
+            const Member m = member_of(s_tab, bl, cell, cmask);
+            const uint32_t id = bl * a.c + m.t;  // the member's parameter within the block
+            const uint32_t bit = 1u << (id & 31u);
+            if (atomicOr(s_claim + (id >> 5), bit) & bit) continue;
+            mine = true;
+            recovered++;
+            const uint32_t ej = m.j == 0 ? m.e[0] : (m.j == 1 ? m.e[1] : m.e[2]);
+            const A xv = Val<A>::sign(s_val[cell], tab_neg(ej));  // x = g_j * Y
+#pragma unroll
+            for (uint32_t jj = 0; jj < 3; jj++) {
+                if (jj == m.j) continue;
+                const uint32_t c2 = tab_cell(m.e[jj], m.t, cmask);
+                const uint32_t old = atomicSub(s_cnt + c2, kDegOne + bl);
+                if ((old >> kDegShift) == 2u) s_q[atomicAdd(s_tail, 1u)] = (uint16_t)c2;
+                LdsAdd<A>::add(s_val + c2, Val<A>::sign(xv, !tab_neg(m.e[jj])));  // -= g * x
+            }
+            s_cnt[cell] = kClaimed | bl;  // keeps g_j * x in s_val[cell]
+        }
+        if (__ballot(mine) != 0ull && lane == 0) s_any[rounds % 3u] = 1u;
+        lds_barrier();
+        if (s_any[rounds % 3u] == 0u) break;
+        rounds++;
+        qs = qe;
+        qe = *s_tail;
+    }
+    while (!single && qs < qe) {
         uint32_t claims = 0;  // bit k: entry qs + tid + 1024 k recovers its member
         for (uint32_t k = 0, idx = qs + tid; idx < qe; k++, idx += kDecThreads) {
             const uint32_t cell = s_q[idx];
@@ -794,8 +841,16 @@ hipError_t launch_decode_blocked_t(const Geo& g, const void* y_agg, const uint32
     a.log2c = g.log2c;
     a.last_mask = (g.n & 31u) ? ((1u << (g.n & 31u)) - 1u) : 0xffffffffu;
     a.x_vec = (reinterpret_cast<uintptr_t>(out.x_out) & 15u) == 0;
-    hipLaunchKernelGGL(decode_blocked_kernel<T>, dim3(g.nblocks), dim3(kDecThreads),
-                       blocked_decode_lds(g), s, a);
+    // int32: claim bits for the block's parameters when they fit beside the
+    // block's sketch (one barrier per peeling round instead of two)
+    size_t lds = blocked_decode_lds(g);
+    const uint32_t claim_words = (uint32_t)(((size_t)g.block * g.c + 31) / 32);
+    a.claim_words = 0;
+    if (!g.f32 && lds + (size_t)claim_words * 4 + kLdsReserve <= kLdsBytes) {
+        a.claim_words = claim_words;
+        lds += (size_t)claim_words * 4;
+    }
+    hipLaunchKernelGGL(decode_blocked_kernel<T>, dim3(g.nblocks), dim3(kDecThreads), lds, s, a);
     return hipGetLastError();
 }
 
