@@ -25,7 +25,7 @@
 //            rounds (section 3.2, parallel peeling).  The frontier of round r is the
 //            list of (cell, element) pairs whose cell became pure during round
 //            r-1, kept in one append-only queue.  An element owning several
-//            frontier cells is claimed by an atomic exchange on its flag: the
+//            frontier cells is claimed by an atomic OR on its flag byte: the
 //            first of its frontier entries to get there recovers
 //            x = g_j * Y from its cell (every pure cell of the element holds the
 //            same value, exactly so in integer arithmetic), and subtracts g * x
