@@ -1316,13 +1316,14 @@ __device__ __forceinline__ T estimate_raw(const EmitArgs<T>& a, uint32_t p) {
 
 // One workgroup per chunk of 1024 bitmap words (32768 parameters).  The
 // chunk's members are one contiguous run of E, so their values and recovered
-// flags are first copied into LDS with coalesced loads (when the run fits):
-// the output loop then has no global loads ahead of its stores.  A stage of
-// 2048 members measured best on MI355X: a 4096 one costs NCF's write stream
-// more occupancy than it saves on the denser workloads.  The dense output
-// goes out with nontemporal stores (measured 1-2 % faster here, though plain
-// stores win for a pure write stream).
-constexpr uint32_t kEmitStage = 2048;  // members staged per chunk (1/16 of its parameters)
+// flags are copied into LDS with coalesced loads, a window of 2048 at a time
+// (chunks denser than 1/16 take several): the output loop then has no global
+// loads ahead of its stores.  A stage of 2048 members measured best on MI355X:
+// a 4096 one costs NCF's write stream more occupancy than it saves on the
+// denser workloads.  The dense output goes out with nontemporal stores
+// (measured 1-2 % faster here, though plain stores win for a pure write
+// stream).
+constexpr uint32_t kEmitStage = 2048;  // members per LDS window (1/16 of a chunk's parameters)
 
 template <typename T>
 __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
@@ -1357,16 +1358,27 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
     // another geometry) every member gets the estimate from the aggregate
     const bool raw = a.ctrl->overflow != 0 || a.ctrl->bad_plan != 0;
     const uint64_t chunk_p = chunk * kChunkBits;
-    const bool staged = !raw && total <= kEmitStage;
-    if (staged) {
-        for (uint32_t i = threadIdx.x; i < total; i += kBlock) {
-            s_val[i] = (T)a.vals[off + i];
-            s_rec[i] = a.peeled[off + i] != 0u ? 1 : 0;
-        }
-        lds_barrier();
-    }
-
+    // the members' values and flags go through LDS in windows of kEmitStage
+    // consecutive ranks, [wlo, whi) of the chunk's; an iteration (1024
+    // parameters) holds at most 1024 members, so a window that starts at its
+    // first member covers it.  wlo, whi and the reload test are uniform.
+    uint32_t wlo = 0, whi = 0;
+    constexpr uint32_t kIterWords = 4 * kBlock / 32;  // bitmap words per iteration
     for (uint32_t it = 0; it < kChunkBits / (4 * kBlock); it++) {
+        if (!raw) {
+            const uint32_t wf = it * kIterWords, wl = wf + kIterWords - 1;
+            const uint32_t r1 = s_pref[wl] + __popc(s_words[wl]);  // past the iteration's last
+            if (r1 > whi) {
+                wlo = s_pref[wf];
+                whi = wlo + kEmitStage < total ? wlo + kEmitStage : total;
+                lds_barrier();  // every lane is done with the previous window
+                for (uint32_t i = wlo + threadIdx.x; i < whi; i += kBlock) {
+                    s_val[i - wlo] = (T)a.vals[off + i];
+                    s_rec[i - wlo] = a.peeled[off + i] != 0u ? 1 : 0;
+                }
+                lds_barrier();
+            }
+        }
         const uint32_t e0 = it * (4 * kBlock) + 4u * threadIdx.x;  // offset in the chunk
         const uint64_t p0 = chunk_p + e0;
         const uint32_t wi = e0 >> 5, sh = e0 & 31u;
@@ -1380,12 +1392,9 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
             rec[k] = false;
             if ((word >> (sh + k)) & 1u) {
                 const uint32_t p = (uint32_t)(p0 + k);
-                if (staged) {
-                    out[k] = s_val[rank - off];
-                    rec[k] = s_rec[rank - off] != 0;
-                } else if (!raw) {
-                    out[k] = (T)a.vals[rank];
-                    rec[k] = a.peeled[rank] != 0u;
+                if (!raw) {
+                    out[k] = s_val[rank - off - wlo];
+                    rec[k] = s_rec[rank - off - wlo] != 0;
                 } else {
                     out[k] = estimate_raw(a, p);
                 }
