@@ -263,10 +263,14 @@ __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
     const uint64_t ntiles = (n + kTile - 1) / kTile;
     const uint64_t npairs = vec ? n / (2 * kTile) : 0;
 
+    // a buffer resource over the pair's 8 KiB, built on the scalar unit: the
+    // lanes' offsets never change, so no per-pair vector address arithmetic
+    // competes for the registers that the loads in flight hold
     auto load_pair = [&](uint64_t q, V (&v)[8]) {
-        const V* src = reinterpret_cast<const V*>(x + q * (2 * kTile)) + lane;
+        const __amdgpu_buffer_rsrc_t rs =
+            buffer_rsrc(x + q * (2 * kTile), (uint32_t)(2 * kTile * sizeof(T)));
 #pragma unroll
-        for (int u = 0; u < 8; u++) v[u] = __builtin_nontemporal_load(src + u * 64);
+        for (int u = 0; u < 8; u++) v[u] = buffer_load16_nt<V>(rs, 16u * lane, 1024u * u);
     };
     auto encode_pair = [&](uint64_t q, const V (&v)[8]) {
 #pragma unroll
