@@ -114,6 +114,35 @@ def test_blocked_one_block_overloaded():
     assert np.array_equal(r["x"][outside], direct[outside])
 
 
+@pytest.mark.parametrize("overload", [False, True])
+def test_blocked_int32_blocks_too_wide_for_claim_bits(overload):
+    # 1024 batches of 1024 per block: a claim bit per block parameter (128 KiB)
+    # does not fit beside the block's sketch in LDS, so the int32 decode peels
+    # with its two-barrier rounds (decision pass, then the claims); the other
+    # blocked tests run the one-barrier rounds.  With `overload` block 2 holds
+    # more members than its cells can peel.
+    _hc()
+    c, block, brows, nbk = 1024, 1024, 3, 4
+    n = nbk * block * c - 777   # a ragged last block
+    rng = np.random.default_rng(31 + overload)
+    idx, val = [], []
+    for wk in range(3):
+        parts = []
+        for q in range(nbk):
+            lo, hi = q * block * c, min(n, (q + 1) * block * c)
+            m = 2600 if (overload and q == 2) else 700
+            parts.append(rng.choice(hi - lo, m, replace=False) + lo)
+        ii = np.unique(np.concatenate(parts)).astype(np.uint32)
+        idx.append(ii)
+        val.append((rng.integers(1, 2**20, ii.size) * rng.choice([-1, 1], ii.size)).astype(np.int32))
+    w = wl.Workload("wide-blocks", n, 3, "i32", idx, val, 1, 123)
+    g = oracle.Geom(n=n, rows=nbk * brows, seed=123, c=c, block=block)
+    r, o = check_blocked_int(w, g)
+    assert r["info"].success == (not overload)
+    if not overload:
+        assert np.array_equal(r["x"], wrap_sum([w.dense(i) for i in range(w.W)]))
+
+
 @pytest.mark.parametrize("n", [1, 31, 32, 33, 1000, 4097])
 def test_blocked_tiny_lengths(n):
     _hc()
