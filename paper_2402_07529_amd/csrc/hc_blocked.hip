@@ -48,6 +48,7 @@ constexpr uint32_t kSumMask = kDegOne - 1u;
 constexpr uint32_t kClaimed = 0x80000000u;
 constexpr uint32_t kScratchWords = 64;
 constexpr int kAhead = 8;  // global loads a lane keeps in flight in the decode's streaming loops
+constexpr uint32_t kDenseGroup = 512;  // members of 64 words from which lanes walk their own words
 
 // Control block of the blocked decode (zeroed before the decode kernel).
 struct BCtrl {
@@ -661,11 +662,14 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
             if (a.mask != nullptr && base + lane < w1) a.mask[base + lane] = word;
             // rank of the first member of each word within the group
             const uint32_t cw = __popc(word);
-            uint32_t excl = 0;
+            uint32_t excl = 0, total = 0;
 #pragma unroll
-            for (int b = 0; b < 6; b++) excl += lanes_below(__ballot((cw >> b) & 1u)) << b;
-            const uint32_t total = for_each_set_bit(word, [&](uint32_t s, bool valid,
-                                                              uint32_t owner, uint32_t bit) {
+            for (int b = 0; b < 6; b++) {
+                const uint64_t mb = __ballot((cw >> b) & 1u);
+                excl += lanes_below(mb) << b;
+                total += (uint32_t)__popcll(mb) << b;
+            }
+            auto member = [&](uint32_t s, bool valid, uint32_t owner, uint32_t bit) {
                 const uint64_t p = (base + owner) * 32ull + bit;
                 A val = A(0);
                 bool found = true;
@@ -701,7 +705,21 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
                     __threadfence_block();  // the plain mask stores above land first
                     if (!found) atomicAnd(a.mask + (p >> 5), ~(1u << (p & 31u)));
                 }
-            });
+            };
+            if (total >= kDenseGroup) {
+                // a dense group: each lane walks its own word's members (no
+                // search across lanes for every member; measured on a 73 %
+                // dense BERT-base aggregate)
+                uint32_t bits = word, rk = 0;
+                while (bits != 0u) {
+                    const uint32_t bit = (uint32_t)__builtin_ctz(bits);
+                    bits &= bits - 1u;
+                    member(excl + rk, true, lane, bit);
+                    rk++;
+                }
+            } else {
+                for_each_set_bit(word, member);
+            }
             rank += total;
             if (a.x_out != nullptr) {
 #pragma unroll
