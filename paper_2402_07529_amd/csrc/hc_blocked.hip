@@ -910,6 +910,16 @@ BlockedLayout blocked_layout(const Geo& g) {
 
 hipError_t launch_encode_blocked(const Geo& g, const void* x, void* y, uint32_t* b,
                                  hipStream_t s) {
+    // Fewer blocks than CUs (large blocks of a sparse gradient): a workgroup
+    // per block would leave CUs idle for the whole stream, so the whole chip
+    // streams the gradient instead and adds its nonzeros into the zero-filled
+    // sketch with global atomics, each batch hashed to its block's rows (the
+    // same cells).  Sparse BERT-base (105 blocks of 1024 batches): 0.115 ms
+    // per encode with a workgroup per block.
+    DeviceInfo di;
+    const hipError_t e = device_info(&di);
+    if (e != hipSuccess) return e;
+    if (g.nblocks < (uint32_t)di.cus) return launch_encode_dense(g, x, y, b, s);
     if (g.f32) return launch_encode_blocked_t<float>(g, x, y, b, s);
     return launch_encode_blocked_t<int32_t>(g, x, y, b, s);
 }

@@ -69,14 +69,17 @@ __global__ __launch_bounds__(kBlock) void fill_u32_kernel(uint32_t* __restrict__
 }
 
 // Sketch updates for the parameters of one load: e[k] is parameter p0 + k of
-// this lane, p0 = lbase + 4 * lane, lbase the load's first parameter.
+// this lane, p0 = lbase + 4 * lane, lbase the load's first parameter.  rows:
+// the sketch's rows, or a blocked sketch's rows per block (block: its batches
+// per block, 0 for the global sketch).
 template <typename T, int MODE>
 __device__ __forceinline__ void scatter_load(const T (&e)[4], const bool (&nz)[4], uint64_t lbase,
                                              uint64_t p0, T* __restrict__ y, uint64_t seed,
-                                             uint32_t rows, uint32_t c, uint32_t cmask,
-                                             uint32_t log2c) {
+                                             uint32_t rows, uint32_t block, uint32_t c,
+                                             uint32_t cmask, uint32_t log2c) {
     if (MODE == 0) {
-        const BatchHash h = batch_hash(seed, rows, cmask, uniform64(lbase >> log2c));
+        const BatchHash h =
+            batch_hash_blocked(seed, rows, cmask, log2c, uniform64(lbase >> log2c), block);
         if (nz[0] | nz[1] | nz[2] | nz[3]) {
 #pragma unroll
             for (int k = 0; k < 4; k++) {
@@ -90,7 +93,7 @@ __device__ __forceinline__ void scatter_load(const T (&e)[4], const bool (&nz)[4
         }
     } else if (MODE == 1) {
         if (nz[0] | nz[1] | nz[2] | nz[3]) {
-            const BatchHash h = batch_hash(seed, rows, cmask, p0 >> log2c);
+            const BatchHash h = batch_hash_blocked(seed, rows, cmask, log2c, p0 >> log2c, block);
 #pragma unroll
             for (int k = 0; k < 4; k++) {
                 if (!nz[k]) continue;
@@ -106,7 +109,7 @@ __device__ __forceinline__ void scatter_load(const T (&e)[4], const bool (&nz)[4
         for (int k = 0; k < 4; k++) {
             if (!nz[k]) continue;
             const uint64_t p = p0 + k;
-            const BatchHash h = batch_hash(seed, rows, cmask, p >> log2c);
+            const BatchHash h = batch_hash_blocked(seed, rows, cmask, log2c, p >> log2c, block);
             const uint32_t t = (uint32_t)p & cmask;
 #pragma unroll
             for (int j = 0; j < 3; j++)
@@ -192,9 +195,9 @@ template <typename T, int MODE, bool BL, bool STAGED>
 __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, uint32_t lane,
                                             T* __restrict__ y, uint32_t* __restrict__ b,
                                             uint64_t words, uint64_t seed, uint32_t rows,
-                                            uint32_t c, uint32_t cmask, uint32_t log2c,
-                                            uint32_t bk, uint32_t brows, const StageOut& so,
-                                            uint2* stage) {
+                                            uint32_t block, uint32_t c, uint32_t cmask,
+                                            uint32_t log2c, uint32_t bk, uint32_t brows,
+                                            const StageOut& so, uint2* stage) {
     bool nz[4][4];
     uint64_t m[4][4], any = 0;
 #pragma unroll
@@ -237,8 +240,8 @@ __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, 
     for (int l = 0; l < 4; l++) {
         if ((m[l][0] | m[l][1] | m[l][2] | m[l][3]) == 0) continue;
         const uint64_t lbase = tbase + 256ull * l;
-        scatter_load<T, MODE>(e[l], nz[l], lbase, lbase + 4ull * lane, y, seed, rows, c, cmask,
-                              log2c);
+        scatter_load<T, MODE>(e[l], nz[l], lbase, lbase + 4ull * lane, y, seed, rows, block, c,
+                              cmask, log2c);
     }
 }
 
@@ -252,8 +255,8 @@ __device__ __forceinline__ void encode_tile(const T (&e)[4][4], uint64_t tbase, 
 template <typename T, int MODE, bool BL, bool STAGED>
 __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
     const T* __restrict__ x, T* __restrict__ y, uint32_t* __restrict__ b, uint64_t n,
-    uint64_t words, uint64_t seed, uint32_t rows, uint32_t c, uint32_t cmask, uint32_t log2c,
-    bool vec, uint32_t bk, uint32_t brows, StageOut so) {
+    uint64_t words, uint64_t seed, uint32_t rows, uint32_t block, uint32_t c, uint32_t cmask,
+    uint32_t log2c, bool vec, uint32_t bk, uint32_t brows, StageOut so) {
     typedef typename Vec4<T>::type V;
     __shared__ uint2 s_stage[STAGED ? kBlock : 1];  // staged: kStageCap entries per wave
     uint2* const stage = s_stage + (STAGED ? (threadIdx.x & ~63u) : 0u);
@@ -284,7 +287,7 @@ __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
                 e[l][3] = v[4 * h + l].w;
             }
             encode_tile<T, MODE, BL, STAGED>(e, (2 * q + h) * kTile, lane, y, b, words, seed, rows,
-                                             c, cmask, log2c, bk, brows, so, stage);
+                                             block, c, cmask, log2c, bk, brows, so, stage);
         }
     };
     // rolling pipeline: the next pair's loads are issued before the current
@@ -321,8 +324,8 @@ __global__ __launch_bounds__(kBlock) void encode_dense_kernel(
                 const uint64_t p = tbase + 256ull * l + 4ull * lane + k;
                 e[l][k] = p < n ? x[p] : T(0);
             }
-        encode_tile<T, MODE, BL, STAGED>(e, tbase, lane, y, b, words, seed, rows, c, cmask, log2c,
-                                         bk, brows, so, stage);
+        encode_tile<T, MODE, BL, STAGED>(e, tbase, lane, y, b, words, seed, rows, block, c, cmask,
+                                         log2c, bk, brows, so, stage);
     }
 }
 
@@ -373,7 +376,7 @@ hipError_t launch_dense_t(const Geo& g, const void* x, void* y, uint32_t* b, hip
     const uint32_t grid = grid_for(ntiles, 2 * (kBlock / 64), (uint32_t)(resident * mult));
     hipLaunchKernelGGL((encode_dense_kernel<T, MODE, BL, STAGED>), dim3(grid), dim3(kBlock), 0, s,
                        static_cast<const T*>(x), static_cast<T*>(y), b, g.n, g.words, g.seed,
-                       g.rows, g.c, g.cmask, g.log2c,
+                       g.brows, g.block, g.c, g.cmask, g.log2c,
                        (reinterpret_cast<uintptr_t>(x) & 15u) == 0, g.bloom_k, g.bloom_rows, so);
     return hipGetLastError();
 }
