@@ -214,9 +214,11 @@ hc_status hc_plan_build(const hc_params *p, void *plan, size_t plan_bytes, hipSt
  * x_p, section 3.1 with the batching of 3.4) and b with the index: the
  * nonzero bitmap b[ceil(n/32)] (section 3.2), or the Bloom filter of every
  * nonzero (section 3.3; b[ceil(bloom_rows * c / 32)]).  No pre-zeroing is
- * needed.  fp32 sums are
- * accumulated with atomics (global, or in LDS for a blocked sketch), so their
- * rounding order is not fixed. */
+ * needed.  A blocked sketch is built in LDS, one block per workgroup, unless
+ * it has fewer blocks than the GPU has CUs: then the whole GPU streams the
+ * gradient and adds with global atomics, as for an unblocked sketch.  fp32
+ * sums are accumulated with atomics (global, or in LDS), so their rounding
+ * order is not fixed. */
 hc_status hc_encode(const hc_params *p, const void *x, void *y, uint32_t *b,
                     hipStream_t stream);
 
