@@ -148,10 +148,11 @@ def line_tag(a, w):
 
 
 def encode_source_sha256(mode):
-    """sha256 of the sources an encode mode's kernels are built from."""
+    """sha256 of the sources an encode mode's kernels are built from (a
+    blocked sketch with fewer blocks than CUs is encoded by the dense kernels)."""
     import hashlib
     csrc = os.path.join(ROOT, "paper_2402_07529_amd", "csrc")
-    files = ["hc_blocked.hip"] if mode == "blocked" else ["hc_encode.hip"]
+    files = ["hc_blocked.hip", "hc_encode.hip"] if mode == "blocked" else ["hc_encode.hip"]
     src = b"".join(open(os.path.join(csrc, f), "rb").read() for f in files + ["hc_device.h"])
     return hashlib.sha256(src).hexdigest()
 
@@ -507,6 +508,7 @@ def main():
     iter_b = W * enc_b + agg_b + dec_b
     value = 4 * w.n / (ms * 1e-3) / 1e9
     nnz_w = float(np.mean([w.nnz(i) for i in range(W)]))  # nonzeros one worker encodes
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
     enc_gbs = enc_b / (enc_ms * 1e-3) / 1e9
     res = {
         "metric": METRIC, "value": round(value, 3), "unit": "GB/s", "n_gpus": 1,
@@ -522,7 +524,9 @@ def main():
                    "encode": encode,
                    **{k: v for k, v in w.params.items() if k in ("density", "overlap", "rows_per_worker")}},
         "roofline": {"bound": "hbm",
-                     "kernel": ("hc_encode (blocked LDS encode)" if a.blocked
+                     "kernel": (("hc_encode (blocked LDS encode)" if p.nblocks >= cus else
+                                 "hc_encode (blocked sketch, fewer blocks than CUs: Y clear + "
+                                 "dense encode over the whole GPU)") if a.blocked
                                 else "hc_encode_gather (rows through the plan)" if gather
                                 else "hc_encode_staged (staging pass + rows through the plan)"
                                 if staged else "hc_encode (Y clear + dense encode)"),
