@@ -732,12 +732,61 @@ __device__ __forceinline__ void add_live_batches(const CounterArgs& a, bool live
     }
 }
 
+constexpr uint32_t kScreen = 4;  // chunks of 64 plan entries a row wave screens together
+
+// Row `row`'s counters, built by one wave in its LDS (acc): the wave screens
+// kScreen chunks of 64 plan entries with their loads in flight (a lane per
+// entry: is any member of the support in the batch?), then adds the live
+// batches' members bit by bit (add_live_batches).
+template <int C>
+__device__ void build_row(const CounterArgs& a, uint32_t row, unsigned long long* acc) {
+    const uint32_t lane = lane_id();
+    // a wave's LDS operations complete in order: the previous row's reads are
+    // done before these stores
+    for (uint32_t k = lane; k < (uint32_t)C; k += 64) acc[k] = 0ull;
+    const uint32_t e0 = a.rowoff[row], e1 = a.rowoff[row + 1];
+    for (uint32_t cs = e0; cs < e1; cs += 64u * kScreen) {
+        // screen: each lane one entry per chunk, all loads in flight
+        uint32_t bidx[kScreen], bias[kScreen], boff[kScreen];
+        bool live[kScreen];
+#pragma unroll
+        for (uint32_t h = 0; h < kScreen; h++) {
+            const uint32_t e = cs + 64u * h + lane;
+            uint2 ent = make_uint2(0xffffffffu, 0u);
+            if (e < e1) ent = a.entry[e];
+            bidx[h] = ent.x;
+            bias[h] = ent.y & 0xffffu;
+        }
+#pragma unroll
+        for (uint32_t h = 0; h < kScreen; h++) {
+            boff[h] = 0;
+            live[h] = false;
+            if (bidx[h] < a.nb) {
+                boff[h] = a.woffb[bidx[h]];
+                live[h] = a.woffb[bidx[h] + 1] != boff[h];
+            }
+        }
+#pragma unroll
+        for (uint32_t h = 0; h < kScreen; h++)
+            add_live_batches<C>(a, live[h], bidx[h], bias[h], boff[h], acc);
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // every lane's LDS adds have landed
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Whether the plan was built for this geometry; if not, flags it (the decode
+// then reports status 3).
+__device__ __forceinline__ bool plan_matches(const CounterArgs& a) {
+    const PlanHeader* hdr = a.hdr;
+    const bool ok = hdr->magic == kPlanMagic && hdr->n == a.n && hdr->seed == a.seed &&
+                    hdr->c == a.c && hdr->rows == a.rows;
+    if (!ok && blockIdx.x == 0 && threadIdx.x == 0) a.ctrl->bad_plan = 1u;
+    return ok;
+}
+
 // One wave per sketch row (grid-stride), its counters in the wave's LDS: the
-// same counters as counter_kernel, for sketches with rows to spare.  The
-// wave screens kScreen chunks of 64 plan entries with their loads in flight
-// (a lane per entry: is any member of the support in the batch?), then adds
-// the live batches' members bit by bit (add_live_batches).  The row is then
-// written once.  A wave per row needs no workgroup barriers and keeps four
+// same counters as counter_kernel, for sketches with rows to spare.  The row
+// is written once.  A wave per row needs no workgroup barriers and keeps four
 // times as many rows in flight as a workgroup per row (VGG19: 10 K rows, the
 // counters went from 178 to 101 us); with few long rows (NCF: 1.9 K rows of
 // 1.7 K entries, a few dense words per batch) it left SIMDs idle and ran
@@ -745,15 +794,8 @@ __device__ __forceinline__ void add_live_batches(const CounterArgs& a, bool live
 template <int C>
 __global__ __launch_bounds__(kBlock) void counter_rows_kernel(CounterArgs a) {
     constexpr uint32_t kWaves = kBlock / 64;
-    constexpr uint32_t kScreen = 4;  // chunks of 64 plan entries screened together
     __shared__ unsigned long long s_acc[kWaves * C];
-    const PlanHeader* hdr = a.hdr;
-    const bool ok = hdr->magic == kPlanMagic && hdr->n == a.n && hdr->seed == a.seed &&
-                    hdr->c == a.c && hdr->rows == a.rows;
-    if (!ok) {
-        if (blockIdx.x == 0 && threadIdx.x == 0) a.ctrl->bad_plan = 1u;
-        return;
-    }
+    if (!plan_matches(a)) return;
     if (a.ctrl->overflow) return;
     const uint32_t kpack = pack_bits(a.ctrl->n_support);
     const uint32_t lane = lane_id();
@@ -761,37 +803,7 @@ __global__ __launch_bounds__(kBlock) void counter_rows_kernel(CounterArgs a) {
     unsigned long long* const acc = s_acc + wave * C;
     const uint32_t nwaves = gridDim.x * kWaves;
     for (uint32_t row = blockIdx.x * kWaves + wave; row < a.rows; row += nwaves) {
-        // a wave's LDS operations complete in order: the previous row's
-        // reads are done before these stores
-        for (uint32_t k = lane; k < (uint32_t)C; k += 64) acc[k] = 0ull;
-        const uint32_t e0 = a.rowoff[row], e1 = a.rowoff[row + 1];
-        for (uint32_t cs = e0; cs < e1; cs += 64u * kScreen) {
-            // screen: each lane one entry per chunk, all loads in flight
-            uint32_t bidx[kScreen], bias[kScreen], boff[kScreen];
-            bool live[kScreen];
-#pragma unroll
-            for (uint32_t h = 0; h < kScreen; h++) {
-                const uint32_t e = cs + 64u * h + lane;
-                uint2 ent = make_uint2(0xffffffffu, 0u);
-                if (e < e1) ent = a.entry[e];
-                bidx[h] = ent.x;
-                bias[h] = ent.y & 0xffffu;
-            }
-#pragma unroll
-            for (uint32_t h = 0; h < kScreen; h++) {
-                boff[h] = 0;
-                live[h] = false;
-                if (bidx[h] < a.nb) {
-                    boff[h] = a.woffb[bidx[h]];
-                    live[h] = a.woffb[bidx[h] + 1] != boff[h];
-                }
-            }
-#pragma unroll
-            for (uint32_t h = 0; h < kScreen; h++)
-                add_live_batches<C>(a, live[h], bidx[h], bias[h], boff[h], acc);
-        }
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // every lane's LDS adds have landed
-        __builtin_amdgcn_wave_barrier();
+        build_row<C>(a, row, acc);
         unsigned long long* dst = a.cnt + (uint64_t)row * C;
         bool fits = true;
         for (uint32_t k = lane; k < (uint32_t)C; k += 64) {
@@ -800,6 +812,301 @@ __global__ __launch_bounds__(kBlock) void counter_rows_kernel(CounterArgs a) {
             fits = fits && fits_packed(v, kpack);
         }
         flag_unpackable(a.ctrl, fits);
+    }
+}
+
+// ---- round 0 by rows (int32 with a plan, large sketches) -------------------------
+//
+// Round 0 of the peel (Algorithm 1) recovers every element that has a pure
+// cell: x = g Y at that cell, exact in int32.  Taken entry by entry, each of
+// those elements costs its two other cells a scattered 64-bit atomic, which
+// bounds the round at the chip's scattered-atomic rate (VGG19: 2.2 M
+// elements, 0.3 ms).  Here round 0 is two passes over the rows through the
+// plan instead, every update landing in the row's counters in LDS:
+//   pure_rows    builds each row's counters as counter_rows_kernel does and,
+//                for each pure cell, writes its element's value and sets its
+//                flag (an element with several pure cells gets the same
+//                value from each);
+//   round0_rows  builds each row's counters again without the flagged
+//                elements, subtracts their values from the residual, writes
+//                the counters the peel kernel continues from (packed with the
+//                residuals, or counters and residuals apart) and queues the
+//                cells left pure: round 1's frontier.
+// The round's elements, values and counters are those of the entry-by-entry
+// round; only the order of round 1's frontier in the queue differs.
+struct Round0Args {
+    CounterArgs c;
+    const int32_t* y_agg;
+    int32_t* vals;
+    uint8_t* peeled;
+    const uint32_t* elem;
+    int32_t* yw;
+    uint2* queue;
+    unsigned int* tail;
+    uint32_t log2c;
+};
+
+template <int C>
+__global__ __launch_bounds__(kBlock) void pure_rows_kernel(Round0Args r) {
+    constexpr uint32_t kWaves = kBlock / 64;
+    constexpr uint32_t CPL = C / 64;  // cells per lane
+    __shared__ unsigned long long s_acc[kWaves * C];
+    const CounterArgs& a = r.c;
+    if (!plan_matches(a)) return;
+    if (a.ctrl->overflow) return;
+    const uint32_t nsup = (uint32_t)a.ctrl->n_support;
+    const uint32_t kpack = pack_bits(nsup);
+    const uint32_t lane = lane_id();
+    const uint32_t wave = uniform(threadIdx.x >> 6);
+    unsigned long long* const acc = s_acc + wave * C;
+    const uint32_t nwaves = gridDim.x * kWaves;
+    for (uint32_t row = blockIdx.x * kWaves + wave; row < a.rows; row += nwaves) {
+        build_row<C>(a, row, acc);
+        bool fits = true;
+        bool pure[CPL];
+        uint32_t pos[CPL], p[CPL];
+        int32_t y[CPL];
+        // the pure cells' elements and sketch values, their loads in flight together
+#pragma unroll
+        for (uint32_t i = 0; i < CPL; i++) {
+            const unsigned long long v = acc[lane + 64u * i];
+            fits = fits && fits_packed(v, kpack);
+            pos[i] = (uint32_t)v;
+            pure[i] = (v >> 32) == 1ull && pos[i] < nsup;
+            p[i] = pure[i] ? r.elem[pos[i]] : 0u;
+            y[i] = pure[i] ? r.y_agg[(uint64_t)row * C + lane + 64u * i] : 0;
+        }
+        flag_unpackable(a.ctrl, fits);
+#pragma unroll
+        for (uint32_t i = 0; i < CPL; i++) {
+            if (!pure[i]) continue;
+            // the element's hash that lands in this row (its three rows differ)
+            const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p[i] >> r.log2c);
+            const uint32_t j = h.row[0] == row ? 0u : (h.row[1] == row ? 1u : 2u);
+            r.vals[pos[i]] = Val<int32_t>::sign(y[i], (h.neg >> j) & 1u);
+            r.peeled[pos[i]] = 1u;
+        }
+    }
+}
+
+// Like add_live_batches, for round0_rows.  PHASE 0: packed counters (the
+// residual in the high word, deg * 2^kp + sum of positions in the low), the
+// flagged members' -g x added to the residual and the others counted;
+// PHASE 1: unpacked counters (deg * 2^32 + sum of positions) of the members
+// not flagged; PHASE 2: the flagged members' -g x in the low word.  Each
+// segment of WPB lanes holds the flags and values of its batch's first kWin
+// members (ranks are consecutive within a batch), which the members' lanes
+// fetch by shuffle; members past that read memory.  Counts into e0 the
+// flagged members met through their hash j = 0: each element once.
+template <int C, int PHASE>
+__device__ __forceinline__ void sub_live_batches(const Round0Args& r, bool live, uint32_t bidx,
+                                                 uint32_t ey, uint32_t boff,
+                                                 unsigned long long* acc, uint32_t kp,
+                                                 uint32_t nsup, uint32_t& e0) {
+    constexpr uint32_t WPB = C / 32;       // bitmap words per batch
+    constexpr uint32_t kGroup = 64 / WPB;  // batches per wave-wide load
+    constexpr uint32_t kUnroll = 2;        // wave-wide loads in flight
+    constexpr uint32_t kWin = 4 * WPB;     // members per batch held by its segment
+    const CounterArgs& a = r.c;
+    const uint32_t lane = lane_id();
+    const uint32_t seg = lane / WPB;
+    const uint32_t wl = lane % WPB;
+    uint64_t m = __ballot(live);
+    while (m != 0ull) {
+        uint32_t word[kUnroll], gy[kUnroll], goff[kUnroll], fw[kUnroll], vw[kUnroll][4];
+        bool have[kUnroll];
+#pragma unroll
+        for (uint32_t u = 0; u < kUnroll; u++) {
+            uint64_t mm = m;
+#pragma unroll
+            for (uint32_t q = 0; q < kGroup; q++)
+                if (q < seg && mm != 0ull) mm &= mm - 1ull;
+            have[u] = mm != 0ull;
+            const uint32_t src = have[u] ? (uint32_t)__ffsll((unsigned long long)mm) - 1u : 0u;
+            const uint32_t gb = (uint32_t)__shfl(bidx, (int)src);
+            gy[u] = (uint32_t)__shfl(ey, (int)src);
+            goff[u] = (uint32_t)__shfl(boff, (int)src);
+            word[u] = have[u] ? load_word(a.b, (uint64_t)gb * WPB + wl, a.words, a.last_mask) : 0u;
+            // flag bytes [fb, fb + 4) and values [vb, vb + 4) of the batch's first kWin members
+            const uint32_t fb = (goff[u] & ~3u) + 4u * wl;
+            fw[u] = have[u] && fb < nsup ? *reinterpret_cast<const uint32_t*>(r.peeled + fb) : 0u;
+#pragma unroll
+            for (uint32_t i = 0; i < 4; i++) {
+                const uint32_t vb = goff[u] + 4u * wl + i;
+                vw[u][i] = PHASE != 1 && have[u] && vb < nsup ? (uint32_t)r.vals[vb] : 0u;
+            }
+#pragma unroll
+            for (uint32_t q = 0; q < kGroup; q++)
+                if (m != 0ull) m &= m - 1ull;
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < kUnroll; u++) {
+            const uint32_t pc = __popc(word[u]);
+            uint32_t x = pc;
+#pragma unroll
+            for (uint32_t d = 1; d < WPB; d <<= 1) {
+                const uint32_t y = __shfl_up(x, d);
+                if (wl >= d) x += y;
+            }
+            uint32_t rank = goff[u] + x - pc;
+            const uint32_t bias = gy[u] & 0xffffu;
+            const uint32_t j = (gy[u] >> 16) & 3u;
+            const bool neg = (gy[u] >> 31) != 0u;
+            const uint32_t fbase = goff[u] & ~3u;
+            uint32_t w = have[u] ? word[u] : 0u;
+            // every lane takes part in each pass (the shuffles read the
+            // window from lanes whose own members may be done)
+            while (__ballot(w != 0u) != 0ull) {
+                const bool has = w != 0u;
+                const uint32_t bit = has ? (uint32_t)__builtin_ctz(w) : 0u;
+                if (has) w &= w - 1u;
+                const uint32_t fi = rank - fbase, vi = rank - goff[u];
+                const uint32_t fword =
+                    (uint32_t)__shfl((int)fw[u], (int)(seg * WPB + ((fi >> 2) & (WPB - 1u))));
+                bool fl = ((fword >> (8u * (fi & 3u))) & 0xffu) != 0u;
+                uint32_t xv = 0u;
+                if (PHASE != 1) {
+                    const int vsrc = (int)(seg * WPB + ((vi >> 2) & (WPB - 1u)));
+                    const uint32_t x0 = (uint32_t)__shfl((int)vw[u][0], vsrc);
+                    const uint32_t x1 = (uint32_t)__shfl((int)vw[u][1], vsrc);
+                    const uint32_t x2 = (uint32_t)__shfl((int)vw[u][2], vsrc);
+                    const uint32_t x3 = (uint32_t)__shfl((int)vw[u][3], vsrc);
+                    const uint32_t c = vi & 3u;
+                    xv = c == 0u ? x0 : (c == 1u ? x1 : (c == 2u ? x2 : x3));
+                }
+                if (has) {
+                    if (fi >= kWin) fl = r.peeled[rank] != 0u;
+                    if (PHASE != 1 && fl && vi >= kWin) xv = (uint32_t)r.vals[rank];
+                    const uint32_t cell = (32u * wl + bit + bias) & (uint32_t)(C - 1);
+                    const uint32_t gx = neg ? xv : 0u - xv;  // -g x
+                    if (PHASE == 0)
+                        atomicAdd(&acc[cell], fl ? ((unsigned long long)gx << 32)
+                                                 : (1ull << kp) + rank);
+                    else if (PHASE == 1 && !fl)
+                        atomicAdd(&acc[cell], kOne + rank);
+                    else if (PHASE == 2 && fl)
+                        atomicAdd(&acc[cell], (unsigned long long)gx);
+                    if (PHASE != 2 && fl && j == 0u) e0++;
+                    rank++;
+                }
+            }
+        }
+    }
+}
+
+template <int C, int PHASE>
+__device__ void round0_row(const Round0Args& r, uint32_t row, unsigned long long* acc,
+                           uint32_t kp, uint32_t nsup, uint32_t& e0) {
+    const CounterArgs& a = r.c;
+    const uint32_t lane = lane_id();
+    // a wave's LDS operations complete in order: the previous row's reads are
+    // done before these stores
+    for (uint32_t k = lane; k < (uint32_t)C; k += 64) {
+        const uint32_t y = PHASE == 1 ? 0u : (uint32_t)r.y_agg[(uint64_t)row * C + k];
+        acc[k] = PHASE == 0 ? (unsigned long long)y << 32 : (unsigned long long)y;
+    }
+    const uint32_t r0 = a.rowoff[row], r1 = a.rowoff[row + 1];
+    for (uint32_t cs = r0; cs < r1; cs += 64u * kScreen) {
+        uint32_t bidx[kScreen], ey[kScreen], boff[kScreen];
+        bool live[kScreen];
+#pragma unroll
+        for (uint32_t h = 0; h < kScreen; h++) {
+            const uint32_t e = cs + 64u * h + lane;
+            uint2 ent = make_uint2(0xffffffffu, 0u);
+            if (e < r1) ent = a.entry[e];
+            bidx[h] = ent.x;
+            ey[h] = ent.y;
+        }
+#pragma unroll
+        for (uint32_t h = 0; h < kScreen; h++) {
+            boff[h] = 0;
+            live[h] = false;
+            if (bidx[h] < a.nb) {
+                boff[h] = a.woffb[bidx[h]];
+                live[h] = a.woffb[bidx[h] + 1] != boff[h];
+            }
+        }
+#pragma unroll
+        for (uint32_t h = 0; h < kScreen; h++)
+            sub_live_batches<C, PHASE>(r, live[h], bidx[h], ey[h], boff[h], acc, kp, nsup, e0);
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // every lane's LDS adds have landed
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Writes the row's counters (cnt) and queues its pure cells with their
+// elements (packed: positions in the low kp bits; unpacked: the low word).
+template <int C>
+__device__ void round0_write_row(const Round0Args& r, uint32_t row,
+                                 const unsigned long long* acc, bool packed, uint32_t kp) {
+    constexpr uint32_t CPL = C / 64;
+    const CounterArgs& a = r.c;
+    const uint32_t lane = lane_id();
+    uint32_t npush = 0, mine = 0;  // bit i of mine: cell lane + 64 i is pure
+    unsigned long long* dst = a.cnt + (uint64_t)row * C;
+#pragma unroll
+    for (uint32_t i = 0; i < CPL; i++) {
+        const unsigned long long v = acc[lane + 64u * i];
+        dst[lane + 64u * i] = v;
+        const bool pure = packed ? ((uint32_t)v >> kp) == 1u : (v >> 32) == 1ull;
+        mine |= (uint32_t)pure << i;
+        npush += (uint32_t)__popcll(__ballot(pure));
+    }
+    if (npush == 0u) return;
+    uint32_t base = 0;
+    if (lane == 0) base = atomicAdd(r.tail, npush);
+    base = (uint32_t)__shfl((int)base, 0);
+#pragma unroll
+    for (uint32_t i = 0; i < CPL; i++) {
+        const bool pure = (mine >> i) & 1u;
+        const uint64_t bal = __ballot(pure);
+        if (pure) {
+            const uint64_t slot = (uint64_t)base + lanes_below(bal);
+            const unsigned long long v = acc[lane + 64u * i];
+            const uint32_t pos = packed ? (uint32_t)v & ((1u << kp) - 1u) : (uint32_t)v;
+            if (slot < a.cells)  // a cell is queued at most once
+                r.queue[slot] = make_uint2(row * (uint32_t)C + lane + 64u * i, pos);
+        }
+        base += (uint32_t)__popcll(bal);
+    }
+}
+
+template <int C>
+__global__ __launch_bounds__(kBlock) void round0_rows_kernel(Round0Args r) {
+    constexpr uint32_t kWaves = kBlock / 64;
+    __shared__ unsigned long long s_acc[kWaves * C];
+    __shared__ uint32_t s_red;
+    const CounterArgs& a = r.c;
+    Ctrl* ctrl = a.ctrl;
+    if (ctrl->overflow != 0 || ctrl->bad_plan != 0) return;
+    if (threadIdx.x == 0) s_red = 0;
+    lds_barrier();
+    const uint32_t nsup = (uint32_t)ctrl->n_support;
+    const uint32_t kp = pack_bits(nsup);
+    const bool packed = ctrl->nopack == 0;
+    const uint32_t lane = lane_id();
+    const uint32_t wave = uniform(threadIdx.x >> 6);
+    unsigned long long* const acc = s_acc + wave * C;
+    const uint32_t nwaves = gridDim.x * kWaves;
+    uint32_t e0 = 0;
+    for (uint32_t row = blockIdx.x * kWaves + wave; row < a.rows; row += nwaves) {
+        if (packed) {
+            round0_row<C, 0>(r, row, acc, kp, nsup, e0);
+            round0_write_row<C>(r, row, acc, true, kp);
+        } else {
+            round0_row<C, 1>(r, row, acc, kp, nsup, e0);
+            round0_write_row<C>(r, row, acc, false, kp);
+            round0_row<C, 2>(r, row, acc, kp, nsup, e0);
+            for (uint32_t k = lane; k < (uint32_t)C; k += 64)
+                r.yw[(uint64_t)row * C + k] = (int32_t)(uint32_t)acc[k];
+        }
+    }
+    e0 = wave_sum(e0);
+    if (lane == 0 && e0 != 0u) atomicAdd(&s_red, e0);
+    lds_barrier();
+    if (threadIdx.x == 0 && s_red != 0u) {
+        atomicAdd(&ctrl->recovered, (unsigned long long)s_red);
+        atomicMax(&ctrl->rounds, 1u);  // recoveries in round 0
     }
 }
 
@@ -1555,6 +1862,41 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
                        dim3(kBlock), 0, s, sa);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
+    // A wave per row when rows are to spare (two or more per SIMD); then, for
+    // large int32 sketches, round 0 as two passes over the rows (pure_rows,
+    // round0_rows) instead of the counter kernel and the entry-by-entry round.
+    const bool wave_rows = planned && (uint64_t)g.rows >= 8ull * (uint64_t)di.cus;
+    const bool rows0 = wave_rows && std::is_same<T, int32_t>::value &&
+                       g.cells >= kRound0SplitCells;
+    Round0Args ra;
+    ra.y_agg = reinterpret_cast<const int32_t*>(y_agg_v);
+    ra.vals = reinterpret_cast<int32_t*>(vals);
+    ra.peeled = peeled;
+    ra.elem = elem;
+    ra.yw = reinterpret_cast<int32_t*>(yw);
+    ra.queue = queue;
+    ra.tail = &sync->tail.v[0];
+    ra.log2c = g.log2c;
+    // one wave per row over the whole chip, as many workgroups as fit
+    auto launch_rows = [&](auto k1024, auto k512, auto k256, auto args) -> hipError_t {
+        const void* kfn = g.c == 1024 ? reinterpret_cast<const void*>(k1024)
+                        : g.c == 512 ? reinterpret_cast<const void*>(k512)
+                                     : reinterpret_cast<const void*>(k256);
+        int per_cu = 0;
+        hipError_t err = occupancy_per_cu(kfn, kBlock, &per_cu);
+        if (err != hipSuccess) return err;
+        const uint64_t want = ((uint64_t)g.rows + kBlock / 64 - 1) / (kBlock / 64);
+        const uint64_t cap = (uint64_t)di.cus * per_cu;
+        const uint32_t cgrid = (uint32_t)(want < cap ? want : cap);
+        if (g.c == 1024)
+            hipLaunchKernelGGL(k1024, dim3(cgrid), dim3(kBlock), 0, s, args);
+        else if (g.c == 512)
+            hipLaunchKernelGGL(k512, dim3(cgrid), dim3(kBlock), 0, s, args);
+        else
+            hipLaunchKernelGGL(k256, dim3(cgrid), dim3(kBlock), 0, s, args);
+        return hipGetLastError();
+    };
+
     if (planned) {
         const PlanLayout PL = plan_layout(g);
         const char* pb = static_cast<const char*>(plan);
@@ -1579,21 +1921,15 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
         // flight together.  Fewer, longer rows (NCF: 1.9 K rows of 1.7 K plan
         // entries) keep more waves busy as a workgroup per row, or, when a
         // row has only a few entries, a wave per row walking them in turn.
-        if ((uint64_t)g.rows >= 8ull * (uint64_t)di.cus) {
-            int per_cu = 0;
-            const void* kfn = g.c == 1024 ? reinterpret_cast<const void*>(&counter_rows_kernel<1024>)
-                            : g.c == 512 ? reinterpret_cast<const void*>(&counter_rows_kernel<512>)
-                                         : reinterpret_cast<const void*>(&counter_rows_kernel<256>);
-            if ((e = occupancy_per_cu(kfn, kBlock, &per_cu)) != hipSuccess) return e;
-            const uint64_t want = ((uint64_t)g.rows + kBlock / 64 - 1) / (kBlock / 64);
-            const uint64_t cap = (uint64_t)di.cus * per_cu;
-            const uint32_t cgrid = (uint32_t)(want < cap ? want : cap);
-            if (g.c == 1024)
-                hipLaunchKernelGGL(counter_rows_kernel<1024>, dim3(cgrid), dim3(kBlock), 0, s, ca);
-            else if (g.c == 512)
-                hipLaunchKernelGGL(counter_rows_kernel<512>, dim3(cgrid), dim3(kBlock), 0, s, ca);
-            else
-                hipLaunchKernelGGL(counter_rows_kernel<256>, dim3(cgrid), dim3(kBlock), 0, s, ca);
+        if (rows0) {
+            ra.c = ca;
+            if ((e = launch_rows(pure_rows_kernel<1024>, pure_rows_kernel<512>,
+                                 pure_rows_kernel<256>, ra)) != hipSuccess)
+                return e;
+        } else if (wave_rows) {
+            if ((e = launch_rows(counter_rows_kernel<1024>, counter_rows_kernel<512>,
+                                 counter_rows_kernel<256>, ca)) != hipSuccess)
+                return e;
         } else if (3ull * ((g.n + g.c - 1) / g.c) <= kWaveRowsEntries * g.rows) {
             const uint64_t want = ((uint64_t)g.rows + 3) / 4;  // four waves per workgroup
             const uint32_t cgrid = want < (uint64_t)di.cus * 8 ? (uint32_t)want : (uint32_t)di.cus * 8;
@@ -1656,7 +1992,11 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     pa.counted = planned;
     // large sketches (large round-0 frontiers) take round 0 on the whole chip
     pa.split0 = g.cells >= kRound0SplitCells;
-    if (pa.split0) {
+    if (rows0) {
+        if ((e = launch_rows(round0_rows_kernel<1024>, round0_rows_kernel<512>,
+                             round0_rows_kernel<256>, ra)) != hipSuccess)
+            return e;
+    } else if (pa.split0) {
         const uint32_t grid0 = (uint32_t)di.cus * 8;
         hipLaunchKernelGGL(scan0_kernel<A>, dim3(grid0), dim3(kBlock), 0, s, pa);
         if ((e = hipGetLastError()) != hipSuccess) return e;
