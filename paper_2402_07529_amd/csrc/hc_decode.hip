@@ -150,6 +150,17 @@ __device__ __forceinline__ uint32_t load_word(const uint32_t* b, uint64_t k, uin
     return k == words - 1 ? (w & last_mask) : w;
 }
 
+// The same for words >= 1, with no branch: past the end it loads the last
+// word and returns 0.  A load under a branch is followed, inside the branch,
+// by the masking that uses it, so the compiler waits for each such load in
+// turn; the row kernels issue theirs together.
+__device__ __forceinline__ uint32_t load_word_nb(const uint32_t* b, uint64_t k, uint64_t words,
+                                                 uint32_t last_mask) {
+    const uint32_t w = b[k < words ? k : words - 1];
+    const uint32_t mask = k < words ? (k == words - 1 ? last_mask : 0xffffffffu) : 0u;
+    return w & mask;
+}
+
 __global__ __launch_bounds__(kBlock) void count_kernel(const uint32_t* __restrict__ b,
                                                        uint64_t words, uint32_t last_mask,
                                                        uint32_t* __restrict__ blk) {
@@ -704,13 +715,17 @@ __device__ __forceinline__ void add_live_batches(const CounterArgs& a, bool live
             const uint32_t gb = (uint32_t)__shfl(bidx, (int)src);
             gbias[u] = (uint32_t)__shfl(bias, (int)src);
             goff[u] = (uint32_t)__shfl(boff, (int)src);
-            word[u] = have[u] ? load_word(a.b, (uint64_t)gb * WPB + wl, a.words, a.last_mask) : 0u;
+            // loaded whether or not the segment has a batch (gb is then some
+            // lane's entry, possibly none: the load is clamped), and dropped
+            // below, so that no load sits under a branch
+            word[u] = load_word_nb(a.b, (uint64_t)gb * WPB + wl, a.words, a.last_mask);
 #pragma unroll
             for (uint32_t q = 0; q < kGroup; q++)  // the group's batches are taken
                 if (m != 0ull) m &= m - 1ull;
         }
 #pragma unroll
         for (uint32_t u = 0; u < kUnroll; u++) {
+            if (!have[u]) word[u] = 0u;
             // rank of the word's first bit: the batch's offset plus the
             // popcounts of its earlier words (a scan within the segment)
             const uint32_t pc = __popc(word[u]);
@@ -734,6 +749,39 @@ __device__ __forceinline__ void add_live_batches(const CounterArgs& a, bool live
 
 constexpr uint32_t kScreen = 4;  // chunks of 64 plan entries a row wave screens together
 
+// Screens kScreen chunks of 64 plan entries of a row, from entry cs (< e1):
+// a lane per entry, is any member of the support in the entry's batch?  Gives
+// each entry's batch (0xffffffff: none), its packed hash word, the batch's
+// rank offset and whether it is live.  Every load is issued unconditionally,
+// at a clamped index, so that the entries' loads are in flight together and
+// then the rank offsets'.
+__device__ __forceinline__ void screen_entries(const CounterArgs& a, uint32_t cs, uint32_t e1,
+                                               uint32_t (&bidx)[kScreen], uint32_t (&ey)[kScreen],
+                                               uint32_t (&boff)[kScreen], bool (&live)[kScreen]) {
+    const uint32_t lane = lane_id();
+    uint2 ent[kScreen];
+#pragma unroll
+    for (uint32_t h = 0; h < kScreen; h++) {
+        const uint32_t e = cs + 64u * h + lane;
+        ent[h] = a.entry[e < e1 ? e : e1 - 1u];
+    }
+    uint32_t lo[kScreen], hi[kScreen];
+#pragma unroll
+    for (uint32_t h = 0; h < kScreen; h++) {
+        const bool ok = cs + 64u * h + lane < e1 && ent[h].x < a.nb;
+        bidx[h] = ok ? ent[h].x : 0xffffffffu;
+        const uint32_t bi = ok ? ent[h].x : 0u;
+        lo[h] = a.woffb[bi];
+        hi[h] = a.woffb[bi + 1];
+    }
+#pragma unroll
+    for (uint32_t h = 0; h < kScreen; h++) {
+        ey[h] = ent[h].y;
+        boff[h] = lo[h];
+        live[h] = bidx[h] != 0xffffffffu && hi[h] != lo[h];
+    }
+}
+
 // Row `row`'s counters, built by one wave in its LDS (acc): the wave screens
 // kScreen chunks of 64 plan entries with their loads in flight (a lane per
 // entry: is any member of the support in the batch?), then adds the live
@@ -746,29 +794,12 @@ __device__ void build_row(const CounterArgs& a, uint32_t row, unsigned long long
     for (uint32_t k = lane; k < (uint32_t)C; k += 64) acc[k] = 0ull;
     const uint32_t e0 = a.rowoff[row], e1 = a.rowoff[row + 1];
     for (uint32_t cs = e0; cs < e1; cs += 64u * kScreen) {
-        // screen: each lane one entry per chunk, all loads in flight
-        uint32_t bidx[kScreen], bias[kScreen], boff[kScreen];
+        uint32_t bidx[kScreen], ey[kScreen], boff[kScreen];
         bool live[kScreen];
-#pragma unroll
-        for (uint32_t h = 0; h < kScreen; h++) {
-            const uint32_t e = cs + 64u * h + lane;
-            uint2 ent = make_uint2(0xffffffffu, 0u);
-            if (e < e1) ent = a.entry[e];
-            bidx[h] = ent.x;
-            bias[h] = ent.y & 0xffffu;
-        }
-#pragma unroll
-        for (uint32_t h = 0; h < kScreen; h++) {
-            boff[h] = 0;
-            live[h] = false;
-            if (bidx[h] < a.nb) {
-                boff[h] = a.woffb[bidx[h]];
-                live[h] = a.woffb[bidx[h] + 1] != boff[h];
-            }
-        }
+        screen_entries(a, cs, e1, bidx, ey, boff, live);
 #pragma unroll
         for (uint32_t h = 0; h < kScreen; h++)
-            add_live_batches<C>(a, live[h], bidx[h], bias[h], boff[h], acc);
+            add_live_batches<C>(a, live[h], bidx[h], ey[h] & 0xffffu, boff[h], acc);
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // every lane's LDS adds have landed
     __builtin_amdgcn_wave_barrier();
@@ -873,8 +904,8 @@ __global__ __launch_bounds__(kBlock) void pure_rows_kernel(Round0Args r) {
             fits = fits && fits_packed(v, kpack);
             pos[i] = (uint32_t)v;
             pure[i] = (v >> 32) == 1ull && pos[i] < nsup;
-            p[i] = pure[i] ? r.elem[pos[i]] : 0u;
-            y[i] = pure[i] ? r.y_agg[(uint64_t)row * C + lane + 64u * i] : 0;
+            p[i] = r.elem[pure[i] ? pos[i] : 0u];
+            y[i] = r.y_agg[(uint64_t)row * C + lane + 64u * i];
         }
         flag_unpackable(a.ctrl, fits);
 #pragma unroll
@@ -893,30 +924,36 @@ __global__ __launch_bounds__(kBlock) void pure_rows_kernel(Round0Args r) {
 // residual in the high word, deg * 2^kp + sum of positions in the low), the
 // flagged members' -g x added to the residual and the others counted;
 // PHASE 1: unpacked counters (deg * 2^32 + sum of positions) of the members
-// not flagged; PHASE 2: the flagged members' -g x in the low word.  Each
-// segment of WPB lanes holds the flags and values of its batch's first kWin
-// members (ranks are consecutive within a batch), which the members' lanes
-// fetch by shuffle; members past that read memory.  Counts into e0 the
-// flagged members met through their hash j = 0: each element once.
+// not flagged; PHASE 2: the flagged members' -g x in the low word.  The flags
+// and values of each batch's first kWin members (ranks are consecutive within
+// a batch) are loaded with the bitmap words, by the batch's WPB lanes, and
+// staged in the wave's window in LDS (win: kR0Unroll * 64 / WPB batches of
+// kWin values, then as many of kWin flag bytes); members past that read
+// memory.  Counts into e0 the flagged members met through their hash j = 0:
+// each element once.
+constexpr uint32_t kR0Unroll = 2;  // wave-wide bitmap loads in flight per round0_rows wave
+
 template <int C, int PHASE>
 __device__ __forceinline__ void sub_live_batches(const Round0Args& r, bool live, uint32_t bidx,
                                                  uint32_t ey, uint32_t boff,
-                                                 unsigned long long* acc, uint32_t kp,
-                                                 uint32_t nsup, uint32_t& e0) {
+                                                 unsigned long long* acc, uint32_t* win,
+                                                 uint32_t kp, uint32_t nsup, uint32_t& e0) {
     constexpr uint32_t WPB = C / 32;       // bitmap words per batch
     constexpr uint32_t kGroup = 64 / WPB;  // batches per wave-wide load
-    constexpr uint32_t kUnroll = 2;        // wave-wide loads in flight
-    constexpr uint32_t kWin = 4 * WPB;     // members per batch held by its segment
+    constexpr uint32_t kWin = 4 * WPB;     // members per batch staged in the window
+    constexpr uint32_t kWinVals = kR0Unroll * kGroup * kWin;  // = 4 * 64 * kR0Unroll
     const CounterArgs& a = r.c;
     const uint32_t lane = lane_id();
     const uint32_t seg = lane / WPB;
     const uint32_t wl = lane % WPB;
+    uint8_t* const wflag = reinterpret_cast<uint8_t*>(win + kWinVals);
     uint64_t m = __ballot(live);
     while (m != 0ull) {
-        uint32_t word[kUnroll], gy[kUnroll], goff[kUnroll], fw[kUnroll], vw[kUnroll][4];
-        bool have[kUnroll];
+        uint32_t word[kR0Unroll], gy[kR0Unroll], goff[kR0Unroll], fw[kR0Unroll],
+            vw[kR0Unroll][4];
+        bool have[kR0Unroll];
 #pragma unroll
-        for (uint32_t u = 0; u < kUnroll; u++) {
+        for (uint32_t u = 0; u < kR0Unroll; u++) {
             uint64_t mm = m;
 #pragma unroll
             for (uint32_t q = 0; q < kGroup; q++)
@@ -926,21 +963,40 @@ __device__ __forceinline__ void sub_live_batches(const Round0Args& r, bool live,
             const uint32_t gb = (uint32_t)__shfl(bidx, (int)src);
             gy[u] = (uint32_t)__shfl(ey, (int)src);
             goff[u] = (uint32_t)__shfl(boff, (int)src);
-            word[u] = have[u] ? load_word(a.b, (uint64_t)gb * WPB + wl, a.words, a.last_mask) : 0u;
-            // flag bytes [fb, fb + 4) and values [vb, vb + 4) of the batch's first kWin members
+            // every load unconditional, at a clamped index, and dropped below
+            // where it is not wanted (see add_live_batches)
+            word[u] = load_word_nb(a.b, (uint64_t)gb * WPB + wl, a.words, a.last_mask);
+            // flag bytes [fb, fb + 4) and values [vb, vb + 4) of the batch's
+            // first kWin members (the arrays hold at least 256 bytes)
             const uint32_t fb = (goff[u] & ~3u) + 4u * wl;
-            fw[u] = have[u] && fb < nsup ? *reinterpret_cast<const uint32_t*>(r.peeled + fb) : 0u;
+            fw[u] = *reinterpret_cast<const uint32_t*>(r.peeled + (fb < nsup ? fb : 0u));
+            if (!(have[u] && fb < nsup)) fw[u] = 0u;
 #pragma unroll
             for (uint32_t i = 0; i < 4; i++) {
                 const uint32_t vb = goff[u] + 4u * wl + i;
-                vw[u][i] = PHASE != 1 && have[u] && vb < nsup ? (uint32_t)r.vals[vb] : 0u;
+                vw[u][i] = PHASE != 1 ? (uint32_t)r.vals[vb < nsup ? vb : 0u] : 0u;
             }
 #pragma unroll
             for (uint32_t q = 0; q < kGroup; q++)
                 if (m != 0ull) m &= m - 1ull;
         }
+        // the window: the previous batches' reads were issued before these
+        // stores, and a wave's LDS operations complete in order
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
 #pragma unroll
-        for (uint32_t u = 0; u < kUnroll; u++) {
+        for (uint32_t u = 0; u < kR0Unroll; u++) {
+            const uint32_t wb = (u * kGroup + seg) * kWin + 4u * wl;
+            *reinterpret_cast<uint32_t*>(wflag + wb) = fw[u];
+            if (PHASE != 1) {
+#pragma unroll
+                for (uint32_t i = 0; i < 4; i++) win[wb + i] = vw[u][i];
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (uint32_t u = 0; u < kR0Unroll; u++) {
+            if (!have[u]) word[u] = 0u;
             const uint32_t pc = __popc(word[u]);
             uint32_t x = pc;
 #pragma unroll
@@ -953,42 +1009,26 @@ __device__ __forceinline__ void sub_live_batches(const Round0Args& r, bool live,
             const uint32_t j = (gy[u] >> 16) & 3u;
             const bool neg = (gy[u] >> 31) != 0u;
             const uint32_t fbase = goff[u] & ~3u;
+            const uint32_t wbase = (u * kGroup + seg) * kWin;
             uint32_t w = have[u] ? word[u] : 0u;
-            // every lane takes part in each pass (the shuffles read the
-            // window from lanes whose own members may be done)
-            while (__ballot(w != 0u) != 0ull) {
-                const bool has = w != 0u;
-                const uint32_t bit = has ? (uint32_t)__builtin_ctz(w) : 0u;
-                if (has) w &= w - 1u;
+            while (w != 0u) {
+                const uint32_t bit = (uint32_t)__builtin_ctz(w);
+                w &= w - 1u;
                 const uint32_t fi = rank - fbase, vi = rank - goff[u];
-                const uint32_t fword =
-                    (uint32_t)__shfl((int)fw[u], (int)(seg * WPB + ((fi >> 2) & (WPB - 1u))));
-                bool fl = ((fword >> (8u * (fi & 3u))) & 0xffu) != 0u;
-                uint32_t xv = 0u;
-                if (PHASE != 1) {
-                    const int vsrc = (int)(seg * WPB + ((vi >> 2) & (WPB - 1u)));
-                    const uint32_t x0 = (uint32_t)__shfl((int)vw[u][0], vsrc);
-                    const uint32_t x1 = (uint32_t)__shfl((int)vw[u][1], vsrc);
-                    const uint32_t x2 = (uint32_t)__shfl((int)vw[u][2], vsrc);
-                    const uint32_t x3 = (uint32_t)__shfl((int)vw[u][3], vsrc);
-                    const uint32_t c = vi & 3u;
-                    xv = c == 0u ? x0 : (c == 1u ? x1 : (c == 2u ? x2 : x3));
-                }
-                if (has) {
-                    if (fi >= kWin) fl = r.peeled[rank] != 0u;
-                    if (PHASE != 1 && fl && vi >= kWin) xv = (uint32_t)r.vals[rank];
-                    const uint32_t cell = (32u * wl + bit + bias) & (uint32_t)(C - 1);
+                const bool fl = (fi < kWin ? wflag[wbase + fi] : r.peeled[rank]) != 0u;
+                const uint32_t cell = (32u * wl + bit + bias) & (uint32_t)(C - 1);
+                if (PHASE == 1) {
+                    if (!fl) atomicAdd(&acc[cell], kOne + rank);
+                } else if (fl) {
+                    const uint32_t xv = vi < kWin ? win[wbase + vi] : (uint32_t)r.vals[rank];
                     const uint32_t gx = neg ? xv : 0u - xv;  // -g x
-                    if (PHASE == 0)
-                        atomicAdd(&acc[cell], fl ? ((unsigned long long)gx << 32)
-                                                 : (1ull << kp) + rank);
-                    else if (PHASE == 1 && !fl)
-                        atomicAdd(&acc[cell], kOne + rank);
-                    else if (PHASE == 2 && fl)
-                        atomicAdd(&acc[cell], (unsigned long long)gx);
-                    if (PHASE != 2 && fl && j == 0u) e0++;
-                    rank++;
+                    atomicAdd(&acc[cell], PHASE == 0 ? (unsigned long long)gx << 32
+                                                     : (unsigned long long)gx);
+                } else if (PHASE == 0) {
+                    atomicAdd(&acc[cell], (1ull << kp) + rank);
                 }
+                if (PHASE != 2 && fl && j == 0u) e0++;
+                rank++;
             }
         }
     }
@@ -996,39 +1036,28 @@ __device__ __forceinline__ void sub_live_batches(const Round0Args& r, bool live,
 
 template <int C, int PHASE>
 __device__ void round0_row(const Round0Args& r, uint32_t row, unsigned long long* acc,
-                           uint32_t kp, uint32_t nsup, uint32_t& e0) {
+                           uint32_t* win, uint32_t kp, uint32_t nsup, uint32_t& e0) {
     const CounterArgs& a = r.c;
     const uint32_t lane = lane_id();
     // a wave's LDS operations complete in order: the previous row's reads are
     // done before these stores
-    for (uint32_t k = lane; k < (uint32_t)C; k += 64) {
-        const uint32_t y = PHASE == 1 ? 0u : (uint32_t)r.y_agg[(uint64_t)row * C + k];
-        acc[k] = PHASE == 0 ? (unsigned long long)y << 32 : (unsigned long long)y;
-    }
+    constexpr uint32_t CPL = C / 64;
+    uint32_t y[CPL];
+#pragma unroll
+    for (uint32_t i = 0; i < CPL; i++)
+        y[i] = PHASE == 1 ? 0u : (uint32_t)r.y_agg[(uint64_t)row * C + lane + 64u * i];
+#pragma unroll
+    for (uint32_t i = 0; i < CPL; i++)
+        acc[lane + 64u * i] = PHASE == 0 ? (unsigned long long)y[i] << 32 : (unsigned long long)y[i];
     const uint32_t r0 = a.rowoff[row], r1 = a.rowoff[row + 1];
     for (uint32_t cs = r0; cs < r1; cs += 64u * kScreen) {
         uint32_t bidx[kScreen], ey[kScreen], boff[kScreen];
         bool live[kScreen];
-#pragma unroll
-        for (uint32_t h = 0; h < kScreen; h++) {
-            const uint32_t e = cs + 64u * h + lane;
-            uint2 ent = make_uint2(0xffffffffu, 0u);
-            if (e < r1) ent = a.entry[e];
-            bidx[h] = ent.x;
-            ey[h] = ent.y;
-        }
-#pragma unroll
-        for (uint32_t h = 0; h < kScreen; h++) {
-            boff[h] = 0;
-            live[h] = false;
-            if (bidx[h] < a.nb) {
-                boff[h] = a.woffb[bidx[h]];
-                live[h] = a.woffb[bidx[h] + 1] != boff[h];
-            }
-        }
+        screen_entries(a, cs, r1, bidx, ey, boff, live);
 #pragma unroll
         for (uint32_t h = 0; h < kScreen; h++)
-            sub_live_batches<C, PHASE>(r, live[h], bidx[h], ey[h], boff[h], acc, kp, nsup, e0);
+            sub_live_batches<C, PHASE>(r, live[h], bidx[h], ey[h], boff[h], acc, win, kp, nsup,
+                                       e0);
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // every lane's LDS adds have landed
     __builtin_amdgcn_wave_barrier();
@@ -1074,7 +1103,11 @@ __device__ void round0_write_row(const Round0Args& r, uint32_t row,
 template <int C>
 __global__ __launch_bounds__(kBlock) void round0_rows_kernel(Round0Args r) {
     constexpr uint32_t kWaves = kBlock / 64;
+    // per wave: the row's counters, and the window of kR0Unroll * 64 * 4
+    // values and as many flag bytes (sub_live_batches)
+    constexpr uint32_t kWinWords = kR0Unroll * 64 * 4 + kR0Unroll * 64;
     __shared__ unsigned long long s_acc[kWaves * C];
+    __shared__ uint32_t s_win[kWaves * kWinWords];
     __shared__ uint32_t s_red;
     const CounterArgs& a = r.c;
     Ctrl* ctrl = a.ctrl;
@@ -1087,16 +1120,17 @@ __global__ __launch_bounds__(kBlock) void round0_rows_kernel(Round0Args r) {
     const uint32_t lane = lane_id();
     const uint32_t wave = uniform(threadIdx.x >> 6);
     unsigned long long* const acc = s_acc + wave * C;
+    uint32_t* const win = s_win + wave * kWinWords;
     const uint32_t nwaves = gridDim.x * kWaves;
     uint32_t e0 = 0;
     for (uint32_t row = blockIdx.x * kWaves + wave; row < a.rows; row += nwaves) {
         if (packed) {
-            round0_row<C, 0>(r, row, acc, kp, nsup, e0);
+            round0_row<C, 0>(r, row, acc, win, kp, nsup, e0);
             round0_write_row<C>(r, row, acc, true, kp);
         } else {
-            round0_row<C, 1>(r, row, acc, kp, nsup, e0);
+            round0_row<C, 1>(r, row, acc, win, kp, nsup, e0);
             round0_write_row<C>(r, row, acc, false, kp);
-            round0_row<C, 2>(r, row, acc, kp, nsup, e0);
+            round0_row<C, 2>(r, row, acc, win, kp, nsup, e0);
             for (uint32_t k = lane; k < (uint32_t)C; k += 64)
                 r.yw[(uint64_t)row * C + k] = (int32_t)(uint32_t)acc[k];
         }
