@@ -184,3 +184,45 @@ def test_fullsize_blocked(name, vtype):
         uniq, sums = sparse_direct_sum(w)
         assert np.array_equal(g["x"][uniq], sums)
         assert np.count_nonzero(g["x"]) == np.count_nonzero(sums)
+
+
+def test_round0_by_rows_with_unpackable_counters():
+    # A sketch of 16 M cells (16,384 rows, wide enough for round 0 by rows)
+    # over 33.6 M elements (positions take 26 bits) with one cell of at least
+    # 77 elements: every batch that hashes into the busiest row gets a nonzero
+    # at the offset that lands on that row's cell 0.  That cell's
+    # deg * 2^26 + (sum of positions) does not fit 32 bits, so the int32 peel
+    # keeps counters and residuals apart, and round 0 by rows takes its
+    # unpacked path.  The sketch is half the support: round 0 recovers the
+    # elements with a pure cell, a few rounds follow, the rest get median
+    # estimates.  Exact against the oracle.
+    _hc()
+    n, rows = 1 << 28, 16384
+    w = wl.make("synthetic", n=n, W=1, density=0.13, data_seed=515)
+    g = oracle.Geom(n=n, rows=rows, seed=w.hash_seed, c=1024)
+    nb = n // 1024
+    cl, _ = oracle.cells(g, np.arange(nb, dtype=np.uint64) * 1024)
+    r = (cl // 1024).astype(np.int64)
+    bias = (cl % 1024).astype(np.int64)
+    busiest = int(np.argmax(np.bincount(r.reshape(-1), minlength=rows)))
+    bb, jj = np.nonzero(r == busiest)
+    hot = (bb.astype(np.int64) * 1024 + ((0 - bias[bb, jj]) & 1023)).astype(np.uint32)
+    idx = np.union1d(w.idx[0], hot).astype(np.uint32)
+    vals = np.ones(idx.size, np.int32)
+    pos = np.searchsorted(w.idx[0], idx)
+    old = (pos < w.idx[0].size) & (w.idx[0][np.minimum(pos, w.idx[0].size - 1)] == idx)
+    vals[old] = w.val[0][pos[old]]
+    w.idx, w.val = [idx], [vals]
+    kp = int(np.ceil(np.log2(idx.size)))
+    hot_pos = np.searchsorted(idx, hot)
+    assert hot.size * 2**kp + int(hot_pos.sum()) >= 2**32  # the busy cell cannot pack
+    assert rows * 1024 >= 8 << 20  # large enough for round 0 by rows
+    print(f"[round0 rows unpacked] n={n} nonzeros={idx.size} rows={rows} hot={hot.size}",
+          flush=True)
+    gr = gpu_run(w, rows, 1024, want_coo_out=False, use_plan=True, max_support=idx.size)
+    o = oracle_run(w, rows, 1024)
+    assert np.array_equal(gr["Ya"], o["Ya"])
+    assert np.array_equal(gr["x"], o["x"])
+    assert np.array_equal(gr["mask"], o["mask"])
+    assert_same_info(gr["info"], o["info"])
+    assert 0 < gr["info"].n_recovered < idx.size
