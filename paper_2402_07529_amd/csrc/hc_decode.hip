@@ -1210,22 +1210,34 @@ __device__ __forceinline__ void peel_entry(const PeelArgs<T>& a, uint32_t cidx, 
     // elements share a word but rarely meet in time
     unsigned int* const fword = reinterpret_cast<unsigned int*>(a.peeled + (pos & ~3u));
     const uint32_t fbit = 1u << (8u * (pos & 3u));
+    // the cell's residual first: a frontier cell holds one element, so no
+    // other entry changes it this round (and with this load ahead of the
+    // claim the two versions of this function share no leading code, which
+    // the compiler had hoisted above their differing loads)
+    unsigned long long wcell = 0;
+    T ycell = T(0);
+    if (PACKED) wcell = a.cnt[cidx];
+    else ycell = a.yw[cidx];
     bool taken;
     if (kMarks)
         taken = (__hip_atomic_load(fword, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & fbit) != 0u;
     else
         taken = (atomicOr(fword, fbit) & fbit) != 0u;
     const uint32_t p = a.elem[pos];
-    unsigned long long wcell = 0;
-    T ycell = T(0);
-    if (PACKED) wcell = a.cnt[cidx];
-    else ycell = a.yw[cidx];
     const BatchHash h = batch_hash(a.seed, a.rows, a.cmask, p >> a.log2c);
     const uint32_t t = p & a.cmask;
     uint32_t cl[3];
 #pragma unroll
     for (int j = 0; j < 3; j++) cl[j] = cell_of(h, j, t, a.c, a.cmask);
     const int j = cl[0] == cidx ? 0 : (cl[1] == cidx ? 1 : 2);
+    // the cell's load stays beside the claim's and the element's: otherwise
+    // the compiler sinks it past the test below, a memory latency later
+    if (PACKED) {
+        const uint32_t hi = (uint32_t)(wcell >> 32);
+        asm volatile("" : : "v"(hi));
+    } else {
+        asm volatile("" : : "v"(ycell));
+    }
     if (taken || cl[j] != cidx) return;
     if (kMarks) {
         for (int jj = 0; jj < j; jj++)
@@ -1642,6 +1654,7 @@ struct EmitArgs {  // T: the gradient type; values are kept in Acc<T>
     uint32_t rows, c, cmask, log2c, last_mask;
     bool x_vec;     // x_out is 16-byte aligned
     bool mask_vec;  // mask is 16-byte aligned
+    bool b_vec;     // b is 16-byte aligned
 };
 
 template <typename T>
@@ -1679,12 +1692,9 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
     const uint32_t wave = threadIdx.x >> 6;
     const uint64_t chunk = blockIdx.x;
     const uint64_t w0 = chunk * kChunkWords + 4ull * threadIdx.x;
-    uint32_t w4[4], mine = 0;
-#pragma unroll
-    for (int k = 0; k < 4; k++) {
-        w4[k] = load_word(a.b, w0 + k, a.words, a.last_mask);
-        mine += __popc(w4[k]);
-    }
+    const uint4 wv = load_words4(a.b, w0, a.words, a.last_mask, a.b_vec);
+    const uint32_t w4[4] = {wv.x, wv.y, wv.z, wv.w};
+    const uint32_t mine = __popc(wv.x) + __popc(wv.y) + __popc(wv.z) + __popc(wv.w);
     uint32_t total;
     uint32_t run = block_exclusive_scan(mine, s_tmp, &total);
 #pragma unroll
@@ -1712,10 +1722,28 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
             if (r1 > whi) {
                 wlo = s_pref[wf];
                 whi = wlo + kEmitStage < total ? wlo + kEmitStage : total;
+                // the window's loads all in flight together, at indexes
+                // clamped to its last member (a reload happens only for an
+                // iteration with members, so the window is never empty)
+                constexpr uint32_t kPer = kEmitStage / kBlock;
+                typename Acc<T>::type v[kPer];
+                uint32_t f[kPer];  // not bytes: packing bytes waited for each load
+                const uint32_t last = whi > wlo ? whi - 1u : wlo;
+#pragma unroll
+                for (uint32_t q = 0; q < kPer; q++) {
+                    const uint32_t i = wlo + threadIdx.x + q * kBlock;
+                    const uint64_t src = off + (i < whi ? i : last);
+                    v[q] = a.vals[src];
+                    f[q] = a.peeled[src];
+                }
                 lds_barrier();  // every lane is done with the previous window
-                for (uint32_t i = wlo + threadIdx.x; i < whi; i += kBlock) {
-                    s_val[i - wlo] = (T)a.vals[off + i];
-                    s_rec[i - wlo] = a.peeled[off + i] != 0u ? 1 : 0;
+#pragma unroll
+                for (uint32_t q = 0; q < kPer; q++) {
+                    const uint32_t i = wlo + threadIdx.x + q * kBlock;
+                    if (i < whi) {
+                        s_val[i - wlo] = (T)v[q];
+                        s_rec[i - wlo] = f[q] != 0u ? 1 : 0;
+                    }
                 }
                 lds_barrier();
             }
@@ -2072,6 +2100,7 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
         ea.last_mask = last_mask;
         ea.x_vec = (reinterpret_cast<uintptr_t>(out.x_out) & 15u) == 0;
         ea.mask_vec = (reinterpret_cast<uintptr_t>(out.mask) & 15u) == 0;
+        ea.b_vec = bvec;
         hipLaunchKernelGGL(emit_kernel<T>, dim3((uint32_t)L.nchunks), dim3(kBlock), 0, s, ea);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
