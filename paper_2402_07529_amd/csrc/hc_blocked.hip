@@ -152,6 +152,18 @@ __device__ __forceinline__ uint32_t load_bword(const uint32_t* b, uint64_t k, ui
     return k == words - 1 ? (w & last_mask) : w;
 }
 
+// The same when ok, else 0, with no branch (words >= 1): the load is issued
+// at a clamped index and the word masked after it.  A load under a branch was
+// followed, inside the branch, by the masking that used it, so the compiler
+// waited for a lane's loads one by one instead of keeping kAhead in flight.
+__device__ __forceinline__ uint32_t load_bword_nb(const uint32_t* b, uint64_t k, bool ok,
+                                                  uint64_t words, uint32_t last_mask) {
+    const bool in = ok && k < words;
+    const uint32_t w = b[in ? k : 0];
+    const uint32_t mask = in ? (k == words - 1 ? last_mask : 0xffffffffu) : 0u;
+    return w & mask;
+}
+
 // ---- encode ------------------------------------------------------------------
 
 template <typename T>
@@ -485,7 +497,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
 #pragma unroll
         for (int u = 0; u < kAhead; u++) {
             const uint64_t wi = w0 + 64ull * (ga + u) + lane;
-            wv[u] = (ga + u < g_hi && wi < w1) ? load_bword(a.b, wi, a.words, a.last_mask) : 0u;
+            wv[u] = load_bword_nb(a.b, wi, ga + u < g_hi && wi < w1, a.words, a.last_mask);
         }
 #pragma unroll
         for (int u = 0; u < kAhead; u++) {
@@ -652,7 +664,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
 #pragma unroll
         for (int u = 0; u < kAhead; u++) {
             const uint64_t wi2 = w0 + 64ull * (ga + u) + lane;
-            wv[u] = (ga + u < g_hi && wi2 < w1) ? load_bword(a.b, wi2, a.words, a.last_mask) : 0u;
+            wv[u] = load_bword_nb(a.b, wi2, ga + u < g_hi && wi2 < w1, a.words, a.last_mask);
         }
 #pragma unroll
         for (int u = 0; u < kAhead; u++) {
