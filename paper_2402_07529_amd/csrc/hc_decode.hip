@@ -931,7 +931,10 @@ __global__ __launch_bounds__(kBlock) void pure_rows_kernel(Round0Args r) {
 // kWin values, then as many of kWin flag bytes); members past that read
 // memory.  Counts into e0 the flagged members met through their hash j = 0:
 // each element once.
-constexpr uint32_t kR0Unroll = 2;  // wave-wide bitmap loads in flight per round0_rows wave
+// wave-wide bitmap loads in flight per round0_rows wave: with two, the larger
+// LDS window left three workgroups per CU instead of four, and VGG19's pass
+// took 20 us longer
+constexpr uint32_t kR0Unroll = 1;
 
 template <int C, int PHASE>
 __device__ __forceinline__ void sub_live_batches(const Round0Args& r, bool live, uint32_t bidx,
