@@ -2,10 +2,11 @@
 // Algorithm 1, run on one GPU in place of the switch / AllReduce:
 // Y <- sum over workers of Y_w, B <- OR over workers of B_w (section 3).
 //
-// A pure HBM stream: every lane reads 16 bytes (one vector of 4 elements,
-// two of 2 or four single ones, as the buffers' alignment allows) from each
-// of the W inputs (all loads in flight together, nontemporal since each is
-// read once) and writes them out.  int32 sums wrap modulo 2^32, like a
+// A pure HBM stream: every lane reads 16 bytes from each of the W inputs
+// (nontemporal, since each is read once) and writes the result out.  With
+// 16-byte aligned buffers the 16 bytes are one aligned vector also when the
+// per-worker count is not a multiple of four (the words are realigned across
+// lanes); other buffers take two vectors of 2 or four single elements.  int32 sums wrap modulo 2^32, like a
 // switch's integer adders; fp32 adds in worker order 0..W-1 so the result
 // does not depend on scheduling.
 #include "hc_device.h"
@@ -49,8 +50,9 @@ template <typename OP> struct VecOf<OP, 1> { typedef typename OP::S type; };
 // elements, so every worker's vectors are aligned).  Each lane takes 16 bytes
 // per worker per pass: one vector of 4, two of 2, or four single elements,
 // spaced a grid apart so that each wave-wide load stays contiguous; all W of
-// a lane's loads are in flight together.  VGG19-sized bitmaps have an even
-// word count that is not a multiple of four, so they take the pairs.
+// a lane's loads are in flight together.  Used for 16-byte aligned buffers
+// whose count is a multiple of four (VW = 4) and for buffers that are not
+// 16-byte aligned (VW = 2 or 1).
 template <typename OP, int VW>
 __global__ __launch_bounds__(kBlock) void reduce_workers_kernel(
     const typename OP::S* __restrict__ in, typename OP::S* __restrict__ out, uint64_t count,
@@ -80,6 +82,69 @@ __global__ __launch_bounds__(kBlock) void reduce_workers_kernel(
     }
 }
 
+// The same for a per-worker count that is not a multiple of four (16-byte
+// aligned in and out): worker w then starts (w * count) mod 4 words past a
+// 16-byte boundary.  Each lane still loads one aligned 16-byte chunk per
+// worker, the one holding the first word of its output vector; the words
+// past that chunk's end are the first words of the next lane's chunk, taken
+// by a shuffle, or, for the wave's last lane and the last vector, loaded
+// word by word.  Four workers' chunks are loaded before any is shuffled.
+// Blocks loop while any lane of the wave has work (the shuffles need every
+// lane); block 0 also writes the count mod 4 tail words.
+template <typename OP>
+__global__ __launch_bounds__(kBlock) void reduce_workers_shift_kernel(
+    const typename OP::S* __restrict__ in, typename OP::S* __restrict__ out, uint64_t count,
+    uint32_t W) {
+    typedef typename OP::S S;
+    typedef typename OP::V V;
+    const uint64_t nvec = count / 4;
+    const uint64_t step = (uint64_t)gridDim.x * kBlock;
+    const uint32_t lane = lane_id();
+    const V* vin = reinterpret_cast<const V*>(in);
+    for (uint64_t i0 = (uint64_t)blockIdx.x * kBlock + (threadIdx.x & ~63u); i0 < nvec;
+         i0 += step) {
+        const uint64_t i = i0 + lane;
+        const bool live = i < nvec;
+        const bool own = live && (lane == 63u || i + 1 >= nvec);
+        V acc = {};
+        for (uint32_t w0 = 0; w0 < W; w0 += 4) {
+            V L[4];
+#pragma unroll
+            for (uint32_t u = 0; u < 4; u++) {
+                const uint64_t wb = (uint64_t)(w0 + u) * count;
+                L[u] = (w0 + u < W && live) ? __builtin_nontemporal_load(vin + (wb >> 2) + i) : V{};
+            }
+#pragma unroll
+            for (uint32_t u = 0; u < 4; u++) {
+                if (w0 + u >= W) break;
+                const uint64_t wb = (uint64_t)(w0 + u) * count;
+                const uint32_t m = (uint32_t)(wb & 3u);
+                S n0 = __shfl_down(L[u].x, 1), n1 = __shfl_down(L[u].y, 1),
+                  n2 = __shfl_down(L[u].z, 1);
+                if (own && m != 0u) {
+                    const S* p = in + wb + 4 * i + 4 - m;  // words wb + 4i + 4 - m .. wb + 4i + 3
+                    n0 = p[0];
+                    n1 = m >= 2u ? p[1] : S(0);
+                    n2 = m >= 3u ? p[2] : S(0);
+                }
+                const V v = m == 0u   ? L[u]
+                            : m == 1u ? V{L[u].y, L[u].z, L[u].w, n0}
+                            : m == 2u ? V{L[u].z, L[u].w, n0, n1}
+                                      : V{L[u].w, n0, n1, n2};
+                acc = (w0 + u == 0) ? v : OP::op(acc, v);
+            }
+        }
+        if (live) reinterpret_cast<V*>(out)[i] = acc;
+    }
+    if (blockIdx.x == 0) {
+        for (uint64_t k = 4 * nvec + threadIdx.x; k < count; k += kBlock) {
+            S a = in[k];
+            for (uint32_t w = 1; w < W; w++) a = OP::op(a, in[(uint64_t)w * count + k]);
+            out[k] = a;
+        }
+    }
+}
+
 template <typename OP>
 hipError_t launch_reduce(const void* in, void* out, uint64_t count, uint32_t W, int cus,
                          hipStream_t s) {
@@ -94,7 +159,14 @@ hipError_t launch_reduce(const void* in, void* out, uint64_t count, uint32_t W, 
     if (grid < 1) grid = 1;
     const S* src = static_cast<const S*>(in);
     S* dst = static_cast<S*>(out);
-    if (vw == 4)
+    if (vw != 4 && (al & 15u) == 0 && count >= 4) {
+        // worker strides off the 16-byte grid: aligned loads, shifted by shuffles
+        const uint64_t nvec = count / 4;
+        uint64_t g2 = (nvec + kBlock - 1) / kBlock;
+        if (g2 > cap) g2 = cap;
+        hipLaunchKernelGGL((reduce_workers_shift_kernel<OP>), dim3((uint32_t)g2), dim3(kBlock), 0,
+                           s, src, dst, count, W);
+    } else if (vw == 4)
         hipLaunchKernelGGL((reduce_workers_kernel<OP, 4>), dim3((uint32_t)grid), dim3(kBlock), 0, s,
                            src, dst, count, count, W);
     else if (vw == 2)

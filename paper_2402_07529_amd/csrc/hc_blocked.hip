@@ -176,43 +176,43 @@ struct EncArgs {
     uint32_t stage_b;  // the block's bitmap words go through LDS (the kernel's SB)
 };
 
-// PF = false: two workgroups (blocks) per CU, i.e. eight waves per SIMD (the
-// launch bound's second argument) and so at most 64 VGPRs, one tile in flight
-// per wave; one block's setup and sketch write-back then overlap the other's
-// gradient stream.  PF = true: one block per CU, each wave prefetching its next
-// tile while it encodes the current one.  Measured on MI355X, the first is
-// about 10 % faster when there are more than two blocks per CU to run (BERT-base
-// and VGG19 at 1 % density, about 990 blocks), the second 10-25 % faster with
-// fewer (LSTM, 497 blocks; sparse BERT-base, 105).  SB: the block's bitmap
-// words are staged in LDS and written after the stream.  As a compile-time
-// choice it leaves no global store in the streaming loop, so the compiler can
-// count the loads in flight exactly: with SB a runtime flag, the prefetching
-// loop waited for the next tile's loads too (vmcnt(0)) before encoding the
-// current one.  BERT-base at 5 % went from 0.217 to 0.208 ms per encode.
-template <typename T, bool PF, bool SB>
-__global__ __launch_bounds__(kEncThreads, PF ? 4 : 8) void encode_blocked_kernel(EncArgs<T> a) {
+// NT threads per workgroup (one block each), D tiles of the gradient in
+// flight per wave (D = 1: load, then encode; D >= 2: a rolling pipeline whose
+// loads for tile t + (D - 1) waves are issued before tile t is encoded), WPE
+// waves per SIMD (the launch bound: 4 leaves 128 VGPRs, 8 leaves 64).  SB: the
+// block's bitmap words are staged in LDS and written after the stream.  As a
+// compile-time choice it leaves no global store in the streaming loop, so the
+// compiler can count the loads in flight exactly: with SB a runtime flag, the
+// prefetching loop waited for the next tile's loads too (vmcnt(0)) before
+// encoding the current one.  BERT-base at 5 % went from 0.217 to 0.208 ms per
+// encode.
+template <typename T, int NT, int D, int WPE, bool SB>
+__global__ __launch_bounds__(NT, WPE) void encode_blocked_kernel(EncArgs<T> a) {
     extern __shared__ __align__(16) unsigned char lds_raw[];
     T* s_y = reinterpret_cast<T*>(lds_raw);
     uint32_t* s_tab = reinterpret_cast<uint32_t*>(lds_raw + (size_t)a.bcells * sizeof(T));
     uint32_t* s_bm = s_tab + ((3 * a.block + 3) & ~3u);  // staged bitmap words (16-byte aligned)
     const uint32_t q = blockIdx.x;
     const BlockRange r = block_range(q, a.block, a.log2c, a.cmask, a.n);
-    for (uint32_t i = threadIdx.x; i < a.bcells; i += kEncThreads) s_y[i] = T(0);
+    for (uint32_t i = threadIdx.x; i < a.bcells; i += NT) s_y[i] = T(0);
     fill_table(s_tab, r, a.seed, a.brows, a.c, a.cmask, a.log2c, a.block);
     lds_barrier();
 
     const uint32_t lane = lane_id();
     const uint32_t wave = uniform(threadIdx.x >> 6);
     const uint32_t ntiles = (uint32_t)((r.p1 - r.p0 + kWaveTile - 1) / kWaveTile);
-    constexpr uint32_t kWaves = kEncThreads / 64;
+    constexpr uint32_t kWaves = NT / 64;
     typedef T V4 __attribute__((ext_vector_type(4)));
+    const uint32_t nfull = a.x_vec ? (uint32_t)((r.p1 - r.p0) / kWaveTile) : 0u;
     // A tile is read as four 16-byte loads per lane: e[l][k] = parameter
     // tp + 256 l + 4 lane + k.  Tiles wholly inside the block (and a 16-byte
     // aligned gradient) take vector loads through one buffer resource over the
-    // block's gradient (at most 4 MiB; the tile's offset is scalar, the lane's
-    // fixed); the block's last, partial tile reads element by element, zero
-    // past the block's end.
-    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(a.x + r.p0, (uint32_t)((r.p1 - r.p0) * sizeof(T)));
+    // block's full tiles (at most 4 MiB; the tile's offset is scalar, the
+    // lane's fixed).  A load past the full tiles lies outside the resource and
+    // returns zeros without touching memory, so the pipeline issues its loads
+    // unconditionally.  The block's last, partial tile reads element by
+    // element, zero past the block's end.
+    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(a.x + r.p0, nfull * (uint32_t)(kWaveTile * sizeof(T)));
     auto load_full = [&](uint32_t tile, T (&e)[4][4]) {
 #pragma unroll
         for (int l = 0; l < 4; l++) {
@@ -290,41 +290,34 @@ __global__ __launch_bounds__(kEncThreads, PF ? 4 : 8) void encode_blocked_kernel
             }
         }
     };
-    const uint32_t nfull = a.x_vec ? (uint32_t)((r.p1 - r.p0) / kWaveTile) : 0u;
-    T ea[4][4];
-    if (!PF) {
+    T e[D][4][4];
+    if constexpr (D == 1) {
         for (uint32_t tile = wave; tile < nfull; tile += kWaves) {
-            load_full(tile, ea);
-            encode_tile(tile, ea);
+            load_full(tile, e[0]);
+            encode_tile(tile, e[0]);
         }
     } else {
-        // rolling pipeline: the next tile's loads are issued before the
-        // current tile is encoded (never conditionally on their own)
-        T eb[4][4];
+        // rolling pipeline over D register tiles: the loads of tile
+        // t + (D - 1) waves are issued before tile t is encoded, every
+        // iteration, so the wait before an encode counts exactly the
+        // (D - 1) groups issued after its own
+#pragma unroll
+        for (int k = 0; k + 1 < D; k++) load_full(wave + (uint32_t)k * kWaves, e[k]);
         uint32_t tile = wave;
-        if (tile < nfull) {
-            load_full(tile, ea);
-            for (;;) {
-                if (tile + kWaves >= nfull) {
-                    encode_tile(tile, ea);
-                    break;
-                }
-                load_full(tile + kWaves, eb);
-                encode_tile(tile, ea);
-                tile += kWaves;
-                if (tile + kWaves >= nfull) {
-                    encode_tile(tile, eb);
-                    break;
-                }
-                load_full(tile + kWaves, ea);
-                encode_tile(tile, eb);
+        for (;;) {
+#pragma unroll
+            for (int k = 0; k < D; k++) {
+                if (tile >= nfull) goto streamed;
+                load_full(tile + (uint32_t)(D - 1) * kWaves, e[(k + D - 1) % D]);
+                encode_tile(tile, e[k]);
                 tile += kWaves;
             }
         }
+    streamed:;
     }
     for (uint32_t tile = nfull + wave; tile < ntiles; tile += kWaves) {
-        load_part(tile, ea);
-        encode_tile(tile, ea);
+        load_part(tile, e[0]);
+        encode_tile(tile, e[0]);
     }
     lds_barrier();
 
@@ -336,23 +329,23 @@ __global__ __launch_bounds__(kEncThreads, PF ? 4 : 8) void encode_blocked_kernel
         uint32_t* bb = a.b + (r.p0 >> 5);
         if (((reinterpret_cast<uintptr_t>(bb) & 15u) == 0)) {
             const uint32_t nv = nw / 4;
-            for (uint32_t i = threadIdx.x; i < nv; i += kEncThreads)
+            for (uint32_t i = threadIdx.x; i < nv; i += NT)
                 reinterpret_cast<v4u32*>(bb)[i] = reinterpret_cast<const v4u32*>(s_bm)[i];
-            for (uint32_t i = 4 * nv + threadIdx.x; i < nw; i += kEncThreads) bb[i] = s_bm[i];
+            for (uint32_t i = 4 * nv + threadIdx.x; i < nw; i += NT) bb[i] = s_bm[i];
         } else {
-            for (uint32_t i = threadIdx.x; i < nw; i += kEncThreads) bb[i] = s_bm[i];
+            for (uint32_t i = threadIdx.x; i < nw; i += NT) bb[i] = s_bm[i];
         }
     }
 
     T* yb = a.y + (uint64_t)q * a.bcells;
     if (a.y_vec) {
         typedef T V4 __attribute__((ext_vector_type(4)));
-        for (uint32_t i = 4u * threadIdx.x; i < a.bcells; i += 4u * kEncThreads) {
+        for (uint32_t i = 4u * threadIdx.x; i < a.bcells; i += 4u * NT) {
             const V4 v = {s_y[i], s_y[i + 1], s_y[i + 2], s_y[i + 3]};
             __builtin_nontemporal_store(v, reinterpret_cast<V4*>(yb + i));
         }
     } else {
-        for (uint32_t i = threadIdx.x; i < a.bcells; i += kEncThreads) yb[i] = s_y[i];
+        for (uint32_t i = threadIdx.x; i < a.bcells; i += NT) yb[i] = s_y[i];
     }
 }
 
@@ -831,18 +824,29 @@ hipError_t launch_encode_blocked_t(const Geo& g, const void* x, void* y, uint32_
     // the variants as compile-time choices: with the bitmap staged in LDS the
     // streaming loop issues no global stores, so the compiler's load waits
     // count exactly the loads it has in flight
-    auto launch = [&](auto kernel) -> hipError_t {
+    auto launch = [&](auto kernel, int nt) -> hipError_t {
         hipError_t err = allow_lds(kernel);
         if (err != hipSuccess) return err;
-        hipLaunchKernelGGL(kernel, dim3(g.nblocks), dim3(kEncThreads), a.stage_b ? staged : lds,
-                           s, a);
+        hipLaunchKernelGGL(kernel, dim3(g.nblocks), dim3(nt), a.stage_b ? staged : lds, s, a);
         return hipGetLastError();
     };
-    if (pf)
-        return a.stage_b ? launch(&encode_blocked_kernel<T, true, true>)
-                         : launch(&encode_blocked_kernel<T, true, false>);
-    return a.stage_b ? launch(&encode_blocked_kernel<T, false, true>)
-                     : launch(&encode_blocked_kernel<T, false, false>);
+    // Variants measured on MI355X (blocked encode per call; int32 at 1 %):
+    // 512 lanes with a two-tile pipeline, two blocks per CU: BERT-base 0.098
+    // -> 0.094 ms, VGG19 0.127 -> 0.121 ms, LSTM 0.093 -> 0.088 ms against
+    // the best of the 1024-lane ones.  Deeper pipelines (three or four tiles)
+    // and 256-lane workgroups were slower.  fp32 (LDS float atomics, whose
+    // latency more waves hide better) and blocks too large for two per CU
+    // (BERT-base at 5 %) keep 1024 lanes: one tile per wave when there are
+    // more than two blocks per CU to run, else a two-tile pipeline.
+    const size_t lds_used = a.stage_b ? staged : lds;
+    const bool two_per_cu = lds_used + kLdsReserve <= kLdsBytes / 2;
+#define HC_ENC_SEL(NT, D, WPE)                                                       \
+    return a.stage_b ? launch(&encode_blocked_kernel<T, NT, D, WPE, true>, NT)      \
+                     : launch(&encode_blocked_kernel<T, NT, D, WPE, false>, NT)
+    if (!g.f32 && two_per_cu) HC_ENC_SEL(512, 2, 4);
+    if (pf) HC_ENC_SEL(1024, 2, 4);
+    HC_ENC_SEL(1024, 1, 8);
+#undef HC_ENC_SEL
 }
 
 template <typename T>

@@ -463,3 +463,45 @@ def test_aggregate_every_vector_width(n, offset):
     assert np.array_equal(Yo[offset:].cpu().numpy(), wrap_sum(list(Yh)))
     assert np.array_equal(Bo[offset:].cpu().numpy().view(np.uint32),
                           np.bitwise_or.reduce(Bh, axis=0))
+
+
+@pytest.mark.parametrize("W", [1, 3, 5, 8, 16])
+@pytest.mark.parametrize("vtype", ["i32", "f32"])
+def test_aggregate_worker_counts_and_strides(W, vtype):
+    # per-worker counts of every residue mod 4 (so worker w starts (w * count)
+    # mod 4 words off the 16-byte grid), worker counts that leave a partial
+    # group of four, and a bitmap long enough for several passes of the
+    # whole grid: sums (fp32 in worker order) and ORs stay exact
+    import torch
+    hc = _hc()
+    dev = torch.device("cuda")
+    cases = [(4097 * 32 + 7, 4097), (4098 * 32, 4098), (4099 * 32 + 31, 4099), (4100 * 32, 4100)]
+    if W == 8 and vtype == "i32":
+        cases.append(((5 * 2**20 + 3) * 32, 5))  # 5 M + 3 bitmap words per worker
+    for n, rows in cases:
+        p = hc.make_params(n, rows, 23, c=1, vtype=vtype)
+        rng = np.random.default_rng(n * 31 + W)
+        if vtype == "i32":
+            Yh = rng.integers(-2**31, 2**31, (W, p.cells), dtype=np.int64).astype(np.int32)
+            want_y = wrap_sum(list(Yh))
+            tdt = torch.int32
+        else:
+            Yh = rng.standard_normal((W, p.cells)).astype(np.float32)
+            want_y = Yh[0].copy()
+            for w in range(1, W):
+                want_y = (want_y + Yh[w]).astype(np.float32)
+            tdt = torch.float32
+        Bh = rng.integers(0, 2**32, (W, p.words), dtype=np.uint64).astype(np.uint32)
+        Y = torch.from_numpy(Yh).to(dev)
+        B = torch.from_numpy(Bh.view(np.int32)).to(dev)
+        Yo = torch.empty(p.cells, dtype=tdt, device=dev)
+        Bo = torch.empty(p.words, dtype=torch.int32, device=dev)
+        print(f"[aggregate] W={W} {vtype} n={n} cells={p.cells} words={p.words}", flush=True)
+        hc.hc_aggregate(p, Y, B, W, Yo, Bo)
+        torch.cuda.synchronize()
+        got_y = Yo.cpu().numpy()
+        if vtype == "i32":
+            assert np.array_equal(got_y, want_y)
+        else:
+            assert np.array_equal(got_y.view(np.uint32), want_y.view(np.uint32))
+        assert np.array_equal(Bo.cpu().numpy().view(np.uint32), np.bitwise_or.reduce(Bh, axis=0))
