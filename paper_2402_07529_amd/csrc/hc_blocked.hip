@@ -235,30 +235,23 @@ __global__ __launch_bounds__(NT, WPE) void encode_blocked_kernel(EncArgs<T> a) {
     };
     auto encode_tile = [&](uint32_t tile, const T (&e)[4][4]) {
         const uint64_t tp = r.p0 + (uint64_t)tile * kWaveTile;
-        uint64_t m[4][4];
-#pragma unroll
-        for (int l = 0; l < 4; l++)
-#pragma unroll
-            for (int k = 0; k < 4; k++) m[l][k] = __ballot(Val<T>::nonzero(e[l][k]));
         // bitmap word w = 8 l + i holds parameters 32 w .. 32 w + 31: lanes
-        // 8i .. 8i+7 of load l, parameter 4 lane' + k at bit 4 (lane' - 8 i) + k
-        if (lane < 32 && tp + 32ull * lane < r.p1) {
-            const uint32_t l = lane >> 3, sh = 8u * (lane & 7u);
-            uint32_t word = 0;
-#pragma unroll
-            for (int k = 0; k < 4; k++) {
-                const uint64_t mk = l == 0 ? m[0][k] : l == 1 ? m[1][k] : l == 2 ? m[2][k] : m[3][k];
-                word |= spread4((uint32_t)(mk >> sh)) << k;
-            }
-            if (SB)
-                s_bm[((tp - r.p0) >> 5) + lane] = word;
-            else
-                a.b[(tp >> 5) + lane] = word;
-        }
-        // sketch: three LDS atomics per nonzero
+        // 8i .. 8i+7 of load l, parameter 4 lane' + k at bit 4 (lane' - 8 i) + k.
+        // Load by load, so that only one load's four ballots are live (all
+        // sixteen at once made the one-tile kernel at 64 VGPRs spill).
+        uint32_t word = 0;
+        const uint32_t sh = 8u * (lane & 7u);
 #pragma unroll
         for (int l = 0; l < 4; l++) {
-            if ((m[l][0] | m[l][1] | m[l][2] | m[l][3]) == 0ull) continue;
+            uint64_t m[4];
+#pragma unroll
+            for (int k = 0; k < 4; k++) m[k] = __ballot(Val<T>::nonzero(e[l][k]));
+            if ((lane >> 3) == (uint32_t)l) {
+#pragma unroll
+                for (int k = 0; k < 4; k++) word |= spread4((uint32_t)(m[k] >> sh)) << k;
+            }
+            // sketch: three LDS atomics per nonzero
+            if ((m[0] | m[1] | m[2] | m[3]) == 0ull) continue;
             const uint64_t lbase = tp + 256u * l;
             if (a.c >= 256) {
                 // a load lies in one batch: its table entries are uniform
@@ -288,6 +281,12 @@ __global__ __launch_bounds__(NT, WPE) void encode_blocked_kernel(EncArgs<T> a) {
                     }
                 }
             }
+        }
+        if (lane < 32 && tp + 32ull * lane < r.p1) {
+            if (SB)
+                s_bm[((tp - r.p0) >> 5) + lane] = word;
+            else
+                a.b[(tp >> 5) + lane] = word;
         }
     };
     T e[D][4][4];
@@ -835,15 +834,18 @@ hipError_t launch_encode_blocked_t(const Geo& g, const void* x, void* y, uint32_
     // -> 0.094 ms, VGG19 0.127 -> 0.121 ms, LSTM 0.093 -> 0.088 ms against
     // the best of the 1024-lane ones.  Deeper pipelines (three or four tiles)
     // and 256-lane workgroups were slower.  fp32 (LDS float atomics, whose
-    // latency more waves hide better) and blocks too large for two per CU
-    // (BERT-base at 5 %) keep 1024 lanes: one tile per wave when there are
-    // more than two blocks per CU to run, else a two-tile pipeline.
+    // latency more waves hide better), blocks too large for two per CU, and
+    // blocks of few tiles (BERT-base at 5 %: 16 tiles of c = 32 batches, where
+    // the block's setup and sketch write-back weigh most and 1024 lanes share
+    // them: 0.194 against 0.209 ms) keep 1024 lanes: one tile per wave when
+    // there are more than two blocks per CU to run, else a two-tile pipeline.
     const size_t lds_used = a.stage_b ? staged : lds;
     const bool two_per_cu = lds_used + kLdsReserve <= kLdsBytes / 2;
+    const uint64_t block_tiles = ((uint64_t)g.block * g.c) / kWaveTile;
 #define HC_ENC_SEL(NT, D, WPE)                                                       \
     return a.stage_b ? launch(&encode_blocked_kernel<T, NT, D, WPE, true>, NT)      \
                      : launch(&encode_blocked_kernel<T, NT, D, WPE, false>, NT)
-    if (!g.f32 && two_per_cu) HC_ENC_SEL(512, 2, 4);
+    if (!g.f32 && two_per_cu && block_tiles >= 64) HC_ENC_SEL(512, 2, 4);
     if (pf) HC_ENC_SEL(1024, 2, 4);
     HC_ENC_SEL(1024, 1, 8);
 #undef HC_ENC_SEL
