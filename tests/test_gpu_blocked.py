@@ -294,3 +294,34 @@ def test_blocked_auto_lowers_c_for_dense_aggregates():
     # sparse aggregates keep the requested c
     q = hc.hc_geometry_blocked(n, 9_305_915, 1.3, 1024, 0, 7, "i32")
     assert int(q.c) == 1024
+
+
+@pytest.mark.parametrize("case", ["many_tiles", "few_tiles_many_blocks", "few_tiles_few_blocks"])
+def test_blocked_encode_every_launch_shape(case):
+    # the int32 blocked encode's three launch shapes: 512-lane workgroups with
+    # a two-tile pipeline (blocks of 64 tiles of 1024 parameters or more, two
+    # per CU), and 1024-lane workgroups with one tile per wave (more than two
+    # blocks per CU to run) or a two-tile pipeline (fewer).  Every worker's
+    # sketch and bitmap, and the decode, bit-exact against the oracle (on
+    # success and on failure)
+    import torch
+    _hc()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n, W, c, br = {"many_tiles": (3_000_017, 3, 1024, 8),
+                   "few_tiles_many_blocks": (12_000_011, 2, 64, 16),
+                   "few_tiles_few_blocks": (1_500_007, 2, 64, 16)}[case]
+    density = 0.02 if c == 1024 else 0.03
+    w = wl.make("synthetic", n=n, W=W, density=density, overlap=0.5, data_seed=71)
+    g = oracle.blocked_geometry(w.n, w.n_agg, w.hash_seed, c, 1.3, br)
+    tiles = g.block * c // 1024
+    if case == "many_tiles":
+        assert tiles >= 64
+    else:
+        assert tiles < 64
+        assert (g.nblocks > 2 * cus) == (case == "few_tiles_many_blocks")
+    r, _ = check_blocked_int(w, g)
+    # blocks of 1024 cells fail to peel now and then at this ratio (the oracle
+    # fails alike); the encode is what differs between the shapes
+    if case == "many_tiles" or r["info"].success:
+        assert r["info"].success
+        assert np.array_equal(r["x"], wrap_sum([w.dense(i) for i in range(w.W)]))
