@@ -413,6 +413,18 @@ __global__ __launch_bounds__(kBlock) void support_kernel(SupportArgs a) {
     if (chunk + 1 == a.nchunks && lane == 0 && a.woffb != nullptr) a.woffb[a.nb] = base;
 }
 
+// Coherent (agent-scope) 64-bit loads and stores: the peel's grid barrier
+// only orders a workgroup's memory operations (it waits for them to complete)
+// and does not write back or invalidate the L2, so every value one workgroup
+// writes and another reads across a round boundary goes through these (or
+// through atomics).
+__device__ __forceinline__ unsigned long long ld_agent64(const unsigned long long* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent64(unsigned long long* p, unsigned long long v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ---- frontier staging ----------------------------------------------------------
 
 // (cell, element position) pairs whose cell became pure, staged in LDS by one
@@ -456,7 +468,10 @@ __device__ void flush_pushes(Q& q, bool force, uint32_t room, unsigned int* tail
     for (uint32_t k = threadIdx.x; k < n; k += blockDim.x) {
         if ((uint64_t)base + k >= cells) continue;  // a cell is pushed at most once
         const uint2 it = q.item[k];
-        queue[base + k] = it;
+        // read by other workgroups after the grid barrier, whose fences do not
+        // write back or invalidate the L2: a coherent (agent-scope) store
+        st_agent64(reinterpret_cast<unsigned long long*>(queue + base + k),
+                   ((unsigned long long)it.y << 32) | it.x);
         if (mark != nullptr)
             __hip_atomic_store(mark + it.x, markval, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
@@ -1178,9 +1193,10 @@ __device__ __forceinline__ void scan_residual(const PeelArgs<T>& a, uint64_t cid
         if (!a.counted || cidx >= a.cells) return;
         const uint32_t y = (uint32_t)a.y_agg[cidx];
         if (packed)
-            a.cnt[cidx] = ((unsigned long long)y << 32) | (((v >> 32) << kp) + (v & 0xffffffffull));
+            st_agent64(a.cnt + cidx,
+                       ((unsigned long long)y << 32) | (((v >> 32) << kp) + (v & 0xffffffffull)));
         else
-            a.yw[cidx] = (int32_t)y;
+            __hip_atomic_store(a.yw + cidx, (int32_t)y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
@@ -1219,8 +1235,8 @@ __device__ __forceinline__ void peel_entry(const PeelArgs<T>& a, uint32_t cidx, 
     // the compiler had hoisted above their differing loads)
     unsigned long long wcell = 0;
     T ycell = T(0);
-    if (PACKED) wcell = a.cnt[cidx];
-    else ycell = a.yw[cidx];
+    if (PACKED) wcell = ld_agent64(a.cnt + cidx);
+    else ycell = __hip_atomic_load(a.yw + cidx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     bool taken;
     if (kMarks)
         taken = (__hip_atomic_load(fword, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & fbit) != 0u;
@@ -1311,24 +1327,31 @@ __device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks, uint32_
     // as one 64-bit word: a workgroup learns the next frontier's end from the
     // same load that ends its wait
     unsigned long long* const genw = reinterpret_cast<unsigned long long*>(&sy->gen.v[0]);
+    // Everything the peel hands from one round to the next goes through
+    // agent-scope atomics and coherent loads and stores, so the barrier only
+    // has to order: every wave's memory operations complete (s_waitcnt 0)
+    // before its workgroup arrives, and each arrival's counter reset before
+    // the next arrival it enables.  Agent-scope fences here wrote back and
+    // invalidated the L2 of every workgroup's XCD at every round.
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_s_waitcnt(0);
     lds_barrier();
     if (threadIdx.x == 0) {
         uint32_t ok = 1;
         const uint32_t groups = nblocks < kBarGroups ? nblocks : kBarGroups;
         const uint32_t grp = blockIdx.x % groups;
         const uint32_t gsize = (nblocks - grp + groups - 1u) / groups;  // blocks in the group
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         bool wait = true;
         uint32_t fe = 0;
         if (add_agent(&sy->group[grp].v[0], 1u) == gsize - 1u) {
             st_agent(&sy->group[grp].v[0], 0u);
-            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "agent");
+            __builtin_amdgcn_s_waitcnt(0);
             if (add_agent(&sy->top.v[0], 1u) == groups - 1u) {
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
                 fe = ld_agent(&sy->tail.v[0]);
                 st_agent(&sy->top.v[0], 0u);
+                __builtin_amdgcn_s_waitcnt(0);
                 __hip_atomic_store(genw, ((unsigned long long)fe << 32) | (gen + 1u),
-                                   __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 wait = false;
             }
         }
@@ -1349,7 +1372,7 @@ __device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks, uint32_
                 }
             }
         }
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
         s_ok = ok;
         s_fend = fe;
     }
@@ -1433,7 +1456,9 @@ __global__ __launch_bounds__(kPeelBlock) void peel_kernel(PeelArgs<T> a) {
                     // cell, in this round or an earlier one.  The element and the
                     // cell's residual are read alongside the claim: once claimed,
                     // nothing else changes that cell this round.
-                    const uint2 it = a.queue[i];
+                    const unsigned long long qw =
+                        ld_agent64(reinterpret_cast<const unsigned long long*>(a.queue + i));
+                    const uint2 it = make_uint2((uint32_t)qw, (uint32_t)(qw >> 32));
                     if (it.y < nsup) {
                         bool done = false;
                         if constexpr (std::is_same<T, int32_t>::value) {
