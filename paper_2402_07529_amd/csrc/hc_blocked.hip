@@ -763,15 +763,18 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
         }
     }
 
-    // block totals; the last workgroup to finish writes the summary
+    // block totals; the last workgroup to finish writes the summary.  The
+    // totals are atomics and are read back with coherent loads, so the ticket
+    // only has to follow them (s_waitcnt 0): an agent-scope fence here wrote
+    // back and invalidated the XCD's L2 at the end of every block, with the
+    // block's dense output still in it
     if (tid == 0) {
         atomicAdd(&a.bctrl->support, (unsigned long long)sup_total);
         atomicAdd(&a.bctrl->recovered, (unsigned long long)recovered);
         atomicMax(&a.bctrl->rounds, rounds);
-        __threadfence();
+        __builtin_amdgcn_s_waitcnt(0);
         const uint32_t ticket = atomicAdd(&a.bctrl->done, 1u);
         if (ticket == gridDim.x - 1) {
-            __threadfence();
             const unsigned long long sup =
                 __hip_atomic_load(&a.bctrl->support, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             const unsigned long long rec =
