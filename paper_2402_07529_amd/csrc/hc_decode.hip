@@ -1330,8 +1330,7 @@ __device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks, uint32_
     // Everything the peel hands from one round to the next goes through
     // agent-scope atomics and coherent loads and stores, so the barrier only
     // has to order: every wave's memory operations complete (s_waitcnt 0)
-    // before its workgroup arrives, and each arrival's counter reset before
-    // the next arrival it enables.  Agent-scope fences here wrote back and
+    // before its workgroup arrives.  Agent-scope fences here wrote back and
     // invalidated the L2 of every workgroup's XCD at every round.
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     __builtin_amdgcn_s_waitcnt(0);
@@ -1343,13 +1342,14 @@ __device__ bool grid_barrier(Ctrl* ctrl, PeelSync* sy, uint32_t nblocks, uint32_
         const uint32_t gsize = (nblocks - grp + groups - 1u) / groups;  // blocks in the group
         bool wait = true;
         uint32_t fe = 0;
-        if (add_agent(&sy->group[grp].v[0], 1u) == gsize - 1u) {
-            st_agent(&sy->group[grp].v[0], 0u);
-            __builtin_amdgcn_s_waitcnt(0);
-            if (add_agent(&sy->top.v[0], 1u) == groups - 1u) {
+        // The arrival counters only grow (the decode zeroes them once): in
+        // barrier gen the last of a group finds (gen + 1) * gsize - 1 arrivals
+        // before its own, and the last group leader (gen + 1) * groups - 1.
+        // No counter is reset on the way, so the chain from the last arrival
+        // to the generation store is two atomics and a load.
+        if (add_agent(&sy->group[grp].v[0], 1u) == (gen + 1u) * gsize - 1u) {
+            if (add_agent(&sy->top.v[0], 1u) == (gen + 1u) * groups - 1u) {
                 fe = ld_agent(&sy->tail.v[0]);
-                st_agent(&sy->top.v[0], 0u);
-                __builtin_amdgcn_s_waitcnt(0);
                 __hip_atomic_store(genw, ((unsigned long long)fe << 32) | (gen + 1u),
                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 wait = false;
