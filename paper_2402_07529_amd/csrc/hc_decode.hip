@@ -2057,10 +2057,17 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     // counters, three atomics per element) measured faster on half the CUs up
     // to 11 M cells, and slower at 97 M (BERT-base at 5 %: 16.1 against
     // 18.3 ms).
+    // With the barrier's fences at workgroup scope (a cheaper round), the
+    // int32 peel with a plan measured fastest on three quarters of the CUs
+    // from 8 M cells up to that bound (VGG19, 10.4 M cells: 1.727 -> 1.683 ms;
+    // BERT-base, 11.0 M: 1.794 -> 1.742 ms) and still on half below it (NCF
+    // 1.417 against 1.425 ms; LSTM 1.167 against 1.177 ms).
     const bool fewer_atomics = std::is_same<T, int32_t>::value && planned;
     const uint64_t half_below = fewer_atomics ? kPeelHalfGridCellsInt : kPeelHalfGridCells;
-    const uint32_t peel_grid = g.cells < half_below && di.cus >= 2 ? (uint32_t)di.cus / 2u
-                                                                   : (uint32_t)di.cus;
+    uint32_t peel_grid = g.cells < half_below && di.cus >= 2 ? (uint32_t)di.cus / 2u
+                                                             : (uint32_t)di.cus;
+    if (fewer_atomics && g.cells >= kPeelHalfGridCells && g.cells < half_below && di.cus >= 4)
+        peel_grid = (uint32_t)di.cus / 4u * 3u;
     PeelArgs<A> pa;
     pa.ctrl = ctrl;
     pa.sync = sync;
