@@ -35,7 +35,9 @@
 //            is already taken (in this round or an earlier one) do nothing, so
 //            the elements peeled in round r are exactly those with a cell in
 //            its frontier that were still live when it began.
-//            One grid barrier per round; rounds end when a frontier is empty;
+//            One grid barrier per round (workgroup-scope fences: what a round
+//            hands to the next goes through atomics and coherent loads and
+//            stores); rounds end when a frontier is empty;
 //   leftovers  elements never peeled get the Count Sketch median estimate
 //            from the residual sketch (Algorithm 1, last recovery step), on
 //            the whole chip: when decoding fails most of the support is left;
