@@ -1700,14 +1700,15 @@ __device__ __forceinline__ T estimate_raw(const EmitArgs<T>& a, uint32_t p) {
 
 // One workgroup per chunk of 1024 bitmap words (32768 parameters).  The
 // chunk's members are one contiguous run of E, so their values and recovered
-// flags are copied into LDS with coalesced loads, a window of 2048 at a time
-// (chunks denser than 1/16 take several): the output loop then has no global
-// loads ahead of its stores.  A stage of 2048 members measured best on MI355X:
-// a 4096 one costs NCF's write stream more occupancy than it saves on the
-// denser workloads.  The dense output goes out with nontemporal stores
-// (measured 1-2 % faster here, though plain stores win for a pure write
-// stream).
-constexpr uint32_t kEmitStage = 2048;  // members per LDS window (1/16 of a chunk's parameters)
+// flags are copied into LDS with coalesced loads, a window of 1024 at a time
+// (chunks denser than 1/32 take several): the output loop then has no global
+// loads ahead of its stores.  The window sets the workgroup's LDS and so how
+// many workgroups a CU keeps writing: measured on MI355X, 1024 members (17 KB,
+// eight workgroups per CU) against 2048 (22 KB, seven) took NCF's decode from
+// 1.422 to 1.413 ms with VGG19's and LSTM's unchanged, and 4096 cost NCF
+// 44 us.  The dense output goes out with nontemporal stores (measured 1-2 %
+// faster here, though plain stores win for a pure write stream).
+constexpr uint32_t kEmitStage = 1024;  // members per LDS window (1/32 of a chunk's parameters)
 
 template <typename T>
 __global__ __launch_bounds__(kBlock) void emit_kernel(EmitArgs<T> a) {
