@@ -550,28 +550,50 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
     while (single && qs < qe) {
         if (tid == 0) s_any[(rounds + 1u) % 3u] = 0u;
         bool mine = false;
-        for (uint32_t idx = qs + tid; idx < qe; idx += kDecThreads) {
-            const uint32_t cell = s_q[idx];
+        // every lane of a wave takes the same number of steps, so the cells
+        // that became pure are appended with one queue atomic per wave and
+        // step; the cell's value is read beside the claim (only the entry that
+        // wins the claim uses it, and no other entry changes that cell this
+        // round), and the two counter updates go out together
+        for (uint32_t base = qs + wave * 64u; base < qe; base += kDecThreads) {
+            const uint32_t idx = base + lane;
+            bool act = idx < qe;
+            const uint32_t cell = s_q[act ? idx : qs];  // a queued cell either way
             const uint32_t cc = s_cnt[cell];
-            if ((cc >> kDegShift) != 1u) continue;  // its member left with another cell
-            const uint32_t bl = cc & kSumMask;
+            act = act && (cc >> kDegShift) == 1u;  // else its member left with another cell
+            const uint32_t bl = act ? (cc & kSumMask) : 0u;
             const Member m = member_of(s_tab, bl, cell, cmask);
+            const A yv = s_val[cell];
             const uint32_t id = bl * a.c + m.t;  // the member's parameter within the block
             const uint32_t bit = 1u << (id & 31u);
-            if (atomicOr(s_claim + (id >> 5), bit) & bit) continue;
-            mine = true;
-            recovered++;
-            const uint32_t ej = m.j == 0 ? m.e[0] : (m.j == 1 ? m.e[1] : m.e[2]);
-            const A xv = Val<A>::sign(s_val[cell], tab_neg(ej));  // x = g_j * Y
-#pragma unroll
-            for (uint32_t jj = 0; jj < 3; jj++) {
-                if (jj == m.j) continue;
-                const uint32_t c2 = tab_cell(m.e[jj], m.t, cmask);
-                const uint32_t old = atomicSub(s_cnt + c2, kDegOne + bl);
-                if ((old >> kDegShift) == 2u) s_q[atomicAdd(s_tail, 1u)] = (uint16_t)c2;
-                LdsAdd<A>::add(s_val + c2, Val<A>::sign(xv, !tab_neg(m.e[jj])));  // -= g * x
+            if (act) act = (atomicOr(s_claim + (id >> 5), bit) & bit) == 0u;
+            const uint32_t jo0 = m.j == 0 ? 1u : 0u, jo1 = m.j == 2 ? 1u : 2u;
+            const uint32_t e0 = jo0 == 0 ? m.e[0] : m.e[1];
+            const uint32_t e1 = jo1 == 1 ? m.e[1] : m.e[2];
+            const uint32_t c0 = tab_cell(e0, m.t, cmask), c1 = tab_cell(e1, m.t, cmask);
+            uint32_t old0 = 0, old1 = 0;
+            if (act) {
+                mine = true;
+                recovered++;
+                const uint32_t ej = m.j == 0 ? m.e[0] : (m.j == 1 ? m.e[1] : m.e[2]);
+                const A xv = Val<A>::sign(yv, tab_neg(ej));  // x = g_j * Y
+                old0 = atomicSub(s_cnt + c0, kDegOne + bl);
+                old1 = atomicSub(s_cnt + c1, kDegOne + bl);
+                LdsAdd<A>::add(s_val + c0, Val<A>::sign(xv, !tab_neg(e0)));  // -= g * x
+                LdsAdd<A>::add(s_val + c1, Val<A>::sign(xv, !tab_neg(e1)));
+                s_cnt[cell] = kClaimed | bl;  // keeps g_j * x in s_val[cell]
             }
-            s_cnt[cell] = kClaimed | bl;  // keeps g_j * x in s_val[cell]
+            const bool p0 = act && (old0 >> kDegShift) == 2u;
+            const bool p1 = act && (old1 >> kDegShift) == 2u;
+            const uint64_t b0 = __ballot(p0), b1 = __ballot(p1);
+            const uint32_t n0 = (uint32_t)__popcll(b0), n = n0 + (uint32_t)__popcll(b1);
+            if (n != 0u) {
+                uint32_t at = 0;
+                if (lane == 0) at = atomicAdd(s_tail, n);
+                at = (uint32_t)__builtin_amdgcn_readfirstlane((int)at);
+                if (p0) s_q[at + lanes_below(b0)] = (uint16_t)c0;
+                if (p1) s_q[at + n0 + lanes_below(b1)] = (uint16_t)c1;
+            }
         }
         if (__ballot(mine) != 0ull && lane == 0) s_any[rounds % 3u] = 1u;
         lds_barrier();
