@@ -255,7 +255,12 @@ class Runner:
         self.torch = torch
         self.w, self.c, self.dev = w, c, dev
         self.vt = torch.int32 if w.vtype == "i32" else torch.float32
-        self.x = torch.zeros((w.W, w.n), dtype=self.vt, device=dev)
+        # each worker's gradient starts on a 256-byte boundary, as separate
+        # per-worker buffers would (the rows of one (W, n) tensor start off
+        # the 16-byte grid when n mod 4 != 0, as LSTM's n does)
+        n_pad = (w.n + 63) // 64 * 64
+        self.x_rows = torch.zeros((w.W, n_pad), dtype=self.vt, device=dev)
+        self.x = self.x_rows[:, :w.n]
         for i in range(w.W):
             self.x[i][torch.from_numpy(w.idx[i].astype(np.int64)).to(dev)] = \
                 torch.from_numpy(w.val[i]).to(dev)
