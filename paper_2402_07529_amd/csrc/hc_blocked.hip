@@ -496,6 +496,22 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
             const uint64_t pw = (w0 + 64ull * (ga + u) + lane) * 32ull;
             uint32_t word = wv[u];
             lane_support += __popc(word);
+            if (a.c >= 32u) {
+                // the word's 32 parameters lie in one batch: its three table
+                // entries are read once, not once per member
+                if (word == 0u) continue;
+                const uint32_t bl = (uint32_t)((pw >> a.log2c) - r.b0);
+                const uint32_t e0 = s_tab[3 * bl], e1 = s_tab[3 * bl + 1], e2 = s_tab[3 * bl + 2];
+                const uint32_t tb = (uint32_t)pw & cmask;
+                while (word) {
+                    const uint32_t t = tb + (uint32_t)__builtin_ctz(word);
+                    word &= word - 1u;
+                    atomicAdd(s_cnt + tab_cell(e0, t, cmask), kDegOne + bl);
+                    atomicAdd(s_cnt + tab_cell(e1, t, cmask), kDegOne + bl);
+                    atomicAdd(s_cnt + tab_cell(e2, t, cmask), kDegOne + bl);
+                }
+                continue;
+            }
             while (word) {
                 const uint32_t bit = __builtin_ctz(word);
                 word &= word - 1u;
@@ -512,18 +528,32 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
     if (lane == 0) s_tmp[32 + wave] = wave_support;
     lds_barrier();
 
-    // round-0 frontier: every cell of degree one, appended to the queue (one
-    // LDS atomic per wave and step)
-    for (uint32_t i0 = wave * 64u; i0 < bcells; i0 += kDecThreads) {
-        const uint32_t i = i0 + lane;
-        const bool pure = i < bcells && (s_cnt[i] >> kDegShift) == 1u;
-        const uint64_t m = __ballot(pure);
-        if (m == 0ull) continue;
-        const uint32_t leader = (uint32_t)__ffsll((unsigned long long)m) - 1u;
-        uint32_t base = 0;
-        if (lane == leader) base = atomicAdd(s_tail, (uint32_t)__popcll(m));
-        base = (uint32_t)__builtin_amdgcn_readlane((int)base, (int)leader);
-        if (pure) s_q[base + lanes_below(m)] = (uint16_t)i;
+    // round-0 frontier: every cell of degree one, appended to the queue.  A
+    // wave counts the pure cells of its own contiguous range of the block's
+    // cells (the counters' loads independent of each other), takes their
+    // places with one LDS atomic, then writes them: one queue atomic per wave
+    // instead of one per wave and step, each waited for in turn
+    {
+        const uint32_t cpw = (bcells + kWaves * 64u - 1u) / (kWaves * 64u) * 64u;
+        const uint32_t lo = wave * cpw < bcells ? wave * cpw : bcells;
+        const uint32_t hi = lo + cpw < bcells ? lo + cpw : bcells;
+        uint32_t npure = 0;
+        for (uint32_t i0 = lo; i0 < hi; i0 += 64u) {
+            const uint32_t i = i0 + lane;
+            npure += (uint32_t)__popcll(__ballot(i < hi && (s_cnt[i] >> kDegShift) == 1u));
+        }
+        uint32_t at = 0;
+        if (npure != 0u) {
+            if (lane == 0) at = atomicAdd(s_tail, npure);
+            at = (uint32_t)__builtin_amdgcn_readfirstlane((int)at);
+            for (uint32_t i0 = lo; i0 < hi; i0 += 64u) {
+                const uint32_t i = i0 + lane;
+                const bool pure = i < hi && (s_cnt[i] >> kDegShift) == 1u;
+                const uint64_t m = __ballot(pure);
+                if (pure) s_q[at + lanes_below(m)] = (uint16_t)i;
+                at += (uint32_t)__popcll(m);
+            }
+        }
     }
     lds_barrier();
 
@@ -695,18 +725,19 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
                 excl += lanes_below(mb) << b;
                 total += (uint32_t)__popcll(mb) << b;
             }
-            auto member = [&](uint32_t s, bool valid, uint32_t owner, uint32_t bit) {
-                const uint64_t p = (base + owner) * 32ull + bit;
+            // member p (of batch bl, whose table entries are e) takes its
+            // value from its claimed cell, or the median estimate
+            auto member_e = [&](uint32_t s, bool valid, uint64_t p, uint32_t bl,
+                                const uint32_t (&ee)[3]) {
                 A val = A(0);
                 bool found = true;
                 if (valid) {
-                    const uint32_t bl = (uint32_t)((p >> a.log2c) - r.b0);
                     const uint32_t t = (uint32_t)p & cmask;
                     A est[3];
                     found = false;
 #pragma unroll
                     for (int j = 0; j < 3; j++) {
-                        const uint32_t e = s_tab[3 * bl + j];
+                        const uint32_t e = ee[j];
                         const uint32_t cell = tab_cell(e, t, cmask);
                         est[j] = Val<A>::sign(s_val[cell], tab_neg(e));
                         if (s_cnt[cell] == (kClaimed | bl)) {
@@ -732,11 +763,29 @@ __global__ __launch_bounds__(kDecThreads) void decode_blocked_kernel(DecArgs<T> 
                     if (!found) atomicAnd(a.mask + (p >> 5), ~(1u << (p & 31u)));
                 }
             };
+            auto member = [&](uint32_t s, bool valid, uint32_t owner, uint32_t bit) {
+                const uint64_t p = (base + owner) * 32ull + bit;
+                const uint32_t bl = valid ? (uint32_t)((p >> a.log2c) - r.b0) : 0u;
+                const uint32_t ee[3] = {s_tab[3 * bl], s_tab[3 * bl + 1], s_tab[3 * bl + 2]};
+                member_e(s, valid, p, bl, ee);
+            };
             if (total >= kDenseGroup) {
                 // a dense group: each lane walks its own word's members (no
                 // search across lanes for every member; measured on a 73 %
-                // dense BERT-base aggregate)
+                // dense BERT-base aggregate).  For c >= 32 the word lies in
+                // one batch, whose table entries are read once.
                 uint32_t bits = word, rk = 0;
+                if (a.c >= 32u) {
+                    const uint64_t pw = (base + lane) * 32ull;
+                    const uint32_t blw = word != 0u ? (uint32_t)((pw >> a.log2c) - r.b0) : 0u;
+                    const uint32_t ew[3] = {s_tab[3 * blw], s_tab[3 * blw + 1], s_tab[3 * blw + 2]};
+                    while (bits != 0u) {
+                        const uint32_t bit = (uint32_t)__builtin_ctz(bits);
+                        bits &= bits - 1u;
+                        member_e(excl + rk, true, pw + bit, blw, ew);
+                        rk++;
+                    }
+                }
                 while (bits != 0u) {
                     const uint32_t bit = (uint32_t)__builtin_ctz(bits);
                     bits &= bits - 1u;
