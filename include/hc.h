@@ -32,7 +32,9 @@
  *     calling host thread.  Invalid arguments are detected before anything
  *     is enqueued.
  *   - Value, index and bitmap buffers need their natural 4-byte alignment
- *     (16-byte alignment lets the kernels use vector memory operations);
+ *     (16-byte alignment lets the kernels use vector memory operations on
+ *     sketches, bitmaps and outputs; hc_encode and hc_encode_staged read the
+ *     gradient with 16-byte loads at any 4-byte alignment);
  *     the decode workspace must be 256-byte aligned and the decode info
  *     8-byte aligned.  hipMalloc and PyTorch allocations satisfy all of it.
  *
