@@ -301,7 +301,10 @@ hc_status hc_aggregate(const hc_params *p, const void *y_in, const uint32_t *b_i
  *   mask[ceil(n/32)]      bit p set iff p was recovered by peeling;
  *   info (one struct)     summary, DEVICE memory.
  * ws/ws_bytes: device workspace of at least the ws_bytes hc_sizes reports for
- * the same max_support; contents on entry are ignored.
+ * the same max_support; contents on entry are ignored.  max_support also picks
+ * how round 0 runs on an int32 sketch with a plan: by rows when the sketch has
+ * a cell per element of max_support, entry by entry otherwise (a bound near
+ * the true support keeps the faster one; results are the same either way).
  * Peeling runs as synchronous rounds entirely on the device (one cooperative
  * kernel; no host round trips).  Decode failure is data (info->success), not
  * an error status. */

@@ -1955,7 +1955,14 @@ hipError_t launch_decode_t(const Geo& g, const void* plan, const void* y_agg_v,
     // instead of the counter kernel and the entry-by-entry round, and the peel
     // kernel starts from round 1 (LSTM, 6.2 M cells: decode 1.40 -> 1.32 ms).
     const bool wave_rows = planned && (uint64_t)g.rows >= 8ull * (uint64_t)di.cus;
-    const bool rows0 = wave_rows && std::is_same<T, int32_t>::value;
+    // Round 0 by rows works through every member of every live batch twice;
+    // it pays when the sketch has at least a cell per support element (the
+    // decode's support bound), where it replaces the entry-by-entry round 0.
+    // Below that the sketch cannot peel anyway and round 0 recovers little:
+    // on section 4.1's VGG19 gradient (69.6 % dense) at sketch sizes of 0.02
+    // to 0.6 of n the decode took 2.35-3.68 ms by rows against 1.18-3.37 ms
+    // without, and from 0.7 up 4.78-7.57 ms against 4.85-14.5 ms.
+    const bool rows0 = wave_rows && std::is_same<T, int32_t>::value && (uint64_t)g.cells >= L.cap;
     Round0Args ra;
     ra.y_agg = reinterpret_cast<const int32_t*>(y_agg_v);
     ra.vals = reinterpret_cast<int32_t*>(vals);

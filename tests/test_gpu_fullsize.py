@@ -186,19 +186,12 @@ def test_fullsize_blocked(name, vtype):
         assert np.count_nonzero(g["x"]) == np.count_nonzero(sums)
 
 
-def test_round0_by_rows_with_unpackable_counters():
-    # A sketch of 16 M cells (16,384 rows, wide enough for round 0 by rows)
-    # over 33.6 M elements (positions take 26 bits) with one cell of at least
-    # 77 elements: every batch that hashes into the busiest row gets a nonzero
-    # at the offset that lands on that row's cell 0.  That cell's
-    # deg * 2^26 + (sum of positions) does not fit 32 bits, so the int32 peel
-    # keeps counters and residuals apart, and round 0 by rows takes its
-    # unpacked path.  The sketch is half the support: round 0 recovers the
-    # elements with a pure cell, a few rounds follow, the rest get median
-    # estimates.  Exact against the oracle.
-    _hc()
-    n, rows = 1 << 28, 16384
-    w = wl.make("synthetic", n=n, W=1, density=0.13, data_seed=515)
+def _hot_cell_workload(n, rows, density, seed):
+    """A synthetic gradient plus one nonzero in every batch that hashes into
+    the busiest row, at the offset that lands on that row's cell 0: a cell of
+    far more elements than any random one, whose deg * 2^k + (sum of
+    positions) does not fit 32 bits."""
+    w = wl.make("synthetic", n=n, W=1, density=density, data_seed=seed)
     g = oracle.Geom(n=n, rows=rows, seed=w.hash_seed, c=1024)
     nb = n // 1024
     cl, _ = oracle.cells(g, np.arange(nb, dtype=np.uint64) * 1024)
@@ -216,9 +209,11 @@ def test_round0_by_rows_with_unpackable_counters():
     kp = int(np.ceil(np.log2(idx.size)))
     hot_pos = np.searchsorted(idx, hot)
     assert hot.size * 2**kp + int(hot_pos.sum()) >= 2**32  # the busy cell cannot pack
-    assert rows >= 8 * 256  # rows to spare for round 0 by rows (8 per CU of a 256-CU GPU)
-    print(f"[round0 rows unpacked] n={n} nonzeros={idx.size} rows={rows} hot={hot.size}",
-          flush=True)
+    return w, idx, hot
+
+
+def _check_unpackable(w, idx, rows, label):
+    print(f"[{label}] n={w.n} nonzeros={idx.size} rows={rows} cells={rows * 1024}", flush=True)
     gr = gpu_run(w, rows, 1024, want_coo_out=False, use_plan=True, max_support=idx.size)
     o = oracle_run(w, rows, 1024)
     assert np.array_equal(gr["Ya"], o["Ya"])
@@ -226,3 +221,36 @@ def test_round0_by_rows_with_unpackable_counters():
     assert np.array_equal(gr["mask"], o["mask"])
     assert_same_info(gr["info"], o["info"])
     assert 0 < gr["info"].n_recovered < idx.size
+
+
+@pytest.mark.timeout(900)
+def test_unpackable_counters_sketch_half_the_support():
+    # 16 M cells (16,384 rows) over 33.6 M elements (positions take 26 bits)
+    # with one cell of at least 77 elements that cannot pack: the int32 peel
+    # keeps counters and residuals apart.  With fewer cells than support
+    # elements the decode takes the counter gather and the entry-by-entry
+    # round 0 (round 0 by rows needs a cell per element).  Round 0 recovers
+    # the elements with a pure cell, a few rounds follow, the rest get median
+    # estimates.  Exact against the oracle.
+    _hc()
+    n, rows = 1 << 28, 16384
+    w, idx, hot = _hot_cell_workload(n, rows, 0.13, 515)
+    assert rows * 1024 < idx.size
+    _check_unpackable(w, idx, rows, "unpackable, half the support")
+
+
+@pytest.mark.timeout(900)
+def test_round0_by_rows_with_unpackable_counters():
+    # 25.2 M cells (24,576 rows, wide enough for round 0 by rows) over 21.5 M
+    # elements of a 2^30-parameter gradient (positions take 25 bits) with one
+    # cell of 177 elements: its deg * 2^25 + (sum of positions) does not fit
+    # 32 bits, so round 0 by rows takes its unpacked path (counters and
+    # residuals apart, two passes over the row).  The sketch is 1.17 cells per
+    # element, under the peeling threshold: the decode ends with median
+    # estimates for what the 2-core keeps.  Exact against the oracle.
+    _hc()
+    n, rows = 1 << 30, 24576
+    w, idx, hot = _hot_cell_workload(n, rows, 0.02, 515)
+    assert rows * 1024 >= idx.size  # round 0 by rows: a cell per support element
+    assert rows >= 8 * 256  # rows to spare (8 per CU of a 256-CU GPU)
+    _check_unpackable(w, idx, rows, "round0 rows unpacked")
