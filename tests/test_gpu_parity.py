@@ -438,6 +438,29 @@ def test_unpackable_counters_fall_back():
     assert g["info"].n_recovered == 0
 
 
+@pytest.mark.parametrize("density", [0.1, 0.12])
+def test_round0_paths_either_side_of_the_support_bound(density):
+    # 2,048 rows (8 per CU of a 256-CU GPU: enough for round 0 by rows) over a
+    # 2^24-parameter gradient.  max_support = cells takes round 0 by rows,
+    # max_support = cells + 1 the entry-by-entry round; both decodes are exact
+    # against the oracle.  Density 0.1 gives 1.68 M elements (1.25 cells per
+    # element: the sketch peels), 0.12 gives 2.0 M (1.04: peeling stops at the
+    # 2-core and the rest get median estimates).
+    _hc()
+    n, rows = 1 << 24, 2048
+    cells = rows * 1024
+    w = wl.make("synthetic", n=n, W=1, density=density, data_seed=77)
+    assert w.n_agg <= cells
+    o = oracle_run(w, rows, 1024)
+    for ms in (cells, cells + 1):
+        print(f"[round0 paths] density={density} nonzeros={w.n_agg} max_support={ms}", flush=True)
+        g = gpu_run(w, rows, 1024, want_coo_out=False, use_plan=True, max_support=ms)
+        assert np.array_equal(g["x"], o["x"])
+        assert np.array_equal(g["mask"], o["mask"])
+        assert_same_info(g["info"], o["info"])
+    assert (o["info"].success == 1) == (density == 0.1)
+
+
 @pytest.mark.parametrize("n", [4096 * 32, 4098 * 32, 4094 * 32 + 5, 4097 * 32 + 1])
 @pytest.mark.parametrize("offset", [0, 1, 2])
 def test_aggregate_every_vector_width(n, offset):
